@@ -1,0 +1,220 @@
+#!/usr/bin/env python3
+"""Benchmark of the KAN-layer forward hot path on one MI355X.
+
+One step = the whole hot path over one batch of synthetic input of the
+3-layer KAN MLP workload (784 -> 256 -> 256 -> 10, G = 10, cubic, grid [-1, 1],
+batch 65536):
+    kan_basis_eval(x)                      basis-only tensor of the input
+    3 x kan_layer_forward                  fused basis + MFMA contraction + SiLU
+Inputs and weights are resident in HBM before timing starts; every launch goes
+through the C ABI onto torch's current stream.
+
+Prints ONE JSON line: samples/s (value), Gbasis/s, the roofline of the
+dominant kernel (per-kernel durations from HIP events on the launch stream)
+and the float64 CPU oracle timed on a bounded row sample of the same step.
+
+    python bench.py [--steps K] [--warmup W] [--dtype bf16|f32]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+WORKLOAD = "c5_mlp_784_256_256_10_g10"
+METRIC = "KAN layer fwd samples/s + Gbasis/s; % of HBM / MFMA peak on MI355X"
+# MI355X published peaks
+PEAK_HBM_GBS = 8000.0
+PEAK_TFLOPS = {"bf16": 2516.6, "f32": 157.3}
+
+
+def parse():
+    p = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--dtype", choices=["bf16", "f32"], default="bf16")
+    p.add_argument("--cpu-seconds", type=float, default=10.0,
+                   help="target wall time of the CPU oracle sample")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
+                   help="only run a plain device copy of BYTES bytes 10 times (HBM counter "
+                        "calibration under rocprofv3) and exit")
+    return p.parse_args()
+
+
+def copy_calibration(nbytes: int) -> None:
+    import torch
+    n = nbytes // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(10):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes": n * 4, "launches": 10}), flush=True)
+
+
+def cpu_baseline(W, n_layers_shapes, target_s: float):
+    """The float64 oracle, untuned, on a row sample of the same step."""
+    import numpy as np
+    import oracle
+
+    oracle.build()
+    threads = oracle.num_threads()
+    G = W["G"]
+    x = W["x"]
+    layers = W["layers"]
+
+    def step(rows):
+        xs = x[:rows].astype(np.float64)
+        oracle.basis_tp(xs, G)
+        oracle.mlp(xs, layers, G)
+
+    t0 = time.perf_counter()
+    step(64)
+    dt64 = time.perf_counter() - t0
+    rows = int(max(64, min(x.shape[0], 64 * target_s / max(dt64, 1e-6))))
+    t0 = time.perf_counter()
+    step(rows)
+    dt = time.perf_counter() - t0
+    return {"value": rows / dt, "unit": "samples/s", "cores": threads, "kind": "oracle",
+            "sample": f"first {rows} rows of the {x.shape[0]}-row batch: float64 basis of the "
+                      f"input + 3-layer forward, {dt:.1f} s wall on {threads} threads"}
+
+
+def main() -> int:
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py: this build measures one GPU only; --gpus {args.gpus} is not run "
+              "(the batch shards across GPUs with no communication; see the design notes)",
+              file=sys.stderr)
+        return 2
+    import numpy as np
+    import torch
+
+    from paper_2609_01956_amd import binding as kb
+    from paper_2609_01956_amd import workloads as wl
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 1
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration)
+        return 0
+    kb.load_library()
+    dev = torch.device("cuda:0")
+    tdt = torch.bfloat16 if args.dtype == "bf16" else torch.float32
+    es = 2 if args.dtype == "bf16" else 4
+
+    W = wl.make_workload(WORKLOAD)
+    G, lo, hi = W["G"], W["lo"], W["hi"]
+    nb = G + 3
+    x_np = W["x"]
+    B, n_in0 = x_np.shape
+    prep = (lambda a: wl.round_to_bf16_f32(a)) if args.dtype == "bf16" else (lambda a: a)
+    x = torch.from_numpy(prep(x_np)).to(dev).to(tdt).contiguous()
+    layers = [(torch.from_numpy(prep(C)).to(dev).to(tdt).contiguous(),
+               torch.from_numpy(prep(Wb)).to(dev).to(tdt).contiguous()) for C, Wb in W["layers"]]
+    shapes = [(C.shape[1], C.shape[0]) for C, _ in layers]  # (in, out)
+    phi = torch.empty((B, n_in0, nb), dtype=tdt, device=dev)
+    hs = [torch.empty((B, o), dtype=tdt, device=dev) for _, o in shapes]
+
+    names = ["basis_eval"] + [f"layer{i + 1}_{i_}x{o}" for i, (i_, o) in enumerate(shapes)]
+
+    def step(events=None):
+        if events is not None:
+            events[0].record()
+        kb.basis(x, G, lo, hi, out=phi)
+        if events is not None:
+            events[1].record()
+        h = x
+        for li, ((C, Wb), out) in enumerate(zip(layers, hs)):
+            kb.layer_forward(h, C, Wb, G, lo, hi, out=out)
+            if events is not None:
+                events[2 + li].record()
+            h = out
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # Timed region: exactly K steps, with one HIP event between kernels.
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(names) + 1)]
+          for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        step(ev[k])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    per_kernel_ms = [float(np.mean([e[i].elapsed_time(e[i + 1]) for e in ev]))
+                     for i in range(len(names))]
+
+    # Algorithmic work per launch.
+    basis_values = B * n_in0 * nb
+    kern = {}
+    kern["basis_eval"] = {
+        "bound": "hbm", "unit": "GB/s", "peak": PEAK_HBM_GBS,
+        "algorithmic": (B * n_in0 * es + basis_values * es) / 1e9,  # GB: read x, write phi
+    }
+    for name, (i_, o) in zip(names[1:], shapes):
+        kern[name] = {"bound": "mfma", "unit": "TFLOP/s", "peak": PEAK_TFLOPS[args.dtype],
+                      "algorithmic": 2.0 * B * o * i_ * (nb + 1) / 1e12}  # dense TFLOP
+    for name, ms in zip(names, per_kernel_ms):
+        k = kern[name]
+        k["avg_us"] = ms * 1e3
+        k["achieved"] = k["algorithmic"] / (ms * 1e-3)
+        k["frac"] = k["achieved"] / k["peak"]
+    dom = max(names, key=lambda n: kern[n]["avg_us"])
+    dk = kern[dom]
+
+    # Parity re-check of this run's output on sampled rows (float64 oracle).
+    parity = None
+    try:
+        import oracle
+        rows = np.arange(0, B, max(1, B // 64))[:64]
+        trace = oracle.mlp(prep(x_np)[rows], [(prep(C), prep(Wb)) for C, Wb in W["layers"]], G,
+                           bf16=args.dtype == "bf16", bf16_operands=args.dtype == "bf16")
+        got = hs[-1][torch.from_numpy(rows).to(dev)].float().cpu().numpy().astype(np.float64)
+        parity = float(np.abs(got - trace).max() / np.abs(trace).max())
+    except Exception as e:  # the oracle is optional for timing
+        parity = f"unavailable: {e}"
+
+    basis_total = B * nb * (n_in0 + sum(i_ for i_, _ in shapes))
+    line = {
+        "metric": METRIC,
+        "value": B / (ms_per_step * 1e-3),
+        "unit": "samples/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": args.dtype,
+        "data": "synthetic",
+        "config": {"workload": WORKLOAD, "global_batch": B, "layers": [n_in0] + [o for _, o in shapes],
+                   "grid_size": G, "spline_order": 3, "grid": [lo, hi],
+                   "step": "kan_basis_eval(x) + 3 x kan_layer_forward"},
+        "gbasis_per_s": basis_total / (ms_per_step * 1e-3) / 1e9,
+        "roofline": {"kernel": dom, "bound": dk["bound"], "achieved": dk["achieved"],
+                     "peak": dk["peak"], "unit": dk["unit"], "frac": dk["frac"], "traffic": None},
+        "kernels": {n: {k: v for k, v in kern[n].items()} for n in names},
+        "parity_e2e_normwise": parity,
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(W, shapes, args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,129 @@
+/*
+ * kan.h -- C ABI of the MI355X (gfx950) InKAN KAN-layer forward.
+ *
+ * The library evaluates uniform cubic B-spline KAN layers with the basis in
+ * clamped truncated-power form (paper: Sec. 2 "Step 4", eq. truncated, with the
+ * bounded coordinate of eq. bounded) and contracts it with the spline
+ * coefficients plus the SiLU base branch (eq. kan_forward).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  * Pointers named x, phi, coef, base_w, y are DEVICE pointers owned by the
+ *    caller.  The library allocates no memory and keeps no global state; calls
+ *    are reentrant and thread-safe.
+ *  * Work is enqueued on `stream` (a hipStream_t passed as void*; NULL is the
+ *    null stream) and returns before it finishes.  Results are visible after the
+ *    caller synchronises that stream.  A device fault inside a kernel surfaces at
+ *    that synchronisation, not in the return code.
+ *  * Tensors are dense and row-major.  `dtype` applies to every tensor of a call:
+ *    KAN_F32 is IEEE binary32 throughout; KAN_BF16 is bfloat16 storage with
+ *    binary32 basis evaluation and accumulation, rounded to nearest-even on
+ *    store.
+ *  * Grid: G = grid_size intervals of width h = (grid_hi - grid_lo) / G.  The
+ *    knot vector is t_j = grid_lo + (j - 3) h, j = 0 .. G + 6, which gives
+ *    nb = G + 3 cubic basis functions; basis j is supported on [t_j, t_{j+4}]
+ *    (uniform simple knots, Sec. 2 "Step 3"; the extension by three spans on
+ *    each side of [grid_lo, grid_hi] is this library's grid convention).
+ *    Only cubic splines are implemented, as in the paper (Sec. 5): any other
+ *    spline_order is KAN_ERR_UNSUPPORTED.  Knots are always uniform; there is
+ *    no way to pass a non-uniform knot vector (Sec. 5).
+ *  * Accuracy: the basis is evaluated in binary32 as
+ *      u_j = x / h - grid_lo / h + 3 - j           (one fused multiply-add),
+ *      N_j = clamp-based truncated power of u_j     (eq. truncated + eq. bounded),
+ *    where the clamp to [0, 4] makes every basis exactly 0 off its support.
+ *    When 1/h and grid_lo/h are exact in binary32 (e.g. [-1, 1] with any G up
+ *    to 2^22) the basis is within 1e-6 of the exact value; otherwise the error
+ *    grows with the rounding of those two constants.
+ *  * Validation happens on the host before any HIP call, and every invalid
+ *    argument returns its code without touching the device.  An empty problem
+ *    (n == 0 or batch == 0) returns KAN_OK and launches nothing.
+ *  * No C++ exception crosses this interface.
+ */
+#ifndef KAN_H
+#define KAN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum kan_status {
+    KAN_OK = 0,
+    KAN_ERR_INVALID_ARG = 1, /* bad size, range, pointer, alignment or overlap   */
+    KAN_ERR_UNSUPPORTED = 2, /* spline_order != 3 or an unknown dtype           */
+    KAN_ERR_DEVICE = 3       /* the HIP runtime rejected a launch               */
+} kan_status;
+
+typedef enum kan_dtype {
+    KAN_F32 = 0,  /* binary32 storage and arithmetic                          */
+    KAN_BF16 = 1  /* bfloat16 storage, binary32 arithmetic and accumulation   */
+} kan_dtype;
+
+typedef struct kan_grid {
+    int32_t grid_size;    /* G, number of grid intervals, 1 <= G <= 4000      */
+    int32_t spline_order; /* k, must be 3                                       */
+    float grid_lo;        /* finite, grid_lo < grid_hi                          */
+    float grid_hi;        /* |grid_lo| / h and |grid_hi| / h at most 2^22       */
+} kan_grid;
+
+/*
+ * kan_basis_eval -- basis-only evaluation (the elementwise truncated-power
+ * basis of eq. truncated with the clamp of eq. bounded).
+ *
+ *   x    [n]           input values, any shape flattened; dtype storage.
+ *   phi  [n, G + 3]    output, basis index fastest: phi[e * (G+3) + j] = N_j(x[e]).
+ *
+ * phi must not overlap x.  x and phi must be aligned to the dtype size.
+ * A NaN input gives NaN in all G + 3 outputs of that element; +-Inf gives 0.
+ *
+ * Returns KAN_OK, KAN_ERR_INVALID_ARG (grid == NULL, bad grid, n < 0,
+ * NULL/misaligned/overlapping pointers with n > 0, n * (G + 3) overflowing
+ * int64), KAN_ERR_UNSUPPORTED (spline_order != 3, unknown dtype) or
+ * KAN_ERR_DEVICE (launch rejected).
+ */
+kan_status kan_basis_eval(const kan_grid* grid, kan_dtype dtype, const void* x,
+                          int64_t n, void* phi, void* stream);
+
+/*
+ * kan_layer_forward -- one KAN layer (eq. kan_forward):
+ *
+ *   y[b, o] = sum_i ( sum_j coef[o, i, j] N_j(x[b, i])  +  base_w[o, i] silu(x[b, i]) )
+ *
+ * with silu(v) = v / (1 + exp(-v)).  coef are the effective spline
+ * coefficients (the layer has no separate spline scaler, Sec. 2 "Integration
+ * with KAN layers").
+ *
+ *   x       [batch, in_features]              dtype storage
+ *   coef    [out_features, in_features, G+3]  dtype storage
+ *   base_w  [out_features, in_features]       dtype storage
+ *   y       [batch, out_features]             dtype storage, fully overwritten
+ *
+ * y must not overlap any input.  Every pointer must be aligned to the dtype
+ * size.  The basis is generated in registers and never written to memory.
+ * A NaN in x[b, :] makes y[b, :] NaN (through the SiLU branch).
+ *
+ * Returns KAN_OK, KAN_ERR_INVALID_ARG (grid == NULL, bad grid, batch < 0,
+ * in_features < 1, out_features < 1, in_features * (G + 4) >= 2^31,
+ * NULL/misaligned/overlapping pointers with batch > 0), KAN_ERR_UNSUPPORTED
+ * (spline_order != 3, unknown dtype) or KAN_ERR_DEVICE (launch rejected).
+ */
+kan_status kan_layer_forward(const kan_grid* grid, kan_dtype dtype, int64_t batch,
+                             int32_t in_features, int32_t out_features,
+                             const void* x, const void* coef, const void* base_w,
+                             void* y, void* stream);
+
+/* Static, NUL-terminated description of a status code (never NULL). */
+const char* kan_status_string(kan_status status);
+
+/* Version of this interface; bumped on any incompatible change. */
+int32_t kan_abi_version(void);
+
+#define KAN_ABI_VERSION 1
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KAN_H */

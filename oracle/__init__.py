@@ -75,7 +75,7 @@ def _load():
             lib.kan_oracle_silu.argtypes = [_D, _I64, _D]
             lib.kan_oracle_layer.argtypes = [_D, _I64, ctypes.c_int, ctypes.c_int, _D, _D,
                                              ctypes.c_int, ctypes.c_int, ctypes.c_double,
-                                             ctypes.c_double, ctypes.c_int, _D]
+                                             ctypes.c_double, ctypes.c_int, ctypes.c_int, _D]
             lib.kan_oracle_round_bf16.argtypes = [_D, _I64, _D]
             lib.kan_oracle_num_threads.restype = ctypes.c_int
             lib.kan_oracle_set_threads.argtypes = [ctypes.c_int]
@@ -154,11 +154,13 @@ def silu(x) -> np.ndarray:
 
 
 def layer(x, C, Wb, G: int, lo: float = -1.0, hi: float = 1.0, k: int = 3,
-          basis: str = "tp") -> np.ndarray:
+          basis: str = "tp", bf16_operands: bool = False) -> np.ndarray:
     """KAN layer y = Phi(x) C^T + silu(x) Wb^T (eq. kan_forward).
 
     x: [B, in]; C: [out, in, G + k]; Wb: [out, in]  ->  y: [B, out], float64.
     ``basis`` selects the truncated-power ("tp") or Cox-de Boor ("cdb") route.
+    ``bf16_operands`` rounds every basis and SiLU value to bfloat16 before the
+    contraction (what a bf16 matrix unit consumes); sums stay in double.
     """
     _check_grid(G, k, lo, hi)
     xa = _f64(x)
@@ -172,7 +174,8 @@ def layer(x, C, Wb, G: int, lo: float = -1.0, hi: float = 1.0, k: int = 3,
         raise ValueError("coefficient shapes do not match x and the grid")
     kind = {"tp": 0, "cdb": 1}[basis]
     y = np.empty((B, n_out), dtype=np.float64)
-    _load().kan_oracle_layer(_p(xa), B, n_in, n_out, _p(Ca), _p(Wa), G, k, lo, hi, kind, _p(y))
+    _load().kan_oracle_layer(_p(xa), B, n_in, n_out, _p(Ca), _p(Wa), G, k, lo, hi, kind,
+                             int(bool(bf16_operands)), _p(y))
     return y
 
 
@@ -185,12 +188,14 @@ def round_bf16(v) -> np.ndarray:
 
 
 def mlp(x, layers, G: int, lo: float = -1.0, hi: float = 1.0, k: int = 3,
-        bf16: bool = False, return_all: bool = False):
+        bf16: bool = False, bf16_operands: bool = False, return_all: bool = False):
     """Apply ``layer`` for each (C, Wb) in ``layers``; each output feeds the next
     layer unchanged (off-grid values are handled by the clamp).  With ``bf16``
     every stored tensor -- the input, the coefficients and each layer's output --
-    is rounded to bfloat16 first, mirroring bf16 storage with wide accumulation.
-    Returns the last output, or every layer's (input, output) pair."""
+    is rounded to bfloat16 first, mirroring bf16 storage with wide accumulation;
+    ``bf16_operands`` additionally rounds the basis and SiLU operands of every
+    contraction.  Returns the last output, or every layer's (input, output)
+    pair."""
     h = _f64(x)
     if bf16:
         h = round_bf16(h)
@@ -199,7 +204,7 @@ def mlp(x, layers, G: int, lo: float = -1.0, hi: float = 1.0, k: int = 3,
         Ca, Wa = _f64(C), _f64(Wb)
         if bf16:
             Ca, Wa = round_bf16(Ca), round_bf16(Wa)
-        y = layer(h, Ca, Wa, G, lo, hi, k)
+        y = layer(h, Ca, Wa, G, lo, hi, k, bf16_operands=bf16_operands)
         if bf16:
             y = round_bf16(y)
         trace.append((h, y))

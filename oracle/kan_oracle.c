@@ -206,6 +206,8 @@ void kan_oracle_silu(const double* x, int64_t n, double* out) {
     for (int64_t e = 0; e < n; ++e) out[e] = silu_one(x[e]);
 }
 
+void kan_oracle_round_bf16(const double* v, int64_t n, double* out);
+
 /* ------------------------------------------------------------ KAN layer */
 
 /* y[b, o] = sum_i ( sum_j C[o, i, j] N_j(x[b, i]) + Wb[o, i] sigma(x[b, i]) )
@@ -213,10 +215,14 @@ void kan_oracle_silu(const double* x, int64_t n, double* out) {
  * clamped) or the Cox-de Boor recursion (basis_kind 1).  x is [B, in],
  * C is [out, in, G + k], Wb is [out, in], y is [B, out]; all row-major.
  * For each output the sum runs over i, and within i over j then the SiLU
- * term, in index order, accumulated in double. */
+ * term, in index order, accumulated in double.  With bf16_operands != 0 every
+ * basis value and every SiLU value is rounded to bfloat16 before it enters the
+ * contraction (the operands a bf16 matrix unit consumes); the products and
+ * sums stay in double. */
 void kan_oracle_layer(const double* x, int64_t B, int in, int out,
                       const double* C, const double* Wb, int G, int k,
-                      double lo, double hi, int basis_kind, double* y) {
+                      double lo, double hi, int basis_kind, int bf16_operands,
+                      double* y) {
     const int nb = G + k;
     #pragma omp parallel
     {
@@ -234,6 +240,10 @@ void kan_oracle_layer(const double* x, int64_t B, int in, int out,
                 else
                     tp_row(xb[i], G, k, lo, hi, 1, &nrow[(int64_t)i * nb]);
                 sg[i] = silu_one(xb[i]);
+                if (bf16_operands) {
+                    kan_oracle_round_bf16(&nrow[(int64_t)i * nb], nb, &nrow[(int64_t)i * nb]);
+                    kan_oracle_round_bf16(&sg[i], 1, &sg[i]);
+                }
             }
             for (int o = 0; o < out; ++o) {
                 double s = 0.0;

@@ -1,0 +1,200 @@
+"""Python binding of the C ABI in include/kan.h (ctypes).
+
+Argument marshalling only: every step of the computation runs in the HIP
+kernels of ``libkan.so``.  The raw entry points keep the C names
+(``kan_basis_eval``, ``kan_layer_forward``, ``kan_status_string``) and take
+device addresses as integers; ``basis``, ``layer_forward`` and ``mlp_forward``
+accept torch tensors on a ROCm device and launch on torch's current stream.
+
+The library must have been built (``python -m paper_2609_01956_amd.build``);
+loading raises if it is missing.  There is no fallback of any kind.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import threading
+from typing import Iterable, Optional, Sequence, Tuple
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libkan.so")
+
+KAN_OK = 0
+KAN_ERR_INVALID_ARG = 1
+KAN_ERR_UNSUPPORTED = 2
+KAN_ERR_DEVICE = 3
+
+KAN_F32 = 0
+KAN_BF16 = 1
+
+EXPORTED_SYMBOLS = ("kan_basis_eval", "kan_layer_forward", "kan_status_string", "kan_abi_version")
+
+
+class kan_grid(ctypes.Structure):
+    _fields_ = [("grid_size", ctypes.c_int32), ("spline_order", ctypes.c_int32),
+                ("grid_lo", ctypes.c_float), ("grid_hi", ctypes.c_float)]
+
+
+class KanError(RuntimeError):
+    pass
+
+
+_lock = threading.Lock()
+_lib = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libkan.so once; raise if it has not been built."""
+    global _lib
+    with _lock:
+        if _lib is None:
+            if not os.path.exists(path):
+                raise RuntimeError(
+                    f"{path} is missing: build the HIP library first "
+                    "(python -m paper_2609_01956_amd.build)")
+            lib = ctypes.CDLL(path)
+            lib.kan_basis_eval.argtypes = [ctypes.POINTER(kan_grid), ctypes.c_int, ctypes.c_void_p,
+                                           ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p]
+            lib.kan_basis_eval.restype = ctypes.c_int
+            lib.kan_layer_forward.argtypes = [ctypes.POINTER(kan_grid), ctypes.c_int, ctypes.c_int64,
+                                              ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
+                                              ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                              ctypes.c_void_p]
+            lib.kan_layer_forward.restype = ctypes.c_int
+            lib.kan_status_string.argtypes = [ctypes.c_int]
+            lib.kan_status_string.restype = ctypes.c_char_p
+            lib.kan_abi_version.argtypes = []
+            lib.kan_abi_version.restype = ctypes.c_int32
+            _lib = lib
+    return _lib
+
+
+# ----------------------------------------------------------- raw C entry points
+
+def make_grid(grid_size: int, grid_lo: float = -1.0, grid_hi: float = 1.0,
+              spline_order: int = 3) -> kan_grid:
+    return kan_grid(int(grid_size), int(spline_order), float(grid_lo), float(grid_hi))
+
+
+def kan_status_string(status: int) -> str:
+    return load_library().kan_status_string(int(status)).decode()
+
+
+def kan_abi_version() -> int:
+    return int(load_library().kan_abi_version())
+
+
+def kan_basis_eval(grid: kan_grid, dtype: int, x: int, n: int, phi: int, stream: int = 0) -> int:
+    """Raw call: device addresses as integers; returns the kan_status code."""
+    return int(load_library().kan_basis_eval(ctypes.byref(grid), int(dtype), ctypes.c_void_p(x),
+                                             int(n), ctypes.c_void_p(phi), ctypes.c_void_p(stream)))
+
+
+def kan_layer_forward(grid: kan_grid, dtype: int, batch: int, in_features: int,
+                      out_features: int, x: int, coef: int, base_w: int, y: int,
+                      stream: int = 0) -> int:
+    """Raw call: device addresses as integers; returns the kan_status code."""
+    return int(load_library().kan_layer_forward(
+        ctypes.byref(grid), int(dtype), int(batch), int(in_features), int(out_features),
+        ctypes.c_void_p(x), ctypes.c_void_p(coef), ctypes.c_void_p(base_w), ctypes.c_void_p(y),
+        ctypes.c_void_p(stream)))
+
+
+def check(status: int) -> None:
+    """Map a kan_status to an exception."""
+    if status == KAN_OK:
+        return
+    msg = kan_status_string(status)
+    if status == KAN_ERR_INVALID_ARG:
+        raise ValueError(msg)
+    if status == KAN_ERR_UNSUPPORTED:
+        raise NotImplementedError(msg)
+    raise KanError(msg)
+
+
+# ------------------------------------------------------------ torch marshalling
+
+def _torch():
+    import torch
+    return torch
+
+
+def _dtype_code(t) -> int:
+    torch = _torch()
+    if t.dtype == torch.float32:
+        return KAN_F32
+    if t.dtype == torch.bfloat16:
+        return KAN_BF16
+    raise NotImplementedError(f"dtype {t.dtype} is not supported (float32 or bfloat16)")
+
+
+def _require_device(*ts) -> None:
+    for t in ts:
+        if not t.is_cuda:
+            raise ValueError("tensors must live on the GPU")
+        if not t.is_contiguous():
+            raise ValueError("tensors must be contiguous")
+    dev = ts[0].device
+    for t in ts[1:]:
+        if t.device != dev:
+            raise ValueError("tensors must live on one device")
+
+
+def _stream(device) -> int:
+    return int(_torch().cuda.current_stream(device).cuda_stream)
+
+
+def basis(x, grid_size: int, grid_lo: float = -1.0, grid_hi: float = 1.0, out=None):
+    """phi[..., j] = N_j(x[...]) for j < grid_size + 3 (kan_basis_eval)."""
+    torch = _torch()
+    _require_device(x)
+    nb = int(grid_size) + 3
+    if out is None:
+        out = torch.empty(tuple(x.shape) + (nb,), dtype=x.dtype, device=x.device)
+    else:
+        _require_device(x, out)
+        if out.dtype != x.dtype or tuple(out.shape) != tuple(x.shape) + (nb,):
+            raise ValueError("out must have shape x.shape + (G + 3,) and x's dtype")
+    with torch.cuda.device(x.device):
+        check(kan_basis_eval(make_grid(grid_size, grid_lo, grid_hi), _dtype_code(x), x.data_ptr(),
+                             x.numel(), out.data_ptr(), _stream(x.device)))
+    return out
+
+
+def layer_forward(x, coef, base_w, grid_size: int, grid_lo: float = -1.0, grid_hi: float = 1.0,
+                  out=None):
+    """One KAN layer (kan_layer_forward): x [B, in], coef [out, in, G + 3],
+    base_w [out, in] -> y [B, out], all of one dtype on one device."""
+    torch = _torch()
+    _require_device(x, coef, base_w)
+    if x.dim() != 2 or base_w.dim() != 2 or coef.dim() != 3:
+        raise ValueError("expected x [B, in], coef [out, in, G+3], base_w [out, in]")
+    B, n_in = x.shape
+    n_out = base_w.shape[0]
+    if tuple(base_w.shape) != (n_out, n_in) or tuple(coef.shape) != (n_out, n_in, int(grid_size) + 3):
+        raise ValueError("coef / base_w shapes do not match x and the grid")
+    if coef.dtype != x.dtype or base_w.dtype != x.dtype:
+        raise ValueError("x, coef and base_w must share one dtype")
+    if out is None:
+        out = torch.empty((B, n_out), dtype=x.dtype, device=x.device)
+    else:
+        _require_device(x, out)
+        if out.dtype != x.dtype or tuple(out.shape) != (B, n_out):
+            raise ValueError("out must be [B, out] with x's dtype")
+    with torch.cuda.device(x.device):
+        check(kan_layer_forward(make_grid(grid_size, grid_lo, grid_hi), _dtype_code(x), B, n_in,
+                                n_out, x.data_ptr(), coef.data_ptr(), base_w.data_ptr(),
+                                out.data_ptr(), _stream(x.device)))
+    return out
+
+
+def mlp_forward(x, layers: Sequence[Tuple[object, object]], grid_size: int, grid_lo: float = -1.0,
+                grid_hi: float = 1.0, return_all: bool = False):
+    """Stacked KAN layers; each output feeds the next layer unchanged (values
+    off the grid are handled by the clamp of the basis)."""
+    h = x
+    outs = []
+    for coef, base_w in layers:
+        h = layer_forward(h, coef, base_w, grid_size, grid_lo, grid_hi)
+        outs.append(h)
+    return outs if return_all else h

@@ -1,0 +1,144 @@
+// kan_api.cpp -- the C ABI declared in include/kan.h: argument validation
+// (host only, before any HIP call), grid constants, launch planning and
+// dispatch onto the caller's stream.
+#include "kan.h"
+
+#include <cmath>
+#include <cstdint>
+
+#include "kan_internal.h"
+
+namespace {
+
+constexpr int32_t kMaxGrid = 4000;
+
+size_t dtype_size(kan_dtype dt) { return dt == KAN_BF16 ? 2 : 4; }
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+// [p, p + n) and [q, q + m) (bytes) intersect?
+bool overlap(const void* p, size_t n, const void* q, size_t m) {
+    const uintptr_t a = reinterpret_cast<uintptr_t>(p), b = reinterpret_cast<uintptr_t>(q);
+    return a < b + m && b < a + n;
+}
+
+// Validates the grid and dtype and fills the grid constants:
+//   nb = G + 3, inv_h = G / (hi - lo), a_int + a_frac = 1 - lo / h, so that
+//   v_j = u_j - 2 = x * inv_h + (a_int - j) + a_frac  (see kan_device.h).
+kan_status check_grid(const kan_grid* grid, kan_dtype dtype, kan::GridConst* gc) {
+    if (grid == nullptr) return KAN_ERR_INVALID_ARG;
+    if (grid->spline_order != 3) return KAN_ERR_UNSUPPORTED;
+    if (dtype != KAN_F32 && dtype != KAN_BF16) return KAN_ERR_UNSUPPORTED;
+    const int32_t G = grid->grid_size;
+    if (G < 1 || G > kMaxGrid) return KAN_ERR_INVALID_ARG;
+    const double lo = grid->grid_lo, hi = grid->grid_hi;
+    if (!std::isfinite(lo) || !std::isfinite(hi) || !(lo < hi)) return KAN_ERR_INVALID_ARG;
+    const double inv_h = (double)G / (hi - lo);
+    if (!std::isfinite(inv_h)) return KAN_ERR_INVALID_ARG;
+    // Keep a_int - j (and x * inv_h near the support) inside fp32's exact
+    // integer range.
+    const double lim = 4194304.0;  // 2^22
+    if (std::fabs(lo) * inv_h > lim || std::fabs(hi) * inv_h > lim) return KAN_ERR_INVALID_ARG;
+    const double A = 1.0 - lo * inv_h;
+    const double ai = std::nearbyint(A);
+    gc->nb = G + 3;
+    gc->inv_h = (float)inv_h;
+    gc->a_int = (float)ai;
+    gc->a_frac = (float)(A - ai);
+    return KAN_OK;
+}
+
+kan_status device_status(hipError_t e) { return e == hipSuccess ? KAN_OK : KAN_ERR_DEVICE; }
+
+}  // namespace
+
+extern "C" {
+
+const char* kan_status_string(kan_status status) {
+    switch (status) {
+        case KAN_OK: return "KAN_OK: success";
+        case KAN_ERR_INVALID_ARG: return "KAN_ERR_INVALID_ARG: invalid size, range, pointer, alignment or overlap";
+        case KAN_ERR_UNSUPPORTED: return "KAN_ERR_UNSUPPORTED: only cubic splines (spline_order 3) and f32/bf16 are implemented";
+        case KAN_ERR_DEVICE: return "KAN_ERR_DEVICE: the HIP runtime rejected a kernel launch";
+    }
+    return "unknown kan_status";
+}
+
+int32_t kan_abi_version(void) { return KAN_ABI_VERSION; }
+
+kan_status kan_basis_eval(const kan_grid* grid, kan_dtype dtype, const void* x, int64_t n,
+                          void* phi, void* stream) {
+    kan::GridConst gc;
+    const kan_status st = check_grid(grid, dtype, &gc);
+    if (st != KAN_OK) return st;
+    if (n < 0) return KAN_ERR_INVALID_ARG;
+    if (n == 0) return KAN_OK;
+    if (n > INT64_MAX / gc.nb) return KAN_ERR_INVALID_ARG;
+    const size_t es = dtype_size(dtype);
+    if (x == nullptr || phi == nullptr) return KAN_ERR_INVALID_ARG;
+    if (!aligned(x, es) || !aligned(phi, es)) return KAN_ERR_INVALID_ARG;
+    if ((uint64_t)n > (uint64_t)(SIZE_MAX / es / gc.nb)) return KAN_ERR_INVALID_ARG;
+    if (overlap(x, (size_t)n * es, phi, (size_t)n * gc.nb * es)) return KAN_ERR_INVALID_ARG;
+    const kan::BasisLaunch L = kan::plan_basis(n, gc.nb, phi);
+    if (L.blocks > 0x7fffffffLL) return KAN_ERR_INVALID_ARG;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (dtype == KAN_F32)
+        return device_status(kan::launch_basis_f32(static_cast<const float*>(x), n,
+                                                   static_cast<float*>(phi), gc, L, s));
+    return device_status(kan::launch_basis_bf16(static_cast<const uint16_t*>(x), n,
+                                                static_cast<uint16_t*>(phi), gc, L, s));
+}
+
+kan_status kan_layer_forward(const kan_grid* grid, kan_dtype dtype, int64_t batch,
+                             int32_t in_features, int32_t out_features, const void* x,
+                             const void* coef, const void* base_w, void* y, void* stream) {
+    kan::GridConst gc;
+    const kan_status st = check_grid(grid, dtype, &gc);
+    if (st != KAN_OK) return st;
+    if (batch < 0 || in_features < 1 || out_features < 1) return KAN_ERR_INVALID_ARG;
+    if (out_features > 65535 * 32) return KAN_ERR_INVALID_ARG;  // column tiles in blockIdx.y
+    if ((int64_t)in_features * (gc.nb + 1) >= 0x80000000LL) return KAN_ERR_INVALID_ARG;
+    if (batch == 0) return KAN_OK;
+    if (x == nullptr || coef == nullptr || base_w == nullptr || y == nullptr)
+        return KAN_ERR_INVALID_ARG;
+    const size_t es = dtype_size(dtype);
+    if (!aligned(x, es) || !aligned(coef, es) || !aligned(base_w, es) || !aligned(y, es))
+        return KAN_ERR_INVALID_ARG;
+    // Grid of the launch: ceil(batch / 32) row tiles at most, in blockIdx.x.
+    if (batch > (int64_t)0x7fffffff * 32) return KAN_ERR_INVALID_ARG;
+    const uint64_t ub = (uint64_t)batch;
+    if (ub > SIZE_MAX / es / (uint64_t)in_features || ub > SIZE_MAX / es / (uint64_t)out_features)
+        return KAN_ERR_INVALID_ARG;
+    const size_t x_bytes = ub * (size_t)in_features * es;
+    const size_t c_bytes = (size_t)out_features * in_features * gc.nb * es;
+    const size_t w_bytes = (size_t)out_features * in_features * es;
+    const size_t y_bytes = ub * (size_t)out_features * es;
+    if (overlap(y, y_bytes, x, x_bytes) || overlap(y, y_bytes, coef, c_bytes) ||
+        overlap(y, y_bytes, base_w, w_bytes))
+        return KAN_ERR_INVALID_ARG;
+
+    kan::LayerArgs a;
+    a.x = x;
+    a.coef = coef;
+    a.wb = base_w;
+    a.y = y;
+    a.batch = batch;
+    a.in = in_features;
+    a.out = out_features;
+    a.g = gc;
+    const int kg = dtype == KAN_F32 ? kan::kLayerKGroupF32 : kan::kLayerKGroupBf16;
+    const int cwmax = dtype == KAN_F32 ? kan::kLayerCwMaxF32 : kan::kLayerCwMaxBf16;
+    a.nbp = (gc.nb + 1 + kg - 1) / kg * kg;
+    int cw = kg;
+    while (cw < a.nbp && cw < cwmax) cw *= 2;
+    a.cw = cw;
+    a.nchunks = (a.nbp + cw - 1) / cw;
+
+    kan::LayerTile t = kan::plan_layer_tile(batch, out_features);
+    kan::parse_layer_tile_override(&t);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (dtype == KAN_F32) return device_status(kan::launch_layer_f32(a, t, s));
+    return device_status(kan::launch_layer_bf16(a, t, s));
+}
+
+}  // extern "C"

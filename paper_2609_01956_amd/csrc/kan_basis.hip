@@ -1,0 +1,124 @@
+// kan_basis.hip -- basis-only kernel: phi[e, j] = N_j(x[e]) for every input
+// element and every basis j (eq. truncated with the clamp of eq. bounded).
+//
+// The kernel is bound by HBM writes (nb outputs per input read).  Each
+// 256-thread workgroup owns xb consecutive inputs, i.e. one contiguous
+// xb * nb run of the output:
+//   phase 1  tpx threads per input evaluate its nb values in registers (one fma
+//            and ~9 VALU ops per value, no span lookup, no data-dependent
+//            branches) and write them to LDS in output order;
+//   phase 2  the workgroup streams the run from LDS to HBM with 16-byte
+//            non-temporal stores, so every store instruction of a wave covers
+//            1 KiB of consecutive output.
+// NaN inputs give NaN outputs: the 1/6 scale is replaced by the NaN itself.
+#include "kan_internal.h"
+
+namespace kan {
+
+namespace {
+
+constexpr int kThreads = 256;
+
+template <typename T>
+__device__ __forceinline__ void store_vec(T* dst, const float* src);
+
+template <>
+__device__ __forceinline__ void store_vec<float>(float* dst, const float* src) {
+    const floatx4 v = *reinterpret_cast<const floatx4*>(src);
+    __builtin_nontemporal_store(v, reinterpret_cast<floatx4*>(dst));
+}
+
+template <>
+__device__ __forceinline__ void store_vec<uint16_t>(uint16_t* dst, const float* src) {
+    const floatx4 lo = *reinterpret_cast<const floatx4*>(src);
+    const floatx4 hi = *reinterpret_cast<const floatx4*>(src + 4);
+    u16x8 v;
+    v[0] = f32_to_bf16(lo[0]); v[1] = f32_to_bf16(lo[1]);
+    v[2] = f32_to_bf16(lo[2]); v[3] = f32_to_bf16(lo[3]);
+    v[4] = f32_to_bf16(hi[0]); v[5] = f32_to_bf16(hi[1]);
+    v[6] = f32_to_bf16(hi[2]); v[7] = f32_to_bf16(hi[3]);
+    __builtin_nontemporal_store(v, reinterpret_cast<u16x8*>(dst));
+}
+
+template <typename T>
+__global__ __launch_bounds__(kThreads) void basis_kernel(const T* __restrict__ x, int64_t n,
+                                                         T* __restrict__ phi, GridConst g,
+                                                         int tpx, int jc, int vec) {
+    extern __shared__ float stage[];
+    const int nb = g.nb;
+    const int xb = kThreads / tpx;
+    const int64_t e0 = (int64_t)blockIdx.x * xb;
+    const int64_t left = n - e0;
+    const int cnt = left < xb ? (int)left : xb;
+
+    // Phase 1: values [jb, je) of input el, written to stage[el * nb + j].
+    const int el = threadIdx.x / tpx;
+    const int jb = (threadIdx.x % tpx) * jc;
+    const int je = min(jb + jc, nb);
+    if (el < cnt) {
+        const float xv = Storage<T>::load(x + e0 + el);
+        const float scale = (xv != xv) ? xv : (1.0f / 6.0f);
+        float cj = g.a_int - (float)jb;
+        float* dst = stage + el * nb;
+#pragma unroll 4
+        for (int j = jb; j < je; ++j) {
+            dst[j] = tp6(coord(xv, g, cj)) * scale;
+            cj -= 1.0f;
+        }
+    }
+    __syncthreads();
+
+    // Phase 2: stream the contiguous run [e0 * nb, (e0 + cnt) * nb) out.
+    const int total = cnt * nb;
+    T* out = phi + e0 * nb;
+    int done = 0;
+    if (vec && (reinterpret_cast<uintptr_t>(out) % 16) == 0) {
+        constexpr int V = 16 / sizeof(T);
+        const int nvec = total / V;
+        for (int q = threadIdx.x; q < nvec; q += kThreads)
+            store_vec<T>(out + q * V, stage + q * V);
+        done = nvec * V;
+    }
+    for (int q = done + threadIdx.x; q < total; q += kThreads)
+        Storage<T>::store(out + q, stage[q]);
+}
+
+}  // namespace
+
+BasisLaunch plan_basis(int64_t n, int nb, const void* phi) {
+    BasisLaunch L;
+    // Smallest power-of-two split of each input's nb values over threads that
+    // keeps the workgroup's LDS run at or below 32 KiB (at most 64 KiB for the
+    // largest grids).  A run whose start is not 16-byte aligned (possible only
+    // when xb * nb * sizeof(T) is not a multiple of 16) falls back to scalar
+    // stores for that workgroup.
+    int tpx = 1;
+    while (tpx < 64 && (size_t)(kThreads / tpx) * nb * 4 > 32768) tpx *= 2;
+    L.tpx = tpx;
+    L.xb = kThreads / tpx;
+    L.jc = (nb + tpx - 1) / tpx;
+    L.lds = (size_t)L.xb * nb * 4;
+    L.blocks = (n + L.xb - 1) / L.xb;
+    L.vec = (reinterpret_cast<uintptr_t>(phi) % 16) == 0;
+    return L;
+}
+
+template <typename T>
+static hipError_t launch(const T* x, int64_t n, T* phi, const GridConst& g, const BasisLaunch& L,
+                         hipStream_t s) {
+    hipLaunchKernelGGL(basis_kernel<T>, dim3((unsigned)L.blocks), dim3(kThreads), L.lds, s, x, n,
+                       phi, g, L.tpx, L.jc, L.vec ? 1 : 0);
+    return hipGetLastError();
+}
+
+hipError_t launch_basis_f32(const float* x, int64_t n, float* phi, const GridConst& g,
+                            const BasisLaunch& L, hipStream_t s) {
+    return launch<float>(x, n, phi, g, L, s);
+}
+
+hipError_t launch_basis_bf16(const uint16_t* x, int64_t n, uint16_t* phi, const GridConst& g,
+                             const BasisLaunch& L, hipStream_t s) {
+    return launch<uint16_t>(x, n, phi, g, L, s);
+}
+
+}  // namespace kan

@@ -1,0 +1,80 @@
+// kan_device.h -- device-side helpers shared by the gfx950 kernels.
+//
+// Basis evaluation.  With the grid convention t_j = lo + (j - 3) h, the
+// normalised coordinate of basis j is u_j = (x - t_j) / h = x/h - lo/h + 3 - j.
+// The kernels form v_j = u_j - 2 with one fused multiply-add,
+//     v_j = fma(x, inv_h, a_int - j) + a_frac,
+// where a_int + a_frac = 1 - lo/h is split on the host into an integer part
+// (so a_int - j is exact) and a small remainder (zero on grids whose lo/h is an
+// integer, e.g. [-1, 1] with even G).  Near the support |v_j| <= 2, so the
+// single rounding of the fma is at most 2^-23 in u.
+//
+// The truncated-power form (eq. truncated) with the bounded coordinate
+// ubar = clamp(u, 0, 4) (eq. bounded) is evaluated at the reflected coordinate
+// w = min(ubar, 4 - ubar) = 2 - min(|v|, 2).  The stencil {1, -4, 6, -4, 1} is
+// symmetric, so N(ubar) = N(4 - ubar) = N(w), and for w <= 2 the terms
+// (w - m)_+^3 with m >= 2 vanish:
+//     6 N = w^3 - 4 (w - 1)_+^3,   (w - 1)_+ = max(1 - min(|v|, 2), 0).
+// The same clamped expression with only its nonzero terms kept; evaluating it
+// at w instead of ubar avoids the cancellation of terms of size up to 64 near
+// ubar = 4 and keeps the fp32 error below 1e-6.  Off the support min(|v|, 2)
+// is 2, so w = 0 and the result is exactly 0 (also for +-Inf inputs).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace kan {
+
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef uint16_t u16x8 __attribute__((ext_vector_type(8)));
+
+// Grid constants shared by all kernels (computed on the host in double).
+struct GridConst {
+    int nb;        // G + 3 basis functions per input
+    float inv_h;   // G / (hi - lo), rounded to fp32
+    float a_int;   // nearest integer to 1 - lo / h
+    float a_frac;  // (1 - lo / h) - a_int, rounded to fp32
+};
+
+// 6 * N(u) from v = u - 2 (see the header comment).
+__device__ __forceinline__ float tp6(float v) {
+    const float d = __builtin_fminf(__builtin_fabsf(v), 2.0f);
+    const float w = 2.0f - d;
+    const float b = __builtin_fmaxf(1.0f - d, 0.0f);
+    return __builtin_fmaf(-4.0f * b * b, b, w * w * w);
+}
+
+// v_j = u_j - 2 for basis j, given cj = a_int - j.
+__device__ __forceinline__ float coord(float x, const GridConst& g, float cj) {
+    return __builtin_fmaf(x, g.inv_h, cj) + g.a_frac;
+}
+
+// silu(x) = x / (1 + exp(-x)).
+__device__ __forceinline__ float silu(float x) {
+    return x / (1.0f + __expf(-x));
+}
+
+// bfloat16 storage <-> fp32.  Widening is exact; narrowing rounds to nearest
+// even (v_cvt_pk_bf16_f32 on gfx950) and keeps NaN a NaN.
+__device__ __forceinline__ float bf16_to_f32(uint16_t u) {
+    return __uint_as_float(((uint32_t)u) << 16);
+}
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+    __bf16 b = (__bf16)f;
+    return __builtin_bit_cast(uint16_t, b);
+}
+
+template <typename T> struct Storage;
+template <> struct Storage<float> {
+    static __device__ __forceinline__ float load(const float* p) { return *p; }
+    static __device__ __forceinline__ void store(float* p, float v) { *p = v; }
+};
+template <> struct Storage<uint16_t> {
+    static __device__ __forceinline__ float load(const uint16_t* p) { return bf16_to_f32(*p); }
+    static __device__ __forceinline__ void store(uint16_t* p, float v) { *p = f32_to_bf16(v); }
+};
+
+}  // namespace kan

@@ -1,8 +1,8 @@
 """Seeded synthetic inputs for the KAN-layer forward.
 
 This module draws random numbers and nothing else: it holds none of the
-method's arithmetic, so both the HIP path and the float64 oracle can consume
-the same arrays.  Shapes and distributions follow the workloads the paper's
+method's arithmetic, so the HIP path and any float64 reference can consume the
+same arrays.  Shapes and distributions follow the workloads the paper's
 method is exercised on (uniform grid on [-1, 1], inputs mostly on the grid with
 an optional off-grid fraction, Gaussian spline coefficients and base weights);
 the second argument of every N(0, s) below is a standard deviation.

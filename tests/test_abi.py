@@ -1,0 +1,139 @@
+"""C ABI checks that need no GPU: the library loads, exports every function
+declared in include/kan.h, and rejects every invalid argument on the host
+with the documented status code before touching the device."""
+import ctypes
+import math
+import os
+import re
+
+import pytest
+
+from paper_2609_01956_amd import binding as kb
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_functions():
+    src = open(os.path.join(ROOT, "include", "kan.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(kan_[a-z_0-9]+)\s*\(", src)))
+
+
+def test_header_declares_the_entry_points():
+    names = _declared_functions()
+    assert names == sorted(kb.EXPORTED_SYMBOLS)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(kb.LIB_PATH)
+    for name in _declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_abi_version_and_status_strings():
+    assert kb.kan_abi_version() == 1
+    for code in range(4):
+        s = kb.kan_status_string(code)
+        assert s.startswith(["KAN_OK", "KAN_ERR_INVALID_ARG", "KAN_ERR_UNSUPPORTED", "KAN_ERR_DEVICE"][code])
+    assert kb.kan_status_string(99) == "unknown kan_status"
+
+
+# Fake, well-aligned, non-overlapping addresses: validation must reject every
+# case below on the host, so these are never dereferenced.
+X, PHI, C, W, Y = 0x100000, 0x200000000, 0x300000000, 0x400000000, 0x500000000
+
+
+@pytest.mark.parametrize("grid,code", [
+    (kb.make_grid(5, spline_order=2), kb.KAN_ERR_UNSUPPORTED),
+    (kb.make_grid(5, spline_order=4), kb.KAN_ERR_UNSUPPORTED),
+    (kb.make_grid(0), kb.KAN_ERR_INVALID_ARG),
+    (kb.make_grid(-3), kb.KAN_ERR_INVALID_ARG),
+    (kb.make_grid(4001), kb.KAN_ERR_INVALID_ARG),
+    (kb.make_grid(5, 1.0, 1.0), kb.KAN_ERR_INVALID_ARG),
+    (kb.make_grid(5, 2.0, -1.0), kb.KAN_ERR_INVALID_ARG),
+    (kb.make_grid(5, math.nan, 1.0), kb.KAN_ERR_INVALID_ARG),
+    (kb.make_grid(5, -1.0, math.inf), kb.KAN_ERR_INVALID_ARG),
+    (kb.make_grid(5, 1e30, 1e30 * (1 + 1e-6)), kb.KAN_ERR_INVALID_ARG),  # lo/h beyond 2^22
+])
+def test_bad_grid(grid, code):
+    assert kb.kan_basis_eval(grid, kb.KAN_F32, X, 16, PHI) == code
+    assert kb.kan_layer_forward(grid, kb.KAN_F32, 16, 4, 4, X, C, W, Y) == code
+
+
+def test_null_grid_and_bad_dtype():
+    lib = kb.load_library()
+    assert lib.kan_basis_eval(None, 0, X, 16, PHI, None) == kb.KAN_ERR_INVALID_ARG
+    assert lib.kan_layer_forward(None, 0, 16, 4, 4, X, C, W, Y, None) == kb.KAN_ERR_INVALID_ARG
+    g = kb.make_grid(5)
+    assert kb.kan_basis_eval(g, 2, X, 16, PHI) == kb.KAN_ERR_UNSUPPORTED
+    assert kb.kan_basis_eval(g, -1, X, 16, PHI) == kb.KAN_ERR_UNSUPPORTED
+
+
+def test_basis_argument_checks():
+    g = kb.make_grid(5)
+    f32, bf = kb.KAN_F32, kb.KAN_BF16
+    assert kb.kan_basis_eval(g, f32, X, -1, PHI) == kb.KAN_ERR_INVALID_ARG
+    assert kb.kan_basis_eval(g, f32, 0, 16, PHI) == kb.KAN_ERR_INVALID_ARG
+    assert kb.kan_basis_eval(g, f32, X, 16, 0) == kb.KAN_ERR_INVALID_ARG
+    assert kb.kan_basis_eval(g, f32, X + 2, 16, PHI) == kb.KAN_ERR_INVALID_ARG   # misaligned f32
+    assert kb.kan_basis_eval(g, f32, X, 16, PHI + 1) == kb.KAN_ERR_INVALID_ARG
+    assert kb.kan_basis_eval(g, bf, X + 1, 16, PHI) == kb.KAN_ERR_INVALID_ARG    # misaligned bf16
+    # output overlapping the input
+    assert kb.kan_basis_eval(g, f32, X, 16, X + 32) == kb.KAN_ERR_INVALID_ARG
+    assert kb.kan_basis_eval(g, f32, X + 64, 16, X) == kb.KAN_ERR_INVALID_ARG
+    # n * (G + 3) overflowing
+    assert kb.kan_basis_eval(g, f32, X, 2 ** 62, PHI) == kb.KAN_ERR_INVALID_ARG
+    # empty problem: OK, launches nothing, pointers unchecked
+    assert kb.kan_basis_eval(g, f32, 0, 0, 0) == kb.KAN_OK
+    assert kb.kan_basis_eval(g, bf, 0, 0, 0) == kb.KAN_OK
+
+
+def test_layer_argument_checks():
+    g = kb.make_grid(10)
+    f32 = kb.KAN_F32
+    bad = kb.KAN_ERR_INVALID_ARG
+    assert kb.kan_layer_forward(g, f32, -1, 4, 4, X, C, W, Y) == bad
+    assert kb.kan_layer_forward(g, f32, 16, 0, 4, X, C, W, Y) == bad
+    assert kb.kan_layer_forward(g, f32, 16, 4, 0, X, C, W, Y) == bad
+    assert kb.kan_layer_forward(g, f32, 16, 2 ** 30, 4, X, C, W, Y) == bad  # in * (G + 4) >= 2^31
+    assert kb.kan_layer_forward(g, f32, 16, 4, 4, 0, C, W, Y) == bad
+    assert kb.kan_layer_forward(g, f32, 16, 4, 4, X, 0, W, Y) == bad
+    assert kb.kan_layer_forward(g, f32, 16, 4, 4, X, C, 0, Y) == bad
+    assert kb.kan_layer_forward(g, f32, 16, 4, 4, X, C, W, 0) == bad
+    assert kb.kan_layer_forward(g, f32, 16, 4, 4, X, C + 2, W, Y) == bad
+    assert kb.kan_layer_forward(g, f32, 16, 4, 4, X, C, W, Y + 2) == bad
+    # y overlapping each input
+    assert kb.kan_layer_forward(g, f32, 16, 4, 4, X, C, W, X + 8) == bad
+    assert kb.kan_layer_forward(g, f32, 16, 4, 4, X, C, W, C + 8) == bad
+    assert kb.kan_layer_forward(g, f32, 16, 4, 4, X, C, W, W) == bad
+    # empty batch: OK without launching
+    assert kb.kan_layer_forward(g, f32, 0, 4, 4, 0, 0, 0, 0) == kb.KAN_OK
+
+
+def test_check_maps_codes_to_exceptions():
+    kb.check(kb.KAN_OK)
+    with pytest.raises(ValueError):
+        kb.check(kb.KAN_ERR_INVALID_ARG)
+    with pytest.raises(NotImplementedError):
+        kb.check(kb.KAN_ERR_UNSUPPORTED)
+    with pytest.raises(kb.KanError):
+        kb.check(kb.KAN_ERR_DEVICE)
+
+
+def test_torch_wrappers_reject_host_tensors():
+    import torch
+    x = torch.zeros(4, 3)
+    with pytest.raises(ValueError):
+        kb.basis(x, 5)
+    with pytest.raises(ValueError):
+        kb.layer_forward(x, torch.zeros(2, 3, 8), torch.zeros(2, 3), 5)
+
+
+def test_product_path_does_not_touch_the_oracle():
+    """The binding and the HIP sources never import, load or name the oracle."""
+    pkg = os.path.join(ROOT, "paper_2609_01956_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for fn in files:
+            if fn.endswith((".py", ".hip", ".cpp", ".h")):
+                text = open(os.path.join(dirpath, fn)).read()
+                assert "oracle" not in text.lower(), os.path.join(dirpath, fn)

@@ -1,0 +1,220 @@
+"""GPU parity of kan_layer_forward (fused basis + MFMA contraction + SiLU
+branch) against the float64 oracle, through the C ABI.  Tolerances, normwise
+max|y - ref| / max|ref|: 1e-5 in fp32, 2e-2 in bf16 (reference computed on the
+same bf16-rounded tensors)."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2609_01956_amd import binding as kb
+from paper_2609_01956_amd import workloads as wl
+from gpu_common import (BF16_LAYER_TOL, F32_LAYER_TOL, device, normwise, say, set_tile,
+                        to_dev, to_host64, torch)
+
+pytestmark = pytest.mark.gpu
+
+DT = {"f32": None, "bf16": None}
+
+
+def _dtype(name):
+    return torch.float32 if name == "f32" else torch.bfloat16
+
+
+def _tol(name):
+    return F32_LAYER_TOL if name == "f32" else BF16_LAYER_TOL
+
+
+def _inputs(B, n_in, n_out, G, seed, off=0.0, dtype_name="f32"):
+    shape = wl.LayerShape(B, n_in, n_out, G, off_grid_frac=off)
+    x, C, Wb = wl.make_layer(shape, seed)
+    if dtype_name == "bf16":
+        x, C, Wb = wl.round_to_bf16_f32(x), wl.round_to_bf16_f32(C), wl.round_to_bf16_f32(Wb)
+    return x, C, Wb
+
+
+def _gpu_layer(x, C, Wb, G, dtype_name):
+    dt = _dtype(dtype_name)
+    y = kb.layer_forward(to_dev(x, dt), to_dev(C, dt), to_dev(Wb, dt), G)
+    torch.cuda.synchronize()
+    return to_host64(y)
+
+
+SHAPES = [
+    (1024, 2, 5, 5),      # the tiny 2 -> 5 layer, full size
+    (4096, 64, 64, 5),    # the 64 -> 64 layer, full size
+    (1000, 3, 37, 7),     # ragged everything, odd feature count
+    (257, 33, 70, 1),     # smallest grid
+    (130, 17, 300, 13),   # more than one column tile
+    (64, 5, 3, 200),      # the largest swept grid, many K chunks
+    (96, 2, 1, 50),       # single output
+    (33, 1, 256, 10),     # single input feature
+]
+
+
+@pytest.mark.parametrize("dtype_name", ["f32", "bf16"])
+@pytest.mark.parametrize("B,n_in,n_out,G", SHAPES)
+def test_layer_matches_oracle(B, n_in, n_out, G, dtype_name):
+    x, C, Wb = _inputs(B, n_in, n_out, G, seed=B + n_in + G, off=0.1, dtype_name=dtype_name)
+    say(f"layer {dtype_name} B={B} in={n_in} out={n_out} G={G}")
+    y = _gpu_layer(x, C, Wb, G, dtype_name)
+    ref = oracle.layer(x, C, Wb, G)
+    if dtype_name == "bf16":
+        ref = oracle.round_bf16(ref)
+    assert normwise(y, ref) <= _tol(dtype_name), normwise(y, ref)
+
+
+TILES = ["1,4,1", "2,4,1", "4,4,1", "8,4,1", "1,2,2", "2,2,2", "4,2,2", "1,1,4", "2,1,4"]
+
+
+@pytest.mark.parametrize("dtype_name", ["f32", "bf16"])
+@pytest.mark.parametrize("tile", TILES)
+def test_layer_every_tile_configuration(tile, dtype_name):
+    B, n_in, n_out, G = 300, 9, 45, 10
+    x, C, Wb = _inputs(B, n_in, n_out, G, seed=3, off=0.1, dtype_name=dtype_name)
+    ref = oracle.layer(x, C, Wb, G)
+    if dtype_name == "bf16":
+        ref = oracle.round_bf16(ref)
+    say(f"layer tile={tile} {dtype_name}")
+    set_tile(tile)
+    try:
+        y = _gpu_layer(x, C, Wb, G, dtype_name)
+    finally:
+        set_tile(None)
+    assert normwise(y, ref) <= _tol(dtype_name)
+
+
+def test_layer_special_cases_f32():
+    B, n_in, n_out, G = 500, 11, 20, 10
+    x, C, Wb = _inputs(B, n_in, n_out, G, seed=4)
+    say("layer special cases")
+    # partition of unity: C = 1, Wb = 0 gives y = in_features on the grid
+    y = _gpu_layer(x, np.ones_like(C), np.zeros_like(Wb), G, "f32")
+    np.testing.assert_allclose(y, float(n_in), rtol=1e-6)
+    # base branch only: C = 0
+    y = _gpu_layer(x * 3, np.zeros_like(C), Wb, G, "f32")
+    ref = oracle.layer(x * 3, np.zeros_like(C), Wb, G)
+    assert normwise(y, ref) <= F32_LAYER_TOL
+    # spline branch only: Wb = 0, with off-grid inputs
+    y = _gpu_layer(x * 3, C, np.zeros_like(Wb), G, "f32")
+    ref = oracle.layer(x * 3, C, np.zeros_like(Wb), G)
+    assert normwise(y, ref) <= F32_LAYER_TOL
+
+
+def test_layer_nan_row_and_determinism_and_guard():
+    B, n_in, n_out, G = 200, 6, 40, 5
+    x, C, Wb = _inputs(B, n_in, n_out, G, seed=5)
+    x[17, 3] = np.nan
+    say("layer nan/determinism/guard")
+    dt = torch.float32
+    xt, Ct, Wt = to_dev(x, dt), to_dev(C, dt), to_dev(Wb, dt)
+    buf = torch.full((B * n_out + 128,), 3.0, device=device())
+    out = buf[64:64 + B * n_out].view(B, n_out)
+    kb.layer_forward(xt, Ct, Wt, G, out=out)
+    y1 = out.clone()
+    kb.layer_forward(xt, Ct, Wt, G, out=out)
+    torch.cuda.synchronize()
+    assert torch.equal(y1.isnan(), out.isnan())
+    assert torch.equal(torch.nan_to_num(y1), torch.nan_to_num(out))
+    y = to_host64(out)
+    assert np.all(np.isnan(y[17]))
+    ok = np.ones(B, bool)
+    ok[17] = False
+    xr = x.copy()
+    xr[17, 3] = 0.0
+    ref = oracle.layer(xr, C, Wb, G)
+    assert normwise(y[ok], ref[ok]) <= F32_LAYER_TOL
+    b = to_host64(buf)
+    assert np.all(b[:64] == 3.0) and np.all(b[64 + B * n_out:] == 3.0)
+
+
+def test_layer_empty_batch():
+    say("layer empty batch")
+    dt = torch.float32
+    y = kb.layer_forward(torch.empty(0, 4, device=device()), torch.zeros(3, 4, 8, device=device()),
+                         torch.zeros(3, 4, device=device()), 5)
+    torch.cuda.synchronize()
+    assert y.shape == (0, 3)
+
+
+def _sample_rows(B, k, seed):
+    rng = np.random.default_rng(seed)
+    return np.unique(np.concatenate([rng.integers(0, B, k), [0, B - 1]]))
+
+
+@pytest.mark.parametrize("name", ["c3_layer_256x256_g10_offgrid", "c4_layer_128x128_g50",
+                                  "c4_layer_128x128_g100", "c4_layer_128x128_g200"])
+def test_named_layer_full_size_sampled_rows(name):
+    """Full-size single-layer workloads in fp32 (launch configuration of the
+    benchmark), checked on sampled rows against the oracle."""
+    W = wl.make_workload(name)
+    x = W["x"]
+    C, Wb = W["layers"][0]
+    G = W["G"]
+    say(f"layer full-size {name}")
+    y = kb.layer_forward(to_dev(x, torch.float32), to_dev(C, torch.float32),
+                         to_dev(Wb, torch.float32), G)
+    torch.cuda.synchronize()
+    rows = _sample_rows(x.shape[0], 256, 1)
+    got = to_host64(y[torch.from_numpy(rows).to(device())])
+    ref = oracle.layer(x[rows], C, Wb, G)
+    assert normwise(got, ref) <= F32_LAYER_TOL, normwise(got, ref)
+
+
+def _downstream_amplification(trace, layers, G, bf16, delta=1e-6, seed=0):
+    """Oracle-measured normwise amplification, to the network output, of a
+    relative perturbation of size delta of each layer's output."""
+    rng = np.random.default_rng(seed)
+    final = trace[-1][1]
+    amps = []
+    for li in range(len(layers)):
+        h = trace[li][1] * (1.0 + delta * rng.standard_normal(trace[li][1].shape))
+        rest = layers[li + 1:]
+        out = oracle.mlp(h, rest, G, bf16=False) if rest else h
+        amps.append(normwise(out, final) / delta)
+    return amps
+
+
+@pytest.mark.parametrize("dtype_name", ["f32", "bf16"])
+def test_mlp_full_size_sampled_rows(dtype_name):
+    """The 3-layer 784 -> 256 -> 256 -> 10 MLP at batch 65536 on sampled rows.
+
+    Per layer: the GPU layer is fed the oracle's own chain input for that layer
+    and must meet the layer tolerance.  End to end the random network amplifies
+    perturbations (about 60x from the first hidden layer to the output), so
+      * fp32: the bound is sum_l A_l * 1e-5, with A_l the oracle-measured
+        amplification of a relative perturbation of layer l's output;
+      * bf16: the oracle chain also rounds the contraction operands (basis and
+        SiLU values) to bf16, as the bf16 matrix unit consumes them, and the
+        layer tolerance 2e-2 applies to the final output.
+    """
+    W = wl.make_workload("c5_mlp_784_256_256_10_g10")
+    G = W["G"]
+    dt = _dtype(dtype_name)
+    bf = dtype_name == "bf16"
+    x = wl.round_to_bf16_f32(W["x"]) if bf else W["x"]
+    layers = [(wl.round_to_bf16_f32(C), wl.round_to_bf16_f32(Wb)) if bf else (C, Wb)
+              for C, Wb in W["layers"]]
+    say(f"mlp full-size {dtype_name}")
+    dev_layers = [(to_dev(C, dt), to_dev(Wb, dt)) for C, Wb in layers]
+    y = kb.mlp_forward(to_dev(x, dt), dev_layers, G)
+    torch.cuda.synchronize()
+    rows = _sample_rows(x.shape[0], 256, 2)
+    got = to_host64(y[torch.from_numpy(rows).to(device())])
+
+    trace = oracle.mlp(x[rows], layers, G, bf16=bf, return_all=True)
+    for li, ((h_in, h_out), (Ct, Wt)) in enumerate(zip(trace, dev_layers)):
+        say(f"mlp {dtype_name} layer {li} on the oracle's input")
+        yl = kb.layer_forward(to_dev(h_in.astype(np.float32), dt), Ct, Wt, G)
+        torch.cuda.synchronize()
+        e = normwise(to_host64(yl), h_out)
+        assert e <= _tol(dtype_name), (li, e)
+
+    if bf:
+        ref = oracle.mlp(x[rows], layers, G, bf16=True, bf16_operands=True)
+        e2e = normwise(got, ref)
+        assert e2e <= BF16_LAYER_TOL, e2e
+    else:
+        amps = _downstream_amplification(trace, layers, G, bf)
+        bound = F32_LAYER_TOL * sum(amps)
+        e2e = normwise(got, trace[-1][1])
+        assert e2e <= bound, (e2e, bound, amps)

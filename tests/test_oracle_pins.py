@@ -410,3 +410,20 @@ def test_mlp_chains_layers_and_rounds_storage():
     r = oracle.round_bf16
     h1 = r(oracle.layer(r(x), r(C1), r(W1), G))
     np.testing.assert_array_equal(yb, r(oracle.layer(h1, r(C2), r(W2), G)))
+
+
+def test_layer_bf16_operands_matches_rounded_matmul():
+    """bf16-operand mode equals numpy matmuls of bf16-rounded scipy basis values
+    and SiLU values, and the rounding agrees with torch's bfloat16 conversion."""
+    import torch
+    G = 10
+    x, C, Wb = _rand_layer(37, 5, 6, G, seed=12, lo=-1.5, hi=1.5)
+    y = oracle.layer(x, C, Wb, G, bf16_operands=True)
+    phi = _scipy_basis(x.ravel(), G, -1.0, 1.0).reshape(37, 5, G + 3)
+    want = (oracle.round_bf16(phi).reshape(37, -1) @ C.reshape(6, -1).T
+            + oracle.round_bf16(x * scipy.special.expit(x)) @ Wb.T)
+    np.testing.assert_allclose(y, want, rtol=1e-12, atol=1e-12)
+    v = phi.astype(np.float32).astype(np.float64)
+    tb = torch.from_numpy(v.astype(np.float32)).to(torch.bfloat16).double().numpy()
+    np.testing.assert_array_equal(oracle.round_bf16(v), tb)
+    assert not np.allclose(y, oracle.layer(x, C, Wb, G), rtol=1e-6, atol=0)
