@@ -125,26 +125,39 @@ def main() -> int:
     phi = torch.empty((B, n_in0, nb), dtype=tdt, device=dev)
     hs = [torch.empty((B, o), dtype=tdt, device=dev) for _, o in shapes]
 
-    names = ["basis_eval"] + [f"layer{i + 1}_{i_}x{o}" for i, (i_, o) in enumerate(shapes)]
+    packs = [kb.pack_layer(C, Wb, G, lo, hi) for C, Wb in layers]
+    names = ["basis_eval"]
+    for i, (i_, o) in enumerate(shapes):
+        names += [f"pack{i + 1}_{i_}x{o}", f"layer{i + 1}_{i_}x{o}"]
 
     def step(events=None):
+        """kan_basis_eval of the input, then per layer kan_layer_pack +
+        kan_layer_forward_packed (the weights are re-packed every step)."""
+        k = 0
         if events is not None:
-            events[0].record()
+            events[k].record()
         kb.basis(x, G, lo, hi, out=phi)
+        k += 1
         if events is not None:
-            events[1].record()
+            events[k].record()
         h = x
-        for li, ((C, Wb), out) in enumerate(zip(layers, hs)):
-            kb.layer_forward(h, C, Wb, G, lo, hi, out=out)
+        for (C, Wb), pk, out in zip(layers, packs, hs):
+            kb.pack_layer(C, Wb, G, lo, hi, out=pk)
+            k += 1
             if events is not None:
-                events[2 + li].record()
+                events[k].record()
+            kb.layer_forward_packed(h, pk, out=out)
+            k += 1
+            if events is not None:
+                events[k].record()
             h = out
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
 
-    # Timed region: exactly K steps, with one HIP event between kernels.
+    # Timed region: exactly K steps, with one HIP event between kernels (all on
+    # torch's current stream, the stream the kernels are launched on).
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(names) + 1)]
           for _ in range(args.steps)]
     torch.cuda.synchronize()
@@ -164,9 +177,14 @@ def main() -> int:
         "bound": "hbm", "unit": "GB/s", "peak": PEAK_HBM_GBS,
         "algorithmic": (B * n_in0 * es + basis_values * es) / 1e9,  # GB: read x, write phi
     }
-    for name, (i_, o) in zip(names[1:], shapes):
-        kern[name] = {"bound": "mfma", "unit": "TFLOP/s", "peak": PEAK_TFLOPS[args.dtype],
-                      "algorithmic": 2.0 * B * o * i_ * (nb + 1) / 1e12}  # dense TFLOP
+    for li, (i_, o) in enumerate(shapes):
+        # pack: read coef + base_w, write the packed buffer
+        kern[names[1 + 2 * li]] = {
+            "bound": "hbm", "unit": "GB/s", "peak": PEAK_HBM_GBS,
+            "algorithmic": (o * i_ * (nb + 1) * es + packs[li].nbytes) / 1e9}
+        kern[names[2 + 2 * li]] = {
+            "bound": "mfma", "unit": "TFLOP/s", "peak": PEAK_TFLOPS[args.dtype],
+            "algorithmic": 2.0 * B * o * i_ * (nb + 1) / 1e12}  # dense TFLOP
     for name, ms in zip(names, per_kernel_ms):
         k = kern[name]
         k["avg_us"] = ms * 1e3
@@ -203,7 +221,7 @@ def main() -> int:
         "data": "synthetic",
         "config": {"workload": WORKLOAD, "global_batch": B, "layers": [n_in0] + [o for _, o in shapes],
                    "grid_size": G, "spline_order": 3, "grid": [lo, hi],
-                   "step": "kan_basis_eval(x) + 3 x kan_layer_forward"},
+                   "step": "kan_basis_eval(x) + 3 x (kan_layer_pack + kan_layer_forward_packed)"},
         "gbasis_per_s": basis_total / (ms_per_step * 1e-3) / 1e9,
         "roofline": {"kernel": dom, "bound": dk["bound"], "achieved": dk["achieved"],
                      "peak": dk["peak"], "unit": dk["unit"], "frac": dk["frac"], "traffic": None},

@@ -8,9 +8,11 @@
  *
  * Conventions shared by every entry point
  * ---------------------------------------
- *  * Pointers named x, phi, coef, base_w, y are DEVICE pointers owned by the
- *    caller.  The library allocates no memory and keeps no global state; calls
- *    are reentrant and thread-safe.
+ *  * Pointers named x, phi, coef, base_w, packed, y are DEVICE pointers owned
+ *    by the caller.  The library keeps no global state; calls are reentrant and
+ *    thread-safe.  Only kan_layer_forward allocates (a temporary from the
+ *    stream-ordered pool, see there); every other entry point allocates
+ *    nothing.
  *  * Work is enqueued on `stream` (a hipStream_t passed as void*; NULL is the
  *    null stream) and returns before it finishes.  Results are visible after the
  *    caller synchronises that stream.  A device fault inside a kernel surfaces at
@@ -100,19 +102,76 @@ kan_status kan_basis_eval(const kan_grid* grid, kan_dtype dtype, const void* x,
  *   base_w  [out_features, in_features]       dtype storage
  *   y       [batch, out_features]             dtype storage, fully overwritten
  *
+ * The contraction runs on the matrix cores over K = in_features * (G + 4)
+ * columns (G + 3 basis values and one SiLU value per input feature); the basis
+ * is generated in registers and never written to memory.  The call is
+ * kan_layer_pack into a temporary buffer followed by kan_layer_forward_packed;
+ * the temporary (kan_layer_packed_bytes bytes) comes from hipMallocAsync on
+ * `stream` and is released with hipFreeAsync on `stream`, so the call stays
+ * asynchronous.  Callers that must not allocate use the two calls below with a
+ * buffer of their own.
+ *
  * y must not overlap any input.  Every pointer must be aligned to the dtype
- * size.  The basis is generated in registers and never written to memory.
- * A NaN in x[b, :] makes y[b, :] NaN (through the SiLU branch).
+ * size.  A NaN in x[b, :] makes y[b, :] NaN (through the SiLU branch).
  *
  * Returns KAN_OK, KAN_ERR_INVALID_ARG (grid == NULL, bad grid, batch < 0,
  * in_features < 1, out_features < 1, in_features * (G + 4) >= 2^31,
  * NULL/misaligned/overlapping pointers with batch > 0), KAN_ERR_UNSUPPORTED
- * (spline_order != 3, unknown dtype) or KAN_ERR_DEVICE (launch rejected).
+ * (spline_order != 3, unknown dtype) or KAN_ERR_DEVICE (allocation or launch
+ * rejected).
  */
 kan_status kan_layer_forward(const kan_grid* grid, kan_dtype dtype, int64_t batch,
                              int32_t in_features, int32_t out_features,
                              const void* x, const void* coef, const void* base_w,
                              void* y, void* stream);
+
+/*
+ * kan_layer_packed_bytes -- size in bytes of the packed weights of a layer
+ * (eq. kan_forward) with this grid, dtype and shape; independent of the batch.
+ * Writes *bytes.  Returns KAN_OK, KAN_ERR_INVALID_ARG (bytes == NULL, bad grid
+ * or sizes) or KAN_ERR_UNSUPPORTED.
+ */
+kan_status kan_layer_packed_bytes(const kan_grid* grid, kan_dtype dtype, int32_t in_features,
+                                  int32_t out_features, size_t* bytes);
+
+/*
+ * kan_layer_pack -- rearranges the weights of a layer (eq. kan_forward: the
+ * spline coefficients coef[o, i, j] and the SiLU weights base_w[o, i]) into
+ * the order in which the matrix cores consume them: for each tile of output
+ * columns, feature pair and block of columns, the weights of both features for
+ * every output column, the SiLU weight after the G + 3 spline coefficients of
+ * its feature and zeros in the padding.  The layout is private to this library
+ * and depends only on (grid, dtype, in_features, out_features).  Weights that
+ * do not change can be packed once and reused by any number of
+ * kan_layer_forward_packed calls.
+ *
+ *   coef    [out_features, in_features, G+3]  dtype storage
+ *   base_w  [out_features, in_features]       dtype storage
+ *   packed  packed_bytes >= kan_layer_packed_bytes(...), 16-byte aligned,
+ *           not overlapping coef or base_w; fully overwritten.
+ *
+ * Enqueued on `stream`.  Returns KAN_OK, KAN_ERR_INVALID_ARG, KAN_ERR_UNSUPPORTED
+ * or KAN_ERR_DEVICE, as kan_layer_forward.
+ */
+kan_status kan_layer_pack(const kan_grid* grid, kan_dtype dtype, int32_t in_features,
+                          int32_t out_features, const void* coef, const void* base_w,
+                          void* packed, size_t packed_bytes, void* stream);
+
+/*
+ * kan_layer_forward_packed -- kan_layer_forward with weights already packed by
+ * kan_layer_pack for the same (grid, dtype, in_features, out_features).
+ *
+ *   x       [batch, in_features]    dtype storage
+ *   packed  output of kan_layer_pack, packed_bytes >= kan_layer_packed_bytes(...)
+ *   y       [batch, out_features]   dtype storage, fully overwritten; must not
+ *           overlap x or packed.
+ *
+ * Allocates nothing.  Returns as kan_layer_forward.
+ */
+kan_status kan_layer_forward_packed(const kan_grid* grid, kan_dtype dtype, int64_t batch,
+                                    int32_t in_features, int32_t out_features, const void* x,
+                                    const void* packed, size_t packed_bytes, void* y,
+                                    void* stream);
 
 /* Static, NUL-terminated description of a status code (never NULL). */
 const char* kan_status_string(kan_status status);
@@ -120,7 +179,7 @@ const char* kan_status_string(kan_status status);
 /* Version of this interface; bumped on any incompatible change. */
 int32_t kan_abi_version(void);
 
-#define KAN_ABI_VERSION 1
+#define KAN_ABI_VERSION 2
 
 #ifdef __cplusplus
 }

@@ -27,7 +27,9 @@ KAN_ERR_DEVICE = 3
 KAN_F32 = 0
 KAN_BF16 = 1
 
-EXPORTED_SYMBOLS = ("kan_basis_eval", "kan_layer_forward", "kan_status_string", "kan_abi_version")
+EXPORTED_SYMBOLS = ("kan_basis_eval", "kan_layer_forward", "kan_layer_packed_bytes",
+                    "kan_layer_pack", "kan_layer_forward_packed", "kan_status_string",
+                    "kan_abi_version")
 
 
 class kan_grid(ctypes.Structure):
@@ -61,6 +63,20 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                               ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                               ctypes.c_void_p]
             lib.kan_layer_forward.restype = ctypes.c_int
+            lib.kan_layer_packed_bytes.argtypes = [ctypes.POINTER(kan_grid), ctypes.c_int,
+                                                   ctypes.c_int32, ctypes.c_int32,
+                                                   ctypes.POINTER(ctypes.c_size_t)]
+            lib.kan_layer_packed_bytes.restype = ctypes.c_int
+            lib.kan_layer_pack.argtypes = [ctypes.POINTER(kan_grid), ctypes.c_int, ctypes.c_int32,
+                                           ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
+                                           ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
+            lib.kan_layer_pack.restype = ctypes.c_int
+            lib.kan_layer_forward_packed.argtypes = [ctypes.POINTER(kan_grid), ctypes.c_int,
+                                                     ctypes.c_int64, ctypes.c_int32,
+                                                     ctypes.c_int32, ctypes.c_void_p,
+                                                     ctypes.c_void_p, ctypes.c_size_t,
+                                                     ctypes.c_void_p, ctypes.c_void_p]
+            lib.kan_layer_forward_packed.restype = ctypes.c_int
             lib.kan_status_string.argtypes = [ctypes.c_int]
             lib.kan_status_string.restype = ctypes.c_char_p
             lib.kan_abi_version.argtypes = []
@@ -98,6 +114,35 @@ def kan_layer_forward(grid: kan_grid, dtype: int, batch: int, in_features: int,
         ctypes.byref(grid), int(dtype), int(batch), int(in_features), int(out_features),
         ctypes.c_void_p(x), ctypes.c_void_p(coef), ctypes.c_void_p(base_w), ctypes.c_void_p(y),
         ctypes.c_void_p(stream)))
+
+
+def kan_layer_packed_bytes(grid: kan_grid, dtype: int, in_features: int,
+                           out_features: int) -> Tuple[int, int]:
+    """Raw call: returns (kan_status, bytes)."""
+    n = ctypes.c_size_t(0)
+    st = int(load_library().kan_layer_packed_bytes(ctypes.byref(grid), int(dtype),
+                                                   int(in_features), int(out_features),
+                                                   ctypes.byref(n)))
+    return st, int(n.value)
+
+
+def kan_layer_pack(grid: kan_grid, dtype: int, in_features: int, out_features: int, coef: int,
+                   base_w: int, packed: int, packed_bytes: int, stream: int = 0) -> int:
+    """Raw call: device addresses as integers; returns the kan_status code."""
+    return int(load_library().kan_layer_pack(
+        ctypes.byref(grid), int(dtype), int(in_features), int(out_features), ctypes.c_void_p(coef),
+        ctypes.c_void_p(base_w), ctypes.c_void_p(packed), ctypes.c_size_t(packed_bytes),
+        ctypes.c_void_p(stream)))
+
+
+def kan_layer_forward_packed(grid: kan_grid, dtype: int, batch: int, in_features: int,
+                             out_features: int, x: int, packed: int, packed_bytes: int, y: int,
+                             stream: int = 0) -> int:
+    """Raw call: device addresses as integers; returns the kan_status code."""
+    return int(load_library().kan_layer_forward_packed(
+        ctypes.byref(grid), int(dtype), int(batch), int(in_features), int(out_features),
+        ctypes.c_void_p(x), ctypes.c_void_p(packed), ctypes.c_size_t(packed_bytes),
+        ctypes.c_void_p(y), ctypes.c_void_p(stream)))
 
 
 def check(status: int) -> None:
@@ -161,31 +206,90 @@ def basis(x, grid_size: int, grid_lo: float = -1.0, grid_hi: float = 1.0, out=No
     return out
 
 
-def layer_forward(x, coef, base_w, grid_size: int, grid_lo: float = -1.0, grid_hi: float = 1.0,
-                  out=None):
-    """One KAN layer (kan_layer_forward): x [B, in], coef [out, in, G + 3],
-    base_w [out, in] -> y [B, out], all of one dtype on one device."""
+class PackedLayer:
+    """Weights of one layer packed by kan_layer_pack (device buffer + shape)."""
+
+    def __init__(self, buf, grid_size, grid_lo, grid_hi, n_in, n_out, dtype):
+        self.buf = buf
+        self.grid_size, self.grid_lo, self.grid_hi = int(grid_size), float(grid_lo), float(grid_hi)
+        self.n_in, self.n_out = int(n_in), int(n_out)
+        self.dtype = dtype
+
+    @property
+    def nbytes(self) -> int:
+        return int(self.buf.numel())
+
+
+def _check_weights(coef, base_w, grid_size):
+    _require_device(coef, base_w)
+    if base_w.dim() != 2 or coef.dim() != 3:
+        raise ValueError("expected coef [out, in, G+3], base_w [out, in]")
+    n_out, n_in = base_w.shape
+    if tuple(coef.shape) != (n_out, n_in, int(grid_size) + 3):
+        raise ValueError("coef / base_w shapes do not match each other and the grid")
+    if coef.dtype != base_w.dtype:
+        raise ValueError("coef and base_w must share one dtype")
+    return n_in, n_out
+
+
+def pack_layer(coef, base_w, grid_size: int, grid_lo: float = -1.0, grid_hi: float = 1.0,
+               out: Optional[PackedLayer] = None) -> PackedLayer:
+    """kan_layer_pack: coef [out, in, G + 3], base_w [out, in] -> PackedLayer
+    (device buffer from torch's allocator, filled on torch's current stream)."""
     torch = _torch()
-    _require_device(x, coef, base_w)
-    if x.dim() != 2 or base_w.dim() != 2 or coef.dim() != 3:
-        raise ValueError("expected x [B, in], coef [out, in, G+3], base_w [out, in]")
-    B, n_in = x.shape
-    n_out = base_w.shape[0]
-    if tuple(base_w.shape) != (n_out, n_in) or tuple(coef.shape) != (n_out, n_in, int(grid_size) + 3):
-        raise ValueError("coef / base_w shapes do not match x and the grid")
-    if coef.dtype != x.dtype or base_w.dtype != x.dtype:
-        raise ValueError("x, coef and base_w must share one dtype")
+    n_in, n_out = _check_weights(coef, base_w, grid_size)
+    dt = _dtype_code(coef)
+    g = make_grid(grid_size, grid_lo, grid_hi)
+    st, nbytes = kan_layer_packed_bytes(g, dt, n_in, n_out)
+    check(st)
     if out is None:
-        out = torch.empty((B, n_out), dtype=x.dtype, device=x.device)
+        buf = torch.empty(nbytes, dtype=torch.uint8, device=coef.device)
+        out = PackedLayer(buf, grid_size, grid_lo, grid_hi, n_in, n_out, coef.dtype)
+    elif out.nbytes < nbytes or out.buf.device != coef.device:
+        raise ValueError("packed buffer too small or on another device")
+    with torch.cuda.device(coef.device):
+        check(kan_layer_pack(g, dt, n_in, n_out, coef.data_ptr(), base_w.data_ptr(),
+                             out.buf.data_ptr(), out.nbytes, _stream(coef.device)))
+    return out
+
+
+def layer_forward_packed(x, packed: PackedLayer, out=None):
+    """kan_layer_forward_packed: x [B, in] with packed weights -> y [B, out]."""
+    torch = _torch()
+    _require_device(x)
+    if x.dim() != 2 or x.shape[1] != packed.n_in:
+        raise ValueError("x must be [B, in] with the packed layer's in")
+    if x.dtype != packed.dtype or packed.buf.device != x.device:
+        raise ValueError("x must match the packed layer's dtype and device")
+    B = x.shape[0]
+    if out is None:
+        out = torch.empty((B, packed.n_out), dtype=x.dtype, device=x.device)
     else:
         _require_device(x, out)
-        if out.dtype != x.dtype or tuple(out.shape) != (B, n_out):
+        if out.dtype != x.dtype or tuple(out.shape) != (B, packed.n_out):
             raise ValueError("out must be [B, out] with x's dtype")
+    g = make_grid(packed.grid_size, packed.grid_lo, packed.grid_hi)
     with torch.cuda.device(x.device):
-        check(kan_layer_forward(make_grid(grid_size, grid_lo, grid_hi), _dtype_code(x), B, n_in,
-                                n_out, x.data_ptr(), coef.data_ptr(), base_w.data_ptr(),
-                                out.data_ptr(), _stream(x.device)))
+        check(kan_layer_forward_packed(g, _dtype_code(x), B, packed.n_in, packed.n_out,
+                                       x.data_ptr(), packed.buf.data_ptr(), packed.nbytes,
+                                       out.data_ptr(), _stream(x.device)))
     return out
+
+
+def layer_forward(x, coef, base_w, grid_size: int, grid_lo: float = -1.0, grid_hi: float = 1.0,
+                  out=None, packed: Optional[PackedLayer] = None):
+    """One KAN layer: x [B, in], coef [out, in, G + 3], base_w [out, in] -> y
+    [B, out], all of one dtype on one device.  Packs the weights (kan_layer_pack,
+    into `packed` if given, else a fresh buffer) and runs
+    kan_layer_forward_packed, both on torch's current stream."""
+    _require_device(x)
+    n_in, _ = _check_weights(coef, base_w, grid_size)
+    if x.dim() != 2 or x.shape[1] != n_in:
+        raise ValueError("x must be [B, in] with coef's in")
+    if coef.dtype != x.dtype:
+        raise ValueError("x, coef and base_w must share one dtype")
+    p = pack_layer(coef, base_w, grid_size, grid_lo, grid_hi, out=packed)
+    return layer_forward_packed(x, p, out=out)
 
 
 def mlp_forward(x, layers: Sequence[Tuple[object, object]], grid_size: int, grid_lo: float = -1.0,

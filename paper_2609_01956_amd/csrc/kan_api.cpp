@@ -89,22 +89,110 @@ kan_status kan_basis_eval(const kan_grid* grid, kan_dtype dtype, const void* x, 
                                                 static_cast<uint16_t*>(phi), gc, L, s));
 }
 
+// Shared validation of the layer entry points: grid, dtype, sizes.
+static kan_status check_layer(const kan_grid* grid, kan_dtype dtype, int32_t in_features,
+                              int32_t out_features, kan::GridConst* gc, kan::LayerGeom* geom) {
+    const kan_status st = check_grid(grid, dtype, gc);
+    if (st != KAN_OK) return st;
+    if (in_features < 1 || out_features < 1) return KAN_ERR_INVALID_ARG;
+    if ((int64_t)in_features * (gc->nb + 1) >= 0x80000000LL) return KAN_ERR_INVALID_ARG;
+    if ((int64_t)out_features * in_features * gc->nb >= (1LL << 40)) return KAN_ERR_INVALID_ARG;
+    if (!kan::layer_geom(gc->nb, dtype == KAN_BF16, in_features, out_features, geom))
+        return KAN_ERR_INVALID_ARG;
+    return KAN_OK;
+}
+
+kan_status kan_layer_packed_bytes(const kan_grid* grid, kan_dtype dtype, int32_t in_features,
+                                  int32_t out_features, size_t* bytes) {
+    if (bytes == nullptr) return KAN_ERR_INVALID_ARG;
+    kan::GridConst gc;
+    kan::LayerGeom geom;
+    const kan_status st = check_layer(grid, dtype, in_features, out_features, &gc, &geom);
+    if (st != KAN_OK) return st;
+    *bytes = geom.packed_bytes;
+    return KAN_OK;
+}
+
+kan_status kan_layer_pack(const kan_grid* grid, kan_dtype dtype, int32_t in_features,
+                          int32_t out_features, const void* coef, const void* base_w,
+                          void* packed, size_t packed_bytes, void* stream) {
+    kan::GridConst gc;
+    kan::LayerGeom geom;
+    const kan_status st = check_layer(grid, dtype, in_features, out_features, &gc, &geom);
+    if (st != KAN_OK) return st;
+    if (coef == nullptr || base_w == nullptr || packed == nullptr) return KAN_ERR_INVALID_ARG;
+    const size_t es = dtype_size(dtype);
+    if (!aligned(coef, es) || !aligned(base_w, es) || !aligned(packed, 16))
+        return KAN_ERR_INVALID_ARG;
+    if (packed_bytes < geom.packed_bytes) return KAN_ERR_INVALID_ARG;
+    const size_t c_bytes = (size_t)out_features * in_features * gc.nb * es;
+    const size_t w_bytes = (size_t)out_features * in_features * es;
+    if (overlap(packed, geom.packed_bytes, coef, c_bytes) ||
+        overlap(packed, geom.packed_bytes, base_w, w_bytes))
+        return KAN_ERR_INVALID_ARG;
+    return device_status(kan::launch_pack(dtype == KAN_BF16, geom, in_features, out_features,
+                                          coef, base_w, packed,
+                                          static_cast<hipStream_t>(stream)));
+}
+
+kan_status kan_layer_forward_packed(const kan_grid* grid, kan_dtype dtype, int64_t batch,
+                                    int32_t in_features, int32_t out_features, const void* x,
+                                    const void* packed, size_t packed_bytes, void* y,
+                                    void* stream) {
+    kan::GridConst gc;
+    kan::LayerGeom geom;
+    const kan_status st = check_layer(grid, dtype, in_features, out_features, &gc, &geom);
+    if (st != KAN_OK) return st;
+    if (batch < 0) return KAN_ERR_INVALID_ARG;
+    if (batch == 0) return KAN_OK;
+    if (x == nullptr || packed == nullptr || y == nullptr) return KAN_ERR_INVALID_ARG;
+    const size_t es = dtype_size(dtype);
+    if (!aligned(x, es) || !aligned(y, es) || !aligned(packed, 16)) return KAN_ERR_INVALID_ARG;
+    if (packed_bytes < geom.packed_bytes) return KAN_ERR_INVALID_ARG;
+    // Row tiles of at least 32 rows go in blockIdx.x.
+    if (batch > (int64_t)0x7fffffff * 32) return KAN_ERR_INVALID_ARG;
+    const uint64_t ub = (uint64_t)batch;
+    if (ub > SIZE_MAX / es / (uint64_t)in_features || ub > SIZE_MAX / es / (uint64_t)out_features)
+        return KAN_ERR_INVALID_ARG;
+    const size_t x_bytes = ub * (size_t)in_features * es;
+    const size_t y_bytes = ub * (size_t)out_features * es;
+    if (overlap(y, y_bytes, x, x_bytes) || overlap(y, y_bytes, packed, geom.packed_bytes))
+        return KAN_ERR_INVALID_ARG;
+
+    kan::LayerArgs a;
+    a.x = x;
+    a.wp = packed;
+    a.y = y;
+    a.batch = batch;
+    a.in = in_features;
+    a.out = out_features;
+    a.nb = gc.nb;
+    a.nsb = geom.nsb;
+    a.nblk = geom.nblk;
+    a.nchunks = 0;  // set by the launcher (depends on the tile shape)
+    a.inv_h = gc.inv_h;
+    a.a_int = gc.a_int;
+    a.a_frac = gc.a_frac;
+    kan::LayerCfg cfg = kan::plan_layer(geom, dtype == KAN_BF16, batch);
+    kan::parse_layer_cfg_override(geom, &cfg);
+    return device_status(kan::launch_layer(dtype == KAN_BF16, geom, cfg, a,
+                                           static_cast<hipStream_t>(stream)));
+}
+
 kan_status kan_layer_forward(const kan_grid* grid, kan_dtype dtype, int64_t batch,
                              int32_t in_features, int32_t out_features, const void* x,
                              const void* coef, const void* base_w, void* y, void* stream) {
     kan::GridConst gc;
-    const kan_status st = check_grid(grid, dtype, &gc);
+    kan::LayerGeom geom;
+    const kan_status st = check_layer(grid, dtype, in_features, out_features, &gc, &geom);
     if (st != KAN_OK) return st;
-    if (batch < 0 || in_features < 1 || out_features < 1) return KAN_ERR_INVALID_ARG;
-    if (out_features > 65535 * 32) return KAN_ERR_INVALID_ARG;  // column tiles in blockIdx.y
-    if ((int64_t)in_features * (gc.nb + 1) >= 0x80000000LL) return KAN_ERR_INVALID_ARG;
+    if (batch < 0) return KAN_ERR_INVALID_ARG;
     if (batch == 0) return KAN_OK;
     if (x == nullptr || coef == nullptr || base_w == nullptr || y == nullptr)
         return KAN_ERR_INVALID_ARG;
     const size_t es = dtype_size(dtype);
     if (!aligned(x, es) || !aligned(coef, es) || !aligned(base_w, es) || !aligned(y, es))
         return KAN_ERR_INVALID_ARG;
-    // Grid of the launch: ceil(batch / 32) row tiles at most, in blockIdx.x.
     if (batch > (int64_t)0x7fffffff * 32) return KAN_ERR_INVALID_ARG;
     const uint64_t ub = (uint64_t)batch;
     if (ub > SIZE_MAX / es / (uint64_t)in_features || ub > SIZE_MAX / es / (uint64_t)out_features)
@@ -117,28 +205,21 @@ kan_status kan_layer_forward(const kan_grid* grid, kan_dtype dtype, int64_t batc
         overlap(y, y_bytes, base_w, w_bytes))
         return KAN_ERR_INVALID_ARG;
 
-    kan::LayerArgs a;
-    a.x = x;
-    a.coef = coef;
-    a.wb = base_w;
-    a.y = y;
-    a.batch = batch;
-    a.in = in_features;
-    a.out = out_features;
-    a.g = gc;
-    const int kg = dtype == KAN_F32 ? kan::kLayerKGroupF32 : kan::kLayerKGroupBf16;
-    const int cwmax = dtype == KAN_F32 ? kan::kLayerCwMaxF32 : kan::kLayerCwMaxBf16;
-    a.nbp = (gc.nb + 1 + kg - 1) / kg * kg;
-    int cw = kg;
-    while (cw < a.nbp && cw < cwmax) cw *= 2;
-    a.cw = cw;
-    a.nchunks = (a.nbp + cw - 1) / cw;
-
-    kan::LayerTile t = kan::plan_layer_tile(batch, out_features);
-    kan::parse_layer_tile_override(&t);
+    // Temporary packed weights from the stream-ordered pool: allocated and
+    // released in stream order, so the call stays asynchronous.
     hipStream_t s = static_cast<hipStream_t>(stream);
-    if (dtype == KAN_F32) return device_status(kan::launch_layer_f32(a, t, s));
-    return device_status(kan::launch_layer_bf16(a, t, s));
+    void* packed = nullptr;
+    if (hipMallocAsync(&packed, geom.packed_bytes, s) != hipSuccess) {
+        (void)hipGetLastError();
+        return KAN_ERR_DEVICE;
+    }
+    kan_status r = kan_layer_pack(grid, dtype, in_features, out_features, coef, base_w, packed,
+                                  geom.packed_bytes, stream);
+    if (r == KAN_OK)
+        r = kan_layer_forward_packed(grid, dtype, batch, in_features, out_features, x, packed,
+                                     geom.packed_bytes, y, stream);
+    if (hipFreeAsync(packed, s) != hipSuccess && r == KAN_OK) r = KAN_ERR_DEVICE;
+    return r;
 }
 
 }  // extern "C"

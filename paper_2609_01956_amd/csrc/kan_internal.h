@@ -3,11 +3,14 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <stddef.h>
 #include <stdint.h>
 
 #include "kan_device.h"
 
 namespace kan {
+
+// ---------------------------------------------------------------- basis only
 
 // Launch geometry of the basis-only kernel, chosen on the host.
 struct BasisLaunch {
@@ -27,40 +30,70 @@ hipError_t launch_basis_f32(const float* x, int64_t n, float* phi, const GridCon
 hipError_t launch_basis_bf16(const uint16_t* x, int64_t n, uint16_t* phi, const GridConst& g,
                              const BasisLaunch& L, hipStream_t s);
 
-// Fused layer: tile configuration.  A workgroup is four waves arranged
-// wm x wn; each wave owns a 32-row x (32 * nt)-column tile of y.
-struct LayerTile {
-    int nt;  // 32-column MFMA tiles per wave: 1, 2, 4 or 8
-    int wm;  // waves along the batch dimension
-    int wn;  // waves along the output dimension (wm * wn == 4)
+// ---------------------------------------------------------------- fused layer
+//
+// The contraction runs over K = in * (nb + 1) columns: for every input feature
+// its nb basis values and its SiLU value.  Features are taken in pairs, one
+// per half of a wave (the two k halves of the MFMA operands), and each pair's
+// nb + 1 columns are cut into "blocks" of kj columns (8 for bf16, one
+// v_mfma_f32_32x32x16_bf16 k-step; 2 for fp32, two v_mfma_f32_32x32x2_f32
+// k-steps), the last block of a pair zero-padded.  The packed weight buffer
+// holds, per N tile of 32 * nf output columns, the blocks in order:
+//
+//   packed[tile][pair][block][h][n][kj]      (h = feature within the pair)
+//
+// i.e. 2 * (32 * nf) * kj elements per block, kj consecutive per (h, n), so a
+// wave reads one block's B operand for 32 columns with one conflict-free 16-
+// or 8-byte LDS load per lane, and a workgroup stages consecutive blocks with
+// plain contiguous copies.
+struct LayerGeom {
+    int nb;       // G + 3
+    int kj;       // columns per block (8 bf16, 2 fp32)
+    int nsb;      // blocks per feature pair, ceil((nb + 1) / kj)
+    int npairs;   // ceil(in / 2)
+    int nblk;     // blocks per N tile, npairs * nsb
+    int nf;       // 32-column MFMA fragments per N tile (1, 2, 4 or 8)
+    int ntiles;   // ceil(out / (32 * nf))
+    size_t packed_bytes;
 };
 
-// Columns per feature per K-step, upper bound (LDS tile width); the host picks
-// cw = min(next power of two >= nbp, this bound).
-constexpr int kLayerCwMaxF32 = 16;
-constexpr int kLayerCwMaxBf16 = 32;
-// MFMA k per lane half: 1 for v_mfma_f32_32x32x2_f32, 8 for 32x32x16 bf16.
-constexpr int kLayerKGroupF32 = 1;
-constexpr int kLayerKGroupBf16 = 8;
+// Returns false when the sizes do not fit the index types of the kernels.
+bool layer_geom(int nb, bool bf16, int in, int out, LayerGeom* g);
+
+// Workgroup shape of the fused kernel: 4 waves, each holding rf 32-row MFMA
+// tiles of all nf column fragments; wk waves split the blocks (K) of a chunk
+// and are summed through LDS at the end, the other 4 / wk waves take
+// different rows.
+struct LayerCfg {
+    int rf;  // 1 or 2
+    int wk;  // 1, 2 or 4; wk > 1 needs rf * nf <= 4
+};
+
+LayerCfg plan_layer(const LayerGeom& g, bool bf16, int64_t batch);
+// KAN_LAYER_CFG="rf,wk" forces a configuration (testing and tuning); ignored
+// when malformed or not valid for the geometry.
+bool parse_layer_cfg_override(const LayerGeom& g, LayerCfg* c);
+bool layer_cfg_valid(const LayerGeom& g, const LayerCfg& c);
 
 struct LayerArgs {
-    const void* x;     // [batch, in]
-    const void* coef;  // [out, in, nb]
-    const void* wb;    // [out, in]
-    void* y;           // [batch, out]
+    const void* x;    // [batch, in]
+    const void* wp;   // packed weights
+    void* y;          // [batch, out]
     int64_t batch;
     int in;
     int out;
-    int nbp;      // per-feature column count (nb spline + 1 SiLU) padded to the MFMA k-group
-    int cw;       // columns per feature per K-step (power of two)
-    int nchunks;  // ceil(nbp / cw)
-    GridConst g;
+    int nb;
+    int nsb;
+    int nblk;
+    int nchunks;      // ceil(nblk / blocks-per-chunk)
+    float inv_h;      // see GridConst
+    float a_int;
+    float a_frac;
 };
 
-LayerTile plan_layer_tile(int64_t batch, int out);
-bool parse_layer_tile_override(LayerTile* t);
-
-hipError_t launch_layer_f32(const LayerArgs& a, const LayerTile& t, hipStream_t s);
-hipError_t launch_layer_bf16(const LayerArgs& a, const LayerTile& t, hipStream_t s);
+hipError_t launch_pack(bool bf16, const LayerGeom& g, int in, int out, const void* coef,
+                       const void* base_w, void* packed, hipStream_t s);
+hipError_t launch_layer(bool bf16, const LayerGeom& g, const LayerCfg& c, LayerArgs a,
+                        hipStream_t s);
 
 }  // namespace kan

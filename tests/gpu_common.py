@@ -39,11 +39,13 @@ def normwise(y: np.ndarray, ref: np.ndarray) -> float:
     return float(np.max(np.abs(y - ref))) / scale
 
 
-def set_tile(spec):
+def set_layer_cfg(spec):
+    """Force the fused layer's workgroup shape ("rows tiles per wave, waves
+    splitting K"); None restores the library's own choice."""
     if spec is None:
-        os.environ.pop("KAN_LAYER_TILE", None)
+        os.environ.pop("KAN_LAYER_CFG", None)
     else:
-        os.environ["KAN_LAYER_TILE"] = spec
+        os.environ["KAN_LAYER_CFG"] = spec
 
 
 F32_LAYER_TOL = 1e-5

@@ -31,7 +31,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_abi_version_and_status_strings():
-    assert kb.kan_abi_version() == 1
+    assert kb.kan_abi_version() == 2
     for code in range(4):
         s = kb.kan_status_string(code)
         assert s.startswith(["KAN_OK", "KAN_ERR_INVALID_ARG", "KAN_ERR_UNSUPPORTED", "KAN_ERR_DEVICE"][code])
@@ -108,6 +108,64 @@ def test_layer_argument_checks():
     assert kb.kan_layer_forward(g, f32, 16, 4, 4, X, C, W, W) == bad
     # empty batch: OK without launching
     assert kb.kan_layer_forward(g, f32, 0, 4, 4, 0, 0, 0, 0) == kb.KAN_OK
+
+
+def _expected_packed_bytes(G, bf16, n_in, n_out):
+    """Size of the packed weights: per tile of 32 * nf output columns, per pair of
+    features, per block of kj columns, kj weights for each of 2 * 32 * nf
+    (feature, column) slots."""
+    kj, es, nfmax = (8, 2, 8) if bf16 else (2, 4, 4)
+    nsb = -(-(G + 4) // kj)
+    npairs = -(-n_in // 2)
+    nf = 1
+    while nf < nfmax and 32 * nf < n_out:
+        nf *= 2
+    ntiles = -(-n_out // (32 * nf))
+    return ntiles * npairs * nsb * 2 * 32 * nf * kj * es
+
+
+@pytest.mark.parametrize("G,n_in,n_out", [(10, 784, 256), (10, 256, 10), (5, 2, 5), (200, 128, 128),
+                                          (7, 3, 300), (1, 1, 1), (50, 129, 65)])
+@pytest.mark.parametrize("bf16", [False, True])
+def test_packed_bytes(G, n_in, n_out, bf16):
+    st, n = kb.kan_layer_packed_bytes(kb.make_grid(G), kb.KAN_BF16 if bf16 else kb.KAN_F32,
+                                      n_in, n_out)
+    assert st == kb.KAN_OK
+    assert n == _expected_packed_bytes(G, bf16, n_in, n_out)
+    # 784 -> 256, G = 10 in bf16: 392 pairs x 2 blocks x 8 KiB
+    if (G, n_in, n_out, bf16) == (10, 784, 256, True):
+        assert n == 392 * 2 * 8192
+
+
+def test_packed_entry_point_checks():
+    g = kb.make_grid(10)
+    f32, bad = kb.KAN_F32, kb.KAN_ERR_INVALID_ARG
+    P = 0x600000000
+    lib = kb.load_library()
+    assert lib.kan_layer_packed_bytes(ctypes.byref(g), f32, 4, 4, None) == bad
+    assert kb.kan_layer_packed_bytes(g, f32, 0, 4)[0] == bad
+    assert kb.kan_layer_packed_bytes(g, f32, 4, 0)[0] == bad
+    assert kb.kan_layer_packed_bytes(kb.make_grid(10, spline_order=2), f32, 4, 4)[0] == \
+        kb.KAN_ERR_UNSUPPORTED
+    need = kb.kan_layer_packed_bytes(g, f32, 4, 4)[1]
+    # pack: null, misaligned (16 bytes for the packed buffer), short, overlapping
+    assert kb.kan_layer_pack(g, f32, 4, 4, 0, W, P, need) == bad
+    assert kb.kan_layer_pack(g, f32, 4, 4, C, 0, P, need) == bad
+    assert kb.kan_layer_pack(g, f32, 4, 4, C, W, 0, need) == bad
+    assert kb.kan_layer_pack(g, f32, 4, 4, C, W, P + 8, need) == bad
+    assert kb.kan_layer_pack(g, f32, 4, 4, C, W, P, need - 1) == bad
+    assert kb.kan_layer_pack(g, f32, 4, 4, C, W, C, need) == bad
+    assert kb.kan_layer_pack(g, f32, 4, 4, C, W, W - 16, need) == bad
+    # forward_packed: null, misaligned, short, overlapping, negative / empty batch
+    assert kb.kan_layer_forward_packed(g, f32, 16, 4, 4, 0, P, need, Y) == bad
+    assert kb.kan_layer_forward_packed(g, f32, 16, 4, 4, X, 0, need, Y) == bad
+    assert kb.kan_layer_forward_packed(g, f32, 16, 4, 4, X, P, need, 0) == bad
+    assert kb.kan_layer_forward_packed(g, f32, 16, 4, 4, X, P + 4, need, Y) == bad
+    assert kb.kan_layer_forward_packed(g, f32, 16, 4, 4, X, P, need - 16, Y) == bad
+    assert kb.kan_layer_forward_packed(g, f32, 16, 4, 4, X, P, need, P + 16) == bad
+    assert kb.kan_layer_forward_packed(g, f32, 16, 4, 4, X, P, need, X + 4) == bad
+    assert kb.kan_layer_forward_packed(g, f32, -1, 4, 4, X, P, need, Y) == bad
+    assert kb.kan_layer_forward_packed(g, f32, 0, 4, 4, 0, 0, 0, 0) == kb.KAN_OK
 
 
 def test_check_maps_codes_to_exceptions():

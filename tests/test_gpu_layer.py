@@ -8,7 +8,7 @@ import pytest
 import oracle
 from paper_2609_01956_amd import binding as kb
 from paper_2609_01956_amd import workloads as wl
-from gpu_common import (BF16_LAYER_TOL, F32_LAYER_TOL, device, normwise, say, set_tile,
+from gpu_common import (BF16_LAYER_TOL, F32_LAYER_TOL, device, normwise, say, set_layer_cfg,
                         to_dev, to_host64, torch)
 
 pytestmark = pytest.mark.gpu
@@ -63,24 +63,93 @@ def test_layer_matches_oracle(B, n_in, n_out, G, dtype_name):
     assert normwise(y, ref) <= _tol(dtype_name), normwise(y, ref)
 
 
-TILES = ["1,4,1", "2,4,1", "4,4,1", "8,4,1", "1,2,2", "2,2,2", "4,2,2", "1,1,4", "2,1,4"]
+# (rows tiles per wave, waves splitting K) of the fused kernel; K splits need
+# rf * nf <= 4 (nf = 32-column fragments of the column tile).
+CFGS = ["1,1", "2,1", "1,2", "1,4", "2,2", "2,4"]
 
 
 @pytest.mark.parametrize("dtype_name", ["f32", "bf16"])
-@pytest.mark.parametrize("tile", TILES)
-def test_layer_every_tile_configuration(tile, dtype_name):
+@pytest.mark.parametrize("cfg", CFGS)
+def test_layer_every_workgroup_shape(cfg, dtype_name):
+    # out = 45 -> two 32-column fragments per tile, so every shape is valid;
+    # 9 features (odd) and 300 rows (ragged) exercise the padding paths.
     B, n_in, n_out, G = 300, 9, 45, 10
     x, C, Wb = _inputs(B, n_in, n_out, G, seed=3, off=0.1, dtype_name=dtype_name)
     ref = oracle.layer(x, C, Wb, G)
     if dtype_name == "bf16":
         ref = oracle.round_bf16(ref)
-    say(f"layer tile={tile} {dtype_name}")
-    set_tile(tile)
+    say(f"layer cfg={cfg} {dtype_name}")
+    set_layer_cfg(cfg)
     try:
         y = _gpu_layer(x, C, Wb, G, dtype_name)
     finally:
-        set_tile(None)
+        set_layer_cfg(None)
     assert normwise(y, ref) <= _tol(dtype_name)
+
+
+WIDE = [
+    # (dtype, B, in, out, G, cfg): the widest column tiles (bf16 256, fp32 128)
+    ("bf16", 600, 20, 256, 10, "2,1"),
+    ("bf16", 600, 20, 256, 10, "1,1"),
+    ("bf16", 333, 7, 200, 50, "2,1"),
+    ("bf16", 97, 3, 130, 200, "1,1"),
+    ("f32", 600, 20, 256, 10, "1,1"),
+    ("f32", 600, 20, 256, 10, "1,4"),
+    ("f32", 333, 7, 128, 50, "2,1"),
+    ("f32", 97, 3, 100, 200, "1,2"),
+]
+
+
+@pytest.mark.parametrize("dtype_name,B,n_in,n_out,G,cfg", WIDE)
+def test_layer_wide_tiles(dtype_name, B, n_in, n_out, G, cfg):
+    x, C, Wb = _inputs(B, n_in, n_out, G, seed=B + G, off=0.1, dtype_name=dtype_name)
+    ref = oracle.layer(x, C, Wb, G)
+    if dtype_name == "bf16":
+        ref = oracle.round_bf16(ref)
+    say(f"layer wide {dtype_name} B={B} in={n_in} out={n_out} G={G} cfg={cfg}")
+    set_layer_cfg(cfg)
+    try:
+        y = _gpu_layer(x, C, Wb, G, dtype_name)
+    finally:
+        set_layer_cfg(None)
+    assert normwise(y, ref) <= _tol(dtype_name)
+
+
+@pytest.mark.parametrize("dtype_name", ["f32", "bf16"])
+def test_c_layer_forward_allocating_entry_point(dtype_name):
+    """kan_layer_forward (packs into a stream-ordered temporary) called through
+    the raw C entry point gives the same bits as pack + forward_packed."""
+    B, n_in, n_out, G = 513, 31, 70, 10
+    x, C, Wb = _inputs(B, n_in, n_out, G, seed=9, off=0.1, dtype_name=dtype_name)
+    dt = _dtype(dtype_name)
+    xt, Ct, Wt = to_dev(x, dt), to_dev(C, dt), to_dev(Wb, dt)
+    y = torch.empty((B, n_out), dtype=dt, device=device())
+    code = kb.KAN_F32 if dtype_name == "f32" else kb.KAN_BF16
+    say(f"layer C entry point {dtype_name}")
+    st = kb.kan_layer_forward(kb.make_grid(G), code, B, n_in, n_out, xt.data_ptr(), Ct.data_ptr(),
+                              Wt.data_ptr(), y.data_ptr(),
+                              int(torch.cuda.current_stream().cuda_stream))
+    assert st == kb.KAN_OK
+    y2 = kb.layer_forward(xt, Ct, Wt, G)
+    torch.cuda.synchronize()
+    assert torch.equal(y, y2)
+    ref = oracle.layer(x, C, Wb, G)
+    if dtype_name == "bf16":
+        ref = oracle.round_bf16(ref)
+    assert normwise(to_host64(y), ref) <= _tol(dtype_name)
+
+
+def test_packed_weights_reused_across_batches():
+    B, n_in, n_out, G = 700, 12, 33, 10
+    x, C, Wb = _inputs(B, n_in, n_out, G, seed=11, off=0.1)
+    say("layer packed reuse")
+    p = kb.pack_layer(to_dev(C, torch.float32), to_dev(Wb, torch.float32), G)
+    ya = kb.layer_forward_packed(to_dev(x, torch.float32), p)
+    yb = kb.layer_forward_packed(to_dev(x[:37], torch.float32), p)
+    torch.cuda.synchronize()
+    ref = oracle.layer(x, C, Wb, G)
+    assert normwise(to_host64(ya), ref) <= F32_LAYER_TOL
+    assert normwise(to_host64(yb), ref[:37]) <= F32_LAYER_TOL
 
 
 def test_layer_special_cases_f32():
