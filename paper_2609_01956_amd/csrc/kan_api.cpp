@@ -168,6 +168,7 @@ kan_status kan_layer_forward_packed(const kan_grid* grid, kan_dtype dtype, int64
     a.out = out_features;
     a.nb = gc.nb;
     a.nsb = geom.nsb;
+    a.npairs = geom.npairs;
     a.nblk = geom.nblk;
     a.nchunks = 0;  // set by the launcher (depends on the tile shape)
     a.inv_h = gc.inv_h;

@@ -46,12 +46,27 @@ hipError_t launch_basis_bf16(const uint16_t* x, int64_t n, uint16_t* phi, const 
 // wave reads one block's B operand for 32 columns with one conflict-free 16-
 // or 8-byte LDS load per lane, and a workgroup stages consecutive blocks with
 // plain contiguous copies.
+// Pipeline shape of the fused kernel (shared by the host planner and the
+// kernel): weights move global -> LDS in chunks of whole blocks by direct
+// global-to-LDS loads, kLayerStages chunks in flight.  A chunk is up to 16 KB
+// (at most 8 blocks) and a multiple of 4 KB (one 16-byte load per thread).
+constexpr int kLayerStages = 4;
+__host__ __device__ constexpr int layer_block_bytes(bool bf16, int nf) {
+    return 2 * 32 * nf * (bf16 ? 8 * 2 : 2 * 4);  // [h][n][kj] elements
+}
+__host__ __device__ constexpr int layer_chunk_blocks(bool bf16, int nf) {
+    return 16384 / layer_block_bytes(bf16, nf) < 8 ? 16384 / layer_block_bytes(bf16, nf) : 8;
+}
+
 struct LayerGeom {
     int nb;       // G + 3
     int kj;       // columns per block (8 bf16, 2 fp32)
     int nsb;      // blocks per feature pair, ceil((nb + 1) / kj)
     int npairs;   // ceil(in / 2)
-    int nblk;     // blocks per N tile, npairs * nsb
+    int nblk;     // blocks per N tile holding data, npairs * nsb
+    int nblk_pad; // blocks per N tile in the packed buffer (whole chunks; the
+                  // padding blocks are zero)
+    int kb;       // blocks per chunk
     int nf;       // 32-column MFMA fragments per N tile (1, 2, 4 or 8)
     int ntiles;   // ceil(out / (32 * nf))
     size_t packed_bytes;
@@ -84,8 +99,10 @@ struct LayerArgs {
     int out;
     int nb;
     int nsb;
-    int nblk;
-    int nchunks;      // ceil(nblk / blocks-per-chunk)
+    int npairs;       // ceil(in / 2)
+    int nblk;         // blocks holding data
+    int nblk_pad;     // blocks per N tile in the packed buffer
+    int nchunks;      // nblk_pad / blocks-per-chunk
     float inv_h;      // see GridConst
     float a_int;
     float a_frac;

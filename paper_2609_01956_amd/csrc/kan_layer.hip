@@ -23,14 +23,17 @@
 // Basis values.  With v = u - 2 (u the coordinate of eq. truncated), the clamp
 // of eq. bounded and the symmetry of the stencil {1, -4, 6, -4, 1} give
 //     6 N = w^3 - 4 b^3,   w = 2 - min(|v|, 2),  b = max(1 - |v|, 0),
-// and with P = w / 2 = clamp01(1 - |v| / 2) and Q = (2/3)^(1/3) b =
-// clamp01((2/3)^(1/3) (1 - |v|)):
-//     N = (4/3) P^3 - Q^3.
+// i.e. N / 2 = P^3 - Q^3 with
+//     P = (2/3)^(1/3) w / 2 = clamp01((2/3)^(1/3) (1 - |v| / 2)),
+//     Q = (1/3)^(1/3) b     = clamp01((1/3)^(1/3) (1 - |v|))
+// (both scale factors are below 1, so the clamp to [0, 1] only acts at 0).
 // Each value is then one subtraction, two clamped fused multiply-adds (the
-// clamp and |v| fold into the instruction), four multiplies and one fused
-// multiply-add.  Off the support both P and Q are 0 and the value is exactly
-// 0.  The MFMA operands are exactly N_j and silu (rounded to bf16 on the bf16
-// path), so the result is the contraction of those rounded operands.
+// clamp and |v| fold into the instruction), three multiplies and one fused
+// multiply-add.  Off the support P = Q = 0 and the value is exactly 0.  The
+// MFMA operands are N_j / 2 and silu / 2, and the epilogue doubles y: scaling
+// by a power of two is exact, so the operands are exactly bf16(N_j) / 2 and
+// bf16(silu) / 2 on the bf16 path and the result is the contraction of the
+// rounded N_j and silu values.
 //
 // fp32: A and W fp32, v_mfma_f32_32x32x2_f32 (one k per lane half, two
 //       k-steps per block).
@@ -49,19 +52,21 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr float kCbrtTwoThirds = 0.87358046473629571f;  // (2/3)^(1/3)
+constexpr float kCbrtOneThird = 0.69336127435063470f;   // (1/3)^(1/3)
 
-// N(u) at v = u - 2 (see the header comment).
-__device__ __forceinline__ float basis(float v) {
+// N(u) / 2 at v = u - 2 (see the header comment).
+__device__ __forceinline__ float half_basis(float v) {
     const float av = __builtin_fabsf(v);
-    const float P = __builtin_amdgcn_fmed3f(__builtin_fmaf(av, -0.5f, 1.0f), 0.0f, 1.0f);
+    const float P = __builtin_amdgcn_fmed3f(
+        __builtin_fmaf(av, -0.5f * kCbrtTwoThirds, kCbrtTwoThirds), 0.0f, 1.0f);
     const float Q = __builtin_amdgcn_fmed3f(
-        __builtin_fmaf(av, -kCbrtTwoThirds, kCbrtTwoThirds), 0.0f, 1.0f);
-    return __builtin_fmaf(P * P, P * (4.0f / 3.0f), -(Q * Q * Q));
+        __builtin_fmaf(av, -kCbrtOneThird, kCbrtOneThird), 0.0f, 1.0f);
+    return __builtin_fmaf(P * P, P, -(Q * Q * Q));
 }
 
-// silu(x) = x / (1 + exp(-x)).
-__device__ __forceinline__ float silu_fast(float x) {
-    return x * __builtin_amdgcn_rcpf(1.0f + __expf(-x));
+// silu(x) / 2 = x / (2 + 2 exp(-x)).
+__device__ __forceinline__ float half_silu(float x) {
+    return x * __builtin_amdgcn_rcpf(__builtin_fmaf(__expf(-x), 2.0f, 2.0f));
 }
 
 template <typename T> struct Tr;
@@ -69,12 +74,18 @@ template <typename T> struct Tr;
 template <> struct Tr<float> {
     static constexpr int KJ = 2;  // columns per block
     static __device__ __forceinline__ float load(const float* p) { return *p; }
+    static __device__ __forceinline__ uint32_t raw(const float* p) {
+        return __float_as_uint(*p);
+    }
+    static __device__ __forceinline__ float value(uint32_t u) { return __uint_as_float(u); }
     static __device__ __forceinline__ void store(float* p, float v) { *p = v; }
 };
 
 template <> struct Tr<uint16_t> {
     static constexpr int KJ = 8;
     static __device__ __forceinline__ float load(const uint16_t* p) { return bf16_to_f32(*p); }
+    static __device__ __forceinline__ uint32_t raw(const uint16_t* p) { return *p; }
+    static __device__ __forceinline__ float value(uint32_t u) { return __uint_as_float(u << 16); }
     static __device__ __forceinline__ void store(uint16_t* p, float v) { *p = f32_to_bf16(v); }
 };
 
@@ -88,7 +99,7 @@ template <typename T>
 __global__ __launch_bounds__(kThreads) void pack_kernel(const T* __restrict__ coef,
                                                         const T* __restrict__ bw,
                                                         T* __restrict__ packed, int in, int out,
-                                                        int nb, int nsb, int npairs, int ntile,
+                                                        int nb, int nsb, int nblk_pad, int ntile,
                                                         int64_t units) {
     constexpr int KJ = Tr<T>::KJ;
     const int64_t u = (int64_t)blockIdx.x * kThreads + threadIdx.x;
@@ -96,15 +107,16 @@ __global__ __launch_bounds__(kThreads) void pack_kernel(const T* __restrict__ co
     int64_t rest = u;
     const int n = (int)(rest % ntile); rest /= ntile;
     const int h = (int)(rest % 2); rest /= 2;
-    const int blk = (int)(rest % nsb); rest /= nsb;
-    const int pair = (int)(rest % npairs);
-    const int tile = (int)(rest / npairs);
+    const int gblk = (int)(rest % nblk_pad);  // block within the tile
+    const int tile = (int)(rest / nblk_pad);
+    const int pair = gblk / nsb;              // >= npairs in the padding
+    const int blk = gblk % nsb;
     const int ng = tile * ntile + n;
     const int f = 2 * pair + h;
     T v[KJ];
 #pragma unroll
     for (int e = 0; e < KJ; ++e) v[e] = T(0);
-    if (ng < out && f < in) {
+    if (ng < out && f < in) {  // (the padding blocks have f >= in)
         const int64_t row = (int64_t)ng * in + f;
 #pragma unroll
         for (int e = 0; e < KJ; ++e) {
@@ -142,28 +154,20 @@ __device__ __forceinline__ void zero_frag(AFrag<float, RF>& A, int rf) {
     A.a[rf][1] = 0.0f;
 }
 
-template <int RF>
-__device__ __forceinline__ void gen(const float (&s)[RF], const float (&sl)[RF], bool first,
-                                    AFrag<uint16_t, RF>& A) {
-#pragma unroll
-    for (int rf = 0; rf < RF; ++rf) {
-        const float v0 = basis(s[rf]);
-        A.a[rf][0] = (__bf16)(first ? sl[rf] : v0);
-#pragma unroll
-        for (int e = 1; e < 8; ++e) A.a[rf][e] = (__bf16)basis(s[rf] - (float)e);
+// Compile-time loop: f(std::integral_constant<int, I>) for I = 0 .. N - 1.
+template <int I, int N>
+struct StaticFor {
+    template <typename F>
+    __device__ __forceinline__ static void run(F& f) {
+        f(std::integral_constant<int, I>{});
+        StaticFor<I + 1, N>::run(f);
     }
-}
-
-template <int RF>
-__device__ __forceinline__ void gen(const float (&s)[RF], const float (&sl)[RF], bool first,
-                                    AFrag<float, RF>& A) {
-#pragma unroll
-    for (int rf = 0; rf < RF; ++rf) {
-        const float v0 = basis(s[rf]);
-        A.a[rf][0] = first ? sl[rf] : v0;
-        A.a[rf][1] = basis(s[rf] - 1.0f);
-    }
-}
+};
+template <int N>
+struct StaticFor<N, N> {
+    template <typename F>
+    __device__ __forceinline__ static void run(F&) {}
+};
 
 // Position of a wave's block: global block index, feature pair and block
 // within the pair.  A wave visits blocks wk, wk + WK, wk + 2 WK, ...
@@ -171,41 +175,85 @@ struct Pos {
     int blk, pair, bsub;
 };
 
-// Straight-line for step <= 4 (no loop, so no basic-block split in the main
-// loop); nsb >= 1.
-__device__ __forceinline__ Pos advance(Pos p, int step, int nsb) {
+// Advance a position by STEP blocks (compile-time STEP <= 8, nsb >= 1):
+// straight-line selects, so no loop (and no basic-block split) in the main
+// loop.
+template <int STEP>
+__device__ __forceinline__ Pos advance(Pos p, int nsb) {
+    p.blk += STEP;
+    p.bsub += STEP;
+#pragma unroll
+    for (int i = 0; i < STEP; ++i) {
+        // wrap = (bsub >= nsb) as plain integer arithmetic (no lane masks,
+        // so the scalar unit does it)
+        const int wrap = (int)((uint32_t)(nsb - 1 - p.bsub) >> 31);
+        p.bsub -= nsb & -wrap;
+        p.pair += wrap;
+    }
+    return p;
+}
+
+// Advance by a runtime step < 4.
+__device__ __forceinline__ Pos advance_n(Pos p, int step, int nsb) {
     p.blk += step;
     p.bsub += step;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const bool wrap = p.bsub >= nsb;
-        p.bsub = wrap ? p.bsub - nsb : p.bsub;
-        p.pair = wrap ? p.pair + 1 : p.pair;
+    for (int i = 0; i < 3; ++i) {
+        const int wrap = (int)((uint32_t)(nsb - 1 - p.bsub) >> 31);
+        p.bsub -= nsb & -wrap;
+        p.pair += wrap;
     }
     return p;
 }
 
 // ------------------------------------------------------------- main kernel
 
+// Waves per SIMD the register budget is sized for: two when the accumulators
+// take at most 128 registers (so a second wave's MFMAs fill the matrix core
+// while one wave runs its basis VALU work), otherwise one.
+template <int RF, int NF>
+struct Occ {
+    static constexpr int waves = RF * NF * 16 <= 128 ? 2 : 1;
+};
+
 template <typename T, int RF, int NF, int WK>
-__global__ __launch_bounds__(kThreads) void layer_kernel(LayerArgs a) {
+__global__ __launch_bounds__(kThreads)
+__attribute__((amdgpu_waves_per_eu(Occ<RF, NF>::waves)))
+void layer_kernel(LayerArgs a) {
     constexpr bool BF16 = sizeof(T) == 2;
     constexpr int KJ = Tr<T>::KJ;
     constexpr int WM = 4 / WK;
     constexpr int NTILE = 32 * NF;
     constexpr int LANEB = KJ * (int)sizeof(T);  // B bytes per lane per block (16 / 8)
-    constexpr int BLKB = 2 * NTILE * LANEB;      // bytes per block: [h][n][KJ]
-    constexpr int KB = (32768 / BLKB) < 8 ? (32768 / BLKB) : 8;  // blocks per chunk
-    constexpr int CHB = KB * BLKB;               // bytes per chunk (<= 32 KB)
-    constexpr int CHU = CHB / 16;                // 16-byte units per chunk
-    constexpr int SPT = CHU / kThreads;          // staged units per thread
+    constexpr int BLKB = layer_block_bytes(BF16, NF);  // bytes per block: [h][n][KJ]
+    constexpr int KB = layer_chunk_blocks(BF16, NF);   // blocks per chunk
+    constexpr int CHB = KB * BLKB;               // bytes per chunk
+    constexpr int S = kLayerStages;              // chunks in LDS / in flight
+    constexpr int DPW = CHB / 4096;              // 1 KB loads per wave per chunk
     constexpr int KBW = KB / WK;                 // blocks per wave per chunk
+    constexpr int NX = KBW * RF;                 // x loads per lane per chunk
     constexpr int BM = 32 * RF * WM;             // rows per workgroup
-    constexpr int RED = WK > 1 ? 4 * 32 * RF * NTILE * 4 : 0;  // K-split reduction bytes
-    constexpr int LDSB = 2 * CHB > RED ? 2 * CHB : RED;
-    static_assert(CHU % kThreads == 0 && KB % WK == 0 && KB >= WK, "chunk shape");
-    static_assert(LDSB <= 65536, "LDS budget");
-    __shared__ u32x4 lds[LDSB / 16];
+    constexpr int PART = WK > 1 ? 32 * RF * NTILE * 4 : 0;  // one wave's partial sums
+    constexpr int STB = CHB > PART ? CHB : PART;            // bytes per stage array
+    static_assert(CHB % 4096 == 0 && KB % WK == 0 && KB >= WK, "chunk shape");
+    static_assert(S == 4 && 4 * STB <= 65536, "LDS budget");
+    static_assert(BLKB == 2 * NTILE * LANEB, "block layout");
+    static_assert(DPW + (S - 3) * (NX + DPW) <= 63, "vmcnt range");
+    // One array per stage: the LDS reads of stage K and the direct loads into
+    // stage K + S - 1 then touch different objects, so the compiler does not
+    // make the reads wait for the loads in flight.  After the main loop the
+    // arrays hold the K-split partial sums, one wave per array.
+    __shared__ u32x4 lds0[STB / 16];
+    __shared__ u32x4 lds1[STB / 16];
+    __shared__ u32x4 lds2[STB / 16];
+    __shared__ u32x4 lds3[STB / 16];
+    auto stage = [&](auto kk) -> u32x4* {
+        constexpr int k = decltype(kk)::value % S;
+        if constexpr (k == 0) return lds0;
+        else if constexpr (k == 1) return lds1;
+        else if constexpr (k == 2) return lds2;
+        else return lds3;
+    };
 
     const T* __restrict__ x = static_cast<const T*>(a.x);
     T* __restrict__ y = static_cast<T*>(a.y);
@@ -219,46 +267,67 @@ __global__ __launch_bounds__(kThreads) void layer_kernel(LayerArgs a) {
     const int wk = wave / WM;
     const int64_t row0 = (int64_t)blockIdx.x * BM + wm * 32 * RF;
     const int nt = blockIdx.y;
-    const u32x4* __restrict__ wp =
-        static_cast<const u32x4*>(a.wp) + (size_t)nt * (size_t)a.nblk * (BLKB / 16);
-    const int64_t last_unit = (int64_t)a.nblk * (BLKB / 16) - 1;
+    // Packed weights of this N tile: nblk_pad blocks = nchunks whole chunks.
+    const char* __restrict__ wpt =
+        static_cast<const char*>(a.wp) + (size_t)nt * (size_t)a.nblk_pad * BLKB;
 
-    // Rows past the batch read row batch - 1 (their results are not stored).
-    const T* xr[RF];
+    // x is addressed as a per-workgroup base plus 32-bit element offsets (the
+    // workgroup's rows span far less than 2^31 elements).  Rows past the
+    // batch read row batch - 1 (their results are not stored).
+    const int64_t wg_row0 = (int64_t)blockIdx.x * BM;
+    const T* __restrict__ xw = x + wg_row0 * (int64_t)a.in;
+    uint32_t xoff[RF];  // element offset of (row, feature h of pair 0)
 #pragma unroll
     for (int rf = 0; rf < RF; ++rf) {
         int64_t row = row0 + rf * 32 + r;
         row = row < a.batch ? row : a.batch - 1;
-        xr[rf] = x + row * (int64_t)a.in;
+        xoff[rf] = (uint32_t)((row - wg_row0) * a.in + h);
     }
+    // With an odd feature count the last pair has a phantom second feature
+    // (zero weights): its lanes read the real last feature and use x = 0.
+    const int last_pair_odd = (a.in & 1) ? a.in / 2 : -1;
 
-    // ---- staging of packed weights (global -> registers -> LDS).  Units past
-    // the end re-read the last unit; they land in LDS blocks nobody reads.
-    u32x4 stg[SPT];
-    auto stage_load = [&](int c) {
-        const int64_t base = (int64_t)c * CHU + tid;
+    // ---- weights: chunk c -> LDS stage c % S by direct global-to-LDS loads.
+    // Wave w, load i moves bytes [i 4096 + w 1024, + 1024) of the chunk, 16 per
+    // lane, to the same offsets of the stage.  Chunks past the last re-load
+    // the last chunk (into a stage no real chunk uses any more).
+    const uint32_t dma_lane = (uint32_t)(wave * 1024 + lane * 16);
+    auto dma = [&](int c, auto kk) {  // kk: c % S as a compile-time constant
+        const int cc = c < a.nchunks ? c : a.nchunks - 1;
+        const char* g = wpt + (size_t)cc * CHB;  // wave-uniform
+        u32x4* l = stage(kk) + wave * 64;
 #pragma unroll
-        for (int i = 0; i < SPT; ++i) {
-            int64_t u = base + i * kThreads;
-            u = u < last_unit ? u : last_unit;
-            stg[i] = wp[u];
-        }
-    };
-    auto stage_store = [&](int buf) {
-#pragma unroll
-        for (int i = 0; i < SPT; ++i) lds[buf * CHU + tid + i * kThreads] = stg[i];
+        for (int i = 0; i < DPW; ++i)
+            __builtin_amdgcn_global_load_lds(g + (dma_lane + (uint32_t)(i * 4096)), l + i * 256,
+                                             16, 0, 0);
     };
 
     // x of this lane's rows for the feature of its half in pair p.pair; the
     // phantom feature of an odd feature count (and positions past the end)
     // give 0.
-    auto load_x = [&](const Pos& p, float (&xv)[RF]) {
-        const int f = 2 * p.pair + h;
-        const int fc = f < a.in ? f : a.in - 1;
+    // The raw bits are kept (conversion and masking happen where the values
+    // are used, so the load is not waited for when it is issued).
+    auto load_x = [&](const Pos& p, uint32_t (&xv)[RF]) {
+        // positions past the end read the last pair (their blocks multiply
+        // zeros); the phantom lanes step back one feature
+        const int pr = p.pair < a.npairs ? p.pair : a.npairs - 1;
+        const uint32_t back = (pr == last_pair_odd) ? (uint32_t)h : 0u;
 #pragma unroll
-        for (int rf = 0; rf < RF; ++rf) {
-            const float v = Tr<T>::load(xr[rf] + fc);
-            xv[rf] = f < a.in ? v : 0.0f;
+        for (int rf = 0; rf < RF; ++rf)
+            xv[rf] = Tr<T>::raw(xw + (xoff[rf] + (uint32_t)(2 * pr) - back));
+    };
+    // Value of raw x bits for the lane's feature at position p.
+    auto x_value = [&](const Pos& p, uint32_t raw) {
+        const float v = Tr<T>::value(raw);
+        if (p.pair == last_pair_odd) return h ? 0.0f : v;
+        return v;
+    };
+    // x of the KBW blocks of a chunk for this wave, starting at position p.
+    auto load_chunk_x = [&](Pos p, uint32_t (&xv)[KBW][RF]) {
+#pragma unroll
+        for (int t = 0; t < KBW; ++t) {
+            load_x(p, xv[t]);
+            p = advance<WK>(p, a.nsb);
         }
     };
 
@@ -270,131 +339,217 @@ __global__ __launch_bounds__(kThreads) void layer_kernel(LayerArgs a) {
 #pragma unroll
             for (int q = 0; q < 16; ++q) acc[rf][nf][q] = 0.0f;
 
-    // ---- the MFMAs of one block, B read from LDS block `bi` of buffer `buf`
-    auto mfma_block = [&](const AFrag<T, RF>& A, int buf, int bi) {
-        const char* lb = reinterpret_cast<const char*>(lds) + buf * CHB + bi * BLKB;
-        if constexpr (BF16) {
-            bf16x8 b[NF];
+    // ---- B fragments of one block (LDS block `bi` of stage `st`)
+    typedef typename std::conditional<BF16, bf16x8, floatx2>::type BVec;
+    struct BFrag { BVec b[NF]; };
+    auto read_b = [&](BFrag& B, const u32x4* st, int bi) {
+        const char* lb = reinterpret_cast<const char*>(st) + bi * BLKB;
 #pragma unroll
-            for (int nf = 0; nf < NF; ++nf)
-                b[nf] = __builtin_bit_cast(
-                    bf16x8, *reinterpret_cast<const u32x4*>(lb + (h * NTILE + nf * 32 + r) * 16));
-#pragma unroll
-            for (int nf = 0; nf < NF; ++nf)
-#pragma unroll
-                for (int rf = 0; rf < RF; ++rf)
-                    acc[rf][nf] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A.a[rf], b[nf],
-                                                                         acc[rf][nf], 0, 0, 0);
-        } else {
-            floatx2 b[NF];
-#pragma unroll
-            for (int nf = 0; nf < NF; ++nf)
-                b[nf] = *reinterpret_cast<const floatx2*>(lb + (h * NTILE + nf * 32 + r) * 8);
-#pragma unroll
-            for (int t = 0; t < 2; ++t)
-#pragma unroll
-                for (int nf = 0; nf < NF; ++nf)
-#pragma unroll
-                    for (int rf = 0; rf < RF; ++rf)
-                        acc[rf][nf] = __builtin_amdgcn_mfma_f32_32x32x2f32(
-                            A.a[rf][t], b[nf][t], acc[rf][nf], 0, 0, 0);
+        for (int nf = 0; nf < NF; ++nf) {
+            const char* q = lb + (h * NTILE + nf * 32 + r) * LANEB;
+            if constexpr (BF16)
+                B.b[nf] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(q));
+            else
+                B.b[nf] = *reinterpret_cast<const floatx2*>(q);
         }
     };
 
-    // A of block p from x values xv; sl holds silu of the same x, computed
-    // when the pair starts.
-    auto gen_block = [&](const Pos& p, const float (&xv)[RF], const float (&sl)[RF],
-                         AFrag<T, RF>& A) {
-        const float c = a.a_int + 1.0f - (float)(KJ * p.bsub);
+    // MFMA number i of a block (NMFMA per block): bf16 (nf, rf); fp32 also
+    // the k-step t of the block's two columns.
+    constexpr int NMFMA = (BF16 ? 1 : 2) * RF * NF;
+    auto do_mfma = [&](int i, const AFrag<T, RF>& A, const BFrag& B) {
+        const int rf = i % RF;
+        const int nf = (i / RF) % NF;
+        if constexpr (BF16) {
+            acc[rf][nf] =
+                __builtin_amdgcn_mfma_f32_32x32x16_bf16(A.a[rf], B.b[nf], acc[rf][nf], 0, 0, 0);
+        } else {
+            const int t = i / (RF * NF);
+            acc[rf][nf] = __builtin_amdgcn_mfma_f32_32x32x2f32(A.a[rf][t], B.b[nf][t],
+                                                               acc[rf][nf], 0, 0, 0);
+        }
+    };
+
+    // One step: the NMFMA MFMAs of the current block (A, B) together with the
+    // generation of the next block's A (block pg from x values xv, slv the
+    // silu of its pair) and, with one wave per SIMD, the LDS reads of the next
+    // block's B (PREF: block bi_n of stage st).  After MFMA i come the VALU
+    // ops of A elements [i NE / NMFMA, (i + 1) NE / NMFMA).
+    constexpr int NE = RF * KJ;  // A elements generated per lane per block
+    auto step = [&](const AFrag<T, RF>& A, const BFrag& B, const Pos& pg,
+                    const float (&xv)[RF], const float (&slv)[RF], AFrag<T, RF>& An,
+                    auto pref_tag, BFrag& Bn, const u32x4* st, int bi_n) {
+        constexpr bool PREF = decltype(pref_tag)::value;
         float s[RF];
+        const float c = a.a_int + 1.0f - (float)(KJ * pg.bsub);
 #pragma unroll
         for (int rf = 0; rf < RF; ++rf) s[rf] = __builtin_fmaf(xv[rf], a.inv_h, c) + a.a_frac;
-        gen<RF>(s, sl, p.bsub == 0, A);
+        // (xv: x values of block pg, already converted)
+        const bool first = pg.bsub == 0;
+        float v[RF][KJ];
+#pragma unroll
+        for (int i = 0; i < NMFMA; ++i) {
+            do_mfma(i, A, B);
+            if constexpr (PREF) {
+                if (i == 0) read_b(Bn, st, bi_n);
+            }
+#pragma unroll
+            for (int k = i * NE / NMFMA; k < (i + 1) * NE / NMFMA; ++k) {
+                const int rf = k / KJ;
+                const int e = k % KJ;
+                const float bv = half_basis(s[rf] - (float)e);
+                v[rf][e] = (e == 0 && first) ? slv[rf] : bv;
+                if constexpr (BF16) {
+                    if (e & 1) {
+                        An.a[rf][e - 1] = (__bf16)v[rf][e - 1];
+                        An.a[rf][e] = (__bf16)v[rf][e];
+                    }
+                } else {
+                    An.a[rf][e] = v[rf][e];
+                }
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        }
     };
+
     auto silu_of = [&](const float (&xv)[RF], float (&sl)[RF]) {
 #pragma unroll
-        for (int rf = 0; rf < RF; ++rf) sl[rf] = silu_fast(xv[rf]);
+        for (int rf = 0; rf < RF; ++rf) sl[rf] = half_silu(xv[rf]);
     };
 
     // ---- pipeline
-    // Chunk c (KB blocks, CHB bytes of packed weights) is multiplied from LDS
-    // buffer c & 1.  At the start of chunk c the wave issues the x loads of
-    // chunk c + 1 and then the weight loads of chunk c + 1; the weights go to
-    // LDS at the end of chunk c.  Loads complete in issue order, so waiting for
-    // x never waits for weights still in flight.  Within a chunk (unrolled),
-    // each step generates A of the next block (VALU) and multiplies the
-    // current block (MFMA) in one basic block.
-    static_assert(WK <= 4, "advance() steps at most 4");
-    const int nq = wk < a.nblk ? (a.nblk - wk + WK - 1) / WK : 0;  // blocks of this wave
-    float xc[KBW][RF], xn[KBW][RF], sl[RF];
+    // Loads are issued in groups, one group per chunk: the x values of the
+    // chunk's blocks for this wave (NX loads) and then its weights (DPW
+    // loads), S - 1 chunks ahead of the chunk being multiplied.  Loads
+    // complete in issue order, so at the top of chunk c waiting until at most
+    // VMW loads are outstanding means this wave's x and weights of chunk c
+    // (and x of chunk c + 1) have arrived; the barrier after it means every
+    // wave's have.  The
+    // chunk loop is unrolled by S so that the S sets of x registers rotate by
+    // name (a register move of a load still in flight would wait for it).
+    // Chunks past the last one (up to S - 1, to fill the unrolled group) load
+    // clamped inputs and multiply zero A.
+    static_assert(WK <= 4, "wave block stride");
+    // At the top of chunk c: groups c + 1 .. c + S - 2 may still be in
+    // flight, except the x loads of chunk c + 1 (issued first in their group,
+    // needed at the end of chunk c to generate the next chunk's first block).
+    constexpr int VMW = DPW + (S - 3) * (NX + DPW);
+    constexpr int WAITCNT = (VMW & 0xF) | (0x7 << 4) | (0xF << 8) | (((VMW >> 4) & 0x3) << 14);
+    const int nq = wk < a.nblk ? (a.nblk - wk + WK - 1) / WK : 0;  // real blocks of this wave
+
+    uint32_t xq[S][KBW][RF];
+    float sl[RF];
     AFrag<T, RF> A_cur, A_nxt;
+    BFrag bq[2];
+    Pos pos_c = advance_n(Pos{0, 0, 0}, wk, a.nsb);  // first block of the current chunk
+    Pos pos_l = pos_c;                               // first block of the next chunk to load
 
-    // x of the KBW blocks of chunk c for this wave, starting at position p.
-    auto load_chunk_x = [&](Pos p, float (&xv)[KBW][RF]) {
-#pragma unroll
-        for (int t = 0; t < KBW; ++t) {
-            load_x(p, xv[t]);
-            p = advance(p, WK, a.nsb);
-        }
+    // prologue: groups of chunks 0 .. S - 2
+    auto prologue = [&](auto jj) {
+        constexpr int j = decltype(jj)::value;
+        load_chunk_x(pos_l, xq[j]);
+        __builtin_amdgcn_sched_barrier(0);  // x loads issue before the weight loads
+        dma(j, jj);
+        __builtin_amdgcn_sched_barrier(0);
+        pos_l = advance<KB>(pos_l, a.nsb);
     };
+    StaticFor<0, S - 1>::run(prologue);
+    __builtin_amdgcn_s_waitcnt(WAITCNT);
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
 
-    Pos pc = advance(Pos{0, 0, 0}, wk, a.nsb);  // first block of the current chunk
-    load_chunk_x(pc, xc);
-    stage_load(0);
-    stage_store(0);
-    __syncthreads();
-    silu_of(xc[0], sl);
-    gen_block(pc, xc[0], sl, A_cur);
-
-    // One chunk.  LAST: no next chunk (no prefetch, no generation past the
-    // end), and blocks past the wave's last one multiply zeros.
-    auto chunk = [&](int c, auto last_tag) {
-        constexpr bool LAST = decltype(last_tag)::value;
-        const int buf = c & 1;
-        Pos pn = pc;
+    // A of the wave's first block (nothing to interleave with yet).
+    {
+        float x0[RF];
 #pragma unroll
-        for (int t = 0; t < KBW; ++t) pn = advance(pn, WK, a.nsb);  // first block of c + 1
-        if constexpr (!LAST) {
-            load_chunk_x(pn, xn);
-            stage_load(c + 1);
-        }
-        Pos p = pc;
+        for (int rf = 0; rf < RF; ++rf) x0[rf] = x_value(pos_c, xq[0][0][rf]);
+        silu_of(x0, sl);
+        const float c0 = a.a_int + 1.0f - (float)(KJ * pos_c.bsub);
 #pragma unroll
-        for (int t = 0; t < KBW; ++t) {
-            const Pos pnext = t + 1 < KBW ? advance(p, WK, a.nsb) : pn;
-            const bool gen_next = !LAST || t + 1 < KBW;
-            if (gen_next) {
-                const float(&xv)[RF] = t + 1 < KBW ? xc[t + 1 < KBW ? t + 1 : 0] : xn[0];
-                if (pnext.bsub == 0) silu_of(xv, sl);
-                gen_block(pnext, xv, sl, A_nxt);
+        for (int rf = 0; rf < RF; ++rf) {
+            const float s0 = __builtin_fmaf(x0[rf], a.inv_h, c0) + a.a_frac;
+#pragma unroll
+            for (int e = 0; e < KJ; ++e) {
+                const float bv = half_basis(s0 - (float)e);
+                const float v = (e == 0 && pos_c.bsub == 0) ? sl[rf] : bv;
+                if constexpr (BF16) A_cur.a[rf][e] = (__bf16)v;
+                else A_cur.a[rf][e] = v;
             }
-            if constexpr (LAST) {
-                if (c * KBW + t >= nq) {  // past the wave's last block: contribute 0
+        }
+    }
+
+    // Chunk c, whose x is in xq[K] (K = c % S, compile-time); the x of the
+    // next chunk is in xq[(K + 1) % S]; the group loaded at its top goes to
+    // xq[(K + S - 1) % S] (the x of chunk c - 1, no longer needed).
+    auto chunk = [&](int c, auto kk, auto last_tag) {
+        constexpr int K = decltype(kk)::value;
+        constexpr bool LASTG = decltype(last_tag)::value;  // in the final group
+        constexpr int KN = (K + 1) % S;
+        constexpr int KL = (K + S - 1) % S;
+        if (c > 0) {  // (chunk 0's wait and barrier are in the prologue)
+            __builtin_amdgcn_s_waitcnt(WAITCNT);
+            __builtin_amdgcn_s_barrier();
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        load_chunk_x(pos_l, xq[KL]);
+        __builtin_amdgcn_sched_barrier(0);  // x loads issue before the weight loads
+        dma(c + S - 1, std::integral_constant<int, KL>{});
+        pos_l = advance<KB>(pos_l, a.nsb);
+        __builtin_amdgcn_sched_barrier(0);
+
+        const u32x4* st = stage(kk);
+        read_b(bq[0], st, wk);
+        Pos p = pos_c;
+        auto one = [&](auto tt) {
+            constexpr int t = decltype(tt)::value;
+            // position of the next block: the next step's, or the first block
+            // of the next chunk
+            const Pos pnext = advance<WK>(p, a.nsb);
+            const uint32_t(&xr)[RF] = t + 1 < KBW ? xq[K][t + 1 < KBW ? t + 1 : 0] : xq[KN][0];
+            float xv[RF];
+#pragma unroll
+            for (int rf = 0; rf < RF; ++rf) xv[rf] = x_value(pnext, xr[rf]);
+            if (pnext.bsub == 0) silu_of(xv, sl);
+            if constexpr (LASTG) {
+                if (c * KBW + t >= nq) {  // past the wave's last real block: contribute 0
 #pragma unroll
                     for (int rf = 0; rf < RF; ++rf) zero_frag(A_cur, rf);
                 }
             }
-            mfma_block(A_cur, buf, wk + WK * t);
-            if (gen_next) A_cur = A_nxt;
+            // One wave per SIMD: the next block's B is read during this step.
+            // Two waves: B is read at the start of each step; the other wave
+            // covers the latency, and the registers of a second B set are
+            // saved.
+            constexpr bool PREF = Occ<RF, NF>::waves == 1 && t + 1 < KBW;
+            if constexpr (Occ<RF, NF>::waves == 2 && t > 0) read_b(bq[t & 1], st, wk + WK * t);
+            step(A_cur, bq[t & 1], pnext, xv, sl, A_nxt, std::integral_constant<bool, PREF>{},
+                 bq[(t + 1) & 1], st, wk + WK * (t + 1));
+            A_cur = A_nxt;
             p = pnext;
-        }
-        if constexpr (!LAST) {
-            stage_store((c + 1) & 1);
-            __syncthreads();
-#pragma unroll
-            for (int t = 0; t < KBW; ++t)
-#pragma unroll
-                for (int rf = 0; rf < RF; ++rf) xc[t][rf] = xn[t][rf];
-        }
-        pc = pn;
+        };
+        StaticFor<0, KBW>::run(one);
+        pos_c = p;
     };
 
+    // Every wave's blocks are all real in every group but the final one.
+    const int ngroups = (a.nchunks + S - 1) / S;
 #pragma unroll 1
-    for (int c = 0; c + 1 < a.nchunks; ++c) chunk(c, std::false_type{});
-    chunk(a.nchunks - 1, std::true_type{});
+    for (int gi = 0; gi + 1 < ngroups; ++gi) {
+        auto group = [&](auto kk) {
+            chunk(gi * S + decltype(kk)::value, kk, std::false_type{});
+        };
+        StaticFor<0, S>::run(group);
+    }
+    {
+        const int gi = ngroups - 1;
+        auto group = [&](auto kk) {
+            chunk(gi * S + decltype(kk)::value, kk, std::true_type{});
+        };
+        StaticFor<0, S>::run(group);
+    }
     __syncthreads();
 
-    // ---- epilogue
+    // ---- epilogue: y = 2 acc (the operands carry N / 2 and silu / 2)
     const int col0 = nt * NTILE;
     if constexpr (WK == 1) {
         const bool full = row0 + 32 * RF <= a.batch && col0 + NTILE <= a.out;
@@ -407,7 +562,7 @@ __global__ __launch_bounds__(kThreads) void layer_kernel(LayerArgs a) {
                 for (int q = 0; q < 16; ++q) {
                     const int64_t row = row0 + rf * 32 + 8 * (q / 4) + 4 * h + (q % 4);
                     if (full || (row < a.batch && col < a.out))
-                        Tr<T>::store(y + row * a.out + col, acc[rf][nf][q]);
+                        Tr<T>::store(y + row * a.out + col, 2.0f * acc[rf][nf][q]);
                 }
             }
         }
@@ -417,7 +572,10 @@ __global__ __launch_bounds__(kThreads) void layer_kernel(LayerArgs a) {
         // barrier), then every thread sums WK partials of some elements and
         // stores them row-major (coalesced).
         constexpr int TILE = 32 * RF * NTILE;  // floats per wave
-        float* red = reinterpret_cast<float*>(lds);
+        auto red = [&](int w) -> float* {
+            return reinterpret_cast<float*>(w == 0 ? lds0 : w == 1 ? lds1 : w == 2 ? lds2 : lds3);
+        };
+        float* mine = red(wave);
 #pragma unroll
         for (int rf = 0; rf < RF; ++rf)
 #pragma unroll
@@ -425,7 +583,7 @@ __global__ __launch_bounds__(kThreads) void layer_kernel(LayerArgs a) {
 #pragma unroll
                 for (int q = 0; q < 16; ++q) {
                     const int rl = rf * 32 + 8 * (q / 4) + 4 * h + (q % 4);
-                    red[wave * TILE + rl * NTILE + nf * 32 + r] = acc[rf][nf][q];
+                    mine[rl * NTILE + nf * 32 + r] = acc[rf][nf][q];
                 }
         __syncthreads();
         const int64_t bm0 = (int64_t)blockIdx.x * BM;
@@ -436,10 +594,10 @@ __global__ __launch_bounds__(kThreads) void layer_kernel(LayerArgs a) {
             const int cl = rem % NTILE;
             float sum = 0.0f;
 #pragma unroll
-            for (int w = 0; w < WK; ++w) sum += red[(g + WM * w) * TILE + rem];
+            for (int w = 0; w < WK; ++w) sum += red(g + WM * w)[rem];
             const int64_t row = bm0 + g * 32 * RF + rl;
             const int col = col0 + cl;
-            if (row < a.batch && col < a.out) Tr<T>::store(y + row * a.out + col, sum);
+            if (row < a.batch && col < a.out) Tr<T>::store(y + row * a.out + col, 2.0f * sum);
         }
     }
 }
@@ -448,9 +606,8 @@ template <typename T, int RF, int NF, int WK>
 hipError_t launch_cfg(const LayerGeom& g, LayerArgs a, hipStream_t s) {
     constexpr int WM = 4 / WK;
     constexpr int BM = 32 * RF * WM;
-    constexpr int BLKB = 2 * 32 * NF * Tr<T>::KJ * (int)sizeof(T);
-    constexpr int KB = (32768 / BLKB) < 8 ? (32768 / BLKB) : 8;
-    a.nchunks = (a.nblk + KB - 1) / KB;
+    a.nblk_pad = g.nblk_pad;
+    a.nchunks = g.nblk_pad / g.kb;
     const dim3 grid((unsigned)((a.batch + BM - 1) / BM), (unsigned)g.ntiles);
     hipLaunchKernelGGL((layer_kernel<T, RF, NF, WK>), grid, dim3(kThreads), 0, s, a);
     return hipGetLastError();
@@ -505,10 +662,14 @@ bool layer_geom(int nb, bool bf16, int in, int out, LayerGeom* g) {
     while (nf < nfmax && nf < need) nf *= 2;
     g->nf = nf;
     g->ntiles = (out + 32 * nf - 1) / (32 * nf);
-    const int64_t blk_bytes = 2LL * 32 * nf * g->kj * (bf16 ? 2 : 4);  // [h][n][kj]
-    if (nblk > 0x7fffffffLL / 8 || g->ntiles > 65535) return false;
+    const int64_t blk_bytes = layer_block_bytes(bf16, nf);
+    const int kb = layer_chunk_blocks(bf16, nf);
+    const int64_t nblk_pad = (nblk + kb - 1) / kb * kb;
+    if (nblk_pad > 0x7fffffffLL / 8 || g->ntiles > 65535) return false;
     g->nblk = (int)nblk;
-    g->packed_bytes = (size_t)g->ntiles * (size_t)nblk * (size_t)blk_bytes;
+    g->nblk_pad = (int)nblk_pad;
+    g->kb = kb;
+    g->packed_bytes = (size_t)g->ntiles * (size_t)nblk_pad * (size_t)blk_bytes;
     return true;
 }
 
@@ -523,18 +684,18 @@ LayerCfg plan_layer(const LayerGeom& g, bool bf16, int64_t batch) {
         const int64_t bm = 32LL * c.rf * (4 / c.wk);
         return ((batch + bm - 1) / bm) * g.ntiles;
     };
-    // bf16 with the widest tile: 64 rows per wave (one wave per SIMD, 256
-    // accumulator registers) halves the LDS traffic per MFMA; one workgroup per
-    // CU is enough.  Otherwise one 32-row tile per wave, two workgroups per CU
-    // wanted, and the K split inside the workgroup when rows run out.
-    if (bf16 && g.nf == 8) {
-        LayerCfg c{2, 1};
-        if (wgs(c) >= 256) return c;
-        return LayerCfg{1, 1};
-    }
-    const LayerCfg cands[] = {{1, 1}, {1, 2}, {1, 4}};
+    // bf16 with 256-column tiles: 32-row waves (two per SIMD, accumulators in
+    // 128 registers) overlap one wave's basis VALU work with the other's MFMAs;
+    // 64-row waves (256 accumulator registers) run one wave per SIMD, which
+    // measured slower on MI355X.
+    if (bf16 && g.nf == 8) return LayerCfg{1, 1};
+    // Otherwise the tallest workgroup (fewest re-reads of the weights) that
+    // still gives at least `want` workgroups; the basis-generation-bound
+    // narrow bf16 layers want more, smaller workgroups.
+    const int64_t want = (bf16 && g.nf == 1) ? 1024 : 512;
+    const LayerCfg cands[] = {{2, 1}, {1, 1}, {1, 2}, {1, 4}};
     for (const LayerCfg& c : cands)
-        if (wgs(c) >= 512) return c;
+        if (layer_cfg_valid(g, c) && wgs(c) >= want) return c;
     return LayerCfg{1, 4};
 }
 
@@ -553,17 +714,17 @@ bool parse_layer_cfg_override(const LayerGeom& g, LayerCfg* c) {
 hipError_t launch_pack(bool bf16, const LayerGeom& g, int in, int out, const void* coef,
                        const void* base_w, void* packed, hipStream_t s) {
     const int ntile = 32 * g.nf;
-    const int64_t units = (int64_t)g.ntiles * g.nblk * 2 * ntile;
+    const int64_t units = (int64_t)g.ntiles * g.nblk_pad * 2 * ntile;
     const unsigned blocks = (unsigned)((units + kThreads - 1) / kThreads);
     if (bf16)
         hipLaunchKernelGGL(pack_kernel<uint16_t>, dim3(blocks), dim3(kThreads), 0, s,
                            static_cast<const uint16_t*>(coef),
                            static_cast<const uint16_t*>(base_w), static_cast<uint16_t*>(packed),
-                           in, out, g.nb, g.nsb, g.npairs, ntile, units);
+                           in, out, g.nb, g.nsb, g.nblk_pad, ntile, units);
     else
         hipLaunchKernelGGL(pack_kernel<float>, dim3(blocks), dim3(kThreads), 0, s,
                            static_cast<const float*>(coef), static_cast<const float*>(base_w),
-                           static_cast<float*>(packed), in, out, g.nb, g.nsb, g.npairs, ntile,
+                           static_cast<float*>(packed), in, out, g.nb, g.nsb, g.nblk_pad, ntile,
                            units);
     return hipGetLastError();
 }

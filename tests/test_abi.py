@@ -113,7 +113,8 @@ def test_layer_argument_checks():
 def _expected_packed_bytes(G, bf16, n_in, n_out):
     """Size of the packed weights: per tile of 32 * nf output columns, per pair of
     features, per block of kj columns, kj weights for each of 2 * 32 * nf
-    (feature, column) slots."""
+    (feature, column) slots; the blocks of a tile are padded to whole chunks of
+    min(8, 16 KiB / block bytes) blocks."""
     kj, es, nfmax = (8, 2, 8) if bf16 else (2, 4, 4)
     nsb = -(-(G + 4) // kj)
     npairs = -(-n_in // 2)
@@ -121,7 +122,10 @@ def _expected_packed_bytes(G, bf16, n_in, n_out):
     while nf < nfmax and 32 * nf < n_out:
         nf *= 2
     ntiles = -(-n_out // (32 * nf))
-    return ntiles * npairs * nsb * 2 * 32 * nf * kj * es
+    blk_bytes = 2 * 32 * nf * kj * es
+    kb = min(8, 16384 // blk_bytes)
+    nblk_pad = -(-(npairs * nsb) // kb) * kb
+    return ntiles * nblk_pad * blk_bytes
 
 
 @pytest.mark.parametrize("G,n_in,n_out", [(10, 784, 256), (10, 256, 10), (5, 2, 5), (200, 128, 128),
