@@ -75,17 +75,18 @@ struct LayerGeom {
 // Returns false when the sizes do not fit the index types of the kernels.
 bool layer_geom(int nb, bool bf16, int in, int out, LayerGeom* g);
 
-// Workgroup shape of the fused kernel: 4 waves, each holding rf 32-row MFMA
+// Workgroup shape of the fused kernel: nw waves, each holding rf 32-row MFMA
 // tiles of all nf column fragments; wk waves split the blocks (K) of a chunk
-// and are summed through LDS at the end, the other 4 / wk waves take
+// and are summed through LDS at the end, the other nw / wk waves take
 // different rows.
 struct LayerCfg {
     int rf;  // 1 or 2
     int wk;  // 1, 2 or 4; wk > 1 needs rf * nf <= 4
+    int nw;  // waves per workgroup: 4, or 8 (rf = 1, wk = 1 only)
 };
 
 LayerCfg plan_layer(const LayerGeom& g, bool bf16, int64_t batch);
-// KAN_LAYER_CFG="rf,wk" forces a configuration (testing and tuning); ignored
+// KAN_LAYER_CFG="rf,wk[,nw]" forces a configuration (testing and tuning); ignored
 // when malformed or not valid for the geometry.
 bool parse_layer_cfg_override(const LayerGeom& g, LayerCfg* c);
 bool layer_cfg_valid(const LayerGeom& g, const LayerCfg& c);

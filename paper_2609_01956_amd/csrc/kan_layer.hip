@@ -216,26 +216,28 @@ struct Occ {
     static constexpr int waves = RF * NF * 16 <= 128 ? 2 : 1;
 };
 
-template <typename T, int RF, int NF, int WK>
-__global__ __launch_bounds__(kThreads)
+template <typename T, int RF, int NF, int WK, int NW>
+__global__ __launch_bounds__(64 * NW)
 __attribute__((amdgpu_waves_per_eu(Occ<RF, NF>::waves)))
 void layer_kernel(LayerArgs a) {
     constexpr bool BF16 = sizeof(T) == 2;
     constexpr int KJ = Tr<T>::KJ;
-    constexpr int WM = 4 / WK;
+    constexpr int NT = 64 * NW;                  // threads per workgroup
+    constexpr int WM = NW / WK;
     constexpr int NTILE = 32 * NF;
     constexpr int LANEB = KJ * (int)sizeof(T);  // B bytes per lane per block (16 / 8)
     constexpr int BLKB = layer_block_bytes(BF16, NF);  // bytes per block: [h][n][KJ]
     constexpr int KB = layer_chunk_blocks(BF16, NF);   // blocks per chunk
     constexpr int CHB = KB * BLKB;               // bytes per chunk
     constexpr int S = kLayerStages;              // chunks in LDS / in flight
-    constexpr int DPW = CHB / 4096;              // 1 KB loads per wave per chunk
+    constexpr int DPW = CHB / (1024 * NW);       // 1 KB loads per wave per chunk
     constexpr int KBW = KB / WK;                 // blocks per wave per chunk
     constexpr int NX = KBW * RF;                 // x loads per lane per chunk
     constexpr int BM = 32 * RF * WM;             // rows per workgroup
     constexpr int PART = WK > 1 ? 32 * RF * NTILE * 4 : 0;  // one wave's partial sums
     constexpr int STB = CHB > PART ? CHB : PART;            // bytes per stage array
-    static_assert(CHB % 4096 == 0 && KB % WK == 0 && KB >= WK, "chunk shape");
+    static_assert(CHB % (1024 * NW) == 0 && KB % WK == 0 && KB >= WK, "chunk shape");
+    static_assert(NW == 4 || (NW == 8 && WK == 1), "waves per workgroup");
     static_assert(S == 4 && 4 * STB <= 65536, "LDS budget");
     static_assert(BLKB == 2 * NTILE * LANEB, "block layout");
     static_assert(DPW + (S - 3) * (NX + DPW) <= 63, "vmcnt range");
@@ -288,8 +290,8 @@ void layer_kernel(LayerArgs a) {
     const int last_pair_odd = (a.in & 1) ? a.in / 2 : -1;
 
     // ---- weights: chunk c -> LDS stage c % S by direct global-to-LDS loads.
-    // Wave w, load i moves bytes [i 4096 + w 1024, + 1024) of the chunk, 16 per
-    // lane, to the same offsets of the stage.  Chunks past the last re-load
+    // Wave w, load i moves bytes [i 1024 NW + w 1024, + 1024) of the chunk, 16
+    // per lane, to the same offsets of the stage.  Chunks past the last re-load
     // the last chunk (into a stage no real chunk uses any more).
     const uint32_t dma_lane = (uint32_t)(wave * 1024 + lane * 16);
     auto dma = [&](int c, auto kk) {  // kk: c % S as a compile-time constant
@@ -298,8 +300,8 @@ void layer_kernel(LayerArgs a) {
         u32x4* l = stage(kk) + wave * 64;
 #pragma unroll
         for (int i = 0; i < DPW; ++i)
-            __builtin_amdgcn_global_load_lds(g + (dma_lane + (uint32_t)(i * 4096)), l + i * 256,
-                                             16, 0, 0);
+            __builtin_amdgcn_global_load_lds(g + (dma_lane + (uint32_t)(i * 1024 * NW)),
+                                             l + i * 64 * NW, 16, 0, 0);
     };
 
     // x of this lane's rows for the feature of its half in pair p.pair; the
@@ -376,6 +378,11 @@ void layer_kernel(LayerArgs a) {
     // block's B (PREF: block bi_n of stage st).  After MFMA i come the VALU
     // ops of A elements [i NE / NMFMA, (i + 1) NE / NMFMA).
     constexpr int NE = RF * KJ;  // A elements generated per lane per block
+#ifdef KAN_SCHED_INTERLEAVE
+    constexpr bool SCHED_PINGPONG = false;
+#else
+    constexpr bool SCHED_PINGPONG = Occ<RF, NF>::waves == 2;
+#endif
     auto step = [&](const AFrag<T, RF>& A, const BFrag& B, const Pos& pg,
                     const float (&xv)[RF], const float (&slv)[RF], AFrag<T, RF>& An,
                     auto pref_tag, BFrag& Bn, const u32x4* st, int bi_n) {
@@ -387,28 +394,47 @@ void layer_kernel(LayerArgs a) {
         // (xv: x values of block pg, already converted)
         const bool first = pg.bsub == 0;
         float v[RF][KJ];
-#pragma unroll
-        for (int i = 0; i < NMFMA; ++i) {
-            do_mfma(i, A, B);
-            if constexpr (PREF) {
-                if (i == 0) read_b(Bn, st, bi_n);
-            }
-#pragma unroll
-            for (int k = i * NE / NMFMA; k < (i + 1) * NE / NMFMA; ++k) {
-                const int rf = k / KJ;
-                const int e = k % KJ;
-                const float bv = half_basis(s[rf] - (float)e);
-                v[rf][e] = (e == 0 && first) ? slv[rf] : bv;
-                if constexpr (BF16) {
-                    if (e & 1) {
-                        An.a[rf][e - 1] = (__bf16)v[rf][e - 1];
-                        An.a[rf][e] = (__bf16)v[rf][e];
-                    }
-                } else {
-                    An.a[rf][e] = v[rf][e];
+        auto gen_elem = [&](int k) {
+            const int rf = k / KJ;
+            const int e = k % KJ;
+            const float bv = half_basis(s[rf] - (float)e);
+            v[rf][e] = (e == 0 && first) ? slv[rf] : bv;
+            if constexpr (BF16) {
+                if (e & 1) {
+                    An.a[rf][e - 1] = (__bf16)v[rf][e - 1];
+                    An.a[rf][e] = (__bf16)v[rf][e];
                 }
+            } else {
+                An.a[rf][e] = v[rf][e];
             }
+        };
+        if constexpr (SCHED_PINGPONG) {
+            // Two waves per SIMD: the whole basis generation (VALU), then the
+            // MFMAs back to back at raised priority.  While one wave runs its
+            // VALU phase the other's MFMA phase keeps the matrix core busy,
+            // and the priority makes the MFMA phase win when both want to
+            // issue.
+#pragma unroll
+            for (int k = 0; k < NE; ++k) gen_elem(k);
             __builtin_amdgcn_sched_barrier(0);
+            __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+            for (int i = 0; i < NMFMA; ++i) do_mfma(i, A, B);
+            __builtin_amdgcn_s_setprio(0);
+            __builtin_amdgcn_sched_barrier(0);
+        } else {
+            // One wave per SIMD: after MFMA i come the VALU ops of elements
+            // [i NE / NMFMA, (i + 1) NE / NMFMA).
+#pragma unroll
+            for (int i = 0; i < NMFMA; ++i) {
+                do_mfma(i, A, B);
+                if constexpr (PREF) {
+                    if (i == 0) read_b(Bn, st, bi_n);
+                }
+#pragma unroll
+                for (int k = i * NE / NMFMA; k < (i + 1) * NE / NMFMA; ++k) gen_elem(k);
+                __builtin_amdgcn_sched_barrier(0);
+            }
         }
     };
 
@@ -587,7 +613,7 @@ void layer_kernel(LayerArgs a) {
                 }
         __syncthreads();
         const int64_t bm0 = (int64_t)blockIdx.x * BM;
-        for (int idx = tid; idx < WM * TILE; idx += kThreads) {
+        for (int idx = tid; idx < WM * TILE; idx += NT) {
             const int g = idx / TILE;
             const int rem = idx % TILE;
             const int rl = rem / NTILE;
@@ -602,19 +628,25 @@ void layer_kernel(LayerArgs a) {
     }
 }
 
-template <typename T, int RF, int NF, int WK>
+template <typename T, int RF, int NF, int WK, int NW = 4>
 hipError_t launch_cfg(const LayerGeom& g, LayerArgs a, hipStream_t s) {
-    constexpr int WM = 4 / WK;
+    constexpr int WM = NW / WK;
     constexpr int BM = 32 * RF * WM;
     a.nblk_pad = g.nblk_pad;
     a.nchunks = g.nblk_pad / g.kb;
     const dim3 grid((unsigned)((a.batch + BM - 1) / BM), (unsigned)g.ntiles);
-    hipLaunchKernelGGL((layer_kernel<T, RF, NF, WK>), grid, dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL((layer_kernel<T, RF, NF, WK, NW>), grid, dim3(64 * NW), 0, s, a);
     return hipGetLastError();
 }
 
 template <typename T, int NF>
 hipError_t launch_nf(const LayerGeom& g, const LayerCfg& c, const LayerArgs& a, hipStream_t s) {
+    if (c.nw == 8) {
+        // eight waves: one 32-row tile each (chunks of at least 8 KB)
+        if constexpr (layer_chunk_blocks(sizeof(T) == 2, NF) * layer_block_bytes(sizeof(T) == 2, NF) >= 8192)
+            if (c.rf == 1 && c.wk == 1) return launch_cfg<T, 1, NF, 1, 8>(g, a, s);
+        return hipErrorInvalidValue;
+    }
     if (c.wk == 1) {
         if (c.rf == 1) return launch_cfg<T, 1, NF, 1>(g, a, s);
         if (c.rf == 2) return launch_cfg<T, 2, NF, 1>(g, a, s);
@@ -676,34 +708,38 @@ bool layer_geom(int nb, bool bf16, int in, int out, LayerGeom* g) {
 bool layer_cfg_valid(const LayerGeom& g, const LayerCfg& c) {
     if (c.rf != 1 && c.rf != 2) return false;
     if (c.wk != 1 && c.wk != 2 && c.wk != 4) return false;
+    if (c.nw == 8)  // eight 32-row waves, no K split, chunks of at least 8 KB
+        return c.rf == 1 && c.wk == 1 && g.kb * 2 * 32 * g.nf * g.kj * (g.kj == 8 ? 2 : 4) >= 8192;
+    if (c.nw != 4) return false;
     return c.wk == 1 || c.rf * g.nf <= 4;
 }
 
 LayerCfg plan_layer(const LayerGeom& g, bool bf16, int64_t batch) {
     auto wgs = [&](const LayerCfg& c) {
-        const int64_t bm = 32LL * c.rf * (4 / c.wk);
+        const int64_t bm = 32LL * c.rf * (c.nw / c.wk);
         return ((batch + bm - 1) / bm) * g.ntiles;
     };
     // bf16 with 256-column tiles: 32-row waves (two per SIMD, accumulators in
     // 128 registers) overlap one wave's basis VALU work with the other's MFMAs;
     // 64-row waves (256 accumulator registers) run one wave per SIMD, which
     // measured slower on MI355X.
-    if (bf16 && g.nf == 8) return LayerCfg{1, 1};
+    if (bf16 && g.nf == 8) return LayerCfg{1, 1, 4};
     // Otherwise the tallest workgroup (fewest re-reads of the weights) that
     // still gives at least `want` workgroups; the basis-generation-bound
     // narrow bf16 layers want more, smaller workgroups.
     const int64_t want = (bf16 && g.nf == 1) ? 1024 : 512;
-    const LayerCfg cands[] = {{2, 1}, {1, 1}, {1, 2}, {1, 4}};
+    const LayerCfg cands[] = {{2, 1, 4}, {1, 1, 4}, {1, 2, 4}, {1, 4, 4}};
     for (const LayerCfg& c : cands)
         if (layer_cfg_valid(g, c) && wgs(c) >= want) return c;
-    return LayerCfg{1, 4};
+    return LayerCfg{1, 4, 4};
 }
 
 bool parse_layer_cfg_override(const LayerGeom& g, LayerCfg* c) {
     const char* s = std::getenv("KAN_LAYER_CFG");
     if (!s || !*s) return false;
-    LayerCfg t{0, 0};
-    if (std::sscanf(s, "%d,%d", &t.rf, &t.wk) != 2) return false;
+    LayerCfg t{0, 0, 4};
+    const int n = std::sscanf(s, "%d,%d,%d", &t.rf, &t.wk, &t.nw);
+    if (n != 2 && n != 3) return false;
     if (!layer_cfg_valid(g, t)) return false;
     *c = t;
     return true;
