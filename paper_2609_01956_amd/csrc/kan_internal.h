@@ -46,11 +46,9 @@ hipError_t launch_basis_bf16(const uint16_t* x, int64_t n, uint16_t* phi, const 
 // wave reads one block's B operand for 32 columns with one conflict-free 16-
 // or 8-byte LDS load per lane, and a workgroup stages consecutive blocks with
 // plain contiguous copies.
-// Pipeline shape of the fused kernel (shared by the host planner and the
-// kernel): weights move global -> LDS in chunks of whole blocks by direct
-// global-to-LDS loads, kLayerStages chunks in flight.  A chunk is up to 16 KB
-// (at most 8 blocks) and a multiple of 4 KB (one 16-byte load per thread).
-constexpr int kLayerStages = 4;
+// Weights move global -> registers -> LDS in chunks of whole blocks: a chunk
+// is up to 16 KB (at most 8 blocks) and a multiple of 4 KB (one 16-byte load
+// per thread of a 256-thread workgroup).
 __host__ __device__ constexpr int layer_block_bytes(bool bf16, int nf) {
     return 2 * 32 * nf * (bf16 ? 8 * 2 : 2 * 4);  // [h][n][kj] elements
 }

@@ -11,14 +11,18 @@
 // Two kernels:
 //   pack_kernel    rearranges coef / base_w into the block order described in
 //                  kan_internal.h (a few MB, read once per call);
-//   layer_kernel   4 waves per workgroup.  The workgroup walks the blocks in
-//                  chunks of 32 KB of packed weights, double-buffered in LDS
-//                  (global loads of chunk c + 1 are in flight while chunk c is
-//                  multiplied).  Each wave owns rf 32-row tiles of all nf
-//                  32-column fragments of the N tile, so every generated A
-//                  element feeds nf MFMAs and every B fragment read from LDS
-//                  feeds rf MFMAs.  A is generated one block ahead of the MFMAs
-//                  that consume it, so VALU work and matrix work interleave.
+//   layer_kernel   4 or 8 waves per workgroup.  The workgroup walks the blocks
+//                  in chunks of up to 16 KB of packed weights: each chunk is
+//                  loaded into registers a few chunks ahead, written to one of
+//                  two LDS stages while the previous chunk is multiplied, and
+//                  read from LDS by every wave.  Each wave owns rf 32-row
+//                  tiles of all nf 32-column fragments of the N tile, so every
+//                  generated A element feeds nf MFMAs and every B fragment read
+//                  from LDS feeds rf MFMAs.  With two waves per SIMD a wave
+//                  generates the next block's A and then issues the current
+//                  block's MFMAs, so one wave's VALU work overlaps the other's
+//                  matrix work; with one wave per SIMD the two interleave
+//                  within the wave.
 //
 // Basis values.  With v = u - 2 (u the coordinate of eq. truncated), the clamp
 // of eq. bounded and the symmetry of the stencil {1, -4, 6, -4, 1} give
@@ -229,33 +233,24 @@ void layer_kernel(LayerArgs a) {
     constexpr int BLKB = layer_block_bytes(BF16, NF);  // bytes per block: [h][n][KJ]
     constexpr int KB = layer_chunk_blocks(BF16, NF);   // blocks per chunk
     constexpr int CHB = KB * BLKB;               // bytes per chunk
-    constexpr int S = kLayerStages;              // chunks in LDS / in flight
-    constexpr int DPW = CHB / (1024 * NW);       // 1 KB loads per wave per chunk
+    constexpr int DPW = CHB / (1024 * NW);       // 16-byte loads per lane per chunk
     constexpr int KBW = KB / WK;                 // blocks per wave per chunk
     constexpr int NX = KBW * RF;                 // x loads per lane per chunk
     constexpr int BM = 32 * RF * WM;             // rows per workgroup
+    // Weights of chunk c are loaded into registers L chunks ahead (register
+    // set c % L), written to LDS stage c % 2 while chunk c - 1 is multiplied,
+    // and read from there during chunk c.
+    constexpr int L = DPW <= 2 ? 3 : 2;
+    constexpr int U = L % 2 == 0 ? L : 2 * L;    // chunk-loop unroll, lcm(2, L)
     constexpr int PART = WK > 1 ? 32 * RF * NTILE * 4 : 0;  // one wave's partial sums
-    constexpr int STB = CHB > PART ? CHB : PART;            // bytes per stage array
+    constexpr int SMEM = 2 * CHB > NW * PART ? 2 * CHB : NW * PART;
     static_assert(CHB % (1024 * NW) == 0 && KB % WK == 0 && KB >= WK, "chunk shape");
     static_assert(NW == 4 || (NW == 8 && WK == 1), "waves per workgroup");
-    static_assert(S == 4 && 4 * STB <= 65536, "LDS budget");
+    static_assert(SMEM <= 64 * 1024, "LDS budget");
     static_assert(BLKB == 2 * NTILE * LANEB, "block layout");
-    static_assert(DPW + (S - 3) * (NX + DPW) <= 63, "vmcnt range");
-    // One array per stage: the LDS reads of stage K and the direct loads into
-    // stage K + S - 1 then touch different objects, so the compiler does not
-    // make the reads wait for the loads in flight.  After the main loop the
-    // arrays hold the K-split partial sums, one wave per array.
-    __shared__ u32x4 lds0[STB / 16];
-    __shared__ u32x4 lds1[STB / 16];
-    __shared__ u32x4 lds2[STB / 16];
-    __shared__ u32x4 lds3[STB / 16];
-    auto stage = [&](auto kk) -> u32x4* {
-        constexpr int k = decltype(kk)::value % S;
-        if constexpr (k == 0) return lds0;
-        else if constexpr (k == 1) return lds1;
-        else if constexpr (k == 2) return lds2;
-        else return lds3;
-    };
+    // LDS: two chunk stages; after the main loop the K-split partial sums.
+    __shared__ u32x4 smem[SMEM / 16];
+    auto stage = [&](auto kk) -> u32x4* { return smem + (decltype(kk)::value % 2) * (CHB / 16); };
 
     const T* __restrict__ x = static_cast<const T*>(a.x);
     T* __restrict__ y = static_cast<T*>(a.y);
@@ -289,48 +284,46 @@ void layer_kernel(LayerArgs a) {
     // (zero weights): its lanes read the real last feature and use x = 0.
     const int last_pair_odd = (a.in & 1) ? a.in / 2 : -1;
 
-    // ---- weights: chunk c -> LDS stage c % S by direct global-to-LDS loads.
-    // Wave w, load i moves bytes [i 1024 NW + w 1024, + 1024) of the chunk, 16
-    // per lane, to the same offsets of the stage.  Chunks past the last re-load
-    // the last chunk (into a stage no real chunk uses any more).
-    const uint32_t dma_lane = (uint32_t)(wave * 1024 + lane * 16);
-    auto dma = [&](int c, auto kk) {  // kk: c % S as a compile-time constant
+    // ---- loads of chunk c into register set j, for the wave's blocks from
+    // position p on: first the x of each block and row tile (per lane: the
+    // lane's row, the feature of its half in the block's pair; positions past
+    // the end read the last pair, the phantom lanes step back one feature),
+    // then the weights (wave w, load i holds bytes [i 1024 NW + w 1024,
+    // + 1024) of the chunk, 16 per lane).  Chunks past the last re-load the
+    // last chunk.  Raw x bits are kept: conversion and masking happen where
+    // the values are used, so nothing waits for a load when it is issued.
+    typedef uint32_t XSet[KBW][RF];
+    typedef u32x4 WSet[DPW];
+    const uint32_t wlane = (uint32_t)(wave * 1024 + lane * 16);
+    auto issue = [&](int c, Pos p, XSet& xs, WSet& ws) {
+#pragma unroll
+        for (int t = 0; t < KBW; ++t) {
+            const int pr = p.pair < a.npairs ? p.pair : a.npairs - 1;
+            const uint32_t back = (pr == last_pair_odd) ? (uint32_t)h : 0u;
+#pragma unroll
+            for (int rf = 0; rf < RF; ++rf)
+                xs[t][rf] = Tr<T>::raw(xw + (xoff[rf] + (uint32_t)(2 * pr) - back));
+            p = advance<WK>(p, a.nsb);
+        }
         const int cc = c < a.nchunks ? c : a.nchunks - 1;
         const char* g = wpt + (size_t)cc * CHB;  // wave-uniform
-        u32x4* l = stage(kk) + wave * 64;
 #pragma unroll
         for (int i = 0; i < DPW; ++i)
-            __builtin_amdgcn_global_load_lds(g + (dma_lane + (uint32_t)(i * 1024 * NW)),
-                                             l + i * 64 * NW, 16, 0, 0);
+            ws[i] = *reinterpret_cast<const u32x4*>(g + (wlane + (uint32_t)(i * 1024 * NW)));
     };
-
-    // x of this lane's rows for the feature of its half in pair p.pair; the
-    // phantom feature of an odd feature count (and positions past the end)
-    // give 0.
-    // The raw bits are kept (conversion and masking happen where the values
-    // are used, so the load is not waited for when it is issued).
-    auto load_x = [&](const Pos& p, uint32_t (&xv)[RF]) {
-        // positions past the end read the last pair (their blocks multiply
-        // zeros); the phantom lanes step back one feature
-        const int pr = p.pair < a.npairs ? p.pair : a.npairs - 1;
-        const uint32_t back = (pr == last_pair_odd) ? (uint32_t)h : 0u;
+    // Register set -> LDS stage kk (the same byte offsets as in the chunk).
+    auto store = [&](auto kk, const WSet& ws) {
+        char* l = reinterpret_cast<char*>(stage(kk));
 #pragma unroll
-        for (int rf = 0; rf < RF; ++rf)
-            xv[rf] = Tr<T>::raw(xw + (xoff[rf] + (uint32_t)(2 * pr) - back));
+        for (int i = 0; i < DPW; ++i)
+            *reinterpret_cast<u32x4*>(l + wlane + i * 1024 * NW) = ws[i];
     };
-    // Value of raw x bits for the lane's feature at position p.
+    // Value of raw x bits for the lane's feature at position p (the phantom
+    // feature of an odd feature count gives 0).
     auto x_value = [&](const Pos& p, uint32_t raw) {
         const float v = Tr<T>::value(raw);
         if (p.pair == last_pair_odd) return h ? 0.0f : v;
         return v;
-    };
-    // x of the KBW blocks of a chunk for this wave, starting at position p.
-    auto load_chunk_x = [&](Pos p, uint32_t (&xv)[KBW][RF]) {
-#pragma unroll
-        for (int t = 0; t < KBW; ++t) {
-            load_x(p, xv[t]);
-            p = advance<WK>(p, a.nsb);
-        }
     };
 
     floatx16 acc[RF][NF];
@@ -378,11 +371,7 @@ void layer_kernel(LayerArgs a) {
     // block's B (PREF: block bi_n of stage st).  After MFMA i come the VALU
     // ops of A elements [i NE / NMFMA, (i + 1) NE / NMFMA).
     constexpr int NE = RF * KJ;  // A elements generated per lane per block
-#ifdef KAN_SCHED_INTERLEAVE
-    constexpr bool SCHED_PINGPONG = false;
-#else
     constexpr bool SCHED_PINGPONG = Occ<RF, NF>::waves == 2;
-#endif
     auto step = [&](const AFrag<T, RF>& A, const BFrag& B, const Pos& pg,
                     const float (&xv)[RF], const float (&slv)[RF], AFrag<T, RF>& An,
                     auto pref_tag, BFrag& Bn, const u32x4* st, int bi_n) {
@@ -438,54 +427,126 @@ void layer_kernel(LayerArgs a) {
         }
     };
 
+    // bf16 with two waves per SIMD: the A of a block is generated by code
+    // chosen by the block's place in its feature pair (uniform branches).
+    //   first block:  x, the coordinate and the SiLU value (element 0), then
+    //                 basis values 1 .. 7;
+    //   middle block: the coordinate steps down by 8 (one wave visits the
+    //                 blocks of a pair in order when WK = 1; with WK > 1 it is
+    //                 recomputed from x), then 8 basis values;
+    //   last block:   as a middle block, but only the real columns of the
+    //                 feature (rounded up to even) are evaluated and the
+    //                 padding columns are set to 0.
+    // Stepping the coordinate by 8 is exact wherever a basis value of the
+    // block is nonzero (there |s| < 17 and s - 8 is computed exactly).
+    constexpr bool GEN_SPLIT = BF16 && Occ<RF, NF>::waves == 2;
+    constexpr bool DIRECT = WK > 1;
+    float sc[RF];  // coordinate of the wave's current block (element 0)
+    // real columns in the last block of a feature, rounded up to even
+    const int last_cols = a.nb + 1 - KJ * (a.nsb - 1);
+    const int last_even = (last_cols + 1) & ~1;
+    auto gen_split = [&](const Pos& pg, const uint32_t (&xr)[RF], AFrag<T, RF>& An) {
+      if constexpr (GEN_SPLIT) {
+        auto basis = [&](int rf, int e0, int e1) {
+#pragma unroll
+            for (int e = e0; e < e1; ++e) An.a[rf][e] = (__bf16)half_basis(sc[rf] - (float)e);
+        };
+        auto zero = [&](int rf, int e0) {
+#pragma unroll
+            for (int e = e0; e < KJ; ++e) An.a[rf][e] = (__bf16)0.0f;
+        };
+        if (pg.bsub == 0) {
+#pragma unroll
+            for (int rf = 0; rf < RF; ++rf) {
+                const float xv = x_value(pg, xr[rf]);
+                sc[rf] = __builtin_fmaf(xv, a.inv_h, a.a_int + 1.0f) + a.a_frac;
+                An.a[rf][0] = (__bf16)half_silu(xv);
+                basis(rf, 1, KJ);
+            }
+            return;
+        }
+        if constexpr (DIRECT) {
+            const float c = a.a_int + 1.0f - (float)(KJ * pg.bsub);
+#pragma unroll
+            for (int rf = 0; rf < RF; ++rf)
+                sc[rf] = __builtin_fmaf(x_value(pg, xr[rf]), a.inv_h, c) + a.a_frac;
+        } else {
+#pragma unroll
+            for (int rf = 0; rf < RF; ++rf) sc[rf] -= (float)KJ;
+        }
+        if (pg.bsub != a.nsb - 1 || last_even == KJ) {
+#pragma unroll
+            for (int rf = 0; rf < RF; ++rf) basis(rf, 0, KJ);
+        } else if (last_even == 6) {
+#pragma unroll
+            for (int rf = 0; rf < RF; ++rf) { basis(rf, 0, 6); zero(rf, 6); }
+        } else if (last_even == 4) {
+#pragma unroll
+            for (int rf = 0; rf < RF; ++rf) { basis(rf, 0, 4); zero(rf, 4); }
+        } else {
+#pragma unroll
+            for (int rf = 0; rf < RF; ++rf) { basis(rf, 0, 2); zero(rf, 2); }
+        }
+      }
+    };
+    // Phase-ordered step with split generation: the next block's A, then the
+    // MFMAs of the current block back to back at raised priority (while one
+    // wave generates, the other's MFMAs keep the matrix core busy).
+    auto step_split = [&](const AFrag<T, RF>& A, const BFrag& B, const Pos& pg,
+                          const uint32_t (&xr)[RF], AFrag<T, RF>& An) {
+        gen_split(pg, xr, An);
+        __builtin_amdgcn_sched_barrier(0);
+        __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+        for (int i = 0; i < NMFMA; ++i) do_mfma(i, A, B);
+        __builtin_amdgcn_s_setprio(0);
+        __builtin_amdgcn_sched_barrier(0);
+    };
+
     auto silu_of = [&](const float (&xv)[RF], float (&sl)[RF]) {
 #pragma unroll
         for (int rf = 0; rf < RF; ++rf) sl[rf] = half_silu(xv[rf]);
     };
 
     // ---- pipeline
-    // Loads are issued in groups, one group per chunk: the x values of the
-    // chunk's blocks for this wave (NX loads) and then its weights (DPW
-    // loads), S - 1 chunks ahead of the chunk being multiplied.  Loads
-    // complete in issue order, so at the top of chunk c waiting until at most
-    // VMW loads are outstanding means this wave's x and weights of chunk c
-    // (and x of chunk c + 1) have arrived; the barrier after it means every
-    // wave's have.  The
-    // chunk loop is unrolled by S so that the S sets of x registers rotate by
-    // name (a register move of a load still in flight would wait for it).
-    // Chunks past the last one (up to S - 1, to fill the unrolled group) load
+    // Chunk c: at its top a barrier (every wave has written chunk c to stage
+    // c % 2 and finished reading chunk c - 1 from the other stage), then the
+    // loads of chunk c + L are issued into register set c % L (free: its
+    // weights went to LDS during chunk c - 1, its x were copied out), the
+    // weights of chunk c + 1 (set (c + 1) % L) are written to stage
+    // (c + 1) % 2, and the chunk's blocks are multiplied.  The chunk loop is
+    // unrolled by U so that stages and register sets are compile-time
+    // choices (a register move of a load still in flight would wait for
+    // it).  Chunks past the last one (to fill the unrolled group) load
     // clamped inputs and multiply zero A.
     static_assert(WK <= 4, "wave block stride");
-    // At the top of chunk c: groups c + 1 .. c + S - 2 may still be in
-    // flight, except the x loads of chunk c + 1 (issued first in their group,
-    // needed at the end of chunk c to generate the next chunk's first block).
-    constexpr int VMW = DPW + (S - 3) * (NX + DPW);
-    constexpr int WAITCNT = (VMW & 0xF) | (0x7 << 4) | (0xF << 8) | (((VMW >> 4) & 0x3) << 14);
+    constexpr int WAIT_LDS = 0xF | (0x7 << 4) | (0x0 << 8) | (0x3 << 14);  // lgkmcnt(0) only
     const int nq = wk < a.nblk ? (a.nblk - wk + WK - 1) / WK : 0;  // real blocks of this wave
 
-    uint32_t xq[S][KBW][RF];
+    XSet xq[L];
+    WSet wq[L];
     float sl[RF];
     AFrag<T, RF> A_cur, A_nxt;
     BFrag bq[2];
     Pos pos_c = advance_n(Pos{0, 0, 0}, wk, a.nsb);  // first block of the current chunk
     Pos pos_l = pos_c;                               // first block of the next chunk to load
 
-    // prologue: groups of chunks 0 .. S - 2
+    // prologue: loads of chunks 0 .. L - 1, chunk 0 to stage 0
     auto prologue = [&](auto jj) {
         constexpr int j = decltype(jj)::value;
-        load_chunk_x(pos_l, xq[j]);
-        __builtin_amdgcn_sched_barrier(0);  // x loads issue before the weight loads
-        dma(j, jj);
-        __builtin_amdgcn_sched_barrier(0);
+        issue(j, pos_l, xq[j], wq[j]);
         pos_l = advance<KB>(pos_l, a.nsb);
     };
-    StaticFor<0, S - 1>::run(prologue);
-    __builtin_amdgcn_s_waitcnt(WAITCNT);
+    StaticFor<0, L>::run(prologue);
+    store(std::integral_constant<int, 0>{}, wq[0]);
+    __builtin_amdgcn_s_waitcnt(WAIT_LDS);
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
 
     // A of the wave's first block (nothing to interleave with yet).
-    {
+    if constexpr (GEN_SPLIT) {
+        gen_split(pos_c, xq[0][0], A_cur);
+    } else {
         float x0[RF];
 #pragma unroll
         for (int rf = 0; rf < RF; ++rf) x0[rf] = x_value(pos_c, xq[0][0][rf]);
@@ -504,23 +565,29 @@ void layer_kernel(LayerArgs a) {
         }
     }
 
-    // Chunk c, whose x is in xq[K] (K = c % S, compile-time); the x of the
-    // next chunk is in xq[(K + 1) % S]; the group loaded at its top goes to
-    // xq[(K + S - 1) % S] (the x of chunk c - 1, no longer needed).
+    // Chunk c with K = c % U (compile-time).
     auto chunk = [&](int c, auto kk, auto last_tag) {
         constexpr int K = decltype(kk)::value;
         constexpr bool LASTG = decltype(last_tag)::value;  // in the final group
-        constexpr int KN = (K + 1) % S;
-        constexpr int KL = (K + S - 1) % S;
-        if (c > 0) {  // (chunk 0's wait and barrier are in the prologue)
-            __builtin_amdgcn_s_waitcnt(WAITCNT);
+        constexpr int J = K % L;          // register set of chunk c (and of c + L)
+        constexpr int JN = (K + 1) % L;   // register set of chunk c + 1
+        if (c > 0) {  // (chunk 0's barrier is in the prologue)
+            __builtin_amdgcn_s_waitcnt(WAIT_LDS);
             __builtin_amdgcn_s_barrier();
             __builtin_amdgcn_sched_barrier(0);
         }
-        load_chunk_x(pos_l, xq[KL]);
-        __builtin_amdgcn_sched_barrier(0);  // x loads issue before the weight loads
-        dma(c + S - 1, std::integral_constant<int, KL>{});
+        // x of the blocks whose A this chunk generates: blocks 1 .. KBW - 1
+        // of this chunk, then block 0 of the next one
+        uint32_t xr[KBW][RF];
+#pragma unroll
+        for (int t = 0; t < KBW; ++t)
+#pragma unroll
+            for (int rf = 0; rf < RF; ++rf) xr[t][rf] = t + 1 < KBW ? xq[J][t + 1][rf] : xq[JN][0][rf];
+        __builtin_amdgcn_sched_barrier(0);
+        issue(c + L, pos_l, xq[J], wq[J]);
         pos_l = advance<KB>(pos_l, a.nsb);
+        __builtin_amdgcn_sched_barrier(0);
+        store(std::integral_constant<int, K + 1>{}, wq[JN]);
         __builtin_amdgcn_sched_barrier(0);
 
         const u32x4* st = stage(kk);
@@ -531,11 +598,12 @@ void layer_kernel(LayerArgs a) {
             // position of the next block: the next step's, or the first block
             // of the next chunk
             const Pos pnext = advance<WK>(p, a.nsb);
-            const uint32_t(&xr)[RF] = t + 1 < KBW ? xq[K][t + 1 < KBW ? t + 1 : 0] : xq[KN][0];
             float xv[RF];
+            if constexpr (!GEN_SPLIT) {
 #pragma unroll
-            for (int rf = 0; rf < RF; ++rf) xv[rf] = x_value(pnext, xr[rf]);
-            if (pnext.bsub == 0) silu_of(xv, sl);
+                for (int rf = 0; rf < RF; ++rf) xv[rf] = x_value(pnext, xr[t][rf]);
+                if (pnext.bsub == 0) silu_of(xv, sl);
+            }
             if constexpr (LASTG) {
                 if (c * KBW + t >= nq) {  // past the wave's last real block: contribute 0
 #pragma unroll
@@ -548,8 +616,11 @@ void layer_kernel(LayerArgs a) {
             // saved.
             constexpr bool PREF = Occ<RF, NF>::waves == 1 && t + 1 < KBW;
             if constexpr (Occ<RF, NF>::waves == 2 && t > 0) read_b(bq[t & 1], st, wk + WK * t);
-            step(A_cur, bq[t & 1], pnext, xv, sl, A_nxt, std::integral_constant<bool, PREF>{},
-                 bq[(t + 1) & 1], st, wk + WK * (t + 1));
+            if constexpr (GEN_SPLIT)
+                step_split(A_cur, bq[t & 1], pnext, xr[t], A_nxt);
+            else
+                step(A_cur, bq[t & 1], pnext, xv, sl, A_nxt, std::integral_constant<bool, PREF>{},
+                     bq[(t + 1) & 1], st, wk + WK * (t + 1));
             A_cur = A_nxt;
             p = pnext;
         };
@@ -558,20 +629,20 @@ void layer_kernel(LayerArgs a) {
     };
 
     // Every wave's blocks are all real in every group but the final one.
-    const int ngroups = (a.nchunks + S - 1) / S;
+    const int ngroups = (a.nchunks + U - 1) / U;
 #pragma unroll 1
     for (int gi = 0; gi + 1 < ngroups; ++gi) {
         auto group = [&](auto kk) {
-            chunk(gi * S + decltype(kk)::value, kk, std::false_type{});
+            chunk(gi * U + decltype(kk)::value, kk, std::false_type{});
         };
-        StaticFor<0, S>::run(group);
+        StaticFor<0, U>::run(group);
     }
     {
         const int gi = ngroups - 1;
         auto group = [&](auto kk) {
-            chunk(gi * S + decltype(kk)::value, kk, std::true_type{});
+            chunk(gi * U + decltype(kk)::value, kk, std::true_type{});
         };
-        StaticFor<0, S>::run(group);
+        StaticFor<0, U>::run(group);
     }
     __syncthreads();
 
@@ -598,9 +669,7 @@ void layer_kernel(LayerArgs a) {
         // barrier), then every thread sums WK partials of some elements and
         // stores them row-major (coalesced).
         constexpr int TILE = 32 * RF * NTILE;  // floats per wave
-        auto red = [&](int w) -> float* {
-            return reinterpret_cast<float*>(w == 0 ? lds0 : w == 1 ? lds1 : w == 2 ? lds2 : lds3);
-        };
+        auto red = [&](int w) -> float* { return reinterpret_cast<float*>(smem) + w * TILE; };
         float* mine = red(wave);
 #pragma unroll
         for (int rf = 0; rf < RF; ++rf)
@@ -722,8 +791,9 @@ LayerCfg plan_layer(const LayerGeom& g, bool bf16, int64_t batch) {
     // bf16 with 256-column tiles: 32-row waves (two per SIMD, accumulators in
     // 128 registers) overlap one wave's basis VALU work with the other's MFMAs;
     // 64-row waves (256 accumulator registers) run one wave per SIMD, which
-    // measured slower on MI355X.
-    if (bf16 && g.nf == 8) return LayerCfg{1, 1, 4};
+    // measured slower on MI355X.  Eight waves per workgroup halve the weight
+    // traffic per row.
+    if (bf16 && g.nf == 8) return LayerCfg{1, 1, 8};
     // Otherwise the tallest workgroup (fewest re-reads of the weights) that
     // still gives at least `want` workgroups; the basis-generation-bound
     // narrow bf16 layers want more, smaller workgroups.
