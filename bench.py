@@ -60,6 +60,40 @@ def copy_calibration(nbytes: int) -> None:
     print(json.dumps({"copy_calibration_bytes": n * 4, "launches": 10}), flush=True)
 
 
+KERNEL_SOURCES = ["kan_layer.hip", "kan_internal.h", "kan_device.h"]
+
+
+def traffic_record(dtype: str, kernel: str):
+    """HBM bytes per launch of `kernel`, from the committed rocprofv3 counter
+    summary (FETCH_SIZE and WRITE_SIZE, each scaled by its plain-copy
+    calibration factor), or None when there is no record for this dtype and
+    kernel or the kernel sources have changed since the counters were taken."""
+    import hashlib
+
+    path = os.path.join(ROOT, "profiles", f"kan_mlp_c5_{dtype}_hbm_traffic.md")
+    if not os.path.exists(path):
+        return None
+    lines = open(path).read().splitlines()
+    if "traffic-record" not in lines:
+        return None
+    rec = {}
+    for ln in lines[lines.index("traffic-record") + 1:]:
+        if ":" not in ln:
+            break
+        k, v = ln.split(":", 1)
+        rec[k.strip()] = v.strip()
+    h = hashlib.md5()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2609_01956_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    if (rec.get("kernel_sources_md5") != h.hexdigest() or rec.get("dtype") != dtype
+            or rec.get("kernel") != kernel):
+        return None
+    kib = (float(rec["fetch_kib"]) * float(rec["fetch_factor"]) +
+           float(rec["write_kib"]) * float(rec["write_factor"]))
+    return kib * 1024.0
+
+
 def cpu_baseline(W, n_layers_shapes, target_s: float):
     """The float64 oracle, untuned, on a row sample of the same step."""
     import numpy as np
@@ -224,7 +258,8 @@ def main() -> int:
                    "step": "kan_basis_eval(x) + 3 x (kan_layer_pack + kan_layer_forward_packed)"},
         "gbasis_per_s": basis_total / (ms_per_step * 1e-3) / 1e9,
         "roofline": {"kernel": dom, "bound": dk["bound"], "achieved": dk["achieved"],
-                     "peak": dk["peak"], "unit": dk["unit"], "frac": dk["frac"], "traffic": None},
+                     "peak": dk["peak"], "unit": dk["unit"], "frac": dk["frac"],
+                     "traffic": traffic_record(args.dtype, dom)},
         "kernels": {n: {k: v for k, v in kern[n].items()} for n in names},
         "parity_e2e_normwise": parity,
     }
