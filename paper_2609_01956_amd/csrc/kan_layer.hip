@@ -96,42 +96,54 @@ template <> struct Tr<uint16_t> {
 // --------------------------------------------------------------- pack kernel
 
 // One unit of the packed buffer per thread: the kj weights of columns
-// [kj * blk, kj * blk + kj) of feature 2 * pair + h for output column n, the
-// columns of a feature ordered [base_w, coef[.., 0], ..., coef[.., nb - 1]]
-// and zero-padded.
+// [kj * blk, kj * blk + kj) of feature f for output column o, the columns of
+// a feature ordered [base_w, coef[.., 0], ..., coef[.., nb - 1]] and
+// zero-padded.  Units are numbered with blk fastest, then f, then o, so a
+// wave reads consecutive coefficients (coef rows are contiguous in f and j);
+// every unit is one 16-byte (bf16) or 8-byte (fp32) store.  Units past
+// `units_main` zero the padding blocks of each tile.
 template <typename T>
 __global__ __launch_bounds__(kThreads) void pack_kernel(const T* __restrict__ coef,
                                                         const T* __restrict__ bw,
                                                         T* __restrict__ packed, int in, int out,
-                                                        int nb, int nsb, int nblk_pad, int ntile,
+                                                        int nb, int nsb, int npairs, int nblk_pad,
+                                                        int ntile, int64_t units_main,
                                                         int64_t units) {
     constexpr int KJ = Tr<T>::KJ;
     const int64_t u = (int64_t)blockIdx.x * kThreads + threadIdx.x;
     if (u >= units) return;
-    int64_t rest = u;
-    const int n = (int)(rest % ntile); rest /= ntile;
-    const int h = (int)(rest % 2); rest /= 2;
-    const int gblk = (int)(rest % nblk_pad);  // block within the tile
-    const int tile = (int)(rest / nblk_pad);
-    const int pair = gblk / nsb;              // >= npairs in the padding
-    const int blk = gblk % nsb;
-    const int ng = tile * ntile + n;
-    const int f = 2 * pair + h;
     T v[KJ];
 #pragma unroll
     for (int e = 0; e < KJ; ++e) v[e] = T(0);
-    if (ng < out && f < in) {  // (the padding blocks have f >= in)
-        const int64_t row = (int64_t)ng * in + f;
+    int64_t dst;  // unit index in the packed buffer
+    if (u < units_main) {
+        const int blk = (int)(u % nsb);
+        const int64_t t = u / nsb;
+        const int f = (int)(t % (2 * npairs));
+        const int o = (int)(t / (2 * npairs));
+        const int tile = o / ntile, n = o % ntile;
+        if (o < out && f < in) {  // (f == in: the phantom feature of an odd count)
+            const int64_t row = (int64_t)o * in + f;
 #pragma unroll
-        for (int e = 0; e < KJ; ++e) {
-            const int c = blk * KJ + e;  // column within the feature: [silu, N_0..N_{nb-1}]
-            if (c == 0) v[e] = bw[row];
-            else if (c <= nb) v[e] = coef[row * nb + c - 1];
+            for (int e = 0; e < KJ; ++e) {
+                const int c = blk * KJ + e;
+                if (c == 0) v[e] = bw[row];
+                else if (c <= nb) v[e] = coef[row * nb + c - 1];
+            }
         }
+        const int64_t gblk = (int64_t)tile * nblk_pad + (int64_t)(f / 2) * nsb + blk;
+        dst = (gblk * 2 + (f & 1)) * ntile + n;
+    } else {
+        // padding blocks [npairs * nsb, nblk_pad) of every tile: zeros
+        const int64_t q = u - units_main;
+        const int64_t per_tile = (int64_t)(nblk_pad - npairs * nsb) * 2 * ntile;
+        const int64_t tile = q / per_tile;
+        dst = tile * (int64_t)nblk_pad * 2 * ntile + (int64_t)npairs * nsb * 2 * ntile +
+              q % per_tile;
     }
-    T* dst = packed + u * KJ;
+    T* d = packed + dst * KJ;
 #pragma unroll
-    for (int e = 0; e < KJ; ++e) dst[e] = v[e];
+    for (int e = 0; e < KJ; ++e) d[e] = v[e];
 }
 
 // ---------------------------------------------------------- A generation
@@ -820,18 +832,20 @@ bool parse_layer_cfg_override(const LayerGeom& g, LayerCfg* c) {
 hipError_t launch_pack(bool bf16, const LayerGeom& g, int in, int out, const void* coef,
                        const void* base_w, void* packed, hipStream_t s) {
     const int ntile = 32 * g.nf;
-    const int64_t units = (int64_t)g.ntiles * g.nblk_pad * 2 * ntile;
+    const int64_t units_main = (int64_t)g.ntiles * ntile * 2 * g.npairs * g.nsb;
+    const int64_t units =
+        units_main + (int64_t)g.ntiles * (g.nblk_pad - g.npairs * g.nsb) * 2 * ntile;
     const unsigned blocks = (unsigned)((units + kThreads - 1) / kThreads);
     if (bf16)
         hipLaunchKernelGGL(pack_kernel<uint16_t>, dim3(blocks), dim3(kThreads), 0, s,
                            static_cast<const uint16_t*>(coef),
                            static_cast<const uint16_t*>(base_w), static_cast<uint16_t*>(packed),
-                           in, out, g.nb, g.nsb, g.nblk_pad, ntile, units);
+                           in, out, g.nb, g.nsb, g.npairs, g.nblk_pad, ntile, units_main, units);
     else
         hipLaunchKernelGGL(pack_kernel<float>, dim3(blocks), dim3(kThreads), 0, s,
                            static_cast<const float*>(coef), static_cast<const float*>(base_w),
-                           static_cast<float*>(packed), in, out, g.nb, g.nsb, g.nblk_pad, ntile,
-                           units);
+                           static_cast<float*>(packed), in, out, g.nb, g.nsb, g.npairs,
+                           g.nblk_pad, ntile, units_main, units);
     return hipGetLastError();
 }
 
