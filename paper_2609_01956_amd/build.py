@@ -1,9 +1,10 @@
-"""Build libkan.so (HIP kernels + C ABI) for gfx950 with hipcc, in-tree.
+"""Build libkan.so (HIP kernels + C ABI) for gfx950 with hipcc, in-tree,
+and libkan_probe.so (the MFMA-rate probe used by ``bench.py --mfma-ceiling``).
 
     python -m paper_2609_01956_amd.build
 
-Every call compiles from source.  The library lands next to this file, where
-``paper_2609_01956_amd.binding`` loads it.
+Every call compiles from source.  The libraries land next to this file, where
+``paper_2609_01956_amd.binding`` and bench.py load them.
 """
 from __future__ import annotations
 
@@ -17,6 +18,8 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libkan.so")
 SOURCES = ["kan_api.cpp", "kan_basis.hip", "kan_layer.hip"]
+PROBE_LIB = os.path.join(HERE, "libkan_probe.so")
+PROBE_SOURCES = ["probe_mfma.hip"]
 ARCH = "gfx950"
 
 
@@ -26,14 +29,14 @@ def hipcc() -> str:
     return cand if os.path.exists(cand) else "hipcc"
 
 
-def build(verbose: bool = False) -> str:
-    tmp = LIB + ".tmp%d" % os.getpid()
+def _compile(sources, out: str, verbose: bool) -> str:
+    tmp = out + ".tmp%d" % os.getpid()
     cmd = [hipcc(), f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
            "-Wall", "-Wno-unused-function",
            # packed fp32 VALU ops stay off: plain fp32 code is scalar per lane
            "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
            "-I", INCLUDE, "-I", CSRC, "-x", "hip"]
-    cmd += [os.path.join(CSRC, s) for s in SOURCES]
+    cmd += [os.path.join(CSRC, s) for s in sources]
     cmd += ["-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
@@ -46,8 +49,15 @@ def build(verbose: bool = False) -> str:
         raise RuntimeError(f"hipcc failed ({res.returncode}):\n{errs}")
     if errs.strip() and verbose:
         print(errs, file=sys.stderr)
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, out)
+    return out
+
+
+def build(verbose: bool = False) -> str:
+    """Compile libkan.so (the product) and libkan_probe.so (the MFMA-rate probe
+    that bench.py --mfma-ceiling runs); returns the path of libkan.so."""
+    _compile(PROBE_SOURCES, PROBE_LIB, verbose)
+    return _compile(SOURCES, LIB, verbose)
 
 
 if __name__ == "__main__":
