@@ -4,13 +4,14 @@
 // The kernel is bound by HBM writes (nb outputs per input read).  Each
 // 256-thread workgroup owns xb consecutive inputs, i.e. one contiguous
 // xb * nb run of the output:
-//   phase 1  tpx threads per input evaluate its nb values in registers (one fma
-//            and ~9 VALU ops per value, no span lookup, no data-dependent
-//            branches) and write them to LDS in output order;
+//   phase 1  tpx threads per input evaluate its nb values in registers (the
+//            coordinate, then 6 VALU ops for N / 2 and one scale, no span
+//            lookup, no data-dependent branches) and write them to LDS in
+//            output order;
 //   phase 2  the workgroup streams the run from LDS to HBM with 16-byte
 //            non-temporal stores, so every store instruction of a wave covers
 //            1 KiB of consecutive output.
-// NaN inputs give NaN outputs: the 1/6 scale is replaced by the NaN itself.
+// NaN inputs give NaN outputs: the scale 2 is replaced by the NaN itself.
 #include "kan_internal.h"
 
 namespace kan {
@@ -57,13 +58,23 @@ __global__ __launch_bounds__(kThreads) void basis_kernel(const T* __restrict__ x
     const int je = min(jb + jc, nb);
     if (el < cnt) {
         const float xv = Storage<T>::load(x + e0 + el);
-        const float scale = (xv != xv) ? xv : (1.0f / 6.0f);
+        const float scale = (xv != xv) ? xv : 2.0f;  // half_basis gives N / 2
         float cj = g.a_int - (float)jb;
         float* dst = stage + el * nb;
+        if (tpx == 1 && g.a_frac == 0.0f) {
+            // (uniform trip count; on grids whose lo / h is an integer the
+            // coordinate is the fma alone)
 #pragma unroll 4
-        for (int j = jb; j < je; ++j) {
-            dst[j] = tp6(coord(xv, g, cj)) * scale;
-            cj -= 1.0f;
+            for (int j = 0; j < nb; ++j) {
+                dst[j] = half_basis(__builtin_fmaf(xv, g.inv_h, cj)) * scale;
+                cj -= 1.0f;
+            }
+        } else {
+#pragma unroll 4
+            for (int j = jb; j < je; ++j) {
+                dst[j] = half_basis(coord(xv, g, cj)) * scale;
+                cj -= 1.0f;
+            }
         }
     }
     __syncthreads();

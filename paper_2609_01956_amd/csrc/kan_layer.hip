@@ -24,18 +24,9 @@
 //                  matrix work; with one wave per SIMD the two interleave
 //                  within the wave.
 //
-// Basis values.  With v = u - 2 (u the coordinate of eq. truncated), the clamp
-// of eq. bounded and the symmetry of the stencil {1, -4, 6, -4, 1} give
-//     6 N = w^3 - 4 b^3,   w = 2 - min(|v|, 2),  b = max(1 - |v|, 0),
-// i.e. N / 2 = P^3 - Q^3 with
-//     P = (2/3)^(1/3) w / 2 = clamp01((2/3)^(1/3) (1 - |v| / 2)),
-//     Q = (1/3)^(1/3) b     = clamp01((1/3)^(1/3) (1 - |v|))
-// (both scale factors are below 1, so the clamp to [0, 1] only acts at 0).
-// Each value is then one subtraction, two clamped fused multiply-adds (the
-// clamp and |v| fold into the instruction), three multiplies and one fused
-// multiply-add.  Off the support P = Q = 0 and the value is exactly 0.  The
-// MFMA operands are N_j / 2 and silu / 2, and the epilogue doubles y: scaling
-// by a power of two is exact, so the operands are exactly bf16(N_j) / 2 and
+// Basis values are N_j / 2 = P^3 - Q^3 (half_basis, kan_device.h).  The MFMA
+// operands are N_j / 2 and silu / 2, and the epilogue doubles y: scaling by a
+// power of two is exact, so the operands are exactly bf16(N_j) / 2 and
 // bf16(silu) / 2 on the bf16 path and the result is the contraction of the
 // rounded N_j and silu values.
 //
@@ -55,19 +46,6 @@ namespace kan {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr float kCbrtTwoThirds = 0.87358046473629571f;  // (2/3)^(1/3)
-constexpr float kCbrtOneThird = 0.69336127435063470f;   // (1/3)^(1/3)
-
-// N(u) / 2 at v = u - 2 (see the header comment).
-__device__ __forceinline__ float half_basis(float v) {
-    const float av = __builtin_fabsf(v);
-    const float P = __builtin_amdgcn_fmed3f(
-        __builtin_fmaf(av, -0.5f * kCbrtTwoThirds, kCbrtTwoThirds), 0.0f, 1.0f);
-    const float Q = __builtin_amdgcn_fmed3f(
-        __builtin_fmaf(av, -kCbrtOneThird, kCbrtOneThird), 0.0f, 1.0f);
-    return __builtin_fmaf(P * P, P, -(Q * Q * Q));
-}
-
 // silu(x) / 2 = x / (2 + 2 exp(-x)).
 __device__ __forceinline__ float half_silu(float x) {
     return x * __builtin_amdgcn_rcpf(__builtin_fmaf(__expf(-x), 2.0f, 2.0f));
