@@ -11,13 +11,15 @@ from __future__ import annotations
 import os
 import subprocess
 import sys
+from concurrent.futures import ThreadPoolExecutor
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libkan.so")
-SOURCES = ["kan_api.cpp", "kan_basis.hip", "kan_layer.hip"]
+SOURCES = ["kan_api.cpp", "kan_basis.hip", "kan_layer.hip", "kan_layer_bf16.hip",
+           "kan_layer_f32.hip"]
 PROBE_LIB = os.path.join(HERE, "libkan_probe.so")
 PROBE_SOURCES = ["probe_mfma.hip"]
 ARCH = "gfx950"
@@ -29,15 +31,15 @@ def hipcc() -> str:
     return cand if os.path.exists(cand) else "hipcc"
 
 
-def _compile(sources, out: str, verbose: bool) -> str:
-    tmp = out + ".tmp%d" % os.getpid()
-    cmd = [hipcc(), f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
-           "-Wall", "-Wno-unused-function",
-           # packed fp32 VALU ops stay off: plain fp32 code is scalar per lane
-           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-           "-I", INCLUDE, "-I", CSRC, "-x", "hip"]
-    cmd += [os.path.join(CSRC, s) for s in sources]
-    cmd += ["-o", tmp]
+def _flags():
+    return [f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-Wall",
+            "-Wno-unused-function",
+            # packed fp32 VALU ops stay off: plain fp32 code is scalar per lane
+            "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+            "-I", INCLUDE, "-I", CSRC]
+
+
+def _run(cmd, verbose: bool) -> None:
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
@@ -49,7 +51,27 @@ def _compile(sources, out: str, verbose: bool) -> str:
         raise RuntimeError(f"hipcc failed ({res.returncode}):\n{errs}")
     if errs.strip() and verbose:
         print(errs, file=sys.stderr)
-    os.replace(tmp, out)
+
+
+def _compile(sources, out: str, verbose: bool) -> str:
+    """Compile each source to an object in parallel, then link `out`."""
+    tag = "%d" % os.getpid()
+    objs = [os.path.join(HERE, "_build_" + os.path.splitext(src)[0] + "." + tag + ".o")
+            for src in sources]
+    cmds = [[hipcc()] + _flags() + ["-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj]
+            for src, obj in zip(sources, objs)]
+    tmp = out + ".tmp" + tag
+    try:
+        with ThreadPoolExecutor(max_workers=min(len(cmds), os.cpu_count() or 1)) as pool:
+            for f in [pool.submit(_run, c, verbose) for c in cmds]:
+                f.result()
+        _run([hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC"] + objs + ["-o", tmp],
+             verbose)
+        os.replace(tmp, out)
+    finally:
+        for o in objs + [tmp]:
+            if os.path.exists(o):
+                os.remove(o)
     return out
 
 

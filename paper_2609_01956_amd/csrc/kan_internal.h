@@ -74,18 +74,38 @@ struct LayerGeom {
 bool layer_geom(int nb, bool bf16, int in, int out, LayerGeom* g);
 
 // Workgroup shape of the fused kernel: nw waves, each holding rf 32-row MFMA
-// tiles of all nf column fragments; wk waves split the blocks (K) of a chunk
-// and are summed through LDS at the end, the other nw / wk waves take
-// different rows.
+// tiles of nf / cs 32-column fragments; wk waves split the blocks (K) of a
+// chunk and are summed through LDS at the end, the other nw / wk waves take
+// different rows; cs workgroups split the columns of an N tile (each stages
+// only its columns of every packed block).
 struct LayerCfg {
     int rf;  // 1 or 2
-    int wk;  // 1, 2 or 4; wk > 1 needs rf * nf <= 4
-    int nw;  // waves per workgroup: 4, or 8 (rf = 1, wk = 1 only)
+    int wk;  // 1, 2 or 4
+    int nw;  // waves per workgroup: 4, or 8 (rf = 1, wk = 1, cs = 1 only)
+    int cs;  // column slices per N tile: 1, 2 or 4 (rf = 1, nw = 4 only)
 };
 
+// The shapes the fused kernel is instantiated for, given the packed tile of
+// nfl fragments: the chunk the slice stages must be whole 16-byte loads of
+// every thread, its blocks must split evenly over the wk waves, and wk > 1
+// keeps rf * (nfl / cs) <= 4 (the partial sums fit in LDS).
+__host__ __device__ constexpr bool layer_shape_ok(bool bf16, int nfl, int rf, int wk, int nw,
+                                                 int cs) {
+    if ((rf != 1 && rf != 2) || (wk != 1 && wk != 2 && wk != 4) || (nw != 4 && nw != 8) ||
+        (cs != 1 && cs != 2 && cs != 4) || nfl % cs != 0 || (!bf16 && nfl > 4))
+        return false;
+    const int nf = nfl / cs;
+    const int kb = layer_chunk_blocks(bf16, nfl);
+    const int chb = kb * layer_block_bytes(bf16, nf);
+    if (chb % (1024 * nw) != 0 || kb % wk != 0) return false;
+    if (nw == 8) return rf == 1 && wk == 1 && cs == 1;
+    if (cs > 1) return rf == 1;
+    return wk == 1 || rf * nf <= 4;
+}
+
 LayerCfg plan_layer(const LayerGeom& g, bool bf16, int64_t batch);
-// KAN_LAYER_CFG="rf,wk[,nw]" forces a configuration (testing and tuning); ignored
-// when malformed or not valid for the geometry.
+// KAN_LAYER_CFG="rf,wk[,nw[,cs]]" forces a configuration (testing and tuning);
+// ignored when malformed or not valid for the geometry.
 bool parse_layer_cfg_override(const LayerGeom& g, LayerCfg* c);
 bool layer_cfg_valid(const LayerGeom& g, const LayerCfg& c);
 
@@ -111,5 +131,10 @@ hipError_t launch_pack(bool bf16, const LayerGeom& g, int in, int out, const voi
                        const void* base_w, void* packed, hipStream_t s);
 hipError_t launch_layer(bool bf16, const LayerGeom& g, const LayerCfg& c, LayerArgs a,
                         hipStream_t s);
+// Per-dtype kernel launches (one translation unit each).
+hipError_t launch_layer_bf16(const LayerGeom& g, const LayerCfg& c, const LayerArgs& a,
+                             hipStream_t s);
+hipError_t launch_layer_f32(const LayerGeom& g, const LayerCfg& c, const LayerArgs& a,
+                            hipStream_t s);
 
 }  // namespace kan

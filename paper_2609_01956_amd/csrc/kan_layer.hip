@@ -1,75 +1,17 @@
-// kan_layer.hip -- fused KAN-layer forward on MFMA (eq. kan_forward):
-//
-//   y[b, o] = sum_i sum_{j <= nb} A[b, (i, j)] * W[o, (i, j)]
-//   A[b, (i, j)] = N_j(x[b, i]) for j < nb,   silu(x[b, i]) for j = nb
-//   W[o, (i, j)] = coef[o, i, j]   for j < nb,   base_w[o, i]  for j = nb
-//
-// a dense [batch, in * (nb + 1)] x [in * (nb + 1), out] contraction whose
-// left operand is never stored: every lane generates its own A elements in
-// registers, directly in the MFMA operand layout, from one x value per block.
-//
-// Two kernels:
-//   pack_kernel    rearranges coef / base_w into the block order described in
-//                  kan_internal.h (a few MB, read once per call);
-//   layer_kernel   4 or 8 waves per workgroup.  The workgroup walks the blocks
-//                  in chunks of up to 16 KB of packed weights: each chunk is
-//                  loaded into registers a few chunks ahead, written to one of
-//                  two LDS stages while the previous chunk is multiplied, and
-//                  read from LDS by every wave.  Each wave owns rf 32-row
-//                  tiles of all nf 32-column fragments of the N tile, so every
-//                  generated A element feeds nf MFMAs and every B fragment read
-//                  from LDS feeds rf MFMAs.  With two waves per SIMD a wave
-//                  generates the next block's A and then issues the current
-//                  block's MFMAs, so one wave's VALU work overlaps the other's
-//                  matrix work; with one wave per SIMD the two interleave
-//                  within the wave.
-//
-// Basis values are N_j / 2 = P^3 - Q^3 (half_basis, kan_device.h).  The MFMA
-// operands are N_j / 2 and silu / 2, and the epilogue doubles y: scaling by a
-// power of two is exact, so the operands are exactly bf16(N_j) / 2 and
-// bf16(silu) / 2 on the bf16 path and the result is the contraction of the
-// rounded N_j and silu values.
-//
-// fp32: A and W fp32, v_mfma_f32_32x32x2_f32 (one k per lane half, two
-//       k-steps per block).
-// bf16: x, W bf16 in memory; A generated in fp32, rounded to bf16 (RNE);
-//       v_mfma_f32_32x32x16_bf16 (eight k per lane half), fp32 accumulation;
-//       y rounded to bf16 on store.
-#include "kan_internal.h"
+// kan_layer.hip -- weight packing, tile planning and launch dispatch of the
+// fused KAN-layer forward (eq. kan_forward); the kernels are in
+// kan_layer_kernel.h.
+#include "kan_layer_kernel.h"
 
 #include <cstdio>
 #include <cstdlib>
-#include <type_traits>
 
 namespace kan {
 
 namespace {
 
-constexpr int kThreads = 256;
-// silu(x) / 2 = x / (2 + 2 exp(-x)).
-__device__ __forceinline__ float half_silu(float x) {
-    return x * __builtin_amdgcn_rcpf(__builtin_fmaf(__expf(-x), 2.0f, 2.0f));
-}
-
-template <typename T> struct Tr;
-
-template <> struct Tr<float> {
-    static constexpr int KJ = 2;  // columns per block
-    static __device__ __forceinline__ float load(const float* p) { return *p; }
-    static __device__ __forceinline__ uint32_t raw(const float* p) {
-        return __float_as_uint(*p);
-    }
-    static __device__ __forceinline__ float value(uint32_t u) { return __uint_as_float(u); }
-    static __device__ __forceinline__ void store(float* p, float v) { *p = v; }
-};
-
-template <> struct Tr<uint16_t> {
-    static constexpr int KJ = 8;
-    static __device__ __forceinline__ float load(const uint16_t* p) { return bf16_to_f32(*p); }
-    static __device__ __forceinline__ uint32_t raw(const uint16_t* p) { return *p; }
-    static __device__ __forceinline__ float value(uint32_t u) { return __uint_as_float(u << 16); }
-    static __device__ __forceinline__ void store(uint16_t* p, float v) { *p = f32_to_bf16(v); }
-};
+using layer_detail::Tr;
+using layer_detail::kThreads;
 
 // --------------------------------------------------------------- pack kernel
 
@@ -124,616 +66,6 @@ __global__ __launch_bounds__(kThreads) void pack_kernel(const T* __restrict__ co
     for (int e = 0; e < KJ; ++e) d[e] = v[e];
 }
 
-// ---------------------------------------------------------- A generation
-//
-// Within a feature the columns are ordered [silu, N_0, N_1, ..., N_{nb-1}]
-// and zero-padded to a whole number of blocks, so column c of the feature is
-// basis c - 1 for c >= 1.  Block b, element e is column KJ * b + e: a basis
-// value at v = s_b - e with s_b = v of basis KJ * b - 1, except column 0 (the
-// SiLU value).  Columns past nb are evaluated like any other basis (finite
-// values) and meet zero weights.  Every block is therefore generated by the
-// same straight-line code; only element 0 of block 0 is replaced.
-template <typename T, int RF> struct AFrag;
-template <int RF> struct AFrag<uint16_t, RF> { bf16x8 a[RF]; };
-template <int RF> struct AFrag<float, RF> { float a[RF][2]; };
-
-template <int RF>
-__device__ __forceinline__ void zero_frag(AFrag<uint16_t, RF>& A, int rf) {
-#pragma unroll
-    for (int e = 0; e < 8; ++e) A.a[rf][e] = (__bf16)0.0f;
-}
-template <int RF>
-__device__ __forceinline__ void zero_frag(AFrag<float, RF>& A, int rf) {
-    A.a[rf][0] = 0.0f;
-    A.a[rf][1] = 0.0f;
-}
-
-// Compile-time loop: f(std::integral_constant<int, I>) for I = 0 .. N - 1.
-template <int I, int N>
-struct StaticFor {
-    template <typename F>
-    __device__ __forceinline__ static void run(F& f) {
-        f(std::integral_constant<int, I>{});
-        StaticFor<I + 1, N>::run(f);
-    }
-};
-template <int N>
-struct StaticFor<N, N> {
-    template <typename F>
-    __device__ __forceinline__ static void run(F&) {}
-};
-
-// Position of a wave's block: global block index, feature pair and block
-// within the pair.  A wave visits blocks wk, wk + WK, wk + 2 WK, ...
-struct Pos {
-    int blk, pair, bsub;
-};
-
-// Advance a position by STEP blocks (compile-time STEP <= 8, nsb >= 1):
-// straight-line selects, so no loop (and no basic-block split) in the main
-// loop.
-template <int STEP>
-__device__ __forceinline__ Pos advance(Pos p, int nsb) {
-    p.blk += STEP;
-    p.bsub += STEP;
-#pragma unroll
-    for (int i = 0; i < STEP; ++i) {
-        // wrap = (bsub >= nsb) as plain integer arithmetic (no lane masks,
-        // so the scalar unit does it)
-        const int wrap = (int)((uint32_t)(nsb - 1 - p.bsub) >> 31);
-        p.bsub -= nsb & -wrap;
-        p.pair += wrap;
-    }
-    return p;
-}
-
-// Advance by a runtime step < 4.
-__device__ __forceinline__ Pos advance_n(Pos p, int step, int nsb) {
-    p.blk += step;
-    p.bsub += step;
-#pragma unroll
-    for (int i = 0; i < 3; ++i) {
-        const int wrap = (int)((uint32_t)(nsb - 1 - p.bsub) >> 31);
-        p.bsub -= nsb & -wrap;
-        p.pair += wrap;
-    }
-    return p;
-}
-
-// ------------------------------------------------------------- main kernel
-
-// Waves per SIMD the register budget is sized for: two when the accumulators
-// take at most 128 registers (so a second wave's MFMAs fill the matrix core
-// while one wave runs its basis VALU work), otherwise one.
-template <int RF, int NF>
-struct Occ {
-    static constexpr int waves = RF * NF * 16 <= 128 ? 2 : 1;
-};
-
-template <typename T, int RF, int NF, int WK, int NW>
-__global__ __launch_bounds__(64 * NW)
-__attribute__((amdgpu_waves_per_eu(Occ<RF, NF>::waves)))
-void layer_kernel(LayerArgs a) {
-    constexpr bool BF16 = sizeof(T) == 2;
-    constexpr int KJ = Tr<T>::KJ;
-    constexpr int NT = 64 * NW;                  // threads per workgroup
-    constexpr int WM = NW / WK;
-    constexpr int NTILE = 32 * NF;
-    constexpr int LANEB = KJ * (int)sizeof(T);  // B bytes per lane per block (16 / 8)
-    constexpr int BLKB = layer_block_bytes(BF16, NF);  // bytes per block: [h][n][KJ]
-    constexpr int KB = layer_chunk_blocks(BF16, NF);   // blocks per chunk
-    constexpr int CHB = KB * BLKB;               // bytes per chunk
-    constexpr int DPW = CHB / (1024 * NW);       // 16-byte loads per lane per chunk
-    constexpr int KBW = KB / WK;                 // blocks per wave per chunk
-    constexpr int NX = KBW * RF;                 // x loads per lane per chunk
-    constexpr int BM = 32 * RF * WM;             // rows per workgroup
-    // Weights of chunk c are loaded into registers L chunks ahead (register
-    // set c % L), written to LDS stage c % 2 while chunk c - 1 is multiplied,
-    // and read from there during chunk c.
-    constexpr int L = DPW <= 2 ? 3 : 2;
-    constexpr int U = L % 2 == 0 ? L : 2 * L;    // chunk-loop unroll, lcm(2, L)
-    constexpr int PART = WK > 1 ? 32 * RF * NTILE * 4 : 0;  // one wave's partial sums
-    constexpr int SMEM = 2 * CHB > NW * PART ? 2 * CHB : NW * PART;
-    static_assert(CHB % (1024 * NW) == 0 && KB % WK == 0 && KB >= WK, "chunk shape");
-    static_assert(NW == 4 || (NW == 8 && WK == 1), "waves per workgroup");
-    static_assert(SMEM <= 64 * 1024, "LDS budget");
-    static_assert(BLKB == 2 * NTILE * LANEB, "block layout");
-    // LDS: two chunk stages; after the main loop the K-split partial sums.
-    __shared__ u32x4 smem[SMEM / 16];
-    auto stage = [&](auto kk) -> u32x4* { return smem + (decltype(kk)::value % 2) * (CHB / 16); };
-
-    const T* __restrict__ x = static_cast<const T*>(a.x);
-    T* __restrict__ y = static_cast<T*>(a.y);
-
-    const int tid = threadIdx.x;
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
-    const int lane = tid & 63;
-    const int r = lane & 31;
-    const int h = lane >> 5;
-    const int wm = wave % WM;
-    const int wk = wave / WM;
-    const int64_t row0 = (int64_t)blockIdx.x * BM + wm * 32 * RF;
-    const int nt = blockIdx.y;
-    // Packed weights of this N tile: nblk_pad blocks = nchunks whole chunks.
-    const char* __restrict__ wpt =
-        static_cast<const char*>(a.wp) + (size_t)nt * (size_t)a.nblk_pad * BLKB;
-
-    // x is addressed as a per-workgroup base plus 32-bit element offsets (the
-    // workgroup's rows span far less than 2^31 elements).  Rows past the
-    // batch read row batch - 1 (their results are not stored).
-    const int64_t wg_row0 = (int64_t)blockIdx.x * BM;
-    const T* __restrict__ xw = x + wg_row0 * (int64_t)a.in;
-    uint32_t xoff[RF];  // element offset of (row, feature h of pair 0)
-#pragma unroll
-    for (int rf = 0; rf < RF; ++rf) {
-        int64_t row = row0 + rf * 32 + r;
-        row = row < a.batch ? row : a.batch - 1;
-        xoff[rf] = (uint32_t)((row - wg_row0) * a.in + h);
-    }
-    // With an odd feature count the last pair has a phantom second feature
-    // (zero weights): its lanes read the real last feature and use x = 0.
-    const int last_pair_odd = (a.in & 1) ? a.in / 2 : -1;
-
-    // ---- loads of chunk c into register set j, for the wave's blocks from
-    // position p on: first the x of each block and row tile (per lane: the
-    // lane's row, the feature of its half in the block's pair; positions past
-    // the end read the last pair, the phantom lanes step back one feature),
-    // then the weights (wave w, load i holds bytes [i 1024 NW + w 1024,
-    // + 1024) of the chunk, 16 per lane).  Chunks past the last re-load the
-    // last chunk.  Raw x bits are kept: conversion and masking happen where
-    // the values are used, so nothing waits for a load when it is issued.
-    typedef uint32_t XSet[KBW][RF];
-    typedef u32x4 WSet[DPW];
-    const uint32_t wlane = (uint32_t)(wave * 1024 + lane * 16);
-    auto issue = [&](int c, Pos p, XSet& xs, WSet& ws) {
-#pragma unroll
-        for (int t = 0; t < KBW; ++t) {
-            const int pr = p.pair < a.npairs ? p.pair : a.npairs - 1;
-            const uint32_t back = (pr == last_pair_odd) ? (uint32_t)h : 0u;
-#pragma unroll
-            for (int rf = 0; rf < RF; ++rf)
-                xs[t][rf] = Tr<T>::raw(xw + (xoff[rf] + (uint32_t)(2 * pr) - back));
-            p = advance<WK>(p, a.nsb);
-        }
-        const int cc = c < a.nchunks ? c : a.nchunks - 1;
-        const char* g = wpt + (size_t)cc * CHB;  // wave-uniform
-#pragma unroll
-        for (int i = 0; i < DPW; ++i)
-            ws[i] = *reinterpret_cast<const u32x4*>(g + (wlane + (uint32_t)(i * 1024 * NW)));
-    };
-    // Register set -> LDS stage kk (the same byte offsets as in the chunk).
-    auto store = [&](auto kk, const WSet& ws) {
-        char* l = reinterpret_cast<char*>(stage(kk));
-#pragma unroll
-        for (int i = 0; i < DPW; ++i)
-            *reinterpret_cast<u32x4*>(l + wlane + i * 1024 * NW) = ws[i];
-    };
-    // Value of raw x bits for the lane's feature at position p (the phantom
-    // feature of an odd feature count gives 0).
-    auto x_value = [&](const Pos& p, uint32_t raw) {
-        const float v = Tr<T>::value(raw);
-        if (p.pair == last_pair_odd) return h ? 0.0f : v;
-        return v;
-    };
-
-    floatx16 acc[RF][NF];
-#pragma unroll
-    for (int rf = 0; rf < RF; ++rf)
-#pragma unroll
-        for (int nf = 0; nf < NF; ++nf)
-#pragma unroll
-            for (int q = 0; q < 16; ++q) acc[rf][nf][q] = 0.0f;
-
-    // ---- B fragments of one block (LDS block `bi` of stage `st`)
-    typedef typename std::conditional<BF16, bf16x8, floatx2>::type BVec;
-    struct BFrag { BVec b[NF]; };
-    auto read_b = [&](BFrag& B, const u32x4* st, int bi) {
-        const char* lb = reinterpret_cast<const char*>(st) + bi * BLKB;
-#pragma unroll
-        for (int nf = 0; nf < NF; ++nf) {
-            const char* q = lb + (h * NTILE + nf * 32 + r) * LANEB;
-            if constexpr (BF16)
-                B.b[nf] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(q));
-            else
-                B.b[nf] = *reinterpret_cast<const floatx2*>(q);
-        }
-    };
-
-    // MFMA number i of a block (NMFMA per block): bf16 (nf, rf); fp32 also
-    // the k-step t of the block's two columns.
-    constexpr int NMFMA = (BF16 ? 1 : 2) * RF * NF;
-    auto do_mfma = [&](int i, const AFrag<T, RF>& A, const BFrag& B) {
-        const int rf = i % RF;
-        const int nf = (i / RF) % NF;
-        if constexpr (BF16) {
-            acc[rf][nf] =
-                __builtin_amdgcn_mfma_f32_32x32x16_bf16(A.a[rf], B.b[nf], acc[rf][nf], 0, 0, 0);
-        } else {
-            const int t = i / (RF * NF);
-            acc[rf][nf] = __builtin_amdgcn_mfma_f32_32x32x2f32(A.a[rf][t], B.b[nf][t],
-                                                               acc[rf][nf], 0, 0, 0);
-        }
-    };
-
-    // One step: the NMFMA MFMAs of the current block (A, B) together with the
-    // generation of the next block's A (block pg from x values xv, slv the
-    // silu of its pair) and, with one wave per SIMD, the LDS reads of the next
-    // block's B (PREF: block bi_n of stage st).  After MFMA i come the VALU
-    // ops of A elements [i NE / NMFMA, (i + 1) NE / NMFMA).
-    constexpr int NE = RF * KJ;  // A elements generated per lane per block
-    constexpr bool SCHED_PINGPONG = Occ<RF, NF>::waves == 2;
-    auto step = [&](const AFrag<T, RF>& A, const BFrag& B, const Pos& pg,
-                    const float (&xv)[RF], const float (&slv)[RF], AFrag<T, RF>& An,
-                    auto pref_tag, BFrag& Bn, const u32x4* st, int bi_n) {
-        constexpr bool PREF = decltype(pref_tag)::value;
-        float s[RF];
-        const float c = a.a_int + 1.0f - (float)(KJ * pg.bsub);
-#pragma unroll
-        for (int rf = 0; rf < RF; ++rf) s[rf] = __builtin_fmaf(xv[rf], a.inv_h, c) + a.a_frac;
-        // (xv: x values of block pg, already converted)
-        const bool first = pg.bsub == 0;
-        float v[RF][KJ];
-        auto gen_elem = [&](int k) {
-            const int rf = k / KJ;
-            const int e = k % KJ;
-            const float bv = half_basis(s[rf] - (float)e);
-            v[rf][e] = (e == 0 && first) ? slv[rf] : bv;
-            if constexpr (BF16) {
-                if (e & 1) {
-                    An.a[rf][e - 1] = (__bf16)v[rf][e - 1];
-                    An.a[rf][e] = (__bf16)v[rf][e];
-                }
-            } else {
-                An.a[rf][e] = v[rf][e];
-            }
-        };
-        if constexpr (SCHED_PINGPONG) {
-            // Two waves per SIMD: the whole basis generation (VALU), then the
-            // MFMAs back to back at raised priority.  While one wave runs its
-            // VALU phase the other's MFMA phase keeps the matrix core busy,
-            // and the priority makes the MFMA phase win when both want to
-            // issue.
-#pragma unroll
-            for (int k = 0; k < NE; ++k) gen_elem(k);
-            __builtin_amdgcn_sched_barrier(0);
-            __builtin_amdgcn_s_setprio(1);
-#pragma unroll
-            for (int i = 0; i < NMFMA; ++i) do_mfma(i, A, B);
-            __builtin_amdgcn_s_setprio(0);
-            __builtin_amdgcn_sched_barrier(0);
-        } else {
-            // One wave per SIMD: after MFMA i come the VALU ops of elements
-            // [i NE / NMFMA, (i + 1) NE / NMFMA).
-#pragma unroll
-            for (int i = 0; i < NMFMA; ++i) {
-                do_mfma(i, A, B);
-                if constexpr (PREF) {
-                    if (i == 0) read_b(Bn, st, bi_n);
-                }
-#pragma unroll
-                for (int k = i * NE / NMFMA; k < (i + 1) * NE / NMFMA; ++k) gen_elem(k);
-                __builtin_amdgcn_sched_barrier(0);
-            }
-        }
-    };
-
-    // bf16 with two waves per SIMD: the A of a block is generated by code
-    // chosen by the block's place in its feature pair (uniform branches).
-    //   first block:  x, the coordinate and the SiLU value (element 0), then
-    //                 basis values 1 .. 7;
-    //   middle block: the coordinate steps down by 8 (one wave visits the
-    //                 blocks of a pair in order when WK = 1; with WK > 1 it is
-    //                 recomputed from x), then 8 basis values;
-    //   last block:   as a middle block, but only the real columns of the
-    //                 feature (rounded up to even) are evaluated and the
-    //                 padding columns are set to 0.
-    // Stepping the coordinate by 8 is exact wherever a basis value of the
-    // block is nonzero (there |s| < 17 and s - 8 is computed exactly).
-    constexpr bool GEN_SPLIT = BF16 && Occ<RF, NF>::waves == 2;
-    constexpr bool DIRECT = WK > 1;
-    float sc[RF];  // coordinate of the wave's current block (element 0)
-    // real columns in the last block of a feature, rounded up to even
-    const int last_cols = a.nb + 1 - KJ * (a.nsb - 1);
-    const int last_even = (last_cols + 1) & ~1;
-    auto gen_split = [&](const Pos& pg, const uint32_t (&xr)[RF], AFrag<T, RF>& An) {
-      if constexpr (GEN_SPLIT) {
-        auto basis = [&](int rf, int e0, int e1) {
-#pragma unroll
-            for (int e = e0; e < e1; ++e) An.a[rf][e] = (__bf16)half_basis(sc[rf] - (float)e);
-        };
-        auto zero = [&](int rf, int e0) {
-#pragma unroll
-            for (int e = e0; e < KJ; ++e) An.a[rf][e] = (__bf16)0.0f;
-        };
-        if (pg.bsub == 0) {
-#pragma unroll
-            for (int rf = 0; rf < RF; ++rf) {
-                const float xv = x_value(pg, xr[rf]);
-                sc[rf] = __builtin_fmaf(xv, a.inv_h, a.a_int + 1.0f) + a.a_frac;
-                An.a[rf][0] = (__bf16)half_silu(xv);
-                basis(rf, 1, KJ);
-            }
-            return;
-        }
-        if constexpr (DIRECT) {
-            const float c = a.a_int + 1.0f - (float)(KJ * pg.bsub);
-#pragma unroll
-            for (int rf = 0; rf < RF; ++rf)
-                sc[rf] = __builtin_fmaf(x_value(pg, xr[rf]), a.inv_h, c) + a.a_frac;
-        } else {
-#pragma unroll
-            for (int rf = 0; rf < RF; ++rf) sc[rf] -= (float)KJ;
-        }
-        if (pg.bsub != a.nsb - 1 || last_even == KJ) {
-#pragma unroll
-            for (int rf = 0; rf < RF; ++rf) basis(rf, 0, KJ);
-        } else if (last_even == 6) {
-#pragma unroll
-            for (int rf = 0; rf < RF; ++rf) { basis(rf, 0, 6); zero(rf, 6); }
-        } else if (last_even == 4) {
-#pragma unroll
-            for (int rf = 0; rf < RF; ++rf) { basis(rf, 0, 4); zero(rf, 4); }
-        } else {
-#pragma unroll
-            for (int rf = 0; rf < RF; ++rf) { basis(rf, 0, 2); zero(rf, 2); }
-        }
-      }
-    };
-    // Phase-ordered step with split generation: the next block's A, then the
-    // MFMAs of the current block back to back at raised priority (while one
-    // wave generates, the other's MFMAs keep the matrix core busy).
-    auto step_split = [&](const AFrag<T, RF>& A, const BFrag& B, const Pos& pg,
-                          const uint32_t (&xr)[RF], AFrag<T, RF>& An) {
-        gen_split(pg, xr, An);
-        __builtin_amdgcn_sched_barrier(0);
-        __builtin_amdgcn_s_setprio(1);
-#pragma unroll
-        for (int i = 0; i < NMFMA; ++i) do_mfma(i, A, B);
-        __builtin_amdgcn_s_setprio(0);
-        __builtin_amdgcn_sched_barrier(0);
-    };
-
-    auto silu_of = [&](const float (&xv)[RF], float (&sl)[RF]) {
-#pragma unroll
-        for (int rf = 0; rf < RF; ++rf) sl[rf] = half_silu(xv[rf]);
-    };
-
-    // ---- pipeline
-    // Chunk c: at its top a barrier (every wave has written chunk c to stage
-    // c % 2 and finished reading chunk c - 1 from the other stage), then the
-    // loads of chunk c + L are issued into register set c % L (free: its
-    // weights went to LDS during chunk c - 1, its x were copied out), the
-    // weights of chunk c + 1 (set (c + 1) % L) are written to stage
-    // (c + 1) % 2, and the chunk's blocks are multiplied.  The chunk loop is
-    // unrolled by U so that stages and register sets are compile-time
-    // choices (a register move of a load still in flight would wait for
-    // it).  Chunks past the last one (to fill the unrolled group) load
-    // clamped inputs and multiply zero A.
-    static_assert(WK <= 4, "wave block stride");
-    constexpr int WAIT_LDS = 0xF | (0x7 << 4) | (0x0 << 8) | (0x3 << 14);  // lgkmcnt(0) only
-    const int nq = wk < a.nblk ? (a.nblk - wk + WK - 1) / WK : 0;  // real blocks of this wave
-
-    XSet xq[L];
-    WSet wq[L];
-    float sl[RF];
-    AFrag<T, RF> A_cur, A_nxt;
-    BFrag bq[2];
-    Pos pos_c = advance_n(Pos{0, 0, 0}, wk, a.nsb);  // first block of the current chunk
-    Pos pos_l = pos_c;                               // first block of the next chunk to load
-
-    // prologue: loads of chunks 0 .. L - 1, chunk 0 to stage 0
-    auto prologue = [&](auto jj) {
-        constexpr int j = decltype(jj)::value;
-        issue(j, pos_l, xq[j], wq[j]);
-        pos_l = advance<KB>(pos_l, a.nsb);
-    };
-    StaticFor<0, L>::run(prologue);
-    store(std::integral_constant<int, 0>{}, wq[0]);
-    __builtin_amdgcn_s_waitcnt(WAIT_LDS);
-    __builtin_amdgcn_s_barrier();
-    __builtin_amdgcn_sched_barrier(0);
-
-    // A of the wave's first block (nothing to interleave with yet).
-    if constexpr (GEN_SPLIT) {
-        gen_split(pos_c, xq[0][0], A_cur);
-    } else {
-        float x0[RF];
-#pragma unroll
-        for (int rf = 0; rf < RF; ++rf) x0[rf] = x_value(pos_c, xq[0][0][rf]);
-        silu_of(x0, sl);
-        const float c0 = a.a_int + 1.0f - (float)(KJ * pos_c.bsub);
-#pragma unroll
-        for (int rf = 0; rf < RF; ++rf) {
-            const float s0 = __builtin_fmaf(x0[rf], a.inv_h, c0) + a.a_frac;
-#pragma unroll
-            for (int e = 0; e < KJ; ++e) {
-                const float bv = half_basis(s0 - (float)e);
-                const float v = (e == 0 && pos_c.bsub == 0) ? sl[rf] : bv;
-                if constexpr (BF16) A_cur.a[rf][e] = (__bf16)v;
-                else A_cur.a[rf][e] = v;
-            }
-        }
-    }
-
-    // Chunk c with K = c % U (compile-time).
-    auto chunk = [&](int c, auto kk, auto last_tag) {
-        constexpr int K = decltype(kk)::value;
-        constexpr bool LASTG = decltype(last_tag)::value;  // in the final group
-        constexpr int J = K % L;          // register set of chunk c (and of c + L)
-        constexpr int JN = (K + 1) % L;   // register set of chunk c + 1
-        if (c > 0) {  // (chunk 0's barrier is in the prologue)
-            __builtin_amdgcn_s_waitcnt(WAIT_LDS);
-            __builtin_amdgcn_s_barrier();
-            __builtin_amdgcn_sched_barrier(0);
-        }
-        // x of the blocks whose A this chunk generates: blocks 1 .. KBW - 1
-        // of this chunk, then block 0 of the next one
-        uint32_t xr[KBW][RF];
-#pragma unroll
-        for (int t = 0; t < KBW; ++t)
-#pragma unroll
-            for (int rf = 0; rf < RF; ++rf) xr[t][rf] = t + 1 < KBW ? xq[J][t + 1][rf] : xq[JN][0][rf];
-        __builtin_amdgcn_sched_barrier(0);
-        issue(c + L, pos_l, xq[J], wq[J]);
-        pos_l = advance<KB>(pos_l, a.nsb);
-        __builtin_amdgcn_sched_barrier(0);
-        store(std::integral_constant<int, K + 1>{}, wq[JN]);
-        __builtin_amdgcn_sched_barrier(0);
-
-        const u32x4* st = stage(kk);
-        read_b(bq[0], st, wk);
-        Pos p = pos_c;
-        auto one = [&](auto tt) {
-            constexpr int t = decltype(tt)::value;
-            // position of the next block: the next step's, or the first block
-            // of the next chunk
-            const Pos pnext = advance<WK>(p, a.nsb);
-            float xv[RF];
-            if constexpr (!GEN_SPLIT) {
-#pragma unroll
-                for (int rf = 0; rf < RF; ++rf) xv[rf] = x_value(pnext, xr[t][rf]);
-                if (pnext.bsub == 0) silu_of(xv, sl);
-            }
-            if constexpr (LASTG) {
-                if (c * KBW + t >= nq) {  // past the wave's last real block: contribute 0
-#pragma unroll
-                    for (int rf = 0; rf < RF; ++rf) zero_frag(A_cur, rf);
-                }
-            }
-            // One wave per SIMD: the next block's B is read during this step.
-            // Two waves: B is read at the start of each step; the other wave
-            // covers the latency, and the registers of a second B set are
-            // saved.
-            constexpr bool PREF = Occ<RF, NF>::waves == 1 && t + 1 < KBW;
-            if constexpr (Occ<RF, NF>::waves == 2 && t > 0) read_b(bq[t & 1], st, wk + WK * t);
-            if constexpr (GEN_SPLIT)
-                step_split(A_cur, bq[t & 1], pnext, xr[t], A_nxt);
-            else
-                step(A_cur, bq[t & 1], pnext, xv, sl, A_nxt, std::integral_constant<bool, PREF>{},
-                     bq[(t + 1) & 1], st, wk + WK * (t + 1));
-            A_cur = A_nxt;
-            p = pnext;
-        };
-        StaticFor<0, KBW>::run(one);
-        pos_c = p;
-    };
-
-    // Every wave's blocks are all real in every group but the final one.
-    const int ngroups = (a.nchunks + U - 1) / U;
-#pragma unroll 1
-    for (int gi = 0; gi + 1 < ngroups; ++gi) {
-        auto group = [&](auto kk) {
-            chunk(gi * U + decltype(kk)::value, kk, std::false_type{});
-        };
-        StaticFor<0, U>::run(group);
-    }
-    {
-        const int gi = ngroups - 1;
-        auto group = [&](auto kk) {
-            chunk(gi * U + decltype(kk)::value, kk, std::true_type{});
-        };
-        StaticFor<0, U>::run(group);
-    }
-    __syncthreads();
-
-    // ---- epilogue: y = 2 acc (the operands carry N / 2 and silu / 2)
-    const int col0 = nt * NTILE;
-    if constexpr (WK == 1) {
-        const bool full = row0 + 32 * RF <= a.batch && col0 + NTILE <= a.out;
-#pragma unroll
-        for (int rf = 0; rf < RF; ++rf) {
-#pragma unroll
-            for (int nf = 0; nf < NF; ++nf) {
-                const int col = col0 + nf * 32 + r;
-#pragma unroll
-                for (int q = 0; q < 16; ++q) {
-                    const int64_t row = row0 + rf * 32 + 8 * (q / 4) + 4 * h + (q % 4);
-                    if (full || (row < a.batch && col < a.out))
-                        Tr<T>::store(y + row * a.out + col, 2.0f * acc[rf][nf][q]);
-                }
-            }
-        }
-    } else {
-        // Waves with the same wm hold partial sums of the same rows: write all
-        // partials to LDS (the weight buffers are free after the last
-        // barrier), then every thread sums WK partials of some elements and
-        // stores them row-major (coalesced).
-        constexpr int TILE = 32 * RF * NTILE;  // floats per wave
-        auto red = [&](int w) -> float* { return reinterpret_cast<float*>(smem) + w * TILE; };
-        float* mine = red(wave);
-#pragma unroll
-        for (int rf = 0; rf < RF; ++rf)
-#pragma unroll
-            for (int nf = 0; nf < NF; ++nf)
-#pragma unroll
-                for (int q = 0; q < 16; ++q) {
-                    const int rl = rf * 32 + 8 * (q / 4) + 4 * h + (q % 4);
-                    mine[rl * NTILE + nf * 32 + r] = acc[rf][nf][q];
-                }
-        __syncthreads();
-        const int64_t bm0 = (int64_t)blockIdx.x * BM;
-        for (int idx = tid; idx < WM * TILE; idx += NT) {
-            const int g = idx / TILE;
-            const int rem = idx % TILE;
-            const int rl = rem / NTILE;
-            const int cl = rem % NTILE;
-            float sum = 0.0f;
-#pragma unroll
-            for (int w = 0; w < WK; ++w) sum += red(g + WM * w)[rem];
-            const int64_t row = bm0 + g * 32 * RF + rl;
-            const int col = col0 + cl;
-            if (row < a.batch && col < a.out) Tr<T>::store(y + row * a.out + col, 2.0f * sum);
-        }
-    }
-}
-
-template <typename T, int RF, int NF, int WK, int NW = 4>
-hipError_t launch_cfg(const LayerGeom& g, LayerArgs a, hipStream_t s) {
-    constexpr int WM = NW / WK;
-    constexpr int BM = 32 * RF * WM;
-    a.nblk_pad = g.nblk_pad;
-    a.nchunks = g.nblk_pad / g.kb;
-    const dim3 grid((unsigned)((a.batch + BM - 1) / BM), (unsigned)g.ntiles);
-    hipLaunchKernelGGL((layer_kernel<T, RF, NF, WK, NW>), grid, dim3(64 * NW), 0, s, a);
-    return hipGetLastError();
-}
-
-template <typename T, int NF>
-hipError_t launch_nf(const LayerGeom& g, const LayerCfg& c, const LayerArgs& a, hipStream_t s) {
-    if (c.nw == 8) {
-        // eight waves: one 32-row tile each (chunks of at least 8 KB)
-        if constexpr (layer_chunk_blocks(sizeof(T) == 2, NF) * layer_block_bytes(sizeof(T) == 2, NF) >= 8192)
-            if (c.rf == 1 && c.wk == 1) return launch_cfg<T, 1, NF, 1, 8>(g, a, s);
-        return hipErrorInvalidValue;
-    }
-    if (c.wk == 1) {
-        if (c.rf == 1) return launch_cfg<T, 1, NF, 1>(g, a, s);
-        if (c.rf == 2) return launch_cfg<T, 2, NF, 1>(g, a, s);
-    }
-    if constexpr (NF <= 4) {
-        if (c.rf == 1 && c.wk == 2) return launch_cfg<T, 1, NF, 2>(g, a, s);
-        if (c.rf == 1 && c.wk == 4) return launch_cfg<T, 1, NF, 4>(g, a, s);
-    }
-    if constexpr (NF <= 2) {
-        if (c.rf == 2 && c.wk == 2) return launch_cfg<T, 2, NF, 2>(g, a, s);
-        if (c.rf == 2 && c.wk == 4) return launch_cfg<T, 2, NF, 4>(g, a, s);
-    }
-    return hipErrorInvalidValue;
-}
-
-template <typename T>
-hipError_t launch_t(const LayerGeom& g, const LayerCfg& c, const LayerArgs& a, hipStream_t s) {
-    switch (g.nf) {
-        case 1: return launch_nf<T, 1>(g, c, a, s);
-        case 2: return launch_nf<T, 2>(g, c, a, s);
-        case 4: return launch_nf<T, 4>(g, c, a, s);
-        case 8:
-            if constexpr (sizeof(T) == 2) return launch_nf<T, 8>(g, c, a, s);
-            return hipErrorInvalidValue;
-        default: return hipErrorInvalidValue;
-    }
-}
-
 }  // namespace
 
 // ------------------------------------------------------------------ planning
@@ -765,41 +97,56 @@ bool layer_geom(int nb, bool bf16, int in, int out, LayerGeom* g) {
 }
 
 bool layer_cfg_valid(const LayerGeom& g, const LayerCfg& c) {
-    if (c.rf != 1 && c.rf != 2) return false;
-    if (c.wk != 1 && c.wk != 2 && c.wk != 4) return false;
-    if (c.nw == 8)  // eight 32-row waves, no K split, chunks of at least 8 KB
-        return c.rf == 1 && c.wk == 1 && g.kb * 2 * 32 * g.nf * g.kj * (g.kj == 8 ? 2 : 4) >= 8192;
-    if (c.nw != 4) return false;
-    return c.wk == 1 || c.rf * g.nf <= 4;
+    return layer_shape_ok(g.kj == 8, g.nf, c.rf, c.wk, c.nw, c.cs);
 }
 
 LayerCfg plan_layer(const LayerGeom& g, bool bf16, int64_t batch) {
     auto wgs = [&](const LayerCfg& c) {
         const int64_t bm = 32LL * c.rf * (c.nw / c.wk);
-        return ((batch + bm - 1) / bm) * g.ntiles;
+        return ((batch + bm - 1) / bm) * g.ntiles * c.cs;
     };
     // bf16 with 256-column tiles: 32-row waves (two per SIMD, accumulators in
     // 128 registers) overlap one wave's basis VALU work with the other's MFMAs;
     // 64-row waves (256 accumulator registers) run one wave per SIMD, which
     // measured slower on MI355X.  Eight waves per workgroup halve the weight
-    // traffic per row.
-    if (bf16 && g.nf == 8) return LayerCfg{1, 1, 8};
-    // Otherwise the tallest workgroup (fewest re-reads of the weights) that
-    // still gives at least `want` workgroups; the basis-generation-bound
-    // narrow bf16 layers want more, smaller workgroups.
+    // traffic per row.  Used when it fills the chip (one workgroup per CU).
+    const LayerCfg wide{1, 1, 8, 1};
+    if (bf16 && g.nf == 8 && wgs(wide) >= 256) return wide;
+    // Otherwise the tallest workgroup over the whole N tile (fewest re-reads
+    // of the weights, basis values generated once per tile) that still gives
+    // at least `want` workgroups; the basis-generation-bound narrow bf16
+    // layers want more, smaller workgroups.  Splitting the tile's columns over
+    // 2 or 4 workgroups (each stages only its columns and regenerates the
+    // basis) measured slower whenever every CU already had a workgroup, so it
+    // is taken only for batches too small for that.
     const int64_t want = (bf16 && g.nf == 1) ? 1024 : 512;
-    const LayerCfg cands[] = {{2, 1, 4}, {1, 1, 4}, {1, 2, 4}, {1, 4, 4}};
-    for (const LayerCfg& c : cands)
-        if (layer_cfg_valid(g, c) && wgs(c) >= want) return c;
-    return LayerCfg{1, 4, 4};
+    const LayerCfg whole[] = {{2, 1, 4, 1}, {1, 1, 4, 1}, {1, 2, 4, 1}, {1, 4, 4, 1}};
+    const LayerCfg sliced[] = {{1, 1, 4, 2}, {1, 2, 4, 2}, {1, 4, 4, 2},
+                               {1, 1, 4, 4}, {1, 2, 4, 4}, {1, 4, 4, 4}};
+    LayerCfg best{1, 1, 4, 1};
+    int64_t best_wgs = 0;
+    for (const LayerCfg& c : whole) {
+        if (!layer_cfg_valid(g, c)) continue;
+        const int64_t w = wgs(c);
+        if (w >= want) return c;
+        if (w > best_wgs) { best = c; best_wgs = w; }
+    }
+    if (best_wgs >= 256) return best;
+    for (const LayerCfg& c : sliced) {
+        if (!layer_cfg_valid(g, c)) continue;
+        const int64_t w = wgs(c);
+        if (w > best_wgs) { best = c; best_wgs = w; }
+        if (w >= 256) return c;
+    }
+    return best;  // the most workgroups any shape gives
 }
 
 bool parse_layer_cfg_override(const LayerGeom& g, LayerCfg* c) {
     const char* s = std::getenv("KAN_LAYER_CFG");
     if (!s || !*s) return false;
-    LayerCfg t{0, 0, 4};
-    const int n = std::sscanf(s, "%d,%d,%d", &t.rf, &t.wk, &t.nw);
-    if (n != 2 && n != 3) return false;
+    LayerCfg t{0, 0, 4, 1};
+    const int n = std::sscanf(s, "%d,%d,%d,%d", &t.rf, &t.wk, &t.nw, &t.cs);
+    if (n < 2) return false;
     if (!layer_cfg_valid(g, t)) return false;
     *c = t;
     return true;
@@ -830,7 +177,7 @@ hipError_t launch_pack(bool bf16, const LayerGeom& g, int in, int out, const voi
 hipError_t launch_layer(bool bf16, const LayerGeom& g, const LayerCfg& c, LayerArgs a,
                         hipStream_t s) {
     if (!layer_cfg_valid(g, c)) return hipErrorInvalidValue;
-    return bf16 ? launch_t<uint16_t>(g, c, a, s) : launch_t<float>(g, c, a, s);
+    return bf16 ? launch_layer_bf16(g, c, a, s) : launch_layer_f32(g, c, a, s);
 }
 
 }  // namespace kan

@@ -63,10 +63,11 @@ def test_layer_matches_oracle(B, n_in, n_out, G, dtype_name):
     assert normwise(y, ref) <= _tol(dtype_name), normwise(y, ref)
 
 
-# (rows tiles per wave, waves splitting K[, waves per workgroup]) of the fused
-# kernel; K splits need rf * nf <= 4 (nf = 32-column fragments of the column
-# tile); eight-wave workgroups take one row tile per wave and no K split.
-CFGS = ["1,1", "2,1", "1,2", "1,4", "2,2", "2,4", "1,1,8"]
+# (rows tiles per wave, waves splitting K[, waves per workgroup[, column
+# slices per tile]]) of the fused kernel; K splits need rf * nf <= 4 (nf =
+# 32-column fragments a workgroup computes); eight-wave workgroups take one
+# row tile per wave and no K split; column slices take rf = 1, four waves.
+CFGS = ["1,1", "2,1", "1,2", "1,4", "2,2", "2,4", "1,1,8", "1,1,4,2", "1,2,4,2", "1,4,4,2"]
 
 
 @pytest.mark.parametrize("dtype_name", ["f32", "bf16"])
@@ -101,6 +102,16 @@ WIDE = [
     ("f32", 333, 7, 128, 50, "2,1"),
     ("f32", 97, 3, 100, 200, "1,2"),
     ("f32", 600, 20, 256, 10, "1,1,8"),
+    # column slices of the widest tiles
+    ("bf16", 600, 20, 256, 10, "1,1,4,2"),
+    ("bf16", 333, 7, 200, 50, "1,2,4,2"),
+    ("bf16", 600, 20, 256, 10, "1,1,4,4"),
+    ("bf16", 97, 3, 130, 200, "1,2,4,4"),
+    ("bf16", 300, 5, 100, 50, "1,4,4,4"),
+    ("f32", 600, 20, 256, 10, "1,1,4,2"),
+    ("f32", 333, 7, 128, 50, "1,4,4,2"),
+    ("f32", 97, 3, 100, 200, "1,2,4,4"),
+    ("f32", 600, 20, 256, 10, "1,4,4,4"),
 ]
 
 
