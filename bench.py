@@ -69,17 +69,34 @@ def copy_calibration(nbytes: int) -> None:
     print(json.dumps({"copy_calibration_bytes": n * 4, "launches": 10}), flush=True)
 
 
-KERNEL_SOURCES = ["kan_layer.hip", "kan_internal.h", "kan_device.h"]
+def layer_roofline(dtype: str, batch: int, n_in: int, n_out: int, nb: int) -> dict:
+    """Roofline of one fused layer: bound by the matrix cores (dense flops,
+    all nb bases plus the SiLU column per input) unless generating its basis
+    values takes longer at the VALU peak than the contraction at the MFMA
+    peak (narrow outputs); then it is reported against the VALU."""
+    flop = 2.0 * batch * n_out * n_in * (nb + 1)
+    valu = VALU_OPS_PER_VALUE[dtype] * batch * n_in * (nb + 1)
+    if valu / (PEAK_VALU_GOPS * 1e9) > flop / (PEAK_TFLOPS[dtype] * 1e12):
+        k = {"bound": "alu", "unit": "Gop/s", "peak": PEAK_VALU_GOPS,
+             "algorithmic": valu / 1e9}  # G lane-ops
+    else:
+        k = {"bound": "mfma", "unit": "TFLOP/s", "peak": PEAK_TFLOPS[dtype],
+             "algorithmic": flop / 1e12}  # dense TFLOP
+    k["valu_gops"] = valu / 1e9
+    return k
 
 
-def traffic_record(dtype: str, kernel: str):
+KERNEL_SOURCES = ["kan_layer_kernel.h", "kan_layer.hip", "kan_internal.h", "kan_device.h"]
+
+
+def traffic_record(dtype: str, kernel: str, root: str = ROOT):
     """HBM bytes per launch of `kernel`, from the committed rocprofv3 counter
     summary (FETCH_SIZE and WRITE_SIZE, each scaled by its plain-copy
     calibration factor), or None when there is no record for this dtype and
     kernel or the kernel sources have changed since the counters were taken."""
     import hashlib
 
-    path = os.path.join(ROOT, "profiles", f"kan_mlp_c5_{dtype}_hbm_traffic.md")
+    path = os.path.join(root, "profiles", f"kan_mlp_c5_{dtype}_hbm_traffic.md")
     if not os.path.exists(path):
         return None
     lines = open(path).read().splitlines()
@@ -93,7 +110,7 @@ def traffic_record(dtype: str, kernel: str):
         rec[k.strip()] = v.strip()
     h = hashlib.md5()
     for f in KERNEL_SOURCES:
-        with open(os.path.join(ROOT, "paper_2609_01956_amd", "csrc", f), "rb") as fh:
+        with open(os.path.join(root, "paper_2609_01956_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     if (rec.get("kernel_sources_md5") != h.hexdigest() or rec.get("dtype") != dtype
             or rec.get("kernel") != kernel):
@@ -270,19 +287,7 @@ def main() -> int:
         kern[names[1 + 2 * li]] = {
             "bound": "hbm", "unit": "GB/s", "peak": PEAK_HBM_GBS,
             "algorithmic": (o * i_ * (nb + 1) * es + packs[li].nbytes) / 1e9}
-        # The fused layer is bound by the matrix cores unless generating its
-        # basis values takes longer at the VALU peak than the contraction at
-        # the MFMA peak (narrow outputs): then it is reported against the VALU.
-        flop = 2.0 * B * o * i_ * (nb + 1)
-        valu = VALU_OPS_PER_VALUE[args.dtype] * B * i_ * (nb + 1)
-        if valu / (PEAK_VALU_GOPS * 1e9) > flop / (PEAK_TFLOPS[args.dtype] * 1e12):
-            kern[names[2 + 2 * li]] = {"bound": "alu", "unit": "Gop/s", "peak": PEAK_VALU_GOPS,
-                                       "algorithmic": valu / 1e9}  # G lane-ops
-        else:
-            kern[names[2 + 2 * li]] = {"bound": "mfma", "unit": "TFLOP/s",
-                                       "peak": PEAK_TFLOPS[args.dtype],
-                                       "algorithmic": flop / 1e12}  # dense TFLOP
-        kern[names[2 + 2 * li]]["valu_gops"] = valu / 1e9
+        kern[names[2 + 2 * li]] = layer_roofline(args.dtype, B, i_, o, nb)
     for name, ms in zip(names, per_kernel_ms):
         k = kern[name]
         k["avg_us"] = ms * 1e3
