@@ -8,21 +8,16 @@
 // left operand is never stored: every lane generates its own A elements in
 // registers, directly in the MFMA operand layout, from one x value per block.
 //
-// Two kernels:
-//   pack_kernel    rearranges coef / base_w into the block order described in
-//                  kan_internal.h (a few MB, read once per call);
-//   layer_kernel   4 or 8 waves per workgroup.  The workgroup walks the blocks
-//                  in chunks of up to 16 KB of packed weights: each chunk is
-//                  loaded into registers a few chunks ahead, written to one of
-//                  two LDS stages while the previous chunk is multiplied, and
-//                  read from LDS by every wave.  Each wave owns rf 32-row
-//                  tiles of all nf 32-column fragments of the N tile, so every
-//                  generated A element feeds nf MFMAs and every B fragment read
-//                  from LDS feeds rf MFMAs.  With two waves per SIMD a wave
-//                  generates the next block's A and then issues the current
-//                  block's MFMAs, so one wave's VALU work overlaps the other's
-//                  matrix work; with one wave per SIMD the two interleave
-//                  within the wave.
+// layer_kernel: 4 or 8 waves per workgroup.  The workgroup walks the blocks
+// of packed weights (kan_internal.h) in chunks of up to 16 KB: each chunk is
+// loaded into registers two chunks ahead, written to one of two LDS stages
+// while the previous chunk is multiplied, and read from LDS by every wave.
+// Each wave owns rf 32-row tiles of nf 32-column fragments, so every
+// generated A element feeds nf MFMAs and every B fragment read from LDS feeds
+// rf MFMAs.  With two waves per SIMD a wave generates the next block's A and
+// then issues the current block's MFMAs, so one wave's VALU work overlaps the
+// other's matrix work; with one wave per SIMD the two interleave within the
+// wave.
 //
 // Basis values are N_j / 2 = P^3 - Q^3 (half_basis, kan_device.h).  The MFMA
 // operands are N_j / 2 and silu / 2, and the epilogue doubles y: scaling by a
@@ -80,9 +75,11 @@ template <> struct Tr<uint16_t> {
 // and zero-padded to a whole number of blocks, so column c of the feature is
 // basis c - 1 for c >= 1.  Block b, element e is column KJ * b + e: a basis
 // value at v = s_b - e with s_b = v of basis KJ * b - 1, except column 0 (the
-// SiLU value).  Columns past nb are evaluated like any other basis (finite
-// values) and meet zero weights.  Every block is therefore generated by the
-// same straight-line code; only element 0 of block 0 is replaced.
+// SiLU value).  fp32 (and bf16 with one wave per SIMD) generates every block
+// with the same straight-line code: columns past nb are evaluated like any
+// other basis (finite values that meet zero weights) and element 0 of block 0
+// is replaced.  bf16 with two waves per SIMD picks the code by the block's
+// place in its pair (gen_split).
 template <typename T, int RF> struct AFrag;
 template <int RF> struct AFrag<uint16_t, RF> { bf16x8 a[RF]; };
 template <int RF> struct AFrag<float, RF> { float a[RF][2]; };
@@ -183,8 +180,9 @@ void layer_kernel(LayerArgs a) {
     constexpr int BM = 32 * RF * WM;             // rows per workgroup
     // Weights of chunk c are loaded into registers L chunks ahead (register
     // set c % L), written to LDS stage c % 2 while chunk c - 1 is multiplied,
-    // and read from there during chunk c.
-    constexpr int L = DPW <= 2 ? 3 : 2;
+    // and read from there during chunk c.  (Two chunks ahead measured faster
+    // than three: the loop body, unrolled by lcm(2, L), stays small.)
+    constexpr int L = 2;
     constexpr int U = L % 2 == 0 ? L : 2 * L;    // chunk-loop unroll, lcm(2, L)
     constexpr int PART = WK > 1 ? 32 * RF * NTILE * 4 : 0;  // one wave's partial sums
     constexpr int SMEM = 2 * CHB > NW * PART ? 2 * CHB : NW * PART;
