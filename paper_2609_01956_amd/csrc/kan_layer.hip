@@ -114,12 +114,12 @@ LayerCfg plan_layer(const LayerGeom& g, bool bf16, int64_t batch) {
     if (bf16 && g.nf == 8 && wgs(wide) >= 256) return wide;
     // Otherwise the tallest workgroup over the whole N tile (fewest re-reads
     // of the weights, basis values generated once per tile) that still gives
-    // at least `want` workgroups; the basis-generation-bound narrow bf16
-    // layers want more, smaller workgroups.  Splitting the tile's columns over
+    // at least `want` workgroups; the basis-generation-bound narrow layers
+    // (one 32-column fragment) want more, smaller workgroups.  Splitting the tile's columns over
     // 2 or 4 workgroups (each stages only its columns and regenerates the
     // basis) measured slower whenever every CU already had a workgroup, so it
     // is taken only for batches too small for that.
-    const int64_t want = (bf16 && g.nf == 1) ? 1024 : 512;
+    const int64_t want = g.nf == 1 ? 1024 : 512;
     const LayerCfg whole[] = {{2, 1, 4, 1}, {1, 1, 4, 1}, {1, 2, 4, 1}, {1, 4, 4, 1}};
     const LayerCfg sliced[] = {{1, 1, 4, 2}, {1, 2, 4, 2}, {1, 4, 4, 2},
                                {1, 1, 4, 4}, {1, 2, 4, 4}, {1, 4, 4, 4}};
