@@ -49,6 +49,10 @@ def parse():
     p.add_argument("--cpu-seconds", type=float, default=10.0,
                    help="target wall time of the CPU oracle sample")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--configs", action="store_true",
+                   help="only time the fused layer and the basis kernel on every configured "
+                        "workload (one JSON line each, with the partition-of-unity error of "
+                        "the grid-size sweep) and exit")
     p.add_argument("--mfma-ceiling", action="store_true",
                    help="only measure back-to-back bf16 MFMA throughput and the shader clock "
                         "with constant and with random operands (libkan_probe.so) and exit")
@@ -118,6 +122,69 @@ def traffic_record(dtype: str, kernel: str, root: str = ROOT):
     kib = (float(rec["fetch_kib"]) * float(rec["fetch_factor"]) +
            float(rec["write_kib"]) * float(rec["write_factor"]))
     return kib * 1024.0
+
+
+def _time_us(fn, warmup: int = 5, reps: int = 20) -> float:
+    import torch
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        fn()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) * 1e3 / reps
+
+
+def configs_sweep(dtype: str) -> None:
+    """Every configured workload, one JSON line each: the fused layer (packed
+    weights, per layer of the MLP) against its roofline, the basis-only kernel
+    of its input, and for the grid-size sweep the partition-of-unity error of
+    the basis kernel on the same x plus 2001 points spread over the grid."""
+    import numpy as np
+    import torch
+
+    from paper_2609_01956_amd import binding as kb
+    from paper_2609_01956_amd import workloads as wl
+
+    kb.load_library()
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    es = 2 if dtype == "bf16" else 4
+    prep = (lambda a: wl.round_to_bf16_f32(a)) if dtype == "bf16" else (lambda a: a)
+    for name in wl.WORKLOADS:
+        W = wl.make_workload(name)
+        G, lo, hi = W["G"], W["lo"], W["hi"]
+        nb = G + 3
+        x = torch.from_numpy(prep(W["x"])).to("cuda").to(tdt).contiguous()
+        B, n_in0 = x.shape
+        phi = torch.empty((B, n_in0, nb), dtype=tdt, device="cuda")
+        us = _time_us(lambda: kb.basis(x, G, lo, hi, out=phi))
+        line = {"workload": name, "dtype": dtype, "batch": B, "grid_size": G,
+                "basis_eval": {"us": us, "gbasis_per_s": B * n_in0 * nb / us / 1e3,
+                               "hbm_frac": B * n_in0 * (nb + 1) * es / us / 1e3 / PEAK_HBM_GBS}}
+        if name.startswith("c4_"):
+            xs = np.concatenate([W["x"].reshape(-1), np.linspace(lo, hi, 2001)]).astype(np.float32)
+            pu = kb.basis(torch.from_numpy(xs).to("cuda"), G, lo, hi).double().sum(dim=1)
+            line["pu_max_err"] = float((pu - 1.0).abs().max())
+        h = x
+        layers = []
+        for C, Wb in W["layers"]:
+            Ct = torch.from_numpy(prep(C)).to("cuda").to(tdt).contiguous()
+            Wt = torch.from_numpy(prep(Wb)).to("cuda").to(tdt).contiguous()
+            pk = kb.pack_layer(Ct, Wt, G, lo, hi)
+            out = torch.empty((B, C.shape[0]), dtype=tdt, device="cuda")
+            lus = _time_us(lambda: kb.layer_forward_packed(h, pk, out=out))
+            k = layer_roofline(dtype, B, C.shape[1], C.shape[0], nb)
+            k.pop("valu_gops")
+            k.update(us=lus, samples_per_s=B / lus * 1e6, achieved=k["algorithmic"] / (lus * 1e-6))
+            k["frac"] = k["achieved"] / k["peak"]
+            layers.append({"in": C.shape[1], "out": C.shape[0], **k})
+            h = out
+        line["layers"] = layers
+        print(json.dumps(line), flush=True)
 
 
 def mfma_ceiling() -> None:
@@ -211,6 +278,9 @@ def main() -> int:
         return 0
     if args.mfma_ceiling:
         mfma_ceiling()
+        return 0
+    if args.configs:
+        configs_sweep(args.dtype)
         return 0
     kb.load_library()
     dev = torch.device("cuda:0")
