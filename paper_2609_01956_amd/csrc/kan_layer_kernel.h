@@ -546,8 +546,13 @@ void layer_kernel(LayerArgs a) {
         issue(c + L, pos_l, xq[J], wq[J]);
         pos_l = advance<KB>(pos_l, a.nsb);
         __builtin_amdgcn_sched_barrier(0);
-        store(std::integral_constant<int, K + 1>{}, wq[JN]);
-        __builtin_amdgcn_sched_barrier(0);
+        // The next chunk's weights go to the other LDS stage before the next
+        // barrier.  With the split generation they are stored after the
+        // first step, which gives their loads that step's time to land.
+        if constexpr (!GEN_SPLIT) {
+            store(std::integral_constant<int, K + 1>{}, wq[JN]);
+            __builtin_amdgcn_sched_barrier(0);
+        }
 
         const u32x4* st = stage(kk);
         read_b(bq[0], st, wk);
@@ -582,6 +587,11 @@ void layer_kernel(LayerArgs a) {
                      bq[(t + 1) & 1], st, wk + WK * (t + 1));
             A_cur = A_nxt;
             p = pnext;
+            if constexpr (GEN_SPLIT && t == 0) {
+                __builtin_amdgcn_sched_barrier(0);
+                store(std::integral_constant<int, K + 1>{}, wq[JN]);
+                __builtin_amdgcn_sched_barrier(0);
+            }
         };
         StaticFor<0, KBW>::run(one);
         pos_c = p;
