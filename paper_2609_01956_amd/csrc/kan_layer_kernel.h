@@ -159,7 +159,8 @@ struct Occ {
 
 // NFL: 32-column fragments per N tile of the packed layout; NF: fragments of
 // the tile this workgroup computes (a column slice, NFL / NF slices per tile).
-template <typename T, int RF, int NFL, int NF, int WK, int NW>
+// NSBC: blocks per feature when fixed at compile time (0: a.nsb at run time).
+template <typename T, int RF, int NFL, int NF, int WK, int NW, int NSBC = 0>
 __global__ __launch_bounds__(64 * NW)
 __attribute__((amdgpu_waves_per_eu(Occ<RF, NF>::waves)))
 void layer_kernel(LayerArgs a) {
@@ -189,6 +190,12 @@ void layer_kernel(LayerArgs a) {
     static_assert(CHB % (1024 * NW) == 0 && KB % WK == 0 && KB >= WK, "chunk shape");
     static_assert(NW == 4 || (NW == 8 && WK == 1), "waves per workgroup");
     static_assert(SMEM <= 64 * 1024, "LDS budget");
+    // With a compile-time block count per feature that divides the wave's
+    // blocks per chunk (and no K split), every chunk starts a feature: the
+    // place of each step's block in its feature is a compile-time constant.
+    constexpr bool ALIGNED = NSBC > 0 && WK == 1 && KBW % NSBC == 0;
+    static_assert(NSBC == 0 || ALIGNED, "compile-time blocks per feature");
+    const int nsb = NSBC > 0 ? NSBC : a.nsb;
     static_assert(BLKB == 2 * NTILE * LANEB && NFL % NF == 0, "block layout");
     // LDS: two chunk stages; after the main loop the K-split partial sums.
     __shared__ u32x4 smem[SMEM / 16];
@@ -260,7 +267,7 @@ void layer_kernel(LayerArgs a) {
 #pragma unroll
             for (int rf = 0; rf < RF; ++rf)
                 xs[t][rf] = Tr<T>::raw(xw + (xoff[rf] + (uint32_t)(2 * pr) - back));
-            p = advance<WK>(p, a.nsb);
+            p = advance<WK>(p, nsb);
         }
         const int cc = c < a.nchunks ? c : a.nchunks - 1;
         const char* g = wpt + (size_t)cc * (KB * BLKBL);  // wave-uniform
@@ -404,7 +411,7 @@ void layer_kernel(LayerArgs a) {
     constexpr bool DIRECT = WK > 1;
     float sc[RF];  // coordinate of the wave's current block (element 0)
     // real columns in the last block of a feature, rounded up to even
-    const int last_cols = a.nb + 1 - KJ * (a.nsb - 1);
+    const int last_cols = a.nb + 1 - KJ * (nsb - 1);
     const int last_even = (last_cols + 1) & ~1;
     auto gen_split = [&](const Pos& pg, const uint32_t (&xr)[RF], AFrag<T, RF>& An) {
       if constexpr (GEN_SPLIT) {
@@ -435,7 +442,7 @@ void layer_kernel(LayerArgs a) {
 #pragma unroll
             for (int rf = 0; rf < RF; ++rf) sc[rf] -= (float)KJ;
         }
-        if (pg.bsub != a.nsb - 1 || last_even == KJ) {
+        if (pg.bsub != nsb - 1 || last_even == KJ) {
 #pragma unroll
             for (int rf = 0; rf < RF; ++rf) basis(rf, 0, KJ);
         } else if (last_even == 6) {
@@ -487,14 +494,14 @@ void layer_kernel(LayerArgs a) {
     float sl[RF];
     AFrag<T, RF> A_cur, A_nxt;
     BFrag bq[2];
-    Pos pos_c = advance_n(Pos{0, 0, 0}, wk, a.nsb);  // first block of the current chunk
+    Pos pos_c = advance_n(Pos{0, 0, 0}, wk, nsb);  // first block of the current chunk
     Pos pos_l = pos_c;                               // first block of the next chunk to load
 
     // prologue: loads of chunks 0 .. L - 1, chunk 0 to stage 0
     auto prologue = [&](auto jj) {
         constexpr int j = decltype(jj)::value;
         issue(j, pos_l, xq[j], wq[j]);
-        pos_l = advance<KB>(pos_l, a.nsb);
+        pos_l = advance<KB>(pos_l, nsb);
     };
     StaticFor<0, L>::run(prologue);
     store(std::integral_constant<int, 0>{}, wq[0]);
@@ -530,6 +537,10 @@ void layer_kernel(LayerArgs a) {
         constexpr bool LASTG = decltype(last_tag)::value;  // in the final group
         constexpr int J = K % L;          // register set of chunk c (and of c + L)
         constexpr int JN = (K + 1) % L;   // register set of chunk c + 1
+        if constexpr (ALIGNED) {
+            pos_c.bsub = 0;
+            pos_l.bsub = 0;
+        }
         if (c > 0) {  // (chunk 0's barrier is in the prologue)
             __builtin_amdgcn_s_waitcnt(WAIT_LDS);
             __builtin_amdgcn_s_barrier();
@@ -544,7 +555,7 @@ void layer_kernel(LayerArgs a) {
             for (int rf = 0; rf < RF; ++rf) xr[t][rf] = t + 1 < KBW ? xq[J][t + 1][rf] : xq[JN][0][rf];
         __builtin_amdgcn_sched_barrier(0);
         issue(c + L, pos_l, xq[J], wq[J]);
-        pos_l = advance<KB>(pos_l, a.nsb);
+        pos_l = advance<KB>(pos_l, nsb);
         __builtin_amdgcn_sched_barrier(0);
         // The next chunk's weights go to the other LDS stage before the next
         // barrier.  With the split generation they are stored after the
@@ -561,7 +572,7 @@ void layer_kernel(LayerArgs a) {
             constexpr int t = decltype(tt)::value;
             // position of the next block: the next step's, or the first block
             // of the next chunk
-            const Pos pnext = advance<WK>(p, a.nsb);
+            const Pos pnext = advance<WK>(p, nsb);
             float xv[RF];
             if constexpr (!GEN_SPLIT) {
 #pragma unroll
@@ -673,6 +684,18 @@ hipError_t launch_cfg(const LayerGeom& g, LayerArgs a, hipStream_t s) {
     a.nblk_pad = g.nblk_pad;
     a.nchunks = g.nblk_pad / g.kb;
     const dim3 grid((unsigned)((a.batch + BM - 1) / BM), (unsigned)(g.ntiles * (NFL / NF)));
+    // Two blocks per feature (bf16, 5 <= G <= 12) get their own build where
+    // the split generation can use it (two waves per SIMD, no K split, whole
+    // features per chunk).
+    constexpr bool BF16 = sizeof(T) == 2;
+    if constexpr (BF16 && Occ<RF, NF>::waves == 2 && WK == 1 &&
+                  layer_chunk_blocks(BF16, NFL) % 2 == 0) {
+        if (g.nsb == 2) {
+            hipLaunchKernelGGL((layer_kernel<T, RF, NFL, NF, WK, NW, 2>), grid, dim3(64 * NW), 0,
+                               s, a);
+            return hipGetLastError();
+        }
+    }
     hipLaunchKernelGGL((layer_kernel<T, RF, NFL, NF, WK, NW>), grid, dim3(64 * NW), 0, s, a);
     return hipGetLastError();
 }
