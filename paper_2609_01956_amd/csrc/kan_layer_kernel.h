@@ -160,7 +160,9 @@ struct Occ {
 // NFL: 32-column fragments per N tile of the packed layout; NF: fragments of
 // the tile this workgroup computes (a column slice, NFL / NF slices per tile).
 // NSBC: blocks per feature when fixed at compile time (0: a.nsb at run time).
-template <typename T, int RF, int NFL, int NF, int WK, int NW, int NSBC = 0>
+// XP (bf16): x read as the aligned 32-bit word holding the element (x 4-byte
+// aligned and batch * in even, so the word never leaves the tensor).
+template <typename T, int RF, int NFL, int NF, int WK, int NW, int NSBC = 0, bool XP = false>
 __global__ __launch_bounds__(64 * NW)
 __attribute__((amdgpu_waves_per_eu(Occ<RF, NF>::waves)))
 void layer_kernel(LayerArgs a) {
@@ -233,6 +235,13 @@ void layer_kernel(LayerArgs a) {
     // With an odd feature count the last pair has a phantom second feature
     // (zero weights): its lanes read the real last feature and use x = 0.
     const int last_pair_odd = (a.in & 1) ? a.in / 2 : -1;
+    // XP: byte selector that moves the lane's half of the loaded word to the
+    // top of a float (the half is the parity of its element offset, the same
+    // for every pair; the phantom lanes' value is replaced by 0 anyway).
+    static_assert(!XP || sizeof(T) == 2, "paired x reads are for bf16");
+    uint32_t xsel[RF];
+#pragma unroll
+    for (int rf = 0; rf < RF; ++rf) xsel[rf] = (xoff[rf] & 1u) ? 0x03020c0cu : 0x01000c0cu;
 
     // ---- loads of chunk c into register set j, for the wave's blocks from
     // position p on: first the x of each block and row tile (per lane: the
@@ -247,6 +256,12 @@ void layer_kernel(LayerArgs a) {
     // and masking happen where the values are used, so nothing waits for a
     // load when it is issued.
     typedef uint32_t XSet[KBW][RF];
+    constexpr bool X_FIRST_ONLY = ALIGNED && BF16 && Occ<RF, NF>::waves == 2;
+    // One feature pair per chunk: the x of the next chunk's pair is converted
+    // where the chunk stores the next chunk's weights (their loads were issued
+    // after it, so it has arrived), and only the float is carried to the step
+    // that uses it.
+    constexpr bool X_AT_STORE = X_FIRST_ONLY && NSBC == KBW;
     typedef u32x4 WSet[DPW];
     const uint32_t wlane = (uint32_t)(wave * 1024 + lane * 16);
     uint32_t goff[CS == 1 ? 1 : DPW];
@@ -264,9 +279,20 @@ void layer_kernel(LayerArgs a) {
         for (int t = 0; t < KBW; ++t) {
             const int pr = p.pair < a.npairs ? p.pair : a.npairs - 1;
             const uint32_t back = (pr == last_pair_odd) ? (uint32_t)h : 0u;
+            // The split generation reads x only at a feature's first block.
+            if (!(X_FIRST_ONLY && t % NSBC != 0)) {
 #pragma unroll
-            for (int rf = 0; rf < RF; ++rf)
-                xs[t][rf] = Tr<T>::raw(xw + (xoff[rf] + (uint32_t)(2 * pr) - back));
+                for (int rf = 0; rf < RF; ++rf) {
+                    const uint32_t off = xoff[rf] + (uint32_t)(2 * pr) - back;
+                    if constexpr (XP)
+                        xs[t][rf] = reinterpret_cast<const uint32_t*>(xw)[off >> 1];
+                    else
+                        xs[t][rf] = Tr<T>::raw(xw + off);
+                }
+            } else {
+#pragma unroll
+                for (int rf = 0; rf < RF; ++rf) xs[t][rf] = 0u;
+            }
             p = advance<WK>(p, nsb);
         }
         const int cc = c < a.nchunks ? c : a.nchunks - 1;
@@ -288,8 +314,12 @@ void layer_kernel(LayerArgs a) {
     };
     // Value of raw x bits for the lane's feature at position p (the phantom
     // feature of an odd feature count gives 0).
-    auto x_value = [&](const Pos& p, uint32_t raw) {
-        const float v = Tr<T>::value(raw);
+    auto x_value = [&](const Pos& p, uint32_t raw, int rf) {
+        float v;
+        if constexpr (XP)
+            v = __uint_as_float(__builtin_amdgcn_perm(raw, raw, xsel[rf]));
+        else
+            v = Tr<T>::value(raw);
         if (p.pair == last_pair_odd) return h ? 0.0f : v;
         return v;
     };
@@ -413,7 +443,8 @@ void layer_kernel(LayerArgs a) {
     // real columns in the last block of a feature, rounded up to even
     const int last_cols = a.nb + 1 - KJ * (nsb - 1);
     const int last_even = (last_cols + 1) & ~1;
-    auto gen_split = [&](const Pos& pg, const uint32_t (&xr)[RF], AFrag<T, RF>& An) {
+    auto gen_split = [&](const Pos& pg, const uint32_t (&xr)[RF], const float (&xf)[RF],
+                         AFrag<T, RF>& An) {
       if constexpr (GEN_SPLIT) {
         auto basis = [&](int rf, int e0, int e1) {
 #pragma unroll
@@ -426,8 +457,12 @@ void layer_kernel(LayerArgs a) {
         if (pg.bsub == 0) {
 #pragma unroll
             for (int rf = 0; rf < RF; ++rf) {
-                const float xv = x_value(pg, xr[rf]);
+                const float xv = X_AT_STORE ? xf[rf] : x_value(pg, xr[rf], rf);
                 sc[rf] = __builtin_fmaf(xv, a.inv_h, a.a_int + 1.0f) + a.a_frac;
+                // keep the coordinate itself for the feature's later blocks
+                // (recomputing it there from x would hold the raw x register,
+                // and a copy of it could wait on a load still in flight)
+                asm volatile("" : "+v"(sc[rf]));
                 An.a[rf][0] = (__bf16)half_silu(xv);
                 basis(rf, 1, KJ);
             }
@@ -437,7 +472,7 @@ void layer_kernel(LayerArgs a) {
             const float c = a.a_int + 1.0f - (float)(KJ * pg.bsub);
 #pragma unroll
             for (int rf = 0; rf < RF; ++rf)
-                sc[rf] = __builtin_fmaf(x_value(pg, xr[rf]), a.inv_h, c) + a.a_frac;
+                sc[rf] = __builtin_fmaf(x_value(pg, xr[rf], rf), a.inv_h, c) + a.a_frac;
         } else {
 #pragma unroll
             for (int rf = 0; rf < RF; ++rf) sc[rf] -= (float)KJ;
@@ -463,10 +498,21 @@ void layer_kernel(LayerArgs a) {
     // which measured as fast as a fixed phase order with raised MFMA
     // priority, and faster for the 256 -> 256 layer).
     auto step_split = [&](const AFrag<T, RF>& A, const BFrag& B, const Pos& pg,
-                          const uint32_t (&xr)[RF], AFrag<T, RF>& An) {
-        gen_split(pg, xr, An);
+                          const uint32_t (&xr)[RF], const float (&xf)[RF], AFrag<T, RF>& An) {
+        gen_split(pg, xr, xf, An);
 #pragma unroll
         for (int i = 0; i < NMFMA; ++i) do_mfma(i, A, B);
+        // The next block's A must be complete here: otherwise code sinking
+        // moves its generation past the next barrier, next to the MFMAs that
+        // read it, and neither step overlaps generation with multiplication.
+        if constexpr (BF16) {
+#pragma unroll
+            for (int rf = 0; rf < RF; ++rf) {
+                u32x4 w = __builtin_bit_cast(u32x4, An.a[rf]);
+                asm volatile("" : "+v"(w));
+                An.a[rf] = __builtin_bit_cast(bf16x8, w);
+            }
+        }
     };
 
     auto silu_of = [&](const float (&xv)[RF], float (&sl)[RF]) {
@@ -511,11 +557,14 @@ void layer_kernel(LayerArgs a) {
 
     // A of the wave's first block (nothing to interleave with yet).
     if constexpr (GEN_SPLIT) {
-        gen_split(pos_c, xq[0][0], A_cur);
+        float x0[RF];
+#pragma unroll
+        for (int rf = 0; rf < RF; ++rf) x0[rf] = x_value(pos_c, xq[0][0][rf], rf);
+        gen_split(pos_c, xq[0][0], x0, A_cur);
     } else {
         float x0[RF];
 #pragma unroll
-        for (int rf = 0; rf < RF; ++rf) x0[rf] = x_value(pos_c, xq[0][0][rf]);
+        for (int rf = 0; rf < RF; ++rf) x0[rf] = x_value(pos_c, xq[0][0][rf], rf);
         silu_of(x0, sl);
         const float c0 = a.a_int + 1.0f - (float)(KJ * pos_c.bsub);
 #pragma unroll
@@ -568,6 +617,9 @@ void layer_kernel(LayerArgs a) {
         const u32x4* st = stage(kk);
         read_b(bq[0], st, wk);
         Pos p = pos_c;
+        float xnext[RF];  // x of the next chunk's first block (X_AT_STORE)
+#pragma unroll
+        for (int rf = 0; rf < RF; ++rf) xnext[rf] = 0.0f;
         auto one = [&](auto tt) {
             constexpr int t = decltype(tt)::value;
             // position of the next block: the next step's, or the first block
@@ -576,7 +628,7 @@ void layer_kernel(LayerArgs a) {
             float xv[RF];
             if constexpr (!GEN_SPLIT) {
 #pragma unroll
-                for (int rf = 0; rf < RF; ++rf) xv[rf] = x_value(pnext, xr[t][rf]);
+                for (int rf = 0; rf < RF; ++rf) xv[rf] = x_value(pnext, xr[t][rf], rf);
                 if (pnext.bsub == 0) silu_of(xv, sl);
             }
             if constexpr (LASTG) {
@@ -592,7 +644,7 @@ void layer_kernel(LayerArgs a) {
             constexpr bool PREF = Occ<RF, NF>::waves == 1 && t + 1 < KBW;
             if constexpr (Occ<RF, NF>::waves == 2 && t > 0) read_b(bq[t & 1], st, wk + WK * t);
             if constexpr (GEN_SPLIT)
-                step_split(A_cur, bq[t & 1], pnext, xr[t], A_nxt);
+                step_split(A_cur, bq[t & 1], pnext, xr[t], xnext, A_nxt);
             else
                 step(A_cur, bq[t & 1], pnext, xv, sl, A_nxt, std::integral_constant<bool, PREF>{},
                      bq[(t + 1) & 1], st, wk + WK * (t + 1));
@@ -601,6 +653,16 @@ void layer_kernel(LayerArgs a) {
             if constexpr (GEN_SPLIT && t == 0) {
                 __builtin_amdgcn_sched_barrier(0);
                 store(std::integral_constant<int, K + 1>{}, wq[JN]);
+                if constexpr (X_AT_STORE) {
+                    Pos pn = pos_c;  // first block of the next chunk
+                    pn.pair += 1;
+                    pn.bsub = 0;
+#pragma unroll
+                    for (int rf = 0; rf < RF; ++rf) {
+                        xnext[rf] = x_value(pn, xq[JN][0][rf], rf);
+                        asm volatile("" : "+v"(xnext[rf]));
+                    }
+                }
                 __builtin_amdgcn_sched_barrier(0);
             }
         };
@@ -686,13 +748,15 @@ hipError_t launch_cfg(const LayerGeom& g, LayerArgs a, hipStream_t s) {
     const dim3 grid((unsigned)((a.batch + BM - 1) / BM), (unsigned)(g.ntiles * (NFL / NF)));
     // Two blocks per feature (bf16, 5 <= G <= 12) get their own build where
     // the split generation can use it (two waves per SIMD, no K split, whole
-    // features per chunk).
+    // features per chunk), with x read as aligned 32-bit words where that
+    // stays inside the tensor.
     constexpr bool BF16 = sizeof(T) == 2;
     if constexpr (BF16 && Occ<RF, NF>::waves == 2 && WK == 1 &&
                   layer_chunk_blocks(BF16, NFL) % 2 == 0) {
-        if (g.nsb == 2) {
-            hipLaunchKernelGGL((layer_kernel<T, RF, NFL, NF, WK, NW, 2>), grid, dim3(64 * NW), 0,
-                               s, a);
+        const bool xp = reinterpret_cast<uintptr_t>(a.x) % 4 == 0 && ((int64_t)a.batch * a.in) % 2 == 0;
+        if (g.nsb == 2 && xp) {
+            hipLaunchKernelGGL((layer_kernel<T, RF, NFL, NF, WK, NW, 2, true>), grid, dim3(64 * NW),
+                               0, s, a);
             return hipGetLastError();
         }
     }

@@ -130,6 +130,36 @@ def test_layer_wide_tiles(dtype_name, B, n_in, n_out, G, cfg):
     assert normwise(y, ref) <= _tol(dtype_name)
 
 
+@pytest.mark.parametrize("case", ["aligned", "odd_total", "x_at_odd_element"])
+@pytest.mark.parametrize("cfg", [None, "1,1", "1,1,4,2"])
+def test_layer_bf16_x_word_reads_and_their_fallbacks(case, cfg):
+    """With two blocks per feature (G = 10) bf16 x is read as the aligned
+    32-bit word holding each element when x is 4-byte aligned and batch * in is
+    even (the word then never leaves the tensor); an odd element count, or an x
+    that starts at an odd element, takes 16-bit reads.  Odd feature counts give
+    rows of both parities.  Every case matches the oracle."""
+    B, n_in, n_out, G = {"aligned": (300, 9, 45, 10), "odd_total": (301, 9, 45, 10),
+                         "x_at_odd_element": (300, 9, 45, 10)}[case]
+    x, C, Wb = _inputs(B, n_in, n_out, G, seed=11, off=0.1, dtype_name="bf16")
+    ref = oracle.round_bf16(oracle.layer(x, C, Wb, G))
+    dt = torch.bfloat16
+    if case == "x_at_odd_element":
+        buf = torch.zeros(B * n_in + 1, dtype=dt, device=device())
+        xd = buf[1:].view(B, n_in)
+        xd.copy_(to_dev(x, dt))
+        assert xd.data_ptr() % 4 == 2
+    else:
+        xd = to_dev(x, dt)
+    say(f"layer bf16 x reads {case} cfg={cfg}")
+    set_layer_cfg(cfg)
+    try:
+        y = kb.layer_forward(xd, to_dev(C, dt), to_dev(Wb, dt), G)
+        torch.cuda.synchronize()
+    finally:
+        set_layer_cfg(None)
+    assert normwise(to_host64(y), ref) <= BF16_LAYER_TOL
+
+
 @pytest.mark.parametrize("dtype_name", ["f32", "bf16"])
 def test_c_layer_forward_allocating_entry_point(dtype_name):
     """kan_layer_forward (packs into a stream-ordered temporary) called through
