@@ -32,11 +32,13 @@ METRIC = "KAN layer fwd samples/s + Gbasis/s; % of HBM / MFMA peak on MI355X"
 # MI355X published peaks
 PEAK_HBM_GBS = 8000.0
 PEAK_TFLOPS = {"bf16": 2516.6, "f32": 157.3}
-# Plain (non-packed) fp32 VALU: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz, in
-# G lane-ops/s, and the lane-ops one basis value of the fused layer costs:
-# coordinate 1, P and Q 2 (clamped fmas), P^2, Q^2, Q^3 3, the final fma 1,
-# plus half a packed bf16 conversion in bf16.
-PEAK_VALU_GOPS = 256 * 4 * 16 * 2.4
+# Plain (non-packed) fp32 VALU in G lane-ops/s: the published 157.3 TFLOP/s
+# fp32 vector rate counts an fma as two flops, i.e. 256 CUs x 4 SIMDs x 32
+# lanes x 2.4 GHz (bench.py --valu-ceiling measures ~28 fma lanes per clock
+# per SIMD with two or more waves on it).  And the lane-ops one basis value of
+# the fused layer costs: coordinate 1, P and Q 2 (clamped fmas), P^2, Q^2,
+# Q^3 3, the final fma 1, plus half a packed bf16 conversion in bf16.
+PEAK_VALU_GOPS = 256 * 4 * 32 * 2.4
 VALU_OPS_PER_VALUE = {"bf16": 7.5, "f32": 7.0}
 
 
@@ -56,6 +58,9 @@ def parse():
     p.add_argument("--mfma-ceiling", action="store_true",
                    help="only measure back-to-back bf16 MFMA throughput and the shader clock "
                         "with constant and with random operands (libkan_probe.so) and exit")
+    p.add_argument("--valu-ceiling", action="store_true",
+                   help="only measure plain fp32 fma throughput per SIMD with 1, 2 and 4 waves "
+                        "on it (libkan_probe.so) and exit")
     p.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                    help="only run a plain device copy of BYTES bytes 10 times (HBM counter "
                         "calibration under rocprofv3) and exit")
@@ -229,6 +234,43 @@ def mfma_ceiling() -> None:
                           "frac_of_2516.6": flops / s / 1e12 / PEAK_TFLOPS["bf16"]}), flush=True)
 
 
+def valu_ceiling() -> None:
+    """Independent fp32 fma chains, nothing else, with 1, 2 and 4 waves per
+    SIMD: fma lanes per shader clock per SIMD (the span of workgroup 0's
+    waves on the shader-clock counter) and the rate over the whole card."""
+    import ctypes
+
+    import torch
+
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2609_01956_amd", "libkan_probe.so"))
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    for w in (1, 2, 4):
+        blocks, trips = cus, 4000
+        out = torch.empty(blocks * 256 * w, device="cuda")
+        clk = torch.zeros(8 * w, dtype=torch.int64, device="cuda")
+        args = [ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(clk.data_ptr()), blocks, w]
+        if lib.kan_probe_valu_f32(*args, 10, stream) != 0:
+            raise RuntimeError("probe launch failed")
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        if lib.kan_probe_valu_f32(*args, trips, stream) != 0:
+            raise RuntimeError("probe launch failed")
+        e1.record()
+        torch.cuda.synchronize()
+        c = clk.cpu().tolist()
+        span = max(c[1::2]) - min(c[0::2])
+        lanes = 64.0 * w * 128 * trips / span
+        s = e0.elapsed_time(e1) * 1e-3
+        print(json.dumps({"probe": "fp32 v_fma_f32, 8 independent chains per wave",
+                          "waves_per_simd": w, "fma_lanes_per_clock_per_simd": lanes,
+                          "card_g_lane_ops_per_s": blocks * 4 * w * 64.0 * 128 * trips / s / 1e9,
+                          "shader_clock_ghz": span / s / 1e9,
+                          "frac_of_32_lanes": lanes / 32.0}), flush=True)
+
+
 def cpu_baseline(W, n_layers_shapes, target_s: float):
     """The float64 oracle, untuned, on a row sample of the same step."""
     import numpy as np
@@ -278,6 +320,9 @@ def main() -> int:
         return 0
     if args.mfma_ceiling:
         mfma_ceiling()
+        return 0
+    if args.valu_ceiling:
+        valu_ceiling()
         return 0
     if args.configs:
         configs_sweep(args.dtype)

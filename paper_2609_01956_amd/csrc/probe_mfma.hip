@@ -1,6 +1,7 @@
 // probe_mfma.hip -- measurement support, not part of the KAN ABI: the rate of
 // back-to-back v_mfma_f32_32x32x16_bf16 on this device with constant or with
-// random operands, and the shader clock while it runs.
+// random operands, and the shader clock while it runs; and the rate of plain
+// (non-packed) fp32 VALU fmas per SIMD with 1, 2 or 4 waves on it.
 //
 // Each wave keeps 8 independent 32x32 fp32 accumulators and issues 16 MFMAs
 // per loop trip (two A fragments, sixteen B fragments, all in registers), so
@@ -58,7 +59,50 @@ void mfma_loop(const u32x4* __restrict__ operands, float* __restrict__ out,
     }
 }
 
+// W waves per SIMD (one workgroup of 4 W waves per CU), each running 8
+// independent fp32 fma chains, 128 fmas per loop trip.  Every wave of
+// workgroup 0 records its own start and end shader-clock counters, so the
+// span over them is the time the SIMDs took for all their waves.
+__global__ __launch_bounds__(1024) void valu_loop(float* __restrict__ out,
+                                                  unsigned long long* __restrict__ clk,
+                                                  int trips, float seed) {
+    const int lane = threadIdx.x & 63;
+    float v[8];
+    for (int k = 0; k < 8; ++k) v[k] = seed * (float)(lane + k);
+    const float c1 = 0.999f + seed, c2 = 0.001f * seed;
+    const unsigned long long t0 = __builtin_amdgcn_s_memtime();
+    for (int t = 0; t < trips; ++t) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i)
+#pragma unroll
+            for (int k = 0; k < 8; ++k) v[k] = __builtin_fmaf(v[k], c1, c2);
+    }
+    const unsigned long long t1 = __builtin_amdgcn_s_memtime();
+    float r = 0.0f;
+    for (int k = 0; k < 8; ++k) r += v[k];
+    out[(size_t)blockIdx.x * blockDim.x + threadIdx.x] = r;
+    if (blockIdx.x == 0 && lane == 0) {
+        clk[2 * (threadIdx.x >> 6)] = t0;
+        clk[2 * (threadIdx.x >> 6) + 1] = t1;
+    }
+}
+
 }  // namespace
+
+// out: device, blocks * 256 * waves_per_simd floats; clk: device, 8 *
+// waves_per_simd counters (start, end of each wave of workgroup 0).  Each wave
+// issues 128 * trips fp32 fmas.  waves_per_simd is 1, 2 or 4.  Returns a
+// hipError_t code.
+extern "C" int kan_probe_valu_f32(void* out, void* clk, int blocks, int waves_per_simd, int trips,
+                                  void* stream) {
+    if (blocks <= 0 || trips <= 0 || !out || !clk ||
+        (waves_per_simd != 1 && waves_per_simd != 2 && waves_per_simd != 4))
+        return (int)hipErrorInvalidValue;
+    hipLaunchKernelGGL(valu_loop, dim3(blocks), dim3(256 * waves_per_simd), 0,
+                       static_cast<hipStream_t>(stream), static_cast<float*>(out),
+                       static_cast<unsigned long long*>(clk), trips, 1e-3f);
+    return (int)hipGetLastError();
+}
 
 // operands: device, at least kan_probe_operand_words() 16-byte words of
 // finite bf16 values (read only with random != 0); out: device, blocks * 256

@@ -15,12 +15,15 @@ sys.path.insert(0, ROOT)
 import bench  # noqa: E402
 
 
-def test_wide_layers_are_matrix_core_bound_narrow_ones_valu_bound():
+def test_wide_layers_are_matrix_core_bound_narrow_bf16_is_valu_bound():
     nb = 13  # G = 10
     for dt in ("bf16", "f32"):
         assert bench.layer_roofline(dt, 65536, 784, 256, nb)["bound"] == "mfma"
         assert bench.layer_roofline(dt, 65536, 256, 256, nb)["bound"] == "mfma"
-        assert bench.layer_roofline(dt, 65536, 256, 10, nb)["bound"] == "alu"
+    # out = 10: 7.5 lane-ops per basis value at 78.6 T/s outlast 20 flops per
+    # value at 2516.6 TFLOP/s, but not at the fp32 matrix-core peak of 157.3
+    assert bench.layer_roofline("bf16", 65536, 256, 10, nb)["bound"] == "alu"
+    assert bench.layer_roofline("f32", 65536, 256, 10, nb)["bound"] == "mfma"
 
 
 def test_layer_roofline_work_counts():
@@ -28,10 +31,10 @@ def test_layer_roofline_work_counts():
     # dense contraction: 2 * B * out * in * (G + 4) flops
     assert k["algorithmic"] == pytest.approx(2.0 * 65536 * 256 * 784 * 14 / 1e12)
     assert k["peak"] == bench.PEAK_TFLOPS["bf16"]
-    n = bench.layer_roofline("f32", 65536, 256, 10, 13)
+    n = bench.layer_roofline("bf16", 65536, 256, 10, 13)
     assert n["unit"] == "Gop/s"
-    assert n["algorithmic"] == pytest.approx(7.0 * 65536 * 256 * 14 / 1e9)
-    assert n["peak"] == pytest.approx(256 * 4 * 16 * 2.4)
+    assert n["algorithmic"] == pytest.approx(7.5 * 65536 * 256 * 14 / 1e9)
+    assert n["peak"] == pytest.approx(256 * 4 * 32 * 2.4)
 
 
 def _fake_tree(tmp_path, record_md5):
