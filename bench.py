@@ -35,11 +35,14 @@ PEAK_TFLOPS = {"bf16": 2516.6, "f32": 157.3}
 # Plain (non-packed) fp32 VALU in G lane-ops/s: the published 157.3 TFLOP/s
 # fp32 vector rate counts an fma as two flops, i.e. 256 CUs x 4 SIMDs x 32
 # lanes x 2.4 GHz (bench.py --valu-ceiling measures ~28 fma lanes per clock
-# per SIMD with two or more waves on it).  And the lane-ops one basis value of
-# the fused layer costs: coordinate 1, P and Q 2 (clamped fmas), P^2, Q^2,
-# Q^3 3, the final fma 1, plus half a packed bf16 conversion in bf16.
+# per SIMD with two or more waves on it).  And the least VALU work the basis
+# and SiLU values of one (row, input feature) take, in lane-ops: of the G + 3
+# basis columns at most four consecutive ones are nonzero, each 7 ops in the
+# truncated power form (v 1, P and Q 2 clamped fmas, P^2, Q^2, Q^3 3, the
+# final fma 1); the coordinate and the interval 4 (fma, add, floor, fraction);
+# SiLU 4 (exp, fma, reciprocal, multiply); in bf16 2 packed conversions.
 PEAK_VALU_GOPS = 256 * 4 * 32 * 2.4
-VALU_OPS_PER_VALUE = {"bf16": 7.5, "f32": 7.0}
+VALU_OPS_PER_FEATURE = {"bf16": 38.0, "f32": 36.0}
 
 
 def parse():
@@ -81,10 +84,11 @@ def copy_calibration(nbytes: int) -> None:
 def layer_roofline(dtype: str, batch: int, n_in: int, n_out: int, nb: int) -> dict:
     """Roofline of one fused layer: bound by the matrix cores (dense flops,
     all nb bases plus the SiLU column per input) unless generating its basis
-    values takes longer at the VALU peak than the contraction at the MFMA
-    peak (narrow outputs); then it is reported against the VALU."""
+    values (the least VALU work, four nonzero columns per input) takes longer
+    at the VALU peak than the contraction at the MFMA peak (narrow outputs);
+    then it is reported against the VALU."""
     flop = 2.0 * batch * n_out * n_in * (nb + 1)
-    valu = VALU_OPS_PER_VALUE[dtype] * batch * n_in * (nb + 1)
+    valu = VALU_OPS_PER_FEATURE[dtype] * batch * n_in
     if valu / (PEAK_VALU_GOPS * 1e9) > flop / (PEAK_TFLOPS[dtype] * 1e12):
         k = {"bound": "alu", "unit": "Gop/s", "peak": PEAK_VALU_GOPS,
              "algorithmic": valu / 1e9}  # G lane-ops

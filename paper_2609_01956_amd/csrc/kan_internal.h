@@ -103,7 +103,13 @@ __host__ __device__ constexpr bool layer_shape_ok(bool bf16, int nfl, int rf, in
     return wk == 1 || rf * nf <= 4;
 }
 
-LayerCfg plan_layer(const LayerGeom& g, bool bf16, int64_t batch);
+// bf16 x can be read as the aligned 32-bit words holding its elements: x is
+// 4-byte aligned and batch * in is even, so no word reaches past the tensor.
+inline bool layer_x_words(const void* x, int64_t batch, int in) {
+    return reinterpret_cast<uintptr_t>(x) % 4 == 0 && (batch * (int64_t)in) % 2 == 0;
+}
+// x_words: layer_x_words holds for the layer's input (bf16).
+LayerCfg plan_layer(const LayerGeom& g, bool bf16, int64_t batch, bool x_words);
 // KAN_LAYER_CFG="rf,wk[,nw[,cs]]" forces a configuration (testing and tuning);
 // ignored when malformed or not valid for the geometry.
 bool parse_layer_cfg_override(const LayerGeom& g, LayerCfg* c);

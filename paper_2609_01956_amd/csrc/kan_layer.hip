@@ -100,7 +100,7 @@ bool layer_cfg_valid(const LayerGeom& g, const LayerCfg& c) {
     return layer_shape_ok(g.kj == 8, g.nf, c.rf, c.wk, c.nw, c.cs);
 }
 
-LayerCfg plan_layer(const LayerGeom& g, bool bf16, int64_t batch) {
+LayerCfg plan_layer(const LayerGeom& g, bool bf16, int64_t batch, bool x_words) {
     auto wgs = [&](const LayerCfg& c) {
         const int64_t bm = 32LL * c.rf * (c.nw / c.wk);
         return ((batch + bm - 1) / bm) * g.ntiles * c.cs;
@@ -112,6 +112,16 @@ LayerCfg plan_layer(const LayerGeom& g, bool bf16, int64_t batch) {
     // traffic per row.  Used when it fills the chip (one workgroup per CU).
     const LayerCfg wide{1, 1, 8, 1};
     if (bf16 && g.nf == 8 && wgs(wide) >= 256) return wide;
+    // Narrow bf16 layers (one or two 32-column fragments) with two blocks per
+    // feature build each feature's A from its four nonzero basis columns,
+    // which needs whole features per wave (no K split): one row tile per
+    // wave, eight waves per workgroup when that fills the chip, else four
+    // (C5 layer 3, 256 -> 10: 74 and 75 us against 94 us with the K split).
+    if (bf16 && g.nf <= 2 && g.nsb == 2 && x_words) {
+        const LayerCfg n8{1, 1, 8, 1}, n4{1, 1, 4, 1};
+        if (layer_cfg_valid(g, n8) && wgs(n8) >= 256) return n8;
+        if (layer_cfg_valid(g, n4) && wgs(n4) >= 256) return n4;
+    }
     // Otherwise the tallest workgroup over the whole N tile (fewest re-reads
     // of the weights, basis values generated once per tile) that still gives
     // at least `want` workgroups; the basis-generation-bound narrow layers

@@ -49,6 +49,12 @@ __device__ __forceinline__ float half_silu(float x) {
     return x * __builtin_amdgcn_rcpf(__builtin_fmaf(__expf(-x), 2.0f, 2.0f));
 }
 
+// Two floats to bf16 (round to nearest even), packed low then high.
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+    return __builtin_bit_cast(uint32_t, bf16x2{(__bf16)lo, (__bf16)hi});
+}
+
 template <typename T> struct Tr;
 
 template <> struct Tr<float> {
@@ -262,6 +268,22 @@ void layer_kernel(LayerArgs a) {
     // after it, so it has arrived), and only the float is carried to the step
     // that uses it.
     constexpr bool X_AT_STORE = X_FIRST_ONLY && NSBC == KBW;
+    // LOCAL (narrow layers, two blocks per feature, whole features per
+    // chunk): of a feature's basis columns at most four consecutive ones are
+    // nonzero (|v| < 2), so the truncated power form is evaluated at those
+    // four only, and the feature's two A fragments are assembled in a
+    // lane-private LDS strip (zeroed, the four values and the SiLU value
+    // written, both fragments read back).  The other columns are the exact
+    // zeros the clamped form gives there.  With one or two 32-column
+    // fragments per block the basis, not the contraction, bounds the layer;
+    // wider layers keep the per-column evaluation (the strip's LDS traffic
+    // and latency cost them more than the VALU work saved).
+    constexpr bool LOCAL = X_FIRST_ONLY && NSBC == 2 && NF <= 2;
+    // strip: 24 bf16 columns per (wave, row tile, lane), feature column c at
+    // index c + 4; a 48-byte stride keeps 16-byte accesses of 8 lanes on
+    // distinct banks, and the 8-byte lead makes columns 0 and 8 16-byte aligned.
+    constexpr int STRIP = 24;
+    __shared__ __align__(16) uint16_t strips[LOCAL ? 4 + NW * RF * 64 * STRIP : 8];
     typedef u32x4 WSet[DPW];
     const uint32_t wlane = (uint32_t)(wave * 1024 + lane * 16);
     uint32_t goff[CS == 1 ? 1 : DPW];
@@ -497,6 +519,35 @@ void layer_kernel(LayerArgs a) {
     // matrix core busy; the compiler is left to schedule within the step,
     // which measured as fast as a fixed phase order with raised MFMA
     // priority, and faster for the 256 -> 256 layer).
+    // LOCAL: both A fragments of a feature with x value xf (block 0 -> AF,
+    // block 1 -> AL).  Column c holds N / 2 at v = s - c; with n = floor(s)
+    // and f = s - n the columns that can be nonzero are n - 1 .. n + 2, at
+    // v = f + 1, f, f - 1, f - 2.
+    auto gen_local = [&](const float (&xf)[RF], AFrag<T, RF>& AF, AFrag<T, RF>& AL) {
+      if constexpr (LOCAL) {
+#pragma unroll
+        for (int rf = 0; rf < RF; ++rf) {
+            const float sv = __builtin_fmaf(xf[rf], a.inv_h, a.a_int + 1.0f) + a.a_frac;
+            const float fl = __builtin_floorf(sv);
+            const float f = sv - fl;
+            // first column, kept within [-4, 16] (NaN and far off-grid x put
+            // the four values outside columns 0 .. 15, where they are not read)
+            const int c0 = (int)__builtin_fminf(__builtin_fmaxf(fl, -3.0f), 17.0f) - 1;
+            const uint32_t w0 = pack_bf16x2(half_basis(f + 1.0f), half_basis(f));
+            const uint32_t w1 = pack_bf16x2(half_basis(f - 1.0f), half_basis(f - 2.0f));
+            uint16_t* st = strips + 4 + ((wave * RF + rf) * 64 + lane) * STRIP;
+            *reinterpret_cast<u32x4*>(st + 4) = u32x4{0u, 0u, 0u, 0u};
+            *reinterpret_cast<u32x4*>(st + 12) = u32x4{0u, 0u, 0u, 0u};
+            st[c0 + 4] = (uint16_t)w0;
+            st[c0 + 5] = (uint16_t)(w0 >> 16);
+            st[c0 + 6] = (uint16_t)w1;
+            st[c0 + 7] = (uint16_t)(w1 >> 16);
+            st[4] = __builtin_bit_cast(uint16_t, (__bf16)half_silu(xf[rf]));  // column 0
+            AF.a[rf] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(st + 4));
+            AL.a[rf] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(st + 12));
+        }
+      }
+    };
     auto step_split = [&](const AFrag<T, RF>& A, const BFrag& B, const Pos& pg,
                           const uint32_t (&xr)[RF], const float (&xf)[RF], AFrag<T, RF>& An) {
         gen_split(pg, xr, xf, An);
@@ -539,6 +590,7 @@ void layer_kernel(LayerArgs a) {
     WSet wq[L];
     float sl[RF];
     AFrag<T, RF> A_cur, A_nxt;
+    AFrag<T, RF> A_last;  // LOCAL: block 1 of the current feature, read from the strip
     BFrag bq[2];
     Pos pos_c = advance_n(Pos{0, 0, 0}, wk, nsb);  // first block of the current chunk
     Pos pos_l = pos_c;                               // first block of the next chunk to load
@@ -560,7 +612,10 @@ void layer_kernel(LayerArgs a) {
         float x0[RF];
 #pragma unroll
         for (int rf = 0; rf < RF; ++rf) x0[rf] = x_value(pos_c, xq[0][0][rf], rf);
-        gen_split(pos_c, xq[0][0], x0, A_cur);
+        if constexpr (LOCAL)
+            gen_local(x0, A_cur, A_last);
+        else
+            gen_split(pos_c, xq[0][0], x0, A_cur);
     } else {
         float x0[RF];
 #pragma unroll
@@ -643,7 +698,21 @@ void layer_kernel(LayerArgs a) {
             // saved.
             constexpr bool PREF = Occ<RF, NF>::waves == 1 && t + 1 < KBW;
             if constexpr (Occ<RF, NF>::waves == 2 && t > 0) read_b(bq[t & 1], st, wk + WK * t);
-            if constexpr (GEN_SPLIT)
+            if constexpr (LOCAL) {
+                // even steps: block 1 of the current feature is already
+                // assembled; odd steps: both blocks of the next feature
+                if constexpr (t % 2 == 0) {
+                    A_nxt = A_last;
+                } else {
+                    float xf[RF];
+#pragma unroll
+                    for (int rf = 0; rf < RF; ++rf)
+                        xf[rf] = X_AT_STORE ? xnext[rf] : x_value(pnext, xr[t][rf], rf);
+                    gen_local(xf, A_nxt, A_last);
+                }
+#pragma unroll
+                for (int i = 0; i < NMFMA; ++i) do_mfma(i, A_cur, bq[t & 1]);
+            } else if constexpr (GEN_SPLIT)
                 step_split(A_cur, bq[t & 1], pnext, xr[t], xnext, A_nxt);
             else
                 step(A_cur, bq[t & 1], pnext, xv, sl, A_nxt, std::integral_constant<bool, PREF>{},
@@ -753,8 +822,7 @@ hipError_t launch_cfg(const LayerGeom& g, LayerArgs a, hipStream_t s) {
     constexpr bool BF16 = sizeof(T) == 2;
     if constexpr (BF16 && Occ<RF, NF>::waves == 2 && WK == 1 &&
                   layer_chunk_blocks(BF16, NFL) % 2 == 0) {
-        const bool xp = reinterpret_cast<uintptr_t>(a.x) % 4 == 0 && ((int64_t)a.batch * a.in) % 2 == 0;
-        if (g.nsb == 2 && xp) {
+        if (g.nsb == 2 && layer_x_words(a.x, a.batch, a.in)) {
             hipLaunchKernelGGL((layer_kernel<T, RF, NFL, NF, WK, NW, 2, true>), grid, dim3(64 * NW),
                                0, s, a);
             return hipGetLastError();

@@ -20,8 +20,8 @@ def test_wide_layers_are_matrix_core_bound_narrow_bf16_is_valu_bound():
     for dt in ("bf16", "f32"):
         assert bench.layer_roofline(dt, 65536, 784, 256, nb)["bound"] == "mfma"
         assert bench.layer_roofline(dt, 65536, 256, 256, nb)["bound"] == "mfma"
-    # out = 10: 7.5 lane-ops per basis value at 78.6 T/s outlast 20 flops per
-    # value at 2516.6 TFLOP/s, but not at the fp32 matrix-core peak of 157.3
+    # out = 10: 38 lane-ops per (row, feature) at 78.6 T/s outlast 2 x 10 x 14
+    # flops at 2516.6 TFLOP/s, but not at the fp32 matrix-core peak of 157.3
     assert bench.layer_roofline("bf16", 65536, 256, 10, nb)["bound"] == "alu"
     assert bench.layer_roofline("f32", 65536, 256, 10, nb)["bound"] == "mfma"
 
@@ -33,7 +33,7 @@ def test_layer_roofline_work_counts():
     assert k["peak"] == bench.PEAK_TFLOPS["bf16"]
     n = bench.layer_roofline("bf16", 65536, 256, 10, 13)
     assert n["unit"] == "Gop/s"
-    assert n["algorithmic"] == pytest.approx(7.5 * 65536 * 256 * 14 / 1e9)
+    assert n["algorithmic"] == pytest.approx(38.0 * 65536 * 256 / 1e9)
     assert n["peak"] == pytest.approx(256 * 4 * 32 * 2.4)
 
 
