@@ -460,6 +460,12 @@ void layer_kernel(LayerArgs a) {
     // Stepping the coordinate by 8 is exact wherever a basis value of the
     // block is nonzero (there |s| < 17 and s - 8 is computed exactly).
     constexpr bool GEN_SPLIT = BF16 && Occ<RF, NF>::waves == 2;
+    // MIDBAR (bf16, one wave per SIMD, whole features per chunk): the chunk's
+    // one barrier sits before its last block, right after the next chunk's
+    // weights are stored, so the B fragments of every block, the next
+    // chunk's first included, are read from LDS one step ahead (a wave alone
+    // on its SIMD has nothing else to cover that latency with).
+    constexpr bool MIDBAR = BF16 && Occ<RF, NF>::waves == 1 && ALIGNED;
     constexpr bool DIRECT = WK > 1;
     float sc[RF];  // coordinate of the wave's current block (element 0)
     // real columns in the last block of a feature, rounded up to even
@@ -606,6 +612,7 @@ void layer_kernel(LayerArgs a) {
     __builtin_amdgcn_s_waitcnt(WAIT_LDS);
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
+    if constexpr (MIDBAR) read_b(bq[0], stage(std::integral_constant<int, 0>{}), wk);
 
     // A of the wave's first block (nothing to interleave with yet).
     if constexpr (GEN_SPLIT) {
@@ -645,7 +652,7 @@ void layer_kernel(LayerArgs a) {
             pos_c.bsub = 0;
             pos_l.bsub = 0;
         }
-        if (c > 0) {  // (chunk 0's barrier is in the prologue)
+        if (!MIDBAR && c > 0) {  // (chunk 0's barrier is in the prologue)
             __builtin_amdgcn_s_waitcnt(WAIT_LDS);
             __builtin_amdgcn_s_barrier();
             __builtin_amdgcn_sched_barrier(0);
@@ -664,13 +671,13 @@ void layer_kernel(LayerArgs a) {
         // The next chunk's weights go to the other LDS stage before the next
         // barrier.  With the split generation they are stored after the
         // first step, which gives their loads that step's time to land.
-        if constexpr (!GEN_SPLIT) {
+        if constexpr (!GEN_SPLIT && !MIDBAR) {
             store(std::integral_constant<int, K + 1>{}, wq[JN]);
             __builtin_amdgcn_sched_barrier(0);
         }
 
         const u32x4* st = stage(kk);
-        read_b(bq[0], st, wk);
+        if constexpr (!MIDBAR) read_b(bq[0], st, wk);  // (MIDBAR: read during the last chunk)
         Pos p = pos_c;
         float xnext[RF];  // x of the next chunk's first block (X_AT_STORE)
 #pragma unroll
@@ -696,7 +703,11 @@ void layer_kernel(LayerArgs a) {
             // Two waves: B is read at the start of each step; the other wave
             // covers the latency, and the registers of a second B set are
             // saved.
-            constexpr bool PREF = Occ<RF, NF>::waves == 1 && t + 1 < KBW;
+            constexpr bool PREF = Occ<RF, NF>::waves == 1 && (t + 1 < KBW || MIDBAR);
+            // block read ahead: the next one of this chunk, or (MIDBAR, last
+            // step) the first block of the next chunk from the other stage
+            const u32x4* st_n = t + 1 < KBW ? st : stage(std::integral_constant<int, K + 1>{});
+            const int bi_n = t + 1 < KBW ? wk + WK * (t + 1) : wk;
             if constexpr (Occ<RF, NF>::waves == 2 && t > 0) read_b(bq[t & 1], st, wk + WK * t);
             if constexpr (LOCAL) {
                 // even steps: block 1 of the current feature is already
@@ -716,9 +727,19 @@ void layer_kernel(LayerArgs a) {
                 step_split(A_cur, bq[t & 1], pnext, xr[t], xnext, A_nxt);
             else
                 step(A_cur, bq[t & 1], pnext, xv, sl, A_nxt, std::integral_constant<bool, PREF>{},
-                     bq[(t + 1) & 1], st, wk + WK * (t + 1));
+                     bq[(t + 1) & 1], st_n, bi_n);
             A_cur = A_nxt;
             p = pnext;
+            if constexpr (MIDBAR && t + 2 == KBW) {
+                // the next chunk's weights to the other stage, then the
+                // chunk's barrier: every wave has stored them, and has read
+                // its last block of the previous chunk from that stage
+                __builtin_amdgcn_sched_barrier(0);
+                store(std::integral_constant<int, K + 1>{}, wq[JN]);
+                __builtin_amdgcn_s_waitcnt(WAIT_LDS);
+                __builtin_amdgcn_s_barrier();
+                __builtin_amdgcn_sched_barrier(0);
+            }
             if constexpr (GEN_SPLIT && t == 0) {
                 __builtin_amdgcn_sched_barrier(0);
                 store(std::integral_constant<int, K + 1>{}, wq[JN]);
@@ -815,12 +836,12 @@ hipError_t launch_cfg(const LayerGeom& g, LayerArgs a, hipStream_t s) {
     a.nblk_pad = g.nblk_pad;
     a.nchunks = g.nblk_pad / g.kb;
     const dim3 grid((unsigned)((a.batch + BM - 1) / BM), (unsigned)(g.ntiles * (NFL / NF)));
-    // Two blocks per feature (bf16, 5 <= G <= 12) get their own build where
-    // the split generation can use it (two waves per SIMD, no K split, whole
-    // features per chunk), with x read as aligned 32-bit words where that
-    // stays inside the tensor.
+    // Two blocks per feature (bf16, 5 <= G <= 12) get their own build (no K
+    // split, whole features per chunk: every step's block is the first or the
+    // last of its feature at compile time), with x read as aligned 32-bit
+    // words where that stays inside the tensor.
     constexpr bool BF16 = sizeof(T) == 2;
-    if constexpr (BF16 && Occ<RF, NF>::waves == 2 && WK == 1 &&
+    if constexpr (BF16 && WK == 1 &&
                   layer_chunk_blocks(BF16, NFL) % 2 == 0) {
         if (g.nsb == 2 && layer_x_words(a.x, a.batch, a.in)) {
             hipLaunchKernelGGL((layer_kernel<T, RF, NFL, NF, WK, NW, 2, true>), grid, dim3(64 * NW),

@@ -97,6 +97,12 @@ WIDE = [
     ("bf16", 97, 3, 130, 200, "1,1"),
     ("bf16", 600, 20, 256, 10, "1,1,8"),
     ("bf16", 300, 5, 100, 50, "1,1,8"),
+    # two blocks per feature (G = 7, 10) with an odd number of chunks (a
+    # padding chunk in the last unrolled pair), an odd feature count and a
+    # ragged batch, for the 64-row one-wave shape and the 8-wave shape
+    ("bf16", 300, 18, 256, 10, "2,1"),
+    ("bf16", 257, 17, 256, 7, "2,1"),
+    ("bf16", 257, 17, 256, 7, "1,1,8"),
     ("f32", 600, 20, 256, 10, "1,1"),
     ("f32", 600, 20, 256, 10, "1,4"),
     ("f32", 333, 7, 128, 50, "2,1"),
