@@ -67,6 +67,12 @@ struct LayerGeom {
     int kb;       // blocks per chunk
     int nf;       // 32-column MFMA fragments per N tile (1, 2, 4 or 8)
     int ntiles;   // ceil(out / (32 * nf))
+    // bf16 with two blocks per feature and 256-column tiles: packed for the
+    // structured-sparse MFMA (block = feature of the pair, half = column
+    // half, element e of half w = column 4 (e % 4) + 2 w + e / 4), and only
+    // the shapes with one row tile per wave, no K split and no column slices
+    // run on it.
+    bool sparse;
     size_t packed_bytes;
 };
 

@@ -18,7 +18,9 @@ using layer_detail::kThreads;
 // One unit of the packed buffer per thread: the kj weights of columns
 // [kj * blk, kj * blk + kj) of feature f for output column o, the columns of
 // a feature ordered [base_w, coef[.., 0], ..., coef[.., nb - 1]] and
-// zero-padded.  Units are numbered with blk fastest, then f, then o, so a
+// zero-padded.  With `sparse` (bf16, two blocks per feature) unit blk is
+// column half w = blk of feature f, holding columns 4 (e % 4) + 2 w + e / 4,
+// and goes to block f % 2 of the pair, half w.  Units are numbered with blk fastest, then f, then o, so a
 // wave reads consecutive coefficients (coef rows are contiguous in f and j);
 // every unit is one 16-byte (bf16) or 8-byte (fp32) store.  Units past
 // `units_main` zero the padding blocks of each tile.
@@ -28,7 +30,7 @@ __global__ __launch_bounds__(kThreads) void pack_kernel(const T* __restrict__ co
                                                         T* __restrict__ packed, int in, int out,
                                                         int nb, int nsb, int npairs, int nblk_pad,
                                                         int ntile, int64_t units_main,
-                                                        int64_t units) {
+                                                        int64_t units, bool sparse) {
     constexpr int KJ = Tr<T>::KJ;
     const int64_t u = (int64_t)blockIdx.x * kThreads + threadIdx.x;
     if (u >= units) return;
@@ -46,13 +48,18 @@ __global__ __launch_bounds__(kThreads) void pack_kernel(const T* __restrict__ co
             const int64_t row = (int64_t)o * in + f;
 #pragma unroll
             for (int e = 0; e < KJ; ++e) {
-                const int c = blk * KJ + e;
+                const int c = sparse ? 4 * (e % 4) + 2 * blk + e / 4 : blk * KJ + e;
                 if (c == 0) v[e] = bw[row];
                 else if (c <= nb) v[e] = coef[row * nb + c - 1];
             }
         }
-        const int64_t gblk = (int64_t)tile * nblk_pad + (int64_t)(f / 2) * nsb + blk;
-        dst = (gblk * 2 + (f & 1)) * ntile + n;
+        if (sparse) {
+            const int64_t gblk = (int64_t)tile * nblk_pad + (int64_t)(f / 2) * nsb + (f & 1);
+            dst = (gblk * 2 + blk) * ntile + n;
+        } else {
+            const int64_t gblk = (int64_t)tile * nblk_pad + (int64_t)(f / 2) * nsb + blk;
+            dst = (gblk * 2 + (f & 1)) * ntile + n;
+        }
     } else {
         // padding blocks [npairs * nsb, nblk_pad) of every tile: zeros
         const int64_t q = u - units_main;
@@ -92,11 +99,13 @@ bool layer_geom(int nb, bool bf16, int in, int out, LayerGeom* g) {
     g->nblk = (int)nblk;
     g->nblk_pad = (int)nblk_pad;
     g->kb = kb;
+    g->sparse = bf16 && g->nsb == 2 && nf == 8;
     g->packed_bytes = (size_t)g->ntiles * (size_t)nblk_pad * (size_t)blk_bytes;
     return true;
 }
 
 bool layer_cfg_valid(const LayerGeom& g, const LayerCfg& c) {
+    if (g.sparse && (c.rf != 1 || c.wk != 1 || c.cs != 1)) return false;
     return layer_shape_ok(g.kj == 8, g.nf, c.rf, c.wk, c.nw, c.cs);
 }
 
@@ -175,12 +184,13 @@ hipError_t launch_pack(bool bf16, const LayerGeom& g, int in, int out, const voi
         hipLaunchKernelGGL(pack_kernel<uint16_t>, dim3(blocks), dim3(kThreads), 0, s,
                            static_cast<const uint16_t*>(coef),
                            static_cast<const uint16_t*>(base_w), static_cast<uint16_t*>(packed),
-                           in, out, g.nb, g.nsb, g.npairs, g.nblk_pad, ntile, units_main, units);
+                           in, out, g.nb, g.nsb, g.npairs, g.nblk_pad, ntile, units_main, units,
+                           g.sparse);
     else
         hipLaunchKernelGGL(pack_kernel<float>, dim3(blocks), dim3(kThreads), 0, s,
                            static_cast<const float*>(coef), static_cast<const float*>(base_w),
                            static_cast<float*>(packed), in, out, g.nb, g.nsb, g.npairs,
-                           g.nblk_pad, ntile, units_main, units);
+                           g.nblk_pad, ntile, units_main, units, false);
     return hipGetLastError();
 }
 

@@ -168,7 +168,9 @@ struct Occ {
 // NSBC: blocks per feature when fixed at compile time (0: a.nsb at run time).
 // XP (bf16): x read as the aligned 32-bit word holding the element (x 4-byte
 // aligned and batch * in even, so the word never leaves the tensor).
-template <typename T, int RF, int NFL, int NF, int WK, int NW, int NSBC = 0, bool XP = false>
+// SP: the structured-sparse MFMA on the sparse packed layout (LayerGeom::sparse).
+template <typename T, int RF, int NFL, int NF, int WK, int NW, int NSBC = 0, bool XP = false,
+          bool SP = false>
 __global__ __launch_bounds__(64 * NW)
 __attribute__((amdgpu_waves_per_eu(Occ<RF, NF>::waves)))
 void layer_kernel(LayerArgs a) {
@@ -554,6 +556,42 @@ void layer_kernel(LayerArgs a) {
         }
       }
     };
+    // SP: the A of a whole feature pair for one v_smfmac_f32_32x32x32_bf16
+    // per 32-column fragment.  Its 32 K slots are four groups of four per
+    // feature; a lane holds its row's feature (the feature of its half), two
+    // values per group, each at the position its 2-bit index gives (values at
+    // one position add up).  Group G holds the columns c = G (mod 4), at
+    // position c / 4, so the four columns that can be nonzero (R20) fall one
+    // per group: value 2G is the basis at that column (0 outside columns
+    // 1 .. 15), value 1 the SiLU value at column 0, values 3, 5, 7 are zero.
+    static_assert(!SP || (BF16 && NSBC == 2 && RF == 1 && NF == 8 && NFL == 8 && WK == 1 &&
+                          KBW == 2 && Occ<RF, NF>::waves == 2),
+                  "sparse MFMA shape");
+    auto gen_sparse = [&](const float (&xf)[RF], AFrag<T, RF>& As, uint32_t (&idx)[RF]) {
+      if constexpr (SP) {
+#pragma unroll
+        for (int rf = 0; rf < RF; ++rf) {
+            const float sv = __builtin_fmaf(xf[rf], a.inv_h, a.a_int + 1.0f) + a.a_frac;
+            const float fl = __builtin_floorf(sv);
+            // first of the four columns that can be nonzero, kept within
+            // [-4, 16] (NaN and far off-grid x leave all four outside 1 .. 15)
+            const int c0 = (int)__builtin_fminf(__builtin_fmaxf(fl, -3.0f), 17.0f) - 1;
+            float val[4];
+            uint32_t ix = 0u;
+#pragma unroll
+            for (int G = 0; G < 4; ++G) {
+                const int c = c0 + ((G - c0) & 3);
+                const bool ok = (unsigned)(c - 1) < 15u;
+                val[G] = ok ? half_basis(sv - (float)c) : 0.0f;
+                ix |= (ok ? (uint32_t)(c >> 2) : 0u) << (4 * G);
+            }
+            const float sl0 = half_silu(xf[rf]);
+            As.a[rf] = bf16x8{(__bf16)val[0], (__bf16)sl0, (__bf16)val[1], (__bf16)0.0f,
+                              (__bf16)val[2], (__bf16)0.0f, (__bf16)val[3], (__bf16)0.0f};
+            idx[rf] = ix;
+        }
+      }
+    };
     auto step_split = [&](const AFrag<T, RF>& A, const BFrag& B, const Pos& pg,
                           const uint32_t (&xr)[RF], const float (&xf)[RF], AFrag<T, RF>& An) {
         gen_split(pg, xr, xf, An);
@@ -597,6 +635,7 @@ void layer_kernel(LayerArgs a) {
     float sl[RF];
     AFrag<T, RF> A_cur, A_nxt;
     AFrag<T, RF> A_last;  // LOCAL: block 1 of the current feature, read from the strip
+    uint32_t idx_cur[RF], idx_nxt[RF];  // SP: positions of the compressed A values
     BFrag bq[2];
     Pos pos_c = advance_n(Pos{0, 0, 0}, wk, nsb);  // first block of the current chunk
     Pos pos_l = pos_c;                               // first block of the next chunk to load
@@ -619,7 +658,9 @@ void layer_kernel(LayerArgs a) {
         float x0[RF];
 #pragma unroll
         for (int rf = 0; rf < RF; ++rf) x0[rf] = x_value(pos_c, xq[0][0][rf], rf);
-        if constexpr (LOCAL)
+        if constexpr (SP)
+            gen_sparse(x0, A_cur, idx_cur);
+        else if constexpr (LOCAL)
             gen_local(x0, A_cur, A_last);
         else
             gen_split(pos_c, xq[0][0], x0, A_cur);
@@ -678,6 +719,44 @@ void layer_kernel(LayerArgs a) {
 
         const u32x4* st = stage(kk);
         if constexpr (!MIDBAR) read_b(bq[0], st, wk);  // (MIDBAR: read during the last chunk)
+        if constexpr (SP) {
+            // one feature pair per chunk, one step: the B of both blocks, the
+            // next pair's A (its x was loaded a chunk ago), the MFMAs of this
+            // pair, then the next chunk's weights to the other LDS stage
+            read_b(bq[1], st, 1);
+            const Pos pn = advance<KB>(pos_c, nsb);
+            float xf[RF];
+#pragma unroll
+            for (int rf = 0; rf < RF; ++rf) xf[rf] = x_value(pn, xq[JN][0][rf], rf);
+            if constexpr (LASTG) {
+                if (c * KBW >= nq) {  // a padding pair: contributes 0
+#pragma unroll
+                    for (int rf = 0; rf < RF; ++rf) zero_frag(A_cur, rf);
+                }
+            }
+            gen_sparse(xf, A_nxt, idx_nxt);
+#pragma unroll
+            for (int nf = 0; nf < NF; ++nf) {
+                const bf16x16 b = __builtin_shufflevector(bq[0].b[nf], bq[1].b[nf], 0, 1, 2, 3, 4,
+                                                          5, 6, 7, 8, 9, 10, 11, 12, 13, 14, 15);
+                acc[0][nf] = __builtin_amdgcn_smfmac_f32_32x32x32_bf16(A_cur.a[0], b, acc[0][nf],
+                                                                       (int)idx_cur[0], 0, 0);
+            }
+            // (the next A complete here, so code sinking cannot move its
+            // generation past the next barrier)
+            {
+                u32x4 w = __builtin_bit_cast(u32x4, A_nxt.a[0]);
+                asm volatile("" : "+v"(w), "+v"(idx_nxt[0]));
+                A_nxt.a[0] = __builtin_bit_cast(bf16x8, w);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+            store(std::integral_constant<int, K + 1>{}, wq[JN]);
+            __builtin_amdgcn_sched_barrier(0);
+            A_cur = A_nxt;
+            idx_cur[0] = idx_nxt[0];
+            pos_c = pn;
+            return;
+        }
         Pos p = pos_c;
         float xnext[RF];  // x of the next chunk's first block (X_AT_STORE)
 #pragma unroll
@@ -841,6 +920,21 @@ hipError_t launch_cfg(const LayerGeom& g, LayerArgs a, hipStream_t s) {
     // last of its feature at compile time), with x read as aligned 32-bit
     // words where that stays inside the tensor.
     constexpr bool BF16 = sizeof(T) == 2;
+    // The sparse packed layout runs only on the structured-sparse MFMA.
+    if (g.sparse) {
+        if constexpr (BF16 && RF == 1 && NFL == 8 && NF == 8 && WK == 1 &&
+                      layer_chunk_blocks(BF16, NFL) == 2) {
+            if (layer_x_words(a.x, a.batch, a.in))
+                hipLaunchKernelGGL((layer_kernel<T, 1, 8, 8, 1, NW, 2, true, true>), grid,
+                                   dim3(64 * NW), 0, s, a);
+            else
+                hipLaunchKernelGGL((layer_kernel<T, 1, 8, 8, 1, NW, 2, false, true>), grid,
+                                   dim3(64 * NW), 0, s, a);
+            return hipGetLastError();
+        } else {
+            return hipErrorInvalidValue;
+        }
+    }
     if constexpr (BF16 && WK == 1 &&
                   layer_chunk_blocks(BF16, NFL) % 2 == 0) {
         if (g.nsb == 2 && layer_x_words(a.x, a.batch, a.in)) {
