@@ -105,7 +105,10 @@ bool layer_geom(int nb, bool bf16, int in, int out, LayerGeom* g) {
 }
 
 bool layer_cfg_valid(const LayerGeom& g, const LayerCfg& c) {
-    if (g.sparse && (c.rf != 1 || c.wk != 1 || c.cs != 1)) return false;
+    // sparse: one row tile per wave, no K split; four-wave workgroups only
+    // on column slices (the whole 256 columns with four waves' larger share
+    // of the weight staging exceed 256 registers and spill)
+    if (g.sparse && (c.rf != 1 || c.wk != 1 || (c.nw == 4 && c.cs == 1))) return false;
     return layer_shape_ok(g.kj == 8, g.nf, c.rf, c.wk, c.nw, c.cs);
 }
 

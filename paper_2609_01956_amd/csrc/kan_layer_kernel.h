@@ -265,11 +265,6 @@ void layer_kernel(LayerArgs a) {
     // load when it is issued.
     typedef uint32_t XSet[KBW][RF];
     constexpr bool X_FIRST_ONLY = ALIGNED && BF16 && Occ<RF, NF>::waves == 2;
-    // One feature pair per chunk: the x of the next chunk's pair is converted
-    // where the chunk stores the next chunk's weights (their loads were issued
-    // after it, so it has arrived), and only the float is carried to the step
-    // that uses it.
-    constexpr bool X_AT_STORE = X_FIRST_ONLY && NSBC == KBW;
     // LOCAL (narrow layers, two blocks per feature, whole features per
     // chunk): of a feature's basis columns at most four consecutive ones are
     // nonzero (|v| < 2), so the truncated power form is evaluated at those
@@ -462,19 +457,12 @@ void layer_kernel(LayerArgs a) {
     // Stepping the coordinate by 8 is exact wherever a basis value of the
     // block is nonzero (there |s| < 17 and s - 8 is computed exactly).
     constexpr bool GEN_SPLIT = BF16 && Occ<RF, NF>::waves == 2;
-    // MIDBAR (bf16, one wave per SIMD, whole features per chunk): the chunk's
-    // one barrier sits before its last block, right after the next chunk's
-    // weights are stored, so the B fragments of every block, the next
-    // chunk's first included, are read from LDS one step ahead (a wave alone
-    // on its SIMD has nothing else to cover that latency with).
-    constexpr bool MIDBAR = BF16 && Occ<RF, NF>::waves == 1 && ALIGNED;
     constexpr bool DIRECT = WK > 1;
     float sc[RF];  // coordinate of the wave's current block (element 0)
     // real columns in the last block of a feature, rounded up to even
     const int last_cols = a.nb + 1 - KJ * (nsb - 1);
     const int last_even = (last_cols + 1) & ~1;
-    auto gen_split = [&](const Pos& pg, const uint32_t (&xr)[RF], const float (&xf)[RF],
-                         AFrag<T, RF>& An) {
+    auto gen_split = [&](const Pos& pg, const uint32_t (&xr)[RF], AFrag<T, RF>& An) {
       if constexpr (GEN_SPLIT) {
         auto basis = [&](int rf, int e0, int e1) {
 #pragma unroll
@@ -487,7 +475,7 @@ void layer_kernel(LayerArgs a) {
         if (pg.bsub == 0) {
 #pragma unroll
             for (int rf = 0; rf < RF; ++rf) {
-                const float xv = X_AT_STORE ? xf[rf] : x_value(pg, xr[rf], rf);
+                const float xv = x_value(pg, xr[rf], rf);
                 sc[rf] = __builtin_fmaf(xv, a.inv_h, a.a_int + 1.0f) + a.a_frac;
                 // keep the coordinate itself for the feature's later blocks
                 // (recomputing it there from x would hold the raw x register,
@@ -564,8 +552,8 @@ void layer_kernel(LayerArgs a) {
     // position c / 4, so the four columns that can be nonzero (R20) fall one
     // per group: value 2G is the basis at that column (0 outside columns
     // 1 .. 15), value 1 the SiLU value at column 0, values 3, 5, 7 are zero.
-    static_assert(!SP || (BF16 && NSBC == 2 && RF == 1 && NF == 8 && NFL == 8 && WK == 1 &&
-                          KBW == 2 && Occ<RF, NF>::waves == 2),
+    static_assert(!SP || (BF16 && NSBC == 2 && RF == 1 && NFL == 8 && WK == 1 && KBW == 2 &&
+                          Occ<RF, NF>::waves == 2),
                   "sparse MFMA shape");
     auto gen_sparse = [&](const float (&xf)[RF], AFrag<T, RF>& As, uint32_t (&idx)[RF]) {
       if constexpr (SP) {
@@ -593,8 +581,8 @@ void layer_kernel(LayerArgs a) {
       }
     };
     auto step_split = [&](const AFrag<T, RF>& A, const BFrag& B, const Pos& pg,
-                          const uint32_t (&xr)[RF], const float (&xf)[RF], AFrag<T, RF>& An) {
-        gen_split(pg, xr, xf, An);
+                          const uint32_t (&xr)[RF], AFrag<T, RF>& An) {
+        gen_split(pg, xr, An);
 #pragma unroll
         for (int i = 0; i < NMFMA; ++i) do_mfma(i, A, B);
         // The next block's A must be complete here: otherwise code sinking
@@ -651,7 +639,6 @@ void layer_kernel(LayerArgs a) {
     __builtin_amdgcn_s_waitcnt(WAIT_LDS);
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
-    if constexpr (MIDBAR) read_b(bq[0], stage(std::integral_constant<int, 0>{}), wk);
 
     // A of the wave's first block (nothing to interleave with yet).
     if constexpr (GEN_SPLIT) {
@@ -663,7 +650,7 @@ void layer_kernel(LayerArgs a) {
         else if constexpr (LOCAL)
             gen_local(x0, A_cur, A_last);
         else
-            gen_split(pos_c, xq[0][0], x0, A_cur);
+            gen_split(pos_c, xq[0][0], A_cur);
     } else {
         float x0[RF];
 #pragma unroll
@@ -693,7 +680,7 @@ void layer_kernel(LayerArgs a) {
             pos_c.bsub = 0;
             pos_l.bsub = 0;
         }
-        if (!MIDBAR && c > 0) {  // (chunk 0's barrier is in the prologue)
+        if (c > 0) {  // (chunk 0's barrier is in the prologue)
             __builtin_amdgcn_s_waitcnt(WAIT_LDS);
             __builtin_amdgcn_s_barrier();
             __builtin_amdgcn_sched_barrier(0);
@@ -712,13 +699,13 @@ void layer_kernel(LayerArgs a) {
         // The next chunk's weights go to the other LDS stage before the next
         // barrier.  With the split generation they are stored after the
         // first step, which gives their loads that step's time to land.
-        if constexpr (!GEN_SPLIT && !MIDBAR) {
+        if constexpr (!GEN_SPLIT) {
             store(std::integral_constant<int, K + 1>{}, wq[JN]);
             __builtin_amdgcn_sched_barrier(0);
         }
 
         const u32x4* st = stage(kk);
-        if constexpr (!MIDBAR) read_b(bq[0], st, wk);  // (MIDBAR: read during the last chunk)
+        read_b(bq[0], st, wk);
         if constexpr (SP) {
             // one feature pair per chunk, one step: the B of both blocks, the
             // next pair's A (its x was loaded a chunk ago), the MFMAs of this
@@ -758,9 +745,6 @@ void layer_kernel(LayerArgs a) {
             return;
         }
         Pos p = pos_c;
-        float xnext[RF];  // x of the next chunk's first block (X_AT_STORE)
-#pragma unroll
-        for (int rf = 0; rf < RF; ++rf) xnext[rf] = 0.0f;
         auto one = [&](auto tt) {
             constexpr int t = decltype(tt)::value;
             // position of the next block: the next step's, or the first block
@@ -782,11 +766,7 @@ void layer_kernel(LayerArgs a) {
             // Two waves: B is read at the start of each step; the other wave
             // covers the latency, and the registers of a second B set are
             // saved.
-            constexpr bool PREF = Occ<RF, NF>::waves == 1 && (t + 1 < KBW || MIDBAR);
-            // block read ahead: the next one of this chunk, or (MIDBAR, last
-            // step) the first block of the next chunk from the other stage
-            const u32x4* st_n = t + 1 < KBW ? st : stage(std::integral_constant<int, K + 1>{});
-            const int bi_n = t + 1 < KBW ? wk + WK * (t + 1) : wk;
+            constexpr bool PREF = Occ<RF, NF>::waves == 1 && t + 1 < KBW;
             if constexpr (Occ<RF, NF>::waves == 2 && t > 0) read_b(bq[t & 1], st, wk + WK * t);
             if constexpr (LOCAL) {
                 // even steps: block 1 of the current feature is already
@@ -797,41 +777,21 @@ void layer_kernel(LayerArgs a) {
                     float xf[RF];
 #pragma unroll
                     for (int rf = 0; rf < RF; ++rf)
-                        xf[rf] = X_AT_STORE ? xnext[rf] : x_value(pnext, xr[t][rf], rf);
+                        xf[rf] = x_value(pnext, xr[t][rf], rf);
                     gen_local(xf, A_nxt, A_last);
                 }
 #pragma unroll
                 for (int i = 0; i < NMFMA; ++i) do_mfma(i, A_cur, bq[t & 1]);
             } else if constexpr (GEN_SPLIT)
-                step_split(A_cur, bq[t & 1], pnext, xr[t], xnext, A_nxt);
+                step_split(A_cur, bq[t & 1], pnext, xr[t], A_nxt);
             else
                 step(A_cur, bq[t & 1], pnext, xv, sl, A_nxt, std::integral_constant<bool, PREF>{},
-                     bq[(t + 1) & 1], st_n, bi_n);
+                     bq[(t + 1) & 1], st, wk + WK * (t + 1));
             A_cur = A_nxt;
             p = pnext;
-            if constexpr (MIDBAR && t + 2 == KBW) {
-                // the next chunk's weights to the other stage, then the
-                // chunk's barrier: every wave has stored them, and has read
-                // its last block of the previous chunk from that stage
-                __builtin_amdgcn_sched_barrier(0);
-                store(std::integral_constant<int, K + 1>{}, wq[JN]);
-                __builtin_amdgcn_s_waitcnt(WAIT_LDS);
-                __builtin_amdgcn_s_barrier();
-                __builtin_amdgcn_sched_barrier(0);
-            }
             if constexpr (GEN_SPLIT && t == 0) {
                 __builtin_amdgcn_sched_barrier(0);
                 store(std::integral_constant<int, K + 1>{}, wq[JN]);
-                if constexpr (X_AT_STORE) {
-                    Pos pn = pos_c;  // first block of the next chunk
-                    pn.pair += 1;
-                    pn.bsub = 0;
-#pragma unroll
-                    for (int rf = 0; rf < RF; ++rf) {
-                        xnext[rf] = x_value(pn, xq[JN][0][rf], rf);
-                        asm volatile("" : "+v"(xnext[rf]));
-                    }
-                }
                 __builtin_amdgcn_sched_barrier(0);
             }
         };
@@ -922,21 +882,21 @@ hipError_t launch_cfg(const LayerGeom& g, LayerArgs a, hipStream_t s) {
     constexpr bool BF16 = sizeof(T) == 2;
     // The sparse packed layout runs only on the structured-sparse MFMA.
     if (g.sparse) {
-        if constexpr (BF16 && RF == 1 && NFL == 8 && NF == 8 && WK == 1 &&
+        if constexpr (BF16 && RF == 1 && NFL == 8 && WK == 1 && (NW == 8 || NF < 8) &&
                       layer_chunk_blocks(BF16, NFL) == 2) {
             if (layer_x_words(a.x, a.batch, a.in))
-                hipLaunchKernelGGL((layer_kernel<T, 1, 8, 8, 1, NW, 2, true, true>), grid,
+                hipLaunchKernelGGL((layer_kernel<T, 1, 8, NF, 1, NW, 2, true, true>), grid,
                                    dim3(64 * NW), 0, s, a);
             else
-                hipLaunchKernelGGL((layer_kernel<T, 1, 8, 8, 1, NW, 2, false, true>), grid,
+                hipLaunchKernelGGL((layer_kernel<T, 1, 8, NF, 1, NW, 2, false, true>), grid,
                                    dim3(64 * NW), 0, s, a);
             return hipGetLastError();
         } else {
             return hipErrorInvalidValue;
         }
     }
-    if constexpr (BF16 && WK == 1 &&
-                  layer_chunk_blocks(BF16, NFL) % 2 == 0) {
+    // (256-column packed tiles with two blocks per feature are sparse)
+    if constexpr (BF16 && WK == 1 && NFL < 8 && layer_chunk_blocks(BF16, NFL) % 2 == 0) {
         if (g.nsb == 2 && layer_x_words(a.x, a.batch, a.in)) {
             hipLaunchKernelGGL((layer_kernel<T, RF, NFL, NF, WK, NW, 2, true>), grid, dim3(64 * NW),
                                0, s, a);
