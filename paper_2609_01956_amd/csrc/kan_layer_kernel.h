@@ -549,9 +549,13 @@ void layer_kernel(LayerArgs a) {
     // feature; a lane holds its row's feature (the feature of its half), two
     // values per group, each at the position its 2-bit index gives (values at
     // one position add up).  Group G holds the columns c = G (mod 4), at
-    // position c / 4, so the four columns that can be nonzero (R20) fall one
-    // per group: value 2G is the basis at that column (0 outside columns
-    // 1 .. 15), value 1 the SiLU value at column 0, values 3, 5, 7 are zero.
+    // position c / 4.  Every nonzero basis column lies in the four columns
+    // c0 .. c0 + 3 with c0 = floor(s) - 1 (R20); clamped to [1, 12], the
+    // window stays inside columns 1 .. 15 and the columns it then takes in
+    // are at |v| >= 2, where the form is exactly 0.  Its columns fall one per
+    // group: value 2G is the basis at column c0 + ((G - c0) mod 4), at
+    // position c0 / 4, plus 1 for G < c0 mod 4; value 1 is the SiLU value at
+    // column 0 (group 0, position 0); values 3, 5, 7 are zero.
     static_assert(!SP || (BF16 && NSBC == 2 && RF == 1 && NFL == 8 && WK == 1 && KBW == 2 &&
                           Occ<RF, NF>::waves == 2),
                   "sparse MFMA shape");
@@ -560,23 +564,19 @@ void layer_kernel(LayerArgs a) {
 #pragma unroll
         for (int rf = 0; rf < RF; ++rf) {
             const float sv = __builtin_fmaf(xf[rf], a.inv_h, a.a_int + 1.0f) + a.a_frac;
-            const float fl = __builtin_floorf(sv);
-            // first of the four columns that can be nonzero, kept within
-            // [-4, 16] (NaN and far off-grid x leave all four outside 1 .. 15)
-            const int c0 = (int)__builtin_fminf(__builtin_fmaxf(fl, -3.0f), 17.0f) - 1;
-            float val[4];
-            uint32_t ix = 0u;
+            // c0 + 1 = floor(s) within [2, 13] (a NaN coordinate gives c0 = 1
+            // and NaN values, as it should)
+            const float f1 = __builtin_fminf(__builtin_fmaxf(__builtin_floorf(sv), 2.0f), 13.0f);
+            const int c0 = (int)f1 - 1;
+            const int r = c0 & 3;
+            const float d = sv - (f1 - 1.0f);  // v of column c0
+            float bv[4];
 #pragma unroll
-            for (int G = 0; G < 4; ++G) {
-                const int c = c0 + ((G - c0) & 3);
-                const bool ok = (unsigned)(c - 1) < 15u;
-                val[G] = ok ? half_basis(sv - (float)c) : 0.0f;
-                ix |= (ok ? (uint32_t)(c >> 2) : 0u) << (4 * G);
-            }
-            const float sl0 = half_silu(xf[rf]);
-            As.a[rf] = bf16x8{(__bf16)val[0], (__bf16)sl0, (__bf16)val[1], (__bf16)0.0f,
-                              (__bf16)val[2], (__bf16)0.0f, (__bf16)val[3], (__bf16)0.0f};
-            idx[rf] = ix;
+            for (int G = 0; G < 4; ++G) bv[G] = half_basis(d - (float)((G - r) & 3));
+            idx[rf] = (uint32_t)(c0 >> 2) * 0x1111u + (0x1111u & ((1u << (4 * r)) - 1u));
+            const u32x4 w = {pack_bf16x2(bv[0], half_silu(xf[rf])), pack_bf16x2(bv[1], 0.0f),
+                             pack_bf16x2(bv[2], 0.0f), pack_bf16x2(bv[3], 0.0f)};
+            As.a[rf] = __builtin_bit_cast(bf16x8, w);
         }
       }
     };
