@@ -174,8 +174,7 @@ kan_status kan_layer_forward_packed(const kan_grid* grid, kan_dtype dtype, int64
     a.inv_h = gc.inv_h;
     a.a_int = gc.a_int;
     a.a_frac = gc.a_frac;
-    kan::LayerCfg cfg = kan::plan_layer(geom, dtype == KAN_BF16, batch,
-                                        kan::layer_x_words(x, batch, in_features));
+    kan::LayerCfg cfg = kan::plan_layer(geom, dtype == KAN_BF16, batch);
     kan::parse_layer_cfg_override(geom, &cfg);
     return device_status(kan::launch_layer(dtype == KAN_BF16, geom, cfg, a,
                                            static_cast<hipStream_t>(stream)));

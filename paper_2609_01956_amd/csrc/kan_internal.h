@@ -67,7 +67,7 @@ struct LayerGeom {
     int kb;       // blocks per chunk
     int nf;       // 32-column MFMA fragments per N tile (1, 2, 4 or 8)
     int ntiles;   // ceil(out / (32 * nf))
-    // bf16 with two blocks per feature and 256-column tiles: packed for the
+    // bf16 with two blocks per feature (5 <= G <= 12): packed for the
     // structured-sparse MFMA (block = feature of the pair, half = column
     // half, element e of half w = column 4 (e % 4) + 2 w + e / 4), and only
     // the shapes with one row tile per wave and no K split run on it (eight
@@ -114,8 +114,7 @@ __host__ __device__ constexpr bool layer_shape_ok(bool bf16, int nfl, int rf, in
 inline bool layer_x_words(const void* x, int64_t batch, int in) {
     return reinterpret_cast<uintptr_t>(x) % 4 == 0 && (batch * (int64_t)in) % 2 == 0;
 }
-// x_words: layer_x_words holds for the layer's input (bf16).
-LayerCfg plan_layer(const LayerGeom& g, bool bf16, int64_t batch, bool x_words);
+LayerCfg plan_layer(const LayerGeom& g, bool bf16, int64_t batch);
 // KAN_LAYER_CFG="rf,wk[,nw[,cs]]" forces a configuration (testing and tuning);
 // ignored when malformed or not valid for the geometry.
 bool parse_layer_cfg_override(const LayerGeom& g, LayerCfg* c);

@@ -99,20 +99,22 @@ bool layer_geom(int nb, bool bf16, int in, int out, LayerGeom* g) {
     g->nblk = (int)nblk;
     g->nblk_pad = (int)nblk_pad;
     g->kb = kb;
-    g->sparse = bf16 && g->nsb == 2 && nf == 8;
+    g->sparse = bf16 && g->nsb == 2;
     g->packed_bytes = (size_t)g->ntiles * (size_t)nblk_pad * (size_t)blk_bytes;
     return true;
 }
 
 bool layer_cfg_valid(const LayerGeom& g, const LayerCfg& c) {
-    // sparse: one row tile per wave, no K split; four-wave workgroups only
-    // on column slices (the whole 256 columns with four waves' larger share
-    // of the weight staging exceed 256 registers and spill)
-    if (g.sparse && (c.rf != 1 || c.wk != 1 || (c.nw == 4 && c.cs == 1))) return false;
+    // sparse: one row tile per wave, no K split; 256-column tiles take
+    // four-wave workgroups only on column slices (the whole 256 columns with
+    // four waves' larger share of the weight staging exceed 256 registers
+    // and spill)
+    if (g.sparse && (c.rf != 1 || c.wk != 1 || (g.nf == 8 && c.nw == 4 && c.cs == 1)))
+        return false;
     return layer_shape_ok(g.kj == 8, g.nf, c.rf, c.wk, c.nw, c.cs);
 }
 
-LayerCfg plan_layer(const LayerGeom& g, bool bf16, int64_t batch, bool x_words) {
+LayerCfg plan_layer(const LayerGeom& g, bool bf16, int64_t batch) {
     auto wgs = [&](const LayerCfg& c) {
         const int64_t bm = 32LL * c.rf * (c.nw / c.wk);
         return ((batch + bm - 1) / bm) * g.ntiles * c.cs;
@@ -124,14 +126,14 @@ LayerCfg plan_layer(const LayerGeom& g, bool bf16, int64_t batch, bool x_words) 
     // traffic per row.  Used when it fills the chip (one workgroup per CU).
     const LayerCfg wide{1, 1, 8, 1};
     if (bf16 && g.nf == 8 && wgs(wide) >= 256) return wide;
-    // Narrow bf16 layers (one or two 32-column fragments) with two blocks per
-    // feature build each feature's A from its four nonzero basis columns,
-    // which needs whole features per wave (no K split): one row tile per
-    // wave, eight waves per workgroup when that fills the chip, else four
-    // (C5 layer 3, 256 -> 10: 74 and 75 us against 94 us with the K split).
-    if (bf16 && g.nf <= 2 && g.nsb == 2 && x_words) {
+    // Sparse layers (bf16, two blocks per feature): one row tile per wave and
+    // no K split; eight waves per workgroup when that fills the chip, else
+    // four over the whole tile (not for 256-column tiles), else column slices
+    // below.  (C5 layer 3, 256 -> 10: 49 us; 256 -> 100: 73 us with eight
+    // waves against 82 us with four.)
+    if (g.sparse) {
         const LayerCfg n8{1, 1, 8, 1}, n4{1, 1, 4, 1};
-        if (layer_cfg_valid(g, n8) && wgs(n8) >= 256) return n8;
+        if (wgs(n8) >= 256) return n8;
         if (layer_cfg_valid(g, n4) && wgs(n4) >= 256) return n4;
     }
     // Otherwise the tallest workgroup over the whole N tile (fewest re-reads

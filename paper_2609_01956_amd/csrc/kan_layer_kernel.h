@@ -265,22 +265,6 @@ void layer_kernel(LayerArgs a) {
     // load when it is issued.
     typedef uint32_t XSet[KBW][RF];
     constexpr bool X_FIRST_ONLY = ALIGNED && BF16 && Occ<RF, NF>::waves == 2;
-    // LOCAL (narrow layers, two blocks per feature, whole features per
-    // chunk): of a feature's basis columns at most four consecutive ones are
-    // nonzero (|v| < 2), so the truncated power form is evaluated at those
-    // four only, and the feature's two A fragments are assembled in a
-    // lane-private LDS strip (zeroed, the four values and the SiLU value
-    // written, both fragments read back).  The other columns are the exact
-    // zeros the clamped form gives there.  With one or two 32-column
-    // fragments per block the basis, not the contraction, bounds the layer;
-    // wider layers keep the per-column evaluation (the strip's LDS traffic
-    // and latency cost them more than the VALU work saved).
-    constexpr bool LOCAL = X_FIRST_ONLY && NSBC == 2 && NF <= 2;
-    // strip: 24 bf16 columns per (wave, row tile, lane), feature column c at
-    // index c + 4; a 48-byte stride keeps 16-byte accesses of 8 lanes on
-    // distinct banks, and the 8-byte lead makes columns 0 and 8 16-byte aligned.
-    constexpr int STRIP = 24;
-    __shared__ __align__(16) uint16_t strips[LOCAL ? 4 + NW * RF * 64 * STRIP : 8];
     typedef u32x4 WSet[DPW];
     const uint32_t wlane = (uint32_t)(wave * 1024 + lane * 16);
     uint32_t goff[CS == 1 ? 1 : DPW];
@@ -515,35 +499,6 @@ void layer_kernel(LayerArgs a) {
     // matrix core busy; the compiler is left to schedule within the step,
     // which measured as fast as a fixed phase order with raised MFMA
     // priority, and faster for the 256 -> 256 layer).
-    // LOCAL: both A fragments of a feature with x value xf (block 0 -> AF,
-    // block 1 -> AL).  Column c holds N / 2 at v = s - c; with n = floor(s)
-    // and f = s - n the columns that can be nonzero are n - 1 .. n + 2, at
-    // v = f + 1, f, f - 1, f - 2.
-    auto gen_local = [&](const float (&xf)[RF], AFrag<T, RF>& AF, AFrag<T, RF>& AL) {
-      if constexpr (LOCAL) {
-#pragma unroll
-        for (int rf = 0; rf < RF; ++rf) {
-            const float sv = __builtin_fmaf(xf[rf], a.inv_h, a.a_int + 1.0f) + a.a_frac;
-            const float fl = __builtin_floorf(sv);
-            const float f = sv - fl;
-            // first column, kept within [-4, 16] (NaN and far off-grid x put
-            // the four values outside columns 0 .. 15, where they are not read)
-            const int c0 = (int)__builtin_fminf(__builtin_fmaxf(fl, -3.0f), 17.0f) - 1;
-            const uint32_t w0 = pack_bf16x2(half_basis(f + 1.0f), half_basis(f));
-            const uint32_t w1 = pack_bf16x2(half_basis(f - 1.0f), half_basis(f - 2.0f));
-            uint16_t* st = strips + 4 + ((wave * RF + rf) * 64 + lane) * STRIP;
-            *reinterpret_cast<u32x4*>(st + 4) = u32x4{0u, 0u, 0u, 0u};
-            *reinterpret_cast<u32x4*>(st + 12) = u32x4{0u, 0u, 0u, 0u};
-            st[c0 + 4] = (uint16_t)w0;
-            st[c0 + 5] = (uint16_t)(w0 >> 16);
-            st[c0 + 6] = (uint16_t)w1;
-            st[c0 + 7] = (uint16_t)(w1 >> 16);
-            st[4] = __builtin_bit_cast(uint16_t, (__bf16)half_silu(xf[rf]));  // column 0
-            AF.a[rf] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(st + 4));
-            AL.a[rf] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(st + 12));
-        }
-      }
-    };
     // SP: the A of a whole feature pair for one v_smfmac_f32_32x32x32_bf16
     // per 32-column fragment.  Its 32 K slots are four groups of four per
     // feature; a lane holds its row's feature (the feature of its half), two
@@ -556,7 +511,7 @@ void layer_kernel(LayerArgs a) {
     // group: value 2G is the basis at column c0 + ((G - c0) mod 4), at
     // position c0 / 4, plus 1 for G < c0 mod 4; value 1 is the SiLU value at
     // column 0 (group 0, position 0); values 3, 5, 7 are zero.
-    static_assert(!SP || (BF16 && NSBC == 2 && RF == 1 && NFL == 8 && WK == 1 && KBW == 2 &&
+    static_assert(!SP || (BF16 && NSBC == 2 && RF == 1 && WK == 1 && KBW % 2 == 0 &&
                           Occ<RF, NF>::waves == 2),
                   "sparse MFMA shape");
     auto gen_sparse = [&](const float (&xf)[RF], AFrag<T, RF>& As, uint32_t (&idx)[RF]) {
@@ -622,7 +577,6 @@ void layer_kernel(LayerArgs a) {
     WSet wq[L];
     float sl[RF];
     AFrag<T, RF> A_cur, A_nxt;
-    AFrag<T, RF> A_last;  // LOCAL: block 1 of the current feature, read from the strip
     uint32_t idx_cur[RF], idx_nxt[RF];  // SP: positions of the compressed A values
     BFrag bq[2];
     Pos pos_c = advance_n(Pos{0, 0, 0}, wk, nsb);  // first block of the current chunk
@@ -647,8 +601,6 @@ void layer_kernel(LayerArgs a) {
         for (int rf = 0; rf < RF; ++rf) x0[rf] = x_value(pos_c, xq[0][0][rf], rf);
         if constexpr (SP)
             gen_sparse(x0, A_cur, idx_cur);
-        else if constexpr (LOCAL)
-            gen_local(x0, A_cur, A_last);
         else
             gen_split(pos_c, xq[0][0], A_cur);
     } else {
@@ -707,41 +659,54 @@ void layer_kernel(LayerArgs a) {
         const u32x4* st = stage(kk);
         read_b(bq[0], st, wk);
         if constexpr (SP) {
-            // one feature pair per chunk, one step: the B of both blocks, the
-            // next pair's A (its x was loaded a chunk ago), the MFMAs of this
-            // pair, then the next chunk's weights to the other LDS stage
-            read_b(bq[1], st, 1);
-            const Pos pn = advance<KB>(pos_c, nsb);
-            float xf[RF];
+            // the chunk's feature pairs, one step each: the B of the pair's two
+            // blocks, the next pair's A (its x was loaded a chunk or more
+            // ago), the MFMAs of this pair; after the first pair the next
+            // chunk's weights go to the other LDS stage
+            constexpr int NPC = KBW / 2;  // pairs per chunk
+            auto pair_step = [&](auto qq) {
+                constexpr int q = decltype(qq)::value;
+                if constexpr (q > 0) read_b(bq[0], st, 2 * q);
+                read_b(bq[1], st, 2 * q + 1);
+                Pos pn = pos_c;  // the next pair
+                pn.pair += q + 1;
+                // (x of the next pair's first block, copied before this
+                // chunk's loads reused its register set)
+                float xf[RF];
 #pragma unroll
-            for (int rf = 0; rf < RF; ++rf) xf[rf] = x_value(pn, xq[JN][0][rf], rf);
-            if constexpr (LASTG) {
-                if (c * KBW >= nq) {  // a padding pair: contributes 0
+                for (int rf = 0; rf < RF; ++rf) xf[rf] = x_value(pn, xr[2 * q + 1][rf], rf);
+                if constexpr (LASTG) {
+                    if (c * KBW + 2 * q >= nq) {  // a padding pair: contributes 0
 #pragma unroll
-                    for (int rf = 0; rf < RF; ++rf) zero_frag(A_cur, rf);
+                        for (int rf = 0; rf < RF; ++rf) zero_frag(A_cur, rf);
+                    }
                 }
-            }
-            gen_sparse(xf, A_nxt, idx_nxt);
+                gen_sparse(xf, A_nxt, idx_nxt);
 #pragma unroll
-            for (int nf = 0; nf < NF; ++nf) {
-                const bf16x16 b = __builtin_shufflevector(bq[0].b[nf], bq[1].b[nf], 0, 1, 2, 3, 4,
-                                                          5, 6, 7, 8, 9, 10, 11, 12, 13, 14, 15);
-                acc[0][nf] = __builtin_amdgcn_smfmac_f32_32x32x32_bf16(A_cur.a[0], b, acc[0][nf],
-                                                                       (int)idx_cur[0], 0, 0);
-            }
-            // (the next A complete here, so code sinking cannot move its
-            // generation past the next barrier)
-            {
-                u32x4 w = __builtin_bit_cast(u32x4, A_nxt.a[0]);
-                asm volatile("" : "+v"(w), "+v"(idx_nxt[0]));
-                A_nxt.a[0] = __builtin_bit_cast(bf16x8, w);
-            }
-            __builtin_amdgcn_sched_barrier(0);
-            store(std::integral_constant<int, K + 1>{}, wq[JN]);
-            __builtin_amdgcn_sched_barrier(0);
-            A_cur = A_nxt;
-            idx_cur[0] = idx_nxt[0];
-            pos_c = pn;
+                for (int nf = 0; nf < NF; ++nf) {
+                    const bf16x16 b = __builtin_shufflevector(bq[0].b[nf], bq[1].b[nf], 0, 1, 2, 3,
+                                                              4, 5, 6, 7, 8, 9, 10, 11, 12, 13, 14,
+                                                              15);
+                    acc[0][nf] = __builtin_amdgcn_smfmac_f32_32x32x32_bf16(
+                        A_cur.a[0], b, acc[0][nf], (int)idx_cur[0], 0, 0);
+                }
+                // (the next A complete here, so code sinking cannot move its
+                // generation past the next barrier)
+                {
+                    u32x4 w = __builtin_bit_cast(u32x4, A_nxt.a[0]);
+                    asm volatile("" : "+v"(w), "+v"(idx_nxt[0]));
+                    A_nxt.a[0] = __builtin_bit_cast(bf16x8, w);
+                }
+                if constexpr (q == 0) {
+                    __builtin_amdgcn_sched_barrier(0);
+                    store(std::integral_constant<int, K + 1>{}, wq[JN]);
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+                A_cur = A_nxt;
+                idx_cur[0] = idx_nxt[0];
+            };
+            StaticFor<0, NPC>::run(pair_step);
+            pos_c = advance<KB>(pos_c, nsb);
             return;
         }
         Pos p = pos_c;
@@ -768,21 +733,7 @@ void layer_kernel(LayerArgs a) {
             // saved.
             constexpr bool PREF = Occ<RF, NF>::waves == 1 && t + 1 < KBW;
             if constexpr (Occ<RF, NF>::waves == 2 && t > 0) read_b(bq[t & 1], st, wk + WK * t);
-            if constexpr (LOCAL) {
-                // even steps: block 1 of the current feature is already
-                // assembled; odd steps: both blocks of the next feature
-                if constexpr (t % 2 == 0) {
-                    A_nxt = A_last;
-                } else {
-                    float xf[RF];
-#pragma unroll
-                    for (int rf = 0; rf < RF; ++rf)
-                        xf[rf] = x_value(pnext, xr[t][rf], rf);
-                    gen_local(xf, A_nxt, A_last);
-                }
-#pragma unroll
-                for (int i = 0; i < NMFMA; ++i) do_mfma(i, A_cur, bq[t & 1]);
-            } else if constexpr (GEN_SPLIT)
+            if constexpr (GEN_SPLIT)
                 step_split(A_cur, bq[t & 1], pnext, xr[t], A_nxt);
             else
                 step(A_cur, bq[t & 1], pnext, xv, sl, A_nxt, std::integral_constant<bool, PREF>{},
@@ -882,25 +833,17 @@ hipError_t launch_cfg(const LayerGeom& g, LayerArgs a, hipStream_t s) {
     constexpr bool BF16 = sizeof(T) == 2;
     // The sparse packed layout runs only on the structured-sparse MFMA.
     if (g.sparse) {
-        if constexpr (BF16 && RF == 1 && NFL == 8 && WK == 1 && (NW == 8 || NF < 8) &&
-                      layer_chunk_blocks(BF16, NFL) == 2) {
+        if constexpr (BF16 && RF == 1 && WK == 1 && (NW == 8 || NF < 8) &&
+                      layer_chunk_blocks(BF16, NFL) % 2 == 0) {
             if (layer_x_words(a.x, a.batch, a.in))
-                hipLaunchKernelGGL((layer_kernel<T, 1, 8, NF, 1, NW, 2, true, true>), grid,
+                hipLaunchKernelGGL((layer_kernel<T, 1, NFL, NF, 1, NW, 2, true, true>), grid,
                                    dim3(64 * NW), 0, s, a);
             else
-                hipLaunchKernelGGL((layer_kernel<T, 1, 8, NF, 1, NW, 2, false, true>), grid,
+                hipLaunchKernelGGL((layer_kernel<T, 1, NFL, NF, 1, NW, 2, false, true>), grid,
                                    dim3(64 * NW), 0, s, a);
             return hipGetLastError();
         } else {
             return hipErrorInvalidValue;
-        }
-    }
-    // (256-column packed tiles with two blocks per feature are sparse)
-    if constexpr (BF16 && WK == 1 && NFL < 8 && layer_chunk_blocks(BF16, NFL) % 2 == 0) {
-        if (g.nsb == 2 && layer_x_words(a.x, a.batch, a.in)) {
-            hipLaunchKernelGGL((layer_kernel<T, RF, NFL, NF, WK, NW, 2, true>), grid, dim3(64 * NW),
-                               0, s, a);
-            return hipGetLastError();
         }
     }
     hipLaunchKernelGGL((layer_kernel<T, RF, NFL, NF, WK, NW>), grid, dim3(64 * NW), 0, s, a);
