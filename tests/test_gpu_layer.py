@@ -70,12 +70,21 @@ def test_layer_matches_oracle(B, n_in, n_out, G, dtype_name):
 CFGS = ["1,1", "2,1", "1,2", "1,4", "2,2", "2,4", "1,1,8", "1,1,4,2", "1,2,4,2", "1,4,4,2"]
 
 
-@pytest.mark.parametrize("dtype_name", ["f32", "bf16"])
+# bf16 with two blocks per feature (5 <= G <= 12) runs the sparse MFMA, which
+# takes one row tile per wave and no K split; G = 20 keeps the dense bf16
+# kernel under every shape.
+SPARSE_CFGS = ["1,1", "1,1,8", "1,1,4,2"]
+
+
+@pytest.mark.parametrize("dtype_name,G", [("f32", 10), ("bf16", 20)] +
+                         [pytest.param("bf16", 10, id="bf16-sparse")])
 @pytest.mark.parametrize("cfg", CFGS)
-def test_layer_every_workgroup_shape(cfg, dtype_name):
+def test_layer_every_workgroup_shape(cfg, dtype_name, G):
     # out = 45 -> two 32-column fragments per tile, so every shape is valid;
     # 9 features (odd) and 300 rows (ragged) exercise the padding paths.
-    B, n_in, n_out, G = 300, 9, 45, 10
+    if dtype_name == "bf16" and G == 10 and cfg not in SPARSE_CFGS:
+        pytest.skip("not a shape of the sparse MFMA")
+    B, n_in, n_out = 300, 9, 45
     x, C, Wb = _inputs(B, n_in, n_out, G, seed=3, off=0.1, dtype_name=dtype_name)
     ref = oracle.layer(x, C, Wb, G)
     if dtype_name == "bf16":
@@ -91,18 +100,19 @@ def test_layer_every_workgroup_shape(cfg, dtype_name):
 
 WIDE = [
     # (dtype, B, in, out, G, cfg): the widest column tiles (bf16 256, fp32 128)
-    ("bf16", 600, 20, 256, 10, "2,1"),
-    ("bf16", 600, 20, 256, 10, "1,1"),
+    ("bf16", 600, 20, 256, 20, "2,1"),
+    ("bf16", 600, 20, 256, 20, "1,1"),
     ("bf16", 333, 7, 200, 50, "2,1"),
     ("bf16", 97, 3, 130, 200, "1,1"),
     ("bf16", 600, 20, 256, 10, "1,1,8"),
     ("bf16", 300, 5, 100, 50, "1,1,8"),
-    # two blocks per feature (G = 7, 10) with an odd number of chunks (a
-    # padding chunk in the last unrolled pair), an odd feature count and a
-    # ragged batch, for the 64-row one-wave shape and the 8-wave shape
-    ("bf16", 300, 18, 256, 10, "2,1"),
-    ("bf16", 257, 17, 256, 7, "2,1"),
+    # two blocks per feature (G = 7, 10; the sparse MFMA) with an odd number
+    # of chunks (a padding chunk in the last unrolled pair), an odd feature
+    # count and a ragged batch; and the 64-row one-wave shape of the dense
+    # kernel (G = 20)
+    ("bf16", 300, 18, 256, 10, "1,1,8"),
     ("bf16", 257, 17, 256, 7, "1,1,8"),
+    ("bf16", 257, 17, 256, 20, "2,1"),
     ("f32", 600, 20, 256, 10, "1,1"),
     ("f32", 600, 20, 256, 10, "1,4"),
     ("f32", 333, 7, 128, 50, "2,1"),
@@ -134,6 +144,27 @@ def test_layer_wide_tiles(dtype_name, B, n_in, n_out, G, cfg):
     finally:
         set_layer_cfg(None)
     assert normwise(y, ref) <= _tol(dtype_name)
+
+
+SPARSE_SHAPES = [
+    # (B, in, out, G): two blocks per feature at G = 5, 8, 11, 12 over one,
+    # two, four and eight 32-column fragments per tile, ragged batches and
+    # odd feature counts
+    (300, 9, 10, 5),
+    (257, 17, 64, 8),
+    (129, 4, 100, 11),
+    (500, 33, 256, 12),
+    (1000, 7, 256, 10),
+]
+
+
+@pytest.mark.parametrize("B,n_in,n_out,G", SPARSE_SHAPES)
+def test_layer_bf16_sparse_mfma(B, n_in, n_out, G):
+    x, C, Wb = _inputs(B, n_in, n_out, G, seed=B + G, off=0.2, dtype_name="bf16")
+    ref = oracle.round_bf16(oracle.layer(x, C, Wb, G))
+    say(f"layer bf16 sparse B={B} in={n_in} out={n_out} G={G}")
+    y = _gpu_layer(x, C, Wb, G, "bf16")
+    assert normwise(y, ref) <= BF16_LAYER_TOL, normwise(y, ref)
 
 
 @pytest.mark.parametrize("case", ["aligned", "odd_total", "x_at_odd_element"])
