@@ -109,7 +109,8 @@ bool layer_cfg_valid(const LayerGeom& g, const LayerCfg& c) {
     // four-wave workgroups only on column slices (the whole 256 columns with
     // four waves' larger share of the weight staging exceed 256 registers
     // and spill)
-    if (g.sparse && (c.rf != 1 || c.wk != 1 || (g.nf == 8 && c.nw == 4 && c.cs == 1)))
+    if (g.sparse && (c.wk != 1 || (c.rf == 1 && g.nf == 8 && c.nw == 4 && c.cs == 1) ||
+                     (c.rf == 2 && (c.nw != 4 || c.cs != 1))))
         return false;
     return layer_shape_ok(g.kj == 8, g.nf, c.rf, c.wk, c.nw, c.cs);
 }

@@ -511,9 +511,7 @@ void layer_kernel(LayerArgs a) {
     // group: value 2G is the basis at column c0 + ((G - c0) mod 4), at
     // position c0 / 4, plus 1 for G < c0 mod 4; value 1 is the SiLU value at
     // column 0 (group 0, position 0); values 3, 5, 7 are zero.
-    static_assert(!SP || (BF16 && NSBC == 2 && RF == 1 && WK == 1 && KBW % 2 == 0 &&
-                          Occ<RF, NF>::waves == 2),
-                  "sparse MFMA shape");
+    static_assert(!SP || (BF16 && NSBC == 2 && WK == 1 && KBW % 2 == 0), "sparse MFMA shape");
     auto gen_sparse = [&](const float (&xf)[RF], AFrag<T, RF>& As, uint32_t (&idx)[RF]) {
       if constexpr (SP) {
 #pragma unroll
@@ -595,14 +593,13 @@ void layer_kernel(LayerArgs a) {
     __builtin_amdgcn_sched_barrier(0);
 
     // A of the wave's first block (nothing to interleave with yet).
-    if constexpr (GEN_SPLIT) {
+    if constexpr (SP) {
         float x0[RF];
 #pragma unroll
         for (int rf = 0; rf < RF; ++rf) x0[rf] = x_value(pos_c, xq[0][0][rf], rf);
-        if constexpr (SP)
-            gen_sparse(x0, A_cur, idx_cur);
-        else
-            gen_split(pos_c, xq[0][0], A_cur);
+        gen_sparse(x0, A_cur, idx_cur);
+    } else if constexpr (GEN_SPLIT) {
+        gen_split(pos_c, xq[0][0], A_cur);
     } else {
         float x0[RF];
 #pragma unroll
@@ -687,15 +684,18 @@ void layer_kernel(LayerArgs a) {
                     const bf16x16 b = __builtin_shufflevector(bq[0].b[nf], bq[1].b[nf], 0, 1, 2, 3,
                                                               4, 5, 6, 7, 8, 9, 10, 11, 12, 13, 14,
                                                               15);
-                    acc[0][nf] = __builtin_amdgcn_smfmac_f32_32x32x32_bf16(
-                        A_cur.a[0], b, acc[0][nf], (int)idx_cur[0], 0, 0);
+#pragma unroll
+                    for (int rf = 0; rf < RF; ++rf)
+                        acc[rf][nf] = __builtin_amdgcn_smfmac_f32_32x32x32_bf16(
+                            A_cur.a[rf], b, acc[rf][nf], (int)idx_cur[rf], 0, 0);
                 }
                 // (the next A complete here, so code sinking cannot move its
                 // generation past the next barrier)
-                {
-                    u32x4 w = __builtin_bit_cast(u32x4, A_nxt.a[0]);
-                    asm volatile("" : "+v"(w), "+v"(idx_nxt[0]));
-                    A_nxt.a[0] = __builtin_bit_cast(bf16x8, w);
+#pragma unroll
+                for (int rf = 0; rf < RF; ++rf) {
+                    u32x4 w = __builtin_bit_cast(u32x4, A_nxt.a[rf]);
+                    asm volatile("" : "+v"(w), "+v"(idx_nxt[rf]));
+                    A_nxt.a[rf] = __builtin_bit_cast(bf16x8, w);
                 }
                 if constexpr (q == 0) {
                     __builtin_amdgcn_sched_barrier(0);
@@ -703,7 +703,8 @@ void layer_kernel(LayerArgs a) {
                     __builtin_amdgcn_sched_barrier(0);
                 }
                 A_cur = A_nxt;
-                idx_cur[0] = idx_nxt[0];
+#pragma unroll
+                for (int rf = 0; rf < RF; ++rf) idx_cur[rf] = idx_nxt[rf];
             };
             StaticFor<0, NPC>::run(pair_step);
             pos_c = advance<KB>(pos_c, nsb);
@@ -833,13 +834,13 @@ hipError_t launch_cfg(const LayerGeom& g, LayerArgs a, hipStream_t s) {
     constexpr bool BF16 = sizeof(T) == 2;
     // The sparse packed layout runs only on the structured-sparse MFMA.
     if (g.sparse) {
-        if constexpr (BF16 && RF == 1 && WK == 1 && (NW == 8 || NF < 8) &&
+        if constexpr (BF16 && WK == 1 && (RF == 1 ? (NW == 8 || NF < 8) : (NW == 4 && NF == NFL)) &&
                       layer_chunk_blocks(BF16, NFL) % 2 == 0) {
             if (layer_x_words(a.x, a.batch, a.in))
-                hipLaunchKernelGGL((layer_kernel<T, 1, NFL, NF, 1, NW, 2, true, true>), grid,
+                hipLaunchKernelGGL((layer_kernel<T, RF, NFL, NF, 1, NW, 2, true, true>), grid,
                                    dim3(64 * NW), 0, s, a);
             else
-                hipLaunchKernelGGL((layer_kernel<T, 1, NFL, NF, 1, NW, 2, false, true>), grid,
+                hipLaunchKernelGGL((layer_kernel<T, RF, NFL, NF, 1, NW, 2, false, true>), grid,
                                    dim3(64 * NW), 0, s, a);
             return hipGetLastError();
         } else {

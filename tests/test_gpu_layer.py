@@ -73,7 +73,7 @@ CFGS = ["1,1", "2,1", "1,2", "1,4", "2,2", "2,4", "1,1,8", "1,1,4,2", "1,2,4,2",
 # bf16 with two blocks per feature (5 <= G <= 12) runs the sparse MFMA, which
 # takes one row tile per wave and no K split; G = 20 keeps the dense bf16
 # kernel under every shape.
-SPARSE_CFGS = ["1,1", "1,1,8", "1,1,4,2"]
+SPARSE_CFGS = ["1,1", "2,1", "1,1,8", "1,1,4,2"]
 
 
 @pytest.mark.parametrize("dtype_name,G", [("f32", 10), ("bf16", 20)] +
@@ -156,6 +156,22 @@ SPARSE_SHAPES = [
     (500, 33, 256, 12),
     (1000, 7, 256, 10),
 ]
+
+
+@pytest.mark.parametrize("cfg", ["1,1,8", "2,1", "1,1,4,2", "1,1,4,4"])
+def test_layer_bf16_sparse_mfma_256_column_shapes(cfg):
+    """The shapes the sparse MFMA takes on 256-column tiles: eight 32-row
+    waves, four 64-row waves (one per SIMD), and column slices."""
+    B, n_in, n_out, G = 700, 13, 256, 10
+    x, C, Wb = _inputs(B, n_in, n_out, G, seed=5, off=0.2, dtype_name="bf16")
+    ref = oracle.round_bf16(oracle.layer(x, C, Wb, G))
+    say(f"layer bf16 sparse 256 columns cfg={cfg}")
+    set_layer_cfg(cfg)
+    try:
+        y = _gpu_layer(x, C, Wb, G, "bf16")
+    finally:
+        set_layer_cfg(None)
+    assert normwise(y, ref) <= BF16_LAYER_TOL, normwise(y, ref)
 
 
 @pytest.mark.parametrize("B,n_in,n_out,G", SPARSE_SHAPES)
