@@ -70,8 +70,7 @@ struct LayerGeom {
     // bf16 with two blocks per feature (5 <= G <= 12): packed for the
     // structured-sparse MFMA (block = feature of the pair, half = column
     // half, element e of half w = column 4 (e % 4) + 2 w + e / 4), and only
-    // the shapes with one row tile per wave and no K split run on it (eight
-    // waves per workgroup, or four on column slices).
+    // the shapes without a K split run on it (layer_cfg_valid).
     bool sparse;
     size_t packed_bytes;
 };

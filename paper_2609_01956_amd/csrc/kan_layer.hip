@@ -105,10 +105,11 @@ bool layer_geom(int nb, bool bf16, int in, int out, LayerGeom* g) {
 }
 
 bool layer_cfg_valid(const LayerGeom& g, const LayerCfg& c) {
-    // sparse: one row tile per wave, no K split; 256-column tiles take
+    // sparse: no K split; one row tile per wave, where 256-column tiles take
     // four-wave workgroups only on column slices (the whole 256 columns with
     // four waves' larger share of the weight staging exceed 256 registers
-    // and spill)
+    // and spill), or two row tiles per wave with four waves over the whole
+    // tile
     if (g.sparse && (c.wk != 1 || (c.rf == 1 && g.nf == 8 && c.nw == 4 && c.cs == 1) ||
                      (c.rf == 2 && (c.nw != 4 || c.cs != 1))))
         return false;

@@ -71,8 +71,8 @@ CFGS = ["1,1", "2,1", "1,2", "1,4", "2,2", "2,4", "1,1,8", "1,1,4,2", "1,2,4,2",
 
 
 # bf16 with two blocks per feature (5 <= G <= 12) runs the sparse MFMA, which
-# takes one row tile per wave and no K split; G = 20 keeps the dense bf16
-# kernel under every shape.
+# takes no K split (one row tile per wave, or two with four waves over the
+# whole tile); G = 20 keeps the dense bf16 kernel under every shape.
 SPARSE_CFGS = ["1,1", "2,1", "1,1,8", "1,1,4,2"]
 
 
