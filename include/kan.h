@@ -139,8 +139,9 @@ kan_status kan_layer_packed_bytes(const kan_grid* grid, kan_dtype dtype, int32_t
  * spline coefficients coef[o, i, j] and the SiLU weights base_w[o, i]) into
  * the order in which the matrix cores consume them: for each tile of output
  * columns, feature pair and block of columns, the weights of both features for
- * every output column, the SiLU weight after the G + 3 spline coefficients of
- * its feature and zeros in the padding.  The layout is private to this library
+ * every output column, the SiLU weight before the G + 3 spline coefficients of
+ * its feature and zeros in the padding (in bf16 with 5 <= G <= 12 a feature's
+ * 16 columns are permuted for the structured-sparse matrix instruction).  The layout is private to this library
  * and depends only on (grid, dtype, in_features, out_features).  Weights that
  * do not change can be packed once and reused by any number of
  * kan_layer_forward_packed calls.
@@ -172,6 +173,27 @@ kan_status kan_layer_forward_packed(const kan_grid* grid, kan_dtype dtype, int64
                                     int32_t in_features, int32_t out_features, const void* x,
                                     const void* packed, size_t packed_bytes, void* y,
                                     void* stream);
+
+/*
+ * kan_layer_plan -- the workgroup shape that kan_layer_forward_packed (and
+ * kan_layer_forward) launches for a layer of this grid, dtype, shape and
+ * batch.  Host only: no HIP call, nothing enqueued.  For testing and tuning.
+ *
+ *   plan[0]  32-row MFMA tiles per wave (1 or 2)
+ *   plan[1]  waves splitting the contraction (K) of a workgroup (1, 2 or 4)
+ *   plan[2]  waves per workgroup (4 or 8)
+ *   plan[3]  workgroups splitting the columns of an output tile (1, 2 or 4)
+ *   plan[4]  1 if the layer runs on the structured-sparse matrix instruction
+ *            (bf16, 5 <= G <= 12), else 0
+ *
+ * The environment variable KAN_LAYER_CFG="rf,wk[,nw[,cs]]", read at every
+ * call, forces plan[0..3] when it is well formed and valid for the layer;
+ * otherwise the library's own choice stands.  Writes plan[0..4].  Returns
+ * KAN_OK, KAN_ERR_INVALID_ARG (plan == NULL, bad grid or sizes, batch < 1) or
+ * KAN_ERR_UNSUPPORTED.
+ */
+kan_status kan_layer_plan(const kan_grid* grid, kan_dtype dtype, int64_t batch,
+                          int32_t in_features, int32_t out_features, int32_t* plan);
 
 /* Static, NUL-terminated description of a status code (never NULL). */
 const char* kan_status_string(kan_status status);

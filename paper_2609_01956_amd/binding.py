@@ -28,8 +28,8 @@ KAN_F32 = 0
 KAN_BF16 = 1
 
 EXPORTED_SYMBOLS = ("kan_basis_eval", "kan_layer_forward", "kan_layer_packed_bytes",
-                    "kan_layer_pack", "kan_layer_forward_packed", "kan_status_string",
-                    "kan_abi_version")
+                    "kan_layer_pack", "kan_layer_forward_packed", "kan_layer_plan",
+                    "kan_status_string", "kan_abi_version")
 
 
 class kan_grid(ctypes.Structure):
@@ -77,6 +77,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                                      ctypes.c_void_p, ctypes.c_size_t,
                                                      ctypes.c_void_p, ctypes.c_void_p]
             lib.kan_layer_forward_packed.restype = ctypes.c_int
+            lib.kan_layer_plan.argtypes = [ctypes.POINTER(kan_grid), ctypes.c_int,
+                                           ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
+                                           ctypes.POINTER(ctypes.c_int32)]
+            lib.kan_layer_plan.restype = ctypes.c_int
             lib.kan_status_string.argtypes = [ctypes.c_int]
             lib.kan_status_string.restype = ctypes.c_char_p
             lib.kan_abi_version.argtypes = []
@@ -124,6 +128,15 @@ def kan_layer_packed_bytes(grid: kan_grid, dtype: int, in_features: int,
                                                    int(in_features), int(out_features),
                                                    ctypes.byref(n)))
     return st, int(n.value)
+
+
+def kan_layer_plan(grid: kan_grid, dtype: int, batch: int, in_features: int,
+                   out_features: int) -> Tuple[int, Tuple[int, ...]]:
+    """Raw call: returns (kan_status, (rf, wk, nw, cs, sparse))."""
+    plan = (ctypes.c_int32 * 5)()
+    st = int(load_library().kan_layer_plan(ctypes.byref(grid), int(dtype), int(batch),
+                                           int(in_features), int(out_features), plan))
+    return st, tuple(int(v) for v in plan)
 
 
 def kan_layer_pack(grid: kan_grid, dtype: int, in_features: int, out_features: int, coef: int,

@@ -180,6 +180,24 @@ kan_status kan_layer_forward_packed(const kan_grid* grid, kan_dtype dtype, int64
                                            static_cast<hipStream_t>(stream)));
 }
 
+kan_status kan_layer_plan(const kan_grid* grid, kan_dtype dtype, int64_t batch,
+                          int32_t in_features, int32_t out_features, int32_t* plan) {
+    if (plan == nullptr) return KAN_ERR_INVALID_ARG;
+    kan::GridConst gc;
+    kan::LayerGeom geom;
+    const kan_status st = check_layer(grid, dtype, in_features, out_features, &gc, &geom);
+    if (st != KAN_OK) return st;
+    if (batch < 1 || batch > (int64_t)0x7fffffff * 32) return KAN_ERR_INVALID_ARG;
+    kan::LayerCfg cfg = kan::plan_layer(geom, dtype == KAN_BF16, batch);
+    kan::parse_layer_cfg_override(geom, &cfg);
+    plan[0] = cfg.rf;
+    plan[1] = cfg.wk;
+    plan[2] = cfg.nw;
+    plan[3] = cfg.cs;
+    plan[4] = geom.sparse ? 1 : 0;
+    return KAN_OK;
+}
+
 kan_status kan_layer_forward(const kan_grid* grid, kan_dtype dtype, int64_t batch,
                              int32_t in_features, int32_t out_features, const void* x,
                              const void* coef, const void* base_w, void* y, void* stream) {

@@ -83,12 +83,19 @@ bool layer_geom(int nb, bool bf16, int in, int out, LayerGeom* g);
 // chunk and are summed through LDS at the end, the other nw / wk waves take
 // different rows; cs workgroups split the columns of an N tile (each stages
 // only its columns of every packed block).
+// On the sparse layout eight waves of two row tiles (rf = 2, nw = 8) pair up:
+// the two waves of a 64-row group take the two column halves of the tile and
+// pass each other the A of one row tile each.
 struct LayerCfg {
     int rf;  // 1 or 2
     int wk;  // 1, 2 or 4
-    int nw;  // waves per workgroup: 4, or 8 (rf = 1, wk = 1, cs = 1 only)
+    int nw;  // waves per workgroup: 4, or 8 (wk = 1, cs = 1; rf = 2 sparse only)
     int cs;  // column slices per N tile: 1, 2 or 4 (rf = 1, nw = 4 only)
 };
+// Rows per workgroup of a shape.
+inline int64_t layer_cfg_rows(const LayerCfg& c) {
+    return 32LL * c.rf * (c.nw / c.wk) / (c.rf == 2 && c.nw == 8 ? 2 : 1);
+}
 
 // The shapes the fused kernel is instantiated for, given the packed tile of
 // nfl fragments: the chunk the slice stages must be whole 16-byte loads of
@@ -103,7 +110,9 @@ __host__ __device__ constexpr bool layer_shape_ok(bool bf16, int nfl, int rf, in
     const int kb = layer_chunk_blocks(bf16, nfl);
     const int chb = kb * layer_block_bytes(bf16, nf);
     if (chb % (1024 * nw) != 0 || kb % wk != 0) return false;
-    if (nw == 8) return rf == 1 && wk == 1 && cs == 1;
+    // (eight waves of two row tiles: the sparse shared-A shape, bf16 256-column
+    // tiles only)
+    if (nw == 8) return wk == 1 && cs == 1 && (rf == 1 || (bf16 && nfl == 8));
     if (cs > 1) return rf == 1;
     return wk == 1 || rf * nf <= 4;
 }

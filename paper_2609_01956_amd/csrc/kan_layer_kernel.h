@@ -169,15 +169,22 @@ struct Occ {
 // XP (bf16): x read as the aligned 32-bit word holding the element (x 4-byte
 // aligned and batch * in even, so the word never leaves the tensor).
 // SP: the structured-sparse MFMA on the sparse packed layout (LayerGeom::sparse).
+// XA (SP, two row tiles per wave, eight waves): the two waves of a row group
+// take the two column halves of the tile, and each generates the A of one of
+// the group's two row tiles and passes it to the other through LDS (half the
+// LDS bytes of B per MFMA of one-row-tile waves, still two waves per SIMD).
 template <typename T, int RF, int NFL, int NF, int WK, int NW, int NSBC = 0, bool XP = false,
-          bool SP = false>
+          bool SP = false, bool XA = false>
 __global__ __launch_bounds__(64 * NW)
-__attribute__((amdgpu_waves_per_eu(Occ<RF, NF>::waves)))
+__attribute__((amdgpu_waves_per_eu(Occ<RF, XA ? NF / 2 : NF>::waves)))
 void layer_kernel(LayerArgs a) {
     constexpr bool BF16 = sizeof(T) == 2;
     constexpr int KJ = Tr<T>::KJ;
     constexpr int NT = 64 * NW;                  // threads per workgroup
-    constexpr int WM = NW / WK;
+    constexpr int CH = XA ? 2 : 1;               // waves sharing a row group's columns
+    constexpr int NFW = NF / CH;                 // 32-column fragments per wave
+    constexpr int GRF = XA ? 1 : RF;             // row tiles whose A a wave generates
+    constexpr int WM = NW / WK / CH;
     constexpr int CS = NFL / NF;                 // column slices per N tile
     constexpr int NTILE = 32 * NF;               // columns of the slice
     constexpr int LANEB = KJ * (int)sizeof(T);  // B bytes per lane per block (16 / 8)
@@ -187,7 +194,6 @@ void layer_kernel(LayerArgs a) {
     constexpr int CHB = KB * BLKB;               // bytes per chunk in LDS
     constexpr int DPW = CHB / (1024 * NW);       // 16-byte loads per lane per chunk
     constexpr int KBW = KB / WK;                 // blocks per wave per chunk
-    constexpr int NX = KBW * RF;                 // x loads per lane per chunk
     constexpr int BM = 32 * RF * WM;             // rows per workgroup
     // Weights of chunk c are loaded into registers L chunks ahead (register
     // set c % L), written to LDS stage c % 2 while chunk c - 1 is multiplied,
@@ -207,8 +213,15 @@ void layer_kernel(LayerArgs a) {
     static_assert(NSBC == 0 || ALIGNED, "compile-time blocks per feature");
     const int nsb = NSBC > 0 ? NSBC : a.nsb;
     static_assert(BLKB == 2 * NTILE * LANEB && NFL % NF == 0, "block layout");
+    static_assert(!XA || (SP && RF == 2 && NW == 8 && WK == 1 && NF == 8 && NFL == 8),
+                  "shared-A shape");
     // LDS: two chunk stages; after the main loop the K-split partial sums.
     __shared__ u32x4 smem[SMEM / 16];
+    // XA: two stages of every wave's generated A (values, positions), one
+    // slot per lane
+    __shared__ u32x4 xa_a[XA ? 2 * NW * 64 : 1];
+    __shared__ uint32_t xa_i[XA ? 2 * NW * 64 : 1];
+    static_assert(SMEM + (XA ? 2 * NW * 64 * 20 : 0) <= 64 * 1024, "LDS budget");
     auto stage = [&](auto kk) -> u32x4* { return smem + (decltype(kk)::value % 2) * (CHB / 16); };
 
     const T* __restrict__ x = static_cast<const T*>(a.x);
@@ -220,7 +233,10 @@ void layer_kernel(LayerArgs a) {
     const int r = lane & 31;
     const int h = lane >> 5;
     const int wm = wave % WM;
-    const int wk = wave / WM;
+    const int wk = XA ? 0 : wave / WM;
+    // XA: the wave's column half, also the row tile whose A it generates
+    // (its partner, wave wm + WM (1 - ch), generates the other)
+    const int ch = XA ? wave / WM : 0;
     const int64_t row0 = (int64_t)blockIdx.x * BM + wm * 32 * RF;
     const int nt = blockIdx.y / CS;     // N tile
     const int slice = blockIdx.y % CS;  // column slice of the tile
@@ -233,10 +249,10 @@ void layer_kernel(LayerArgs a) {
     // batch read row batch - 1 (their results are not stored).
     const int64_t wg_row0 = (int64_t)blockIdx.x * BM;
     const T* __restrict__ xw = x + wg_row0 * (int64_t)a.in;
-    uint32_t xoff[RF];  // element offset of (row, feature h of pair 0)
+    uint32_t xoff[GRF];  // element offset of (row, feature h of pair 0)
 #pragma unroll
-    for (int rf = 0; rf < RF; ++rf) {
-        int64_t row = row0 + rf * 32 + r;
+    for (int rf = 0; rf < GRF; ++rf) {
+        int64_t row = row0 + (XA ? ch : rf) * 32 + r;
         row = row < a.batch ? row : a.batch - 1;
         xoff[rf] = (uint32_t)((row - wg_row0) * a.in + h);
     }
@@ -247,9 +263,9 @@ void layer_kernel(LayerArgs a) {
     // top of a float (the half is the parity of its element offset, the same
     // for every pair; the phantom lanes' value is replaced by 0 anyway).
     static_assert(!XP || sizeof(T) == 2, "paired x reads are for bf16");
-    uint32_t xsel[RF];
+    uint32_t xsel[GRF];
 #pragma unroll
-    for (int rf = 0; rf < RF; ++rf) xsel[rf] = (xoff[rf] & 1u) ? 0x03020c0cu : 0x01000c0cu;
+    for (int rf = 0; rf < GRF; ++rf) xsel[rf] = (xoff[rf] & 1u) ? 0x03020c0cu : 0x01000c0cu;
 
     // ---- loads of chunk c into register set j, for the wave's blocks from
     // position p on: first the x of each block and row tile (per lane: the
@@ -263,8 +279,8 @@ void layer_kernel(LayerArgs a) {
     // past the last re-load the last chunk.  Raw x bits are kept: conversion
     // and masking happen where the values are used, so nothing waits for a
     // load when it is issued.
-    typedef uint32_t XSet[KBW][RF];
-    constexpr bool X_FIRST_ONLY = ALIGNED && BF16 && Occ<RF, NF>::waves == 2;
+    typedef uint32_t XSet[KBW][GRF];
+    constexpr bool X_FIRST_ONLY = ALIGNED && BF16 && (SP || Occ<RF, NF>::waves == 2);
     typedef u32x4 WSet[DPW];
     const uint32_t wlane = (uint32_t)(wave * 1024 + lane * 16);
     uint32_t goff[CS == 1 ? 1 : DPW];
@@ -285,7 +301,7 @@ void layer_kernel(LayerArgs a) {
             // The split generation reads x only at a feature's first block.
             if (!(X_FIRST_ONLY && t % NSBC != 0)) {
 #pragma unroll
-                for (int rf = 0; rf < RF; ++rf) {
+                for (int rf = 0; rf < GRF; ++rf) {
                     const uint32_t off = xoff[rf] + (uint32_t)(2 * pr) - back;
                     if constexpr (XP)
                         xs[t][rf] = reinterpret_cast<const uint32_t*>(xw)[off >> 1];
@@ -294,7 +310,7 @@ void layer_kernel(LayerArgs a) {
                 }
             } else {
 #pragma unroll
-                for (int rf = 0; rf < RF; ++rf) xs[t][rf] = 0u;
+                for (int rf = 0; rf < GRF; ++rf) xs[t][rf] = 0u;
             }
             p = advance<WK>(p, nsb);
         }
@@ -327,22 +343,24 @@ void layer_kernel(LayerArgs a) {
         return v;
     };
 
-    floatx16 acc[RF][NF];
+    // acc[rf]: row tile rf ^ ch of the wave's row group (XA: the tile whose A
+    // the wave generates first), its NFW fragments from column half ch
+    floatx16 acc[RF][NFW];
 #pragma unroll
     for (int rf = 0; rf < RF; ++rf)
 #pragma unroll
-        for (int nf = 0; nf < NF; ++nf)
+        for (int nf = 0; nf < NFW; ++nf)
 #pragma unroll
             for (int q = 0; q < 16; ++q) acc[rf][nf][q] = 0.0f;
 
     // ---- B fragments of one block (LDS block `bi` of stage `st`)
     typedef typename std::conditional<BF16, bf16x8, floatx2>::type BVec;
-    struct BFrag { BVec b[NF]; };
+    struct BFrag { BVec b[NFW]; };
     auto read_b = [&](BFrag& B, const u32x4* st, int bi) {
         const char* lb = reinterpret_cast<const char*>(st) + bi * BLKB;
 #pragma unroll
-        for (int nf = 0; nf < NF; ++nf) {
-            const char* q = lb + (h * NTILE + nf * 32 + r) * LANEB;
+        for (int nf = 0; nf < NFW; ++nf) {
+            const char* q = lb + (h * NTILE + (ch * NFW + nf) * 32 + r) * LANEB;
             if constexpr (BF16)
                 B.b[nf] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(q));
             else
@@ -352,15 +370,15 @@ void layer_kernel(LayerArgs a) {
 
     // MFMA number i of a block (NMFMA per block): bf16 (nf, rf); fp32 also
     // the k-step t of the block's two columns.
-    constexpr int NMFMA = (BF16 ? 1 : 2) * RF * NF;
+    constexpr int NMFMA = (BF16 ? 1 : 2) * RF * NFW;
     auto do_mfma = [&](int i, const AFrag<T, RF>& A, const BFrag& B) {
         const int rf = i % RF;
-        const int nf = (i / RF) % NF;
+        const int nf = (i / RF) % NFW;
         if constexpr (BF16) {
             acc[rf][nf] =
                 __builtin_amdgcn_mfma_f32_32x32x16_bf16(A.a[rf], B.b[nf], acc[rf][nf], 0, 0, 0);
         } else {
-            const int t = i / (RF * NF);
+            const int t = i / (RF * NFW);
             acc[rf][nf] = __builtin_amdgcn_mfma_f32_32x32x2f32(A.a[rf][t], B.b[nf][t],
                                                                acc[rf][nf], 0, 0, 0);
         }
@@ -512,10 +530,10 @@ void layer_kernel(LayerArgs a) {
     // position c0 / 4, plus 1 for G < c0 mod 4; value 1 is the SiLU value at
     // column 0 (group 0, position 0); values 3, 5, 7 are zero.
     static_assert(!SP || (BF16 && NSBC == 2 && WK == 1 && KBW % 2 == 0), "sparse MFMA shape");
-    auto gen_sparse = [&](const float (&xf)[RF], AFrag<T, RF>& As, uint32_t (&idx)[RF]) {
+    auto gen_sparse = [&](const float (&xf)[GRF], AFrag<T, RF>& As, uint32_t (&idx)[RF]) {
       if constexpr (SP) {
 #pragma unroll
-        for (int rf = 0; rf < RF; ++rf) {
+        for (int rf = 0; rf < GRF; ++rf) {
             const float sv = __builtin_fmaf(xf[rf], a.inv_h, a.a_int + 1.0f) + a.a_frac;
             // c0 + 1 = floor(s) within [2, 13] (a NaN coordinate gives c0 = 1
             // and NaN values, as it should)
@@ -576,6 +594,22 @@ void layer_kernel(LayerArgs a) {
     float sl[RF];
     AFrag<T, RF> A_cur, A_nxt;
     uint32_t idx_cur[RF], idx_nxt[RF];  // SP: positions of the compressed A values
+    // XA: the wave's generated A (tile 0 of A) to stage stg of its slot; the
+    // partner's from stage stg to tile 1
+    auto xa_put = [&](int stg, const AFrag<T, RF>& A, const uint32_t (&idx)[RF]) {
+      if constexpr (XA) {
+        const int o = stg * NW * 64 + wave * 64 + lane;
+        xa_a[o] = __builtin_bit_cast(u32x4, A.a[0]);
+        xa_i[o] = idx[0];
+      }
+    };
+    auto xa_get = [&](int stg, AFrag<T, RF>& A, uint32_t (&idx)[RF]) {
+      if constexpr (XA) {
+        const int o = stg * NW * 64 + (wm + WM * (1 - ch)) * 64 + lane;
+        A.a[1] = __builtin_bit_cast(bf16x8, xa_a[o]);
+        idx[1] = xa_i[o];
+      }
+    };
     BFrag bq[2];
     Pos pos_c = advance_n(Pos{0, 0, 0}, wk, nsb);  // first block of the current chunk
     Pos pos_l = pos_c;                               // first block of the next chunk to load
@@ -588,16 +622,24 @@ void layer_kernel(LayerArgs a) {
     };
     StaticFor<0, L>::run(prologue);
     store(std::integral_constant<int, 0>{}, wq[0]);
+    // A of the wave's first block (nothing to interleave with yet); XA
+    // generates it before the barrier, to pass it on.
+    auto gen_first_sparse = [&]() {
+        float x0[GRF];
+#pragma unroll
+        for (int rf = 0; rf < GRF; ++rf) x0[rf] = x_value(pos_c, xq[0][0][rf], rf);
+        gen_sparse(x0, A_cur, idx_cur);
+    };
+    if constexpr (XA) {
+        gen_first_sparse();
+        xa_put(0, A_cur, idx_cur);
+    }
     __builtin_amdgcn_s_waitcnt(WAIT_LDS);
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
 
-    // A of the wave's first block (nothing to interleave with yet).
     if constexpr (SP) {
-        float x0[RF];
-#pragma unroll
-        for (int rf = 0; rf < RF; ++rf) x0[rf] = x_value(pos_c, xq[0][0][rf], rf);
-        gen_sparse(x0, A_cur, idx_cur);
+        if constexpr (!XA) gen_first_sparse();
     } else if constexpr (GEN_SPLIT) {
         gen_split(pos_c, xq[0][0], A_cur);
     } else {
@@ -636,11 +678,12 @@ void layer_kernel(LayerArgs a) {
         }
         // x of the blocks whose A this chunk generates: blocks 1 .. KBW - 1
         // of this chunk, then block 0 of the next one
-        uint32_t xr[KBW][RF];
+        uint32_t xr[KBW][GRF];
 #pragma unroll
         for (int t = 0; t < KBW; ++t)
 #pragma unroll
-            for (int rf = 0; rf < RF; ++rf) xr[t][rf] = t + 1 < KBW ? xq[J][t + 1][rf] : xq[JN][0][rf];
+            for (int rf = 0; rf < GRF; ++rf)
+                xr[t][rf] = t + 1 < KBW ? xq[J][t + 1][rf] : xq[JN][0][rf];
         __builtin_amdgcn_sched_barrier(0);
         issue(c + L, pos_l, xq[J], wq[J]);
         pos_l = advance<KB>(pos_l, nsb);
@@ -648,7 +691,7 @@ void layer_kernel(LayerArgs a) {
         // The next chunk's weights go to the other LDS stage before the next
         // barrier.  With the split generation they are stored after the
         // first step, which gives their loads that step's time to land.
-        if constexpr (!GEN_SPLIT) {
+        if constexpr (!GEN_SPLIT && !SP) {
             store(std::integral_constant<int, K + 1>{}, wq[JN]);
             __builtin_amdgcn_sched_barrier(0);
         }
@@ -657,21 +700,32 @@ void layer_kernel(LayerArgs a) {
         read_b(bq[0], st, wk);
         if constexpr (SP) {
             // the chunk's feature pairs, one step each: the B of the pair's two
-            // blocks, the next pair's A (its x was loaded a chunk or more
-            // ago), the MFMAs of this pair; after the first pair the next
-            // chunk's weights go to the other LDS stage
+            // blocks (XA: and the partner's A), at the first pair the next
+            // chunk's weights to the other LDS stage, the next pair's A (its x
+            // was loaded a chunk or more ago), the MFMAs of this pair
             constexpr int NPC = KBW / 2;  // pairs per chunk
             auto pair_step = [&](auto qq) {
                 constexpr int q = decltype(qq)::value;
                 if constexpr (q > 0) read_b(bq[0], st, 2 * q);
                 read_b(bq[1], st, 2 * q + 1);
+                xa_get(K % 2, A_cur, idx_cur);  // (XA: one pair per chunk)
+                if constexpr (q == 0) {
+                    // the next chunk's weights to the other LDS stage, before
+                    // this pair's generation and MFMAs (their loads were
+                    // issued a chunk ago; stored after the MFMAs instead, the
+                    // writes and their wait end the chunk, just before its
+                    // barrier)
+                    __builtin_amdgcn_sched_barrier(0);
+                    store(std::integral_constant<int, K + 1>{}, wq[JN]);
+                    __builtin_amdgcn_sched_barrier(0);
+                }
                 Pos pn = pos_c;  // the next pair
                 pn.pair += q + 1;
                 // (x of the next pair's first block, copied before this
                 // chunk's loads reused its register set)
-                float xf[RF];
+                float xf[GRF];
 #pragma unroll
-                for (int rf = 0; rf < RF; ++rf) xf[rf] = x_value(pn, xr[2 * q + 1][rf], rf);
+                for (int rf = 0; rf < GRF; ++rf) xf[rf] = x_value(pn, xr[2 * q + 1][rf], rf);
                 if constexpr (LASTG) {
                     if (c * KBW + 2 * q >= nq) {  // a padding pair: contributes 0
 #pragma unroll
@@ -679,76 +733,87 @@ void layer_kernel(LayerArgs a) {
                     }
                 }
                 gen_sparse(xf, A_nxt, idx_nxt);
-#pragma unroll
-                for (int nf = 0; nf < NF; ++nf) {
+                auto smfmac = [&](int rf, int nf) {
                     const bf16x16 b = __builtin_shufflevector(bq[0].b[nf], bq[1].b[nf], 0, 1, 2, 3,
                                                               4, 5, 6, 7, 8, 9, 10, 11, 12, 13, 14,
                                                               15);
+                    acc[rf][nf] = __builtin_amdgcn_smfmac_f32_32x32x32_bf16(
+                        A_cur.a[rf], b, acc[rf][nf], (int)idx_cur[rf], 0, 0);
+                };
+                if constexpr (XA) {
+                    // the wave's own tile first: the partner's A comes from LDS
 #pragma unroll
                     for (int rf = 0; rf < RF; ++rf)
-                        acc[rf][nf] = __builtin_amdgcn_smfmac_f32_32x32x32_bf16(
-                            A_cur.a[rf], b, acc[rf][nf], (int)idx_cur[rf], 0, 0);
+#pragma unroll
+                        for (int nf = 0; nf < NFW; ++nf) smfmac(rf, nf);
+                } else {
+#pragma unroll
+                    for (int nf = 0; nf < NFW; ++nf)
+#pragma unroll
+                        for (int rf = 0; rf < RF; ++rf) smfmac(rf, nf);
                 }
                 // (the next A complete here, so code sinking cannot move its
                 // generation past the next barrier)
 #pragma unroll
-                for (int rf = 0; rf < RF; ++rf) {
+                for (int rf = 0; rf < GRF; ++rf) {
                     u32x4 w = __builtin_bit_cast(u32x4, A_nxt.a[rf]);
                     asm volatile("" : "+v"(w), "+v"(idx_nxt[rf]));
                     A_nxt.a[rf] = __builtin_bit_cast(bf16x8, w);
                 }
-                if constexpr (q == 0) {
+                if constexpr (XA) {
+                    xa_put((K + 1) % 2, A_nxt, idx_nxt);
+                    A_cur.a[0] = A_nxt.a[0];
+                    idx_cur[0] = idx_nxt[0];
+                } else {
+                    A_cur = A_nxt;
+#pragma unroll
+                    for (int rf = 0; rf < RF; ++rf) idx_cur[rf] = idx_nxt[rf];
+                }
+            };
+            StaticFor<0, NPC>::run(pair_step);
+            pos_c = advance<KB>(pos_c, nsb);
+        } else {
+            Pos p = pos_c;
+            auto one = [&](auto tt) {
+                constexpr int t = decltype(tt)::value;
+                // position of the next block: the next step's, or the first block
+                // of the next chunk
+                const Pos pnext = advance<WK>(p, nsb);
+                float xv[RF];
+                if constexpr (!GEN_SPLIT) {
+#pragma unroll
+                    for (int rf = 0; rf < RF; ++rf) xv[rf] = x_value(pnext, xr[t][rf], rf);
+                    if (pnext.bsub == 0) silu_of(xv, sl);
+                }
+                if constexpr (LASTG) {
+                    if (c * KBW + t >= nq) {  // past the wave's last real block: contribute 0
+#pragma unroll
+                        for (int rf = 0; rf < RF; ++rf) zero_frag(A_cur, rf);
+                    }
+                }
+                // One wave per SIMD: the next block's B is read during this step.
+                // Two waves: B is read at the start of each step; the other wave
+                // covers the latency, and the registers of a second B set are
+                // saved.
+                constexpr bool PREF = Occ<RF, NF>::waves == 1 && t + 1 < KBW;
+                if constexpr (Occ<RF, NF>::waves == 2 && t > 0) read_b(bq[t & 1], st, wk + WK * t);
+                if constexpr (GEN_SPLIT)
+                    step_split(A_cur, bq[t & 1], pnext, xr[t], A_nxt);
+                else
+                    step(A_cur, bq[t & 1], pnext, xv, sl, A_nxt,
+                         std::integral_constant<bool, PREF>{}, bq[(t + 1) & 1], st,
+                         wk + WK * (t + 1));
+                A_cur = A_nxt;
+                p = pnext;
+                if constexpr (GEN_SPLIT && t == 0) {
                     __builtin_amdgcn_sched_barrier(0);
                     store(std::integral_constant<int, K + 1>{}, wq[JN]);
                     __builtin_amdgcn_sched_barrier(0);
                 }
-                A_cur = A_nxt;
-#pragma unroll
-                for (int rf = 0; rf < RF; ++rf) idx_cur[rf] = idx_nxt[rf];
             };
-            StaticFor<0, NPC>::run(pair_step);
-            pos_c = advance<KB>(pos_c, nsb);
-            return;
+            StaticFor<0, KBW>::run(one);
+            pos_c = p;
         }
-        Pos p = pos_c;
-        auto one = [&](auto tt) {
-            constexpr int t = decltype(tt)::value;
-            // position of the next block: the next step's, or the first block
-            // of the next chunk
-            const Pos pnext = advance<WK>(p, nsb);
-            float xv[RF];
-            if constexpr (!GEN_SPLIT) {
-#pragma unroll
-                for (int rf = 0; rf < RF; ++rf) xv[rf] = x_value(pnext, xr[t][rf], rf);
-                if (pnext.bsub == 0) silu_of(xv, sl);
-            }
-            if constexpr (LASTG) {
-                if (c * KBW + t >= nq) {  // past the wave's last real block: contribute 0
-#pragma unroll
-                    for (int rf = 0; rf < RF; ++rf) zero_frag(A_cur, rf);
-                }
-            }
-            // One wave per SIMD: the next block's B is read during this step.
-            // Two waves: B is read at the start of each step; the other wave
-            // covers the latency, and the registers of a second B set are
-            // saved.
-            constexpr bool PREF = Occ<RF, NF>::waves == 1 && t + 1 < KBW;
-            if constexpr (Occ<RF, NF>::waves == 2 && t > 0) read_b(bq[t & 1], st, wk + WK * t);
-            if constexpr (GEN_SPLIT)
-                step_split(A_cur, bq[t & 1], pnext, xr[t], A_nxt);
-            else
-                step(A_cur, bq[t & 1], pnext, xv, sl, A_nxt, std::integral_constant<bool, PREF>{},
-                     bq[(t + 1) & 1], st, wk + WK * (t + 1));
-            A_cur = A_nxt;
-            p = pnext;
-            if constexpr (GEN_SPLIT && t == 0) {
-                __builtin_amdgcn_sched_barrier(0);
-                store(std::integral_constant<int, K + 1>{}, wq[JN]);
-                __builtin_amdgcn_sched_barrier(0);
-            }
-        };
-        StaticFor<0, KBW>::run(one);
-        pos_c = p;
     };
 
     // Every wave's blocks are all real in every group but the final one.
@@ -776,11 +841,11 @@ void layer_kernel(LayerArgs a) {
 #pragma unroll
         for (int rf = 0; rf < RF; ++rf) {
 #pragma unroll
-            for (int nf = 0; nf < NF; ++nf) {
-                const int col = col0 + nf * 32 + r;
+            for (int nf = 0; nf < NFW; ++nf) {
+                const int col = col0 + (ch * NFW + nf) * 32 + r;
 #pragma unroll
                 for (int q = 0; q < 16; ++q) {
-                    const int64_t row = row0 + rf * 32 + 8 * (q / 4) + 4 * h + (q % 4);
+                    const int64_t row = row0 + (rf ^ ch) * 32 + 8 * (q / 4) + 4 * h + (q % 4);
                     if (full || (row < a.batch && col < a.out))
                         Tr<T>::store(y + row * a.out + col, 2.0f * acc[rf][nf][q]);
                 }
@@ -797,7 +862,7 @@ void layer_kernel(LayerArgs a) {
 #pragma unroll
         for (int rf = 0; rf < RF; ++rf)
 #pragma unroll
-            for (int nf = 0; nf < NF; ++nf)
+            for (int nf = 0; nf < NFW; ++nf)
 #pragma unroll
                 for (int q = 0; q < 16; ++q) {
                     const int rl = rf * 32 + 8 * (q / 4) + 4 * h + (q % 4);
@@ -822,33 +887,39 @@ void layer_kernel(LayerArgs a) {
 
 template <typename T, int RF, int NFL, int NF, int WK, int NW>
 hipError_t launch_cfg(const LayerGeom& g, LayerArgs a, hipStream_t s) {
-    constexpr int WM = NW / WK;
-    constexpr int BM = 32 * RF * WM;
+    // Eight waves of two row tiles: the sparse shared-A shape (layer_shape_ok)
+    constexpr bool XA = RF == 2 && NW == 8;
+    constexpr int BM = 32 * RF * (NW / WK) / (XA ? 2 : 1);
     a.nblk_pad = g.nblk_pad;
     a.nchunks = g.nblk_pad / g.kb;
     const dim3 grid((unsigned)((a.batch + BM - 1) / BM), (unsigned)(g.ntiles * (NFL / NF)));
-    // Two blocks per feature (bf16, 5 <= G <= 12) get their own build (no K
-    // split, whole features per chunk: every step's block is the first or the
-    // last of its feature at compile time), with x read as aligned 32-bit
-    // words where that stays inside the tensor.
+    // The sparse packed layout (bf16, two blocks per feature, 5 <= G <= 12)
+    // runs only on the structured-sparse MFMA: no K split, whole feature
+    // pairs per chunk (every block's place in its feature is a compile-time
+    // constant), x read as aligned 32-bit words where that stays inside the
+    // tensor.
     constexpr bool BF16 = sizeof(T) == 2;
-    // The sparse packed layout runs only on the structured-sparse MFMA.
     if (g.sparse) {
-        if constexpr (BF16 && WK == 1 && (RF == 1 ? (NW == 8 || NF < 8) : (NW == 4 && NF == NFL)) &&
+        if constexpr (BF16 && WK == 1 &&
+                      (RF == 1 ? (NW == 8 || NF < 8) : (NF == NFL && (NW == 4 || NF == 8))) &&
                       layer_chunk_blocks(BF16, NFL) % 2 == 0) {
             if (layer_x_words(a.x, a.batch, a.in))
-                hipLaunchKernelGGL((layer_kernel<T, RF, NFL, NF, 1, NW, 2, true, true>), grid,
+                hipLaunchKernelGGL((layer_kernel<T, RF, NFL, NF, 1, NW, 2, true, true, XA>), grid,
                                    dim3(64 * NW), 0, s, a);
             else
-                hipLaunchKernelGGL((layer_kernel<T, RF, NFL, NF, 1, NW, 2, false, true>), grid,
-                                   dim3(64 * NW), 0, s, a);
+                hipLaunchKernelGGL((layer_kernel<T, RF, NFL, NF, 1, NW, 2, false, true, XA>),
+                                   grid, dim3(64 * NW), 0, s, a);
             return hipGetLastError();
         } else {
             return hipErrorInvalidValue;
         }
     }
-    hipLaunchKernelGGL((layer_kernel<T, RF, NFL, NF, WK, NW>), grid, dim3(64 * NW), 0, s, a);
-    return hipGetLastError();
+    if constexpr (XA) {
+        return hipErrorInvalidValue;
+    } else {
+        hipLaunchKernelGGL((layer_kernel<T, RF, NFL, NF, WK, NW>), grid, dim3(64 * NW), 0, s, a);
+        return hipGetLastError();
+    }
 }
 
 // Launches the configuration c if it is this (RF, WK, NW, CS) and the shape

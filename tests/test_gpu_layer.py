@@ -112,6 +112,9 @@ WIDE = [
     # kernel (G = 20)
     ("bf16", 300, 18, 256, 10, "1,1,8"),
     ("bf16", 257, 17, 256, 7, "1,1,8"),
+    ("bf16", 300, 18, 256, 10, "2,1,8"),
+    ("bf16", 257, 17, 200, 7, "2,1,8"),
+    ("bf16", 33, 1, 256, 12, "2,1,8"),
     ("bf16", 257, 17, 256, 20, "2,1"),
     ("f32", 600, 20, 256, 10, "1,1"),
     ("f32", 600, 20, 256, 10, "1,4"),
@@ -158,10 +161,14 @@ SPARSE_SHAPES = [
 ]
 
 
-@pytest.mark.parametrize("cfg", ["1,1,8", "2,1", "1,1,4,2", "1,1,4,4"])
+SPARSE_256_CFGS = ["1,1,8", "2,1", "2,1,8", "1,1,4,2", "1,1,4,4"]
+
+
+@pytest.mark.parametrize("cfg", SPARSE_256_CFGS)
 def test_layer_bf16_sparse_mfma_256_column_shapes(cfg):
     """The shapes the sparse MFMA takes on 256-column tiles: eight 32-row
-    waves, four 64-row waves (one per SIMD), and column slices."""
+    waves, four 64-row waves (one per SIMD), eight 64-row waves on column
+    halves passing each other the A of one row tile, and column slices."""
     B, n_in, n_out, G = 700, 13, 256, 10
     x, C, Wb = _inputs(B, n_in, n_out, G, seed=5, off=0.2, dtype_name="bf16")
     ref = oracle.round_bf16(oracle.layer(x, C, Wb, G))
@@ -183,8 +190,11 @@ def test_layer_bf16_sparse_mfma(B, n_in, n_out, G):
     assert normwise(y, ref) <= BF16_LAYER_TOL, normwise(y, ref)
 
 
+X_WORD_CFGS = [None, "1,1", "1,1,4,2"]
+
+
 @pytest.mark.parametrize("case", ["aligned", "odd_total", "x_at_odd_element"])
-@pytest.mark.parametrize("cfg", [None, "1,1", "1,1,4,2"])
+@pytest.mark.parametrize("cfg", X_WORD_CFGS)
 def test_layer_bf16_x_word_reads_and_their_fallbacks(case, cfg):
     """With two blocks per feature (G = 10) bf16 x is read as the aligned
     32-bit word holding each element when x is 4-byte aligned and batch * in is

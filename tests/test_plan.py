@@ -1,0 +1,98 @@
+"""Host-side shape planning of the fused layer through kan_layer_plan (no GPU):
+the shapes chosen for the layers of the 784-256-256-10 MLP, which grids run
+on the structured-sparse matrix instruction, that every shape the GPU parity
+tests force is the one that runs (an invalid KAN_LAYER_CFG would silently
+fall back to the library's choice), and argument checks."""
+import pytest
+
+from paper_2609_01956_amd import binding as kb
+
+import test_gpu_layer as gl
+
+DT = {"f32": kb.KAN_F32, "bf16": kb.KAN_BF16}
+
+
+def _plan(monkeypatch, G, dtype_name, B, n_in, n_out, cfg=None):
+    if cfg is None:
+        monkeypatch.delenv("KAN_LAYER_CFG", raising=False)
+    else:
+        monkeypatch.setenv("KAN_LAYER_CFG", cfg)
+    st, plan = kb.kan_layer_plan(kb.make_grid(G), DT[dtype_name], B, n_in, n_out)
+    assert st == kb.KAN_OK
+    return plan
+
+
+def _shape(cfg):
+    v = [int(t) for t in cfg.split(",")]
+    return tuple(v + [4, 1][len(v) - 2:])
+
+
+@pytest.mark.parametrize("dtype_name,n_in,n_out,want", [
+    # one workgroup of eight waves per CU: on the 256-column layers 64-row
+    # waves over column halves sharing A, on the narrow layer 32-row waves
+    ("bf16", 784, 256, (2, 1, 8, 1, 1)),
+    ("bf16", 256, 256, (2, 1, 8, 1, 1)),
+    ("bf16", 256, 10, (1, 1, 8, 1, 1)),
+    # fp32: 64-row waves over 128-column tiles; the narrow layer splits K
+    ("f32", 784, 256, (2, 1, 4, 1, 0)),
+    ("f32", 256, 256, (2, 1, 4, 1, 0)),
+    ("f32", 256, 10, (1, 2, 4, 1, 0)),
+])
+def test_mlp_layers_planned_shapes(monkeypatch, dtype_name, n_in, n_out, want):
+    assert _plan(monkeypatch, 10, dtype_name, 65536, n_in, n_out) == want
+
+
+@pytest.mark.parametrize("G,sparse", [(1, 0), (4, 0), (5, 1), (10, 1), (12, 1), (13, 0),
+                                      (200, 0)])
+def test_sparse_instruction_for_two_blocks_per_feature(monkeypatch, G, sparse):
+    # bf16 blocks hold 8 of a feature's G + 4 columns: two blocks for 5..12
+    assert _plan(monkeypatch, G, "bf16", 4096, 64, 64)[4] == sparse
+    assert _plan(monkeypatch, G, "f32", 4096, 64, 64)[4] == 0
+
+
+def test_shared_a_shape_only_on_sparse_256_column_tiles(monkeypatch):
+    assert _plan(monkeypatch, 10, "bf16", 65536, 784, 256, "2,1,8") == (2, 1, 8, 1, 1)
+    # dense bf16, fp32 and narrower sparse tiles keep the library's choice
+    for G, dt, n_out in [(20, "bf16", 256), (10, "f32", 256), (10, "bf16", 45)]:
+        own = _plan(monkeypatch, G, dt, 65536, 784, n_out)
+        assert _plan(monkeypatch, G, dt, 65536, 784, n_out, "2,1,8") == own
+
+
+def test_malformed_override_is_ignored(monkeypatch):
+    own = _plan(monkeypatch, 10, "bf16", 65536, 784, 256)
+    for cfg in ["", "x", "3", "3,1", "1,3", "1,1,6", "1,1,4,3", "1,2,8"]:
+        assert _plan(monkeypatch, 10, "bf16", 65536, 784, 256, cfg) == own
+
+
+def _forced_cases():
+    for dtype_name, G in [("f32", 10), ("bf16", 20), ("bf16", 10)]:
+        for cfg in gl.CFGS:
+            if dtype_name == "bf16" and G == 10 and cfg not in gl.SPARSE_CFGS:
+                continue
+            yield dtype_name, G, 300, 9, 45, cfg
+    for dtype_name, B, n_in, n_out, G, cfg in gl.WIDE:
+        yield dtype_name, G, B, n_in, n_out, cfg
+    for cfg in gl.SPARSE_256_CFGS:
+        yield "bf16", 10, 700, 13, 256, cfg
+    for cfg in gl.X_WORD_CFGS:
+        if cfg is not None:
+            yield "bf16", 10, 300, 9, 45, cfg
+
+
+@pytest.mark.parametrize("dtype_name,G,B,n_in,n_out,cfg", list(_forced_cases()))
+def test_every_shape_the_gpu_tests_force_is_the_one_that_runs(monkeypatch, dtype_name, G, B,
+                                                              n_in, n_out, cfg):
+    assert _plan(monkeypatch, G, dtype_name, B, n_in, n_out, cfg)[:4] == _shape(cfg)
+
+
+def test_plan_argument_checks():
+    g = kb.make_grid(10)
+    bad = kb.KAN_ERR_INVALID_ARG
+    assert kb.kan_layer_plan(g, kb.KAN_BF16, 0, 4, 4)[0] == bad
+    assert kb.kan_layer_plan(g, kb.KAN_BF16, -1, 4, 4)[0] == bad
+    assert kb.kan_layer_plan(g, kb.KAN_BF16, 16, 0, 4)[0] == bad
+    assert kb.kan_layer_plan(g, kb.KAN_BF16, 16, 4, 0)[0] == bad
+    assert kb.kan_layer_plan(g, 2, 16, 4, 4)[0] == kb.KAN_ERR_UNSUPPORTED
+    lib = kb.load_library()
+    assert lib.kan_layer_plan(None, 0, 16, 4, 4, None) == bad
+    assert lib.kan_layer_plan(g, 0, 16, 4, 4, None) == bad
