@@ -54,6 +54,14 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
     typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
     return __builtin_bit_cast(uint32_t, bf16x2{(__bf16)lo, (__bf16)hi});
 }
+// bf16(v) (RNE) in the low half, 0 in the high half: one conversion (written
+// through pack_bf16x2(v, 0) the compiler converts with an arbitrary high
+// operand and then clears the high half with a second instruction).
+__device__ __forceinline__ uint32_t bf16_lo(float v) {
+    uint32_t r;
+    asm("v_cvt_pk_bf16_f32 %0, %1, 0" : "=v"(r) : "v"(v));
+    return r;
+}
 
 template <typename T> struct Tr;
 
@@ -199,10 +207,19 @@ void layer_kernel(LayerArgs a) {
     // set c % L), written to LDS stage c % 2 while chunk c - 1 is multiplied,
     // and read from there during chunk c.  (Two chunks ahead measured faster
     // than three: the loop body, unrolled by lcm(2, L), stays small.)
-    constexpr int L = 2;
-    constexpr int U = L % 2 == 0 ? L : 2 * L;    // chunk-loop unroll, lcm(2, L)
+    // PRE (the shared-A shape, one feature pair per chunk): four LDS stages
+    // and four register sets; loads four chunks ahead, weights stored to LDS
+    // two chunks after their loads and two chunks before their use, and the
+    // B of chunk c + 1 read into registers during chunk c, so every chunk's
+    // MFMAs start right after its barrier.  (784 -> 256: 298 us against 308
+    // with three stages and 304-306 with five or six.  The other 256-column
+    // sparse shapes hold twice the B registers and spill with it.)
+    constexpr bool PRE = XA;
+    constexpr int NST = PRE ? 4 : 2;             // LDS stages
+    constexpr int L = PRE ? 4 : 2;
+    constexpr int U = PRE ? 4 : (L % 2 == 0 ? L : 2 * L);  // chunk-loop unroll, lcm(NST, L)
     constexpr int PART = WK > 1 ? 32 * RF * NTILE * 4 : 0;  // one wave's partial sums
-    constexpr int SMEM = 2 * CHB > NW * PART ? 2 * CHB : NW * PART;
+    constexpr int SMEM = NST * CHB > NW * PART ? NST * CHB : NW * PART;
     static_assert(CHB % (1024 * NW) == 0 && KB % WK == 0 && KB >= WK, "chunk shape");
     static_assert(NW == 4 || (NW == 8 && WK == 1), "waves per workgroup");
     static_assert(SMEM <= 64 * 1024, "LDS budget");
@@ -221,8 +238,11 @@ void layer_kernel(LayerArgs a) {
     // slot per lane
     __shared__ u32x4 xa_a[XA ? 2 * NW * 64 : 1];
     __shared__ uint32_t xa_i[XA ? 2 * NW * 64 : 1];
-    static_assert(SMEM + (XA ? 2 * NW * 64 * 20 : 0) <= 64 * 1024, "LDS budget");
-    auto stage = [&](auto kk) -> u32x4* { return smem + (decltype(kk)::value % 2) * (CHB / 16); };
+    // (gfx950: 160 KB of LDS per workgroup; XA takes 84 KB, one workgroup per CU)
+    static_assert(SMEM + (XA ? 2 * NW * 64 * 20 : 0) <= 96 * 1024, "LDS budget");
+    auto stage = [&](auto kk) -> u32x4* {
+        return smem + (decltype(kk)::value % NST) * (CHB / 16);
+    };
 
     const T* __restrict__ x = static_cast<const T*>(a.x);
     T* __restrict__ y = static_cast<T*>(a.y);
@@ -537,16 +557,22 @@ void layer_kernel(LayerArgs a) {
             const float sv = __builtin_fmaf(xf[rf], a.inv_h, a.a_int + 1.0f) + a.a_frac;
             // c0 + 1 = floor(s) within [2, 13] (a NaN coordinate gives c0 = 1
             // and NaN values, as it should)
-            const float f1 = __builtin_fminf(__builtin_fmaxf(__builtin_floorf(sv), 2.0f), 13.0f);
+            const float f1 = __builtin_amdgcn_fmed3f(__builtin_floorf(sv), 2.0f, 13.0f);
             const int c0 = (int)f1 - 1;
             const int r = c0 & 3;
             const float d = sv - (f1 - 1.0f);  // v of column c0
+            // (G - c0) mod 4 is byte G of 0x03020100 rotated left by 8 c0
+            // bits, i.e. right by 24 c0 (mod 32), which is 0x00030201 rotated
+            // right by 24 (c0 + 1) = 24 f1 (exact in fp32; an integer
+            // multiply here compiles to the quarter-rate v_mul_lo_u32)
+            const uint32_t kg = __builtin_amdgcn_alignbit(0x00030201u, 0x00030201u,
+                                                          (uint32_t)(24.0f * f1));
             float bv[4];
 #pragma unroll
-            for (int G = 0; G < 4; ++G) bv[G] = half_basis(d - (float)((G - r) & 3));
-            idx[rf] = (uint32_t)(c0 >> 2) * 0x1111u + (0x1111u & ((1u << (4 * r)) - 1u));
-            const u32x4 w = {pack_bf16x2(bv[0], half_silu(xf[rf])), pack_bf16x2(bv[1], 0.0f),
-                             pack_bf16x2(bv[2], 0.0f), pack_bf16x2(bv[3], 0.0f)};
+            for (int G = 0; G < 4; ++G) bv[G] = half_basis(d - (float)((kg >> (8 * G)) & 0xffu));
+            idx[rf] = __umul24((uint32_t)(c0 >> 2), 0x1111u) + (0x1111u & ((1u << (4 * r)) - 1u));
+            const u32x4 w = {pack_bf16x2(bv[0], half_silu(xf[rf])), bf16_lo(bv[1]),
+                             bf16_lo(bv[2]), bf16_lo(bv[3])};
             As.a[rf] = __builtin_bit_cast(bf16x8, w);
         }
       }
@@ -585,6 +611,13 @@ void layer_kernel(LayerArgs a) {
     // choices (a register move of a load still in flight would wait for
     // it).  Chunks past the last one (to fill the unrolled group) load
     // clamped inputs and multiply zero A.
+    // PRE: stage c % 4 holds chunk c, written during chunk c - 2 and read
+    // into registers during chunk c - 1; chunk c issues the loads of chunk
+    // c + 4 into set c % 4, writes the weights of chunk c + 2 (set
+    // (c + 2) % 4, loaded two chunks earlier) to stage (c + 2) % 4 (last
+    // read during chunk c - 3), multiplies chunk c and then reads the B of
+    // chunk c + 1 from stage (c + 1) % 4 (written during chunk c - 1).  XA's
+    // A exchange alternates between its two stages by the parity of c.
     static_assert(WK <= 4, "wave block stride");
     constexpr int WAIT_LDS = 0xF | (0x7 << 4) | (0x0 << 8) | (0x3 << 14);  // lgkmcnt(0) only
     const int nq = wk < a.nblk ? (a.nblk - wk + WK - 1) / WK : 0;  // real blocks of this wave
@@ -622,6 +655,7 @@ void layer_kernel(LayerArgs a) {
     };
     StaticFor<0, L>::run(prologue);
     store(std::integral_constant<int, 0>{}, wq[0]);
+    if constexpr (PRE) store(std::integral_constant<int, 1>{}, wq[1]);
     // A of the wave's first block (nothing to interleave with yet); XA
     // generates it before the barrier, to pass it on.
     auto gen_first_sparse = [&]() {
@@ -639,6 +673,10 @@ void layer_kernel(LayerArgs a) {
     __builtin_amdgcn_sched_barrier(0);
 
     if constexpr (SP) {
+        if constexpr (PRE) {
+            read_b(bq[0], stage(std::integral_constant<int, 0>{}), 0);
+            read_b(bq[1], stage(std::integral_constant<int, 0>{}), 1);
+        }
         if constexpr (!XA) gen_first_sparse();
     } else if constexpr (GEN_SPLIT) {
         gen_split(pos_c, xq[0][0], A_cur);
@@ -697,7 +735,7 @@ void layer_kernel(LayerArgs a) {
         }
 
         const u32x4* st = stage(kk);
-        read_b(bq[0], st, wk);
+        if constexpr (!PRE) read_b(bq[0], st, wk);
         if constexpr (SP) {
             // the chunk's feature pairs, one step each: the B of the pair's two
             // blocks (XA: and the partner's A), at the first pair the next
@@ -706,9 +744,11 @@ void layer_kernel(LayerArgs a) {
             constexpr int NPC = KBW / 2;  // pairs per chunk
             auto pair_step = [&](auto qq) {
                 constexpr int q = decltype(qq)::value;
-                if constexpr (q > 0) read_b(bq[0], st, 2 * q);
-                read_b(bq[1], st, 2 * q + 1);
-                xa_get(K % 2, A_cur, idx_cur);  // (XA: one pair per chunk)
+                if constexpr (!PRE) {
+                    if constexpr (q > 0) read_b(bq[0], st, 2 * q);
+                    read_b(bq[1], st, 2 * q + 1);
+                }
+                xa_get(c & 1, A_cur, idx_cur);  // (XA: one pair per chunk)
                 if constexpr (q == 0) {
                     // the next chunk's weights to the other LDS stage, before
                     // this pair's generation and MFMAs (their loads were
@@ -716,7 +756,10 @@ void layer_kernel(LayerArgs a) {
                     // writes and their wait end the chunk, just before its
                     // barrier)
                     __builtin_amdgcn_sched_barrier(0);
-                    store(std::integral_constant<int, K + 1>{}, wq[JN]);
+                    if constexpr (PRE)
+                        store(std::integral_constant<int, K + 2>{}, wq[(K + 2) % L]);
+                    else
+                        store(std::integral_constant<int, K + 1>{}, wq[JN]);
                     __builtin_amdgcn_sched_barrier(0);
                 }
                 Pos pn = pos_c;  // the next pair
@@ -760,8 +803,13 @@ void layer_kernel(LayerArgs a) {
                     asm volatile("" : "+v"(w), "+v"(idx_nxt[rf]));
                     A_nxt.a[rf] = __builtin_bit_cast(bf16x8, w);
                 }
+                if constexpr (PRE) {
+                    // the next chunk's B (stored during the previous chunk)
+                    read_b(bq[0], stage(std::integral_constant<int, K + 1>{}), 0);
+                    read_b(bq[1], stage(std::integral_constant<int, K + 1>{}), 1);
+                }
                 if constexpr (XA) {
-                    xa_put((K + 1) % 2, A_nxt, idx_nxt);
+                    xa_put((c + 1) & 1, A_nxt, idx_nxt);
                     A_cur.a[0] = A_nxt.a[0];
                     idx_cur[0] = idx_nxt[0];
                 } else {
