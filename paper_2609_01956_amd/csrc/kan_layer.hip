@@ -20,10 +20,13 @@ using layer_detail::kThreads;
 // a feature ordered [base_w, coef[.., 0], ..., coef[.., nb - 1]] and
 // zero-padded.  With `sparse` (bf16, two blocks per feature) unit blk is
 // column half w = blk of feature f, holding columns 4 (e % 4) + 2 w + e / 4,
-// and goes to block f % 2 of the pair, half w.  Units are numbered with blk fastest, then f, then o, so a
-// wave reads consecutive coefficients (coef rows are contiguous in f and j);
-// every unit is one 16-byte (bf16) or 8-byte (fp32) store.  Units past
-// `units_main` zero the padding blocks of each tile.
+// and goes to block f % 2 of the pair, half w.  Every unit is one 16-byte
+// (bf16) or 8-byte (fp32) store.  Units are numbered in 8 x 8 tiles: eight
+// output columns (fastest) by eight consecutive (feature, block) pairs fb =
+// f nsb + blk, so a wave stores eight runs of eight consecutive units (whole
+// 128-byte lines for bf16) and reads eight coefficient rows over four
+// features each.  Units past `units_main` zero the padding blocks of each
+// tile.
 template <typename T>
 __global__ __launch_bounds__(kThreads) void pack_kernel(const T* __restrict__ coef,
                                                         const T* __restrict__ bw,
@@ -39,10 +42,16 @@ __global__ __launch_bounds__(kThreads) void pack_kernel(const T* __restrict__ co
     for (int e = 0; e < KJ; ++e) v[e] = T(0);
     int64_t dst;  // unit index in the packed buffer
     if (u < units_main) {
-        const int blk = (int)(u % nsb);
-        const int64_t t = u / nsb;
-        const int f = (int)(t % (2 * npairs));
-        const int o = (int)(t / (2 * npairs));
+        const int fb_count = 2 * npairs * nsb;
+        const int fb_tiles = (fb_count + 7) / 8;
+        const int n_lo = (int)(u % 8);
+        const int fb_lo = (int)((u / 8) % 8);
+        const int64_t w = u / 64;
+        const int fb = (int)(w % fb_tiles) * 8 + fb_lo;
+        const int o = (int)(w / fb_tiles) * 8 + n_lo;
+        if (fb >= fb_count) return;  // (the last (feature, block) tile's padding)
+        const int blk = fb % nsb;
+        const int f = fb / nsb;
         const int tile = o / ntile, n = o % ntile;
         if (o < out && f < in) {  // (f == in: the phantom feature of an odd count)
             const int64_t row = (int64_t)o * in + f;
@@ -191,7 +200,8 @@ bool parse_layer_cfg_override(const LayerGeom& g, LayerCfg* c) {
 hipError_t launch_pack(bool bf16, const LayerGeom& g, int in, int out, const void* coef,
                        const void* base_w, void* packed, hipStream_t s) {
     const int ntile = 32 * g.nf;
-    const int64_t units_main = (int64_t)g.ntiles * ntile * 2 * g.npairs * g.nsb;
+    // (feature, block) pairs rounded up to whole tiles of eight (pack_kernel)
+    const int64_t units_main = (int64_t)g.ntiles * ntile * ((2 * g.npairs * g.nsb + 7) / 8 * 8);
     const int64_t units =
         units_main + (int64_t)g.ntiles * (g.nblk_pad - g.npairs * g.nsb) * 2 * ntile;
     const unsigned blocks = (unsigned)((units + kThreads - 1) / kThreads);
