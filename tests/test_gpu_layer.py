@@ -115,6 +115,8 @@ WIDE = [
     ("bf16", 300, 18, 256, 10, "2,1,8"),
     ("bf16", 257, 17, 200, 7, "2,1,8"),
     ("bf16", 33, 1, 256, 12, "2,1,8"),
+    ("bf16", 129, 5, 256, 5, "2,1,8"),   # three chunks: fewer than the unroll
+    ("bf16", 260, 40, 256, 8, "2,1,8"),
     ("bf16", 257, 17, 256, 20, "2,1"),
     ("f32", 600, 20, 256, 10, "1,1"),
     ("f32", 600, 20, 256, 10, "1,4"),
