@@ -111,8 +111,11 @@ __host__ __device__ constexpr bool layer_shape_ok(bool bf16, int nfl, int rf, in
     const int chb = kb * layer_block_bytes(bf16, nf);
     if (chb % (1024 * nw) != 0 || kb % wk != 0) return false;
     // (eight waves of two row tiles: the sparse shared-A shape, bf16 256-column
-    // tiles only)
-    if (nw == 8) return wk == 1 && cs == 1 && (rf == 1 || (bf16 && nfl == 8));
+    // tiles only; eight waves splitting K: sparse tiles of one or two
+    // fragments only)
+    if (nw == 8)
+        return cs == 1 && ((wk == 1 && (rf == 1 || (bf16 && nfl == 8))) ||
+                           (wk > 1 && rf == 1 && bf16 && nfl <= 2));
     if (cs > 1) return rf == 1;
     return wk == 1 || rf * nf <= 4;
 }

@@ -114,16 +114,21 @@ bool layer_geom(int nb, bool bf16, int in, int out, LayerGeom* g) {
 }
 
 bool layer_cfg_valid(const LayerGeom& g, const LayerCfg& c) {
-    // sparse: no K split; one row tile per wave, where 256-column tiles take
+    // sparse: one row tile per wave, where 256-column tiles take
     // four-wave workgroups only on column slices (the whole 256 columns with
     // four waves' larger share of the weight staging exceed 256 registers
     // and spill), or two row tiles per wave over the whole tile (four waves,
     // or eight on 256-column tiles: column halves sharing A)
-    if (g.sparse && (c.wk != 1 || (c.rf == 1 && g.nf == 8 && c.nw == 4 && c.cs == 1) ||
-                     (c.rf == 2 && c.cs != 1)))
+    // (sparse K splits: tiles of one or two fragments, one row tile per wave,
+    // whole feature pairs per wave slice)
+    if (g.sparse && c.wk != 1 &&
+        (g.nf > 2 || c.rf != 1 || c.cs != 1 || (g.kb / 2) % c.wk != 0))
         return false;
-    // eight waves of two row tiles: sparse only
-    if (!g.sparse && c.rf == 2 && c.nw == 8) return false;
+    if (g.sparse && c.wk == 1 &&
+        ((c.rf == 1 && g.nf == 8 && c.nw == 4 && c.cs == 1) || (c.rf == 2 && c.cs != 1)))
+        return false;
+    // eight waves of two row tiles, or eight waves splitting K: sparse only
+    if (!g.sparse && c.nw == 8 && (c.rf == 2 || c.wk != 1)) return false;
     return layer_shape_ok(g.kj == 8, g.nf, c.rf, c.wk, c.nw, c.cs);
 }
 
@@ -151,6 +156,11 @@ LayerCfg plan_layer(const LayerGeom& g, bool bf16, int64_t batch) {
     // below.  (C5 layer 3, 256 -> 10: 49 us; 256 -> 100: 73 us with eight
     // waves against 82 us with four.)
     if (g.sparse) {
+        // Tiles of one or two fragments: two wave slices splitting the
+        // feature pairs (twice the waves for the basis-generation-bound
+        // loop; 256 -> 10: 43 us against 46 us, 256 -> 64: 52 against 57).
+        const LayerCfg k2{1, 2, 8, 1};
+        if (g.nf <= 2 && layer_cfg_valid(g, k2) && wgs(k2) >= 256) return k2;
         const LayerCfg n8{1, 1, 8, 1}, n4{1, 1, 4, 1};
         if (wgs(n8) >= 256) return n8;
         if (layer_cfg_valid(g, n4) && wgs(n4) >= 256) return n4;

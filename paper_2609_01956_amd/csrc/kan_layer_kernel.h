@@ -221,12 +221,18 @@ void layer_kernel(LayerArgs a) {
     constexpr int PART = WK > 1 ? 32 * RF * NTILE * 4 : 0;  // one wave's partial sums
     constexpr int SMEM = NST * CHB > NW * PART ? NST * CHB : NW * PART;
     static_assert(CHB % (1024 * NW) == 0 && KB % WK == 0 && KB >= WK, "chunk shape");
-    static_assert(NW == 4 || (NW == 8 && WK == 1), "waves per workgroup");
+    static_assert(NW == 4 || (NW == 8 && (WK == 1 || SP)), "waves per workgroup");
     static_assert(SMEM <= 64 * 1024, "LDS budget");
     // With a compile-time block count per feature that divides the wave's
     // blocks per chunk (and no K split), every chunk starts a feature: the
     // place of each step's block in its feature is a compile-time constant.
-    constexpr bool ALIGNED = NSBC > 0 && WK == 1 && KBW % NSBC == 0;
+    constexpr bool ALIGNED = NSBC > 0 && (WK == 1 || SP) && KBW % NSBC == 0;
+    // Sparse with a K split (SPK): wave slice wk takes the chunk's feature
+    // pairs wk, wk + WK, ... (pairs per chunk PPC), i.e. pair
+    // c PPC + wk + WK q as the wave's q-th pair of chunk c, blocks
+    // 2 (wk + WK q) and 2 (wk + WK q) + 1 of the chunk.
+    constexpr bool SPK = SP && WK > 1;
+    constexpr int PPC = KB / 2;
     static_assert(NSBC == 0 || ALIGNED, "compile-time blocks per feature");
     const int nsb = NSBC > 0 ? NSBC : a.nsb;
     static_assert(BLKB == 2 * NTILE * LANEB && NFL % NF == 0, "block layout");
@@ -316,7 +322,9 @@ void layer_kernel(LayerArgs a) {
     auto issue = [&](int c, Pos p, XSet& xs, WSet& ws) {
 #pragma unroll
         for (int t = 0; t < KBW; ++t) {
-            const int pr = p.pair < a.npairs ? p.pair : a.npairs - 1;
+            int pr = p.pair;
+            if constexpr (SPK) pr = c * PPC + wk + WK * (t / 2);
+            pr = pr < a.npairs ? pr : a.npairs - 1;
             const uint32_t back = (pr == last_pair_odd) ? (uint32_t)h : 0u;
             // The split generation reads x only at a feature's first block.
             if (!(X_FIRST_ONLY && t % NSBC != 0)) {
@@ -549,7 +557,8 @@ void layer_kernel(LayerArgs a) {
     // group: value 2G is the basis at column c0 + ((G - c0) mod 4), at
     // position c0 / 4, plus 1 for G < c0 mod 4; value 1 is the SiLU value at
     // column 0 (group 0, position 0); values 3, 5, 7 are zero.
-    static_assert(!SP || (BF16 && NSBC == 2 && WK == 1 && KBW % 2 == 0), "sparse MFMA shape");
+    static_assert(!SP || (BF16 && NSBC == 2 && KBW % 2 == 0 && (WK == 1 || (!XA && RF == 1))),
+                  "sparse MFMA shape");
     auto gen_sparse = [&](const float (&xf)[GRF], AFrag<T, RF>& As, uint32_t (&idx)[RF]) {
       if constexpr (SP) {
 #pragma unroll
@@ -644,7 +653,8 @@ void layer_kernel(LayerArgs a) {
       }
     };
     BFrag bq[2];
-    Pos pos_c = advance_n(Pos{0, 0, 0}, wk, nsb);  // first block of the current chunk
+    // first block of the current chunk (SPK: the first block of pair wk)
+    Pos pos_c = SPK ? Pos{2 * wk, wk, 0} : advance_n(Pos{0, 0, 0}, wk, nsb);
     Pos pos_l = pos_c;                               // first block of the next chunk to load
 
     // prologue: loads of chunks 0 .. L - 1, chunk 0 to stage 0
@@ -735,18 +745,19 @@ void layer_kernel(LayerArgs a) {
         }
 
         const u32x4* st = stage(kk);
-        if constexpr (!PRE) read_b(bq[0], st, wk);
+        if constexpr (!PRE) read_b(bq[0], st, SP ? 2 * wk : wk);
         if constexpr (SP) {
             // the chunk's feature pairs, one step each: the B of the pair's two
             // blocks (XA: and the partner's A), at the first pair the next
             // chunk's weights to the other LDS stage, the next pair's A (its x
             // was loaded a chunk or more ago), the MFMAs of this pair
-            constexpr int NPC = KBW / 2;  // pairs per chunk
+            constexpr int NPC = KBW / 2;  // pairs per chunk of this wave
             auto pair_step = [&](auto qq) {
                 constexpr int q = decltype(qq)::value;
                 if constexpr (!PRE) {
-                    if constexpr (q > 0) read_b(bq[0], st, 2 * q);
-                    read_b(bq[1], st, 2 * q + 1);
+                    // (blocks of the wave's q-th pair of the chunk)
+                    if constexpr (q > 0) read_b(bq[0], st, 2 * (wk + WK * q));
+                    read_b(bq[1], st, 2 * (wk + WK * q) + 1);
                 }
                 xa_get(c & 1, A_cur, idx_cur);  // (XA: one pair per chunk)
                 if constexpr (q == 0) {
@@ -762,15 +773,15 @@ void layer_kernel(LayerArgs a) {
                         store(std::integral_constant<int, K + 1>{}, wq[JN]);
                     __builtin_amdgcn_sched_barrier(0);
                 }
-                Pos pn = pos_c;  // the next pair
-                pn.pair += q + 1;
+                Pos pn = pos_c;  // the wave's next pair
+                pn.pair += WK * (q + 1);
                 // (x of the next pair's first block, copied before this
                 // chunk's loads reused its register set)
                 float xf[GRF];
 #pragma unroll
                 for (int rf = 0; rf < GRF; ++rf) xf[rf] = x_value(pn, xr[2 * q + 1][rf], rf);
                 if constexpr (LASTG) {
-                    if (c * KBW + 2 * q >= nq) {  // a padding pair: contributes 0
+                    if (pos_c.pair + WK * q >= a.npairs) {  // a padding pair: contributes 0
 #pragma unroll
                         for (int rf = 0; rf < RF; ++rf) zero_frag(A_cur, rf);
                     }
@@ -948,21 +959,24 @@ hipError_t launch_cfg(const LayerGeom& g, LayerArgs a, hipStream_t s) {
     // tensor.
     constexpr bool BF16 = sizeof(T) == 2;
     if (g.sparse) {
-        if constexpr (BF16 && WK == 1 &&
-                      (RF == 1 ? (NW == 8 || NF < 8) : (NF == NFL && (NW == 4 || NF == 8))) &&
-                      layer_chunk_blocks(BF16, NFL) % 2 == 0) {
+        // (K splits: narrow tiles, whole feature pairs per wave slice)
+        constexpr int KBL = layer_chunk_blocks(BF16, NFL);
+        if constexpr (BF16 && KBL % 2 == 0 &&
+                      ((WK == 1 && (RF == 1 ? (NW == 8 || NF < 8)
+                                            : (NF == NFL && (NW == 4 || NF == 8)))) ||
+                       (WK > 1 && RF == 1 && NF == NFL && NFL <= 2 && (KBL / 2) % WK == 0))) {
             if (layer_x_words(a.x, a.batch, a.in))
-                hipLaunchKernelGGL((layer_kernel<T, RF, NFL, NF, 1, NW, 2, true, true, XA>), grid,
-                                   dim3(64 * NW), 0, s, a);
+                hipLaunchKernelGGL((layer_kernel<T, RF, NFL, NF, WK, NW, 2, true, true, XA>),
+                                   grid, dim3(64 * NW), 0, s, a);
             else
-                hipLaunchKernelGGL((layer_kernel<T, RF, NFL, NF, 1, NW, 2, false, true, XA>),
+                hipLaunchKernelGGL((layer_kernel<T, RF, NFL, NF, WK, NW, 2, false, true, XA>),
                                    grid, dim3(64 * NW), 0, s, a);
             return hipGetLastError();
         } else {
             return hipErrorInvalidValue;
         }
     }
-    if constexpr (XA) {
+    if constexpr (XA || (NW == 8 && WK > 1)) {  // (sparse-only shapes)
         return hipErrorInvalidValue;
     } else {
         hipLaunchKernelGGL((layer_kernel<T, RF, NFL, NF, WK, NW>), grid, dim3(64 * NW), 0, s, a);

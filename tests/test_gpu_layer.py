@@ -70,9 +70,9 @@ def test_layer_matches_oracle(B, n_in, n_out, G, dtype_name):
 CFGS = ["1,1", "2,1", "1,2", "1,4", "2,2", "2,4", "1,1,8", "1,1,4,2", "1,2,4,2", "1,4,4,2"]
 
 
-# bf16 with two blocks per feature (5 <= G <= 12) runs the sparse MFMA, which
-# takes no K split (one row tile per wave, or two with four waves over the
-# whole tile); G = 20 keeps the dense bf16 kernel under every shape.
+# bf16 with two blocks per feature (5 <= G <= 12) runs the sparse MFMA, whose
+# K splits take tiles of one or two fragments (NARROW_CFGS below); G = 20 keeps
+# the dense bf16 kernel under every shape.
 SPARSE_CFGS = ["1,1", "2,1", "1,1,8", "1,1,4,2"]
 
 
@@ -175,6 +175,35 @@ def test_layer_bf16_sparse_mfma_256_column_shapes(cfg):
     x, C, Wb = _inputs(B, n_in, n_out, G, seed=5, off=0.2, dtype_name="bf16")
     ref = oracle.round_bf16(oracle.layer(x, C, Wb, G))
     say(f"layer bf16 sparse 256 columns cfg={cfg}")
+    set_layer_cfg(cfg)
+    try:
+        y = _gpu_layer(x, C, Wb, G, "bf16")
+    finally:
+        set_layer_cfg(None)
+    assert normwise(y, ref) <= BF16_LAYER_TOL, normwise(y, ref)
+
+
+# The sparse MFMA with a K split (tiles of one or two 32-column fragments,
+# wave slices taking whole feature pairs, partial sums added through LDS):
+# slices of two and four over four- and eight-wave workgroups.
+NARROW_CFGS = ["1,2", "1,4", "1,2,8", "1,4,8"]
+NARROW_SHAPES = [
+    # (B, in, out, G): one and two fragments, odd feature counts (a phantom
+    # feature), ragged batches, fewer feature pairs than K slices, one feature
+    (300, 9, 10, 10),
+    (257, 17, 64, 7),
+    (1000, 256, 10, 10),
+    (129, 3, 33, 12),
+    (65, 1, 5, 5),
+]
+
+
+@pytest.mark.parametrize("cfg", NARROW_CFGS)
+@pytest.mark.parametrize("B,n_in,n_out,G", NARROW_SHAPES)
+def test_layer_bf16_sparse_k_split(B, n_in, n_out, G, cfg):
+    x, C, Wb = _inputs(B, n_in, n_out, G, seed=B + n_in + G, off=0.2, dtype_name="bf16")
+    ref = oracle.round_bf16(oracle.layer(x, C, Wb, G))
+    say(f"layer bf16 sparse K split B={B} in={n_in} out={n_out} G={G} cfg={cfg}")
     set_layer_cfg(cfg)
     try:
         y = _gpu_layer(x, C, Wb, G, "bf16")

@@ -28,11 +28,12 @@ def _shape(cfg):
 
 
 @pytest.mark.parametrize("dtype_name,n_in,n_out,want", [
-    # one workgroup of eight waves per CU: on the 256-column layers 64-row
-    # waves over column halves sharing A, on the narrow layer 32-row waves
+    # eight waves per workgroup: on the 256-column layers 64-row waves over
+    # column halves sharing A, on the narrow layer 32-row waves in two slices
+    # of the feature pairs
     ("bf16", 784, 256, (2, 1, 8, 1, 1)),
     ("bf16", 256, 256, (2, 1, 8, 1, 1)),
-    ("bf16", 256, 10, (1, 1, 8, 1, 1)),
+    ("bf16", 256, 10, (1, 2, 8, 1, 1)),
     # fp32: 64-row waves over 128-column tiles; the narrow layer splits K
     ("f32", 784, 256, (2, 1, 4, 1, 0)),
     ("f32", 256, 256, (2, 1, 4, 1, 0)),
@@ -58,6 +59,17 @@ def test_shared_a_shape_only_on_sparse_256_column_tiles(monkeypatch):
         assert _plan(monkeypatch, G, dt, 65536, 784, n_out, "2,1,8") == own
 
 
+def test_sparse_k_split_only_on_narrow_tiles(monkeypatch):
+    # waves splitting K on the sparse layout: tiles of one or two fragments;
+    # eight-wave K splits are not shapes of the dense kernel
+    assert _plan(monkeypatch, 10, "bf16", 65536, 256, 10, "1,4,8") == (1, 4, 8, 1, 1)
+    assert _plan(monkeypatch, 10, "bf16", 65536, 256, 64, "1,2") == (1, 2, 4, 1, 1)
+    for G, dt, n_out, cfg in [(10, "bf16", 256, "1,2"), (10, "bf16", 100, "1,4"),
+                              (20, "bf16", 10, "1,4,8"), (10, "f32", 10, "1,2,8")]:
+        own = _plan(monkeypatch, G, dt, 65536, 256, n_out)
+        assert _plan(monkeypatch, G, dt, 65536, 256, n_out, cfg) == own
+
+
 def test_malformed_override_is_ignored(monkeypatch):
     own = _plan(monkeypatch, 10, "bf16", 65536, 784, 256)
     for cfg in ["", "x", "3", "3,1", "1,3", "1,1,6", "1,1,4,3", "1,2,8"]:
@@ -77,6 +89,9 @@ def _forced_cases():
     for cfg in gl.X_WORD_CFGS:
         if cfg is not None:
             yield "bf16", 10, 300, 9, 45, cfg
+    for B, n_in, n_out, G in gl.NARROW_SHAPES:
+        for cfg in gl.NARROW_CFGS:
+            yield "bf16", G, B, n_in, n_out, cfg
 
 
 @pytest.mark.parametrize("dtype_name,G,B,n_in,n_out,cfg", list(_forced_cases()))
