@@ -307,7 +307,7 @@ def main() -> int:
     args = parse()
     if args.gpus != 1:
         print(f"bench.py: this build measures one GPU only; --gpus {args.gpus} is not run "
-              "(the batch shards across GPUs with no communication; see the design notes)",
+              "(rows are independent: the batch would shard across GPUs with the weights replicated and no communication inside a layer)",
               file=sys.stderr)
         return 2
     import numpy as np
