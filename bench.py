@@ -306,9 +306,9 @@ def cpu_baseline(W, n_layers_shapes, target_s: float):
 def main() -> int:
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py: this build measures one GPU only; --gpus {args.gpus} is not run "
-              "(rows are independent: the batch would shard across GPUs with the weights replicated and no communication inside a layer)",
-              file=sys.stderr)
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not run (rows are "
+              "independent: the batch would shard across GPUs with the weights replicated "
+              "and no communication inside a layer)", file=sys.stderr)
         return 2
     import numpy as np
     import torch
