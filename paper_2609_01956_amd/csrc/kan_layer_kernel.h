@@ -629,6 +629,12 @@ void layer_kernel(LayerArgs a) {
     // A exchange alternates between its two stages by the parity of c.
     static_assert(WK <= 4, "wave block stride");
     constexpr int WAIT_LDS = 0xF | (0x7 << 4) | (0x0 << 8) | (0x3 << 14);  // lgkmcnt(0) only
+    // XA (PRE): lgkmcnt(2 NFW), every LDS operation but the chunk's last 2 NFW
+    // (the B reads of the next chunk, issued after all of the chunk's LDS
+    // writes; LDS operations complete in order and the loop has no scalar
+    // memory loads, which would also count)
+    constexpr int WAIT_XA = 0xF | (0x7 << 4) | ((2 * NFW) << 8) | (0x3 << 14);
+    static_assert(!PRE || 2 * NFW <= 15, "lgkmcnt field");
     const int nq = wk < a.nblk ? (a.nblk - wk + WK - 1) / WK : 0;  // real blocks of this wave
 
     XSet xq[L];
@@ -720,7 +726,7 @@ void layer_kernel(LayerArgs a) {
             pos_l.bsub = 0;
         }
         if (c > 0) {  // (chunk 0's barrier is in the prologue)
-            __builtin_amdgcn_s_waitcnt(WAIT_LDS);
+            __builtin_amdgcn_s_waitcnt(PRE ? WAIT_XA : WAIT_LDS);
             __builtin_amdgcn_s_barrier();
             __builtin_amdgcn_sched_barrier(0);
         }
@@ -814,13 +820,18 @@ void layer_kernel(LayerArgs a) {
                     asm volatile("" : "+v"(w), "+v"(idx_nxt[rf]));
                     A_nxt.a[rf] = __builtin_bit_cast(bf16x8, w);
                 }
+                if constexpr (XA) {
+                    xa_put((c + 1) & 1, A_nxt, idx_nxt);
+                    __builtin_amdgcn_sched_barrier(0);
+                }
                 if constexpr (PRE) {
-                    // the next chunk's B (stored during the previous chunk)
+                    // the next chunk's B (stored during the previous chunk),
+                    // the chunk's last LDS operations: the barrier waits only
+                    // for the LDS writes before them (WAIT_XA)
                     read_b(bq[0], stage(std::integral_constant<int, K + 1>{}), 0);
                     read_b(bq[1], stage(std::integral_constant<int, K + 1>{}), 1);
                 }
                 if constexpr (XA) {
-                    xa_put((c + 1) & 1, A_nxt, idx_nxt);
                     A_cur.a[0] = A_nxt.a[0];
                     idx_cur[0] = idx_nxt[0];
                 } else {
