@@ -335,6 +335,30 @@ def test_layer_nan_row_and_determinism_and_guard():
     assert np.all(b[:64] == 3.0) and np.all(b[64 + B * n_out:] == 3.0)
 
 
+@pytest.mark.parametrize("n_out,cfg", [(256, "2,1,8"), (10, "1,2,8"), (256, None)])
+def test_layer_bf16_sparse_nan_row(n_out, cfg):
+    """A NaN input makes its whole output row NaN (through the SiLU branch) on
+    the sparse MFMA shapes too: the shared-A exchange and the K split carry it
+    like any other value; every other row matches the oracle."""
+    B, n_in, G = 300, 18, 10
+    x, C, Wb = _inputs(B, n_in, n_out, G, seed=9, off=0.2, dtype_name="bf16")
+    x[17, 3] = np.nan
+    say(f"layer bf16 sparse nan row out={n_out} cfg={cfg}")
+    set_layer_cfg(cfg)
+    try:
+        y = _gpu_layer(x, C, Wb, G, "bf16")
+    finally:
+        set_layer_cfg(None)
+    assert np.all(np.isnan(y[17]))
+    ok = np.ones(B, bool)
+    ok[17] = False
+    assert not np.any(np.isnan(y[ok]))
+    xr = x.copy()
+    xr[17, 3] = 0.0
+    ref = oracle.round_bf16(oracle.layer(xr, C, Wb, G))
+    assert normwise(y[ok], ref[ok]) <= BF16_LAYER_TOL
+
+
 def test_layer_empty_batch():
     say("layer empty batch")
     dt = torch.float32
