@@ -43,6 +43,19 @@ def test_mlp_layers_planned_shapes(monkeypatch, dtype_name, n_in, n_out, want):
     assert _plan(monkeypatch, 10, dtype_name, 65536, n_in, n_out) == want
 
 
+@pytest.mark.parametrize("B,n_out,want", [
+    # narrow sparse tiles: two K slices of eight-wave workgroups when that
+    # still gives a workgroup per CU, more slices of four waves below that
+    (65536, 64, (1, 2, 8, 1, 1)),
+    (32768, 10, (1, 2, 8, 1, 1)),
+    (16384, 10, (1, 4, 4, 1, 1)),
+    # four fragments: no K split on the sparse layout's wider tiles
+    (65536, 100, (1, 1, 8, 1, 1)),
+])
+def test_narrow_sparse_layers_planned_shapes(monkeypatch, B, n_out, want):
+    assert _plan(monkeypatch, 10, "bf16", B, 256, n_out) == want
+
+
 @pytest.mark.parametrize("G,sparse", [(1, 0), (4, 0), (5, 1), (10, 1), (12, 1), (13, 0),
                                       (200, 0)])
 def test_sparse_instruction_for_two_blocks_per_feature(monkeypatch, G, sparse):
