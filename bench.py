@@ -58,12 +58,6 @@ def parse():
                    help="only time the fused layer and the basis kernel on every configured "
                         "workload (one JSON line each, with the partition-of-unity error of "
                         "the grid-size sweep) and exit")
-    p.add_argument("--mfma-ceiling", action="store_true",
-                   help="only measure back-to-back bf16 MFMA throughput and the shader clock "
-                        "with constant and with random operands (libkan_probe.so) and exit")
-    p.add_argument("--valu-ceiling", action="store_true",
-                   help="only measure plain fp32 fma throughput per SIMD with 1, 2 and 4 waves "
-                        "on it (libkan_probe.so) and exit")
     p.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                    help="only run a plain device copy of BYTES bytes 10 times (HBM counter "
                         "calibration under rocprofv3) and exit")
@@ -196,85 +190,6 @@ def configs_sweep(dtype: str) -> None:
         print(json.dumps(line), flush=True)
 
 
-def mfma_ceiling() -> None:
-    """Back-to-back v_mfma_f32_32x32x16_bf16 (no other work) with constant and
-    with random finite operands: TFLOP/s, the average shader clock over the
-    run and the flops per clock per SIMD (1024 at the full matrix-core rate)."""
-    import ctypes
-
-    import torch
-
-    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2609_01956_amd", "libkan_probe.so"))
-    words = lib.kan_probe_operand_words()
-    g = torch.Generator().manual_seed(1)
-    vals = (torch.rand(words * 8, generator=g) * 2 - 1).to(torch.bfloat16)
-    operands = vals.view(torch.int32).to("cuda")
-    clk = torch.zeros(4, dtype=torch.int64, device="cuda")
-    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
-    simds = 4 * torch.cuda.get_device_properties(0).multi_processor_count
-    for random in (0, 1):
-        blocks, trips = 1024, 2000
-        out = torch.empty(blocks * 256, device="cuda")
-        args = [ctypes.c_void_p(operands.data_ptr()), ctypes.c_void_p(out.data_ptr()),
-                ctypes.c_void_p(clk.data_ptr())]
-        if lib.kan_probe_mfma_bf16(*args, blocks, 10, random, stream) != 0:
-            raise RuntimeError("probe launch failed")
-        torch.cuda.synchronize()
-        e0 = torch.cuda.Event(enable_timing=True)
-        e1 = torch.cuda.Event(enable_timing=True)
-        e0.record()
-        if lib.kan_probe_mfma_bf16(*args, blocks, trips, random, stream) != 0:
-            raise RuntimeError("probe launch failed")
-        e1.record()
-        torch.cuda.synchronize()
-        s = e0.elapsed_time(e1) * 1e-3
-        c = clk.cpu().tolist()
-        ghz = (c[2] - c[0]) / ((c[3] - c[1]) / 100e6) / 1e9
-        flops = blocks * 4 * 16 * trips * 32768.0
-        print(json.dumps({"probe": "v_mfma_f32_32x32x16_bf16 back to back",
-                          "operands": "random" if random else "constant",
-                          "tflops": flops / s / 1e12, "shader_clock_ghz": ghz,
-                          "flop_per_clock_per_simd": flops / s / (ghz * 1e9) / simds,
-                          "frac_of_2516.6": flops / s / 1e12 / PEAK_TFLOPS["bf16"]}), flush=True)
-
-
-def valu_ceiling() -> None:
-    """Independent fp32 fma chains, nothing else, with 1, 2 and 4 waves per
-    SIMD: fma lanes per shader clock per SIMD (the span of workgroup 0's
-    waves on the shader-clock counter) and the rate over the whole card."""
-    import ctypes
-
-    import torch
-
-    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2609_01956_amd", "libkan_probe.so"))
-    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
-    cus = torch.cuda.get_device_properties(0).multi_processor_count
-    for w in (1, 2, 4):
-        blocks, trips = cus, 4000
-        out = torch.empty(blocks * 256 * w, device="cuda")
-        clk = torch.zeros(8 * w, dtype=torch.int64, device="cuda")
-        args = [ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(clk.data_ptr()), blocks, w]
-        if lib.kan_probe_valu_f32(*args, 10, stream) != 0:
-            raise RuntimeError("probe launch failed")
-        torch.cuda.synchronize()
-        e0 = torch.cuda.Event(enable_timing=True)
-        e1 = torch.cuda.Event(enable_timing=True)
-        e0.record()
-        if lib.kan_probe_valu_f32(*args, trips, stream) != 0:
-            raise RuntimeError("probe launch failed")
-        e1.record()
-        torch.cuda.synchronize()
-        c = clk.cpu().tolist()
-        span = max(c[1::2]) - min(c[0::2])
-        lanes = 64.0 * w * 128 * trips / span
-        s = e0.elapsed_time(e1) * 1e-3
-        print(json.dumps({"probe": "fp32 v_fma_f32, 8 independent chains per wave",
-                          "waves_per_simd": w, "fma_lanes_per_clock_per_simd": lanes,
-                          "card_g_lane_ops_per_s": blocks * 4 * w * 64.0 * 128 * trips / s / 1e9,
-                          "shader_clock_ghz": span / s / 1e9,
-                          "frac_of_32_lanes": lanes / 32.0}), flush=True)
-
-
 def cpu_baseline(W, n_layers_shapes, target_s: float):
     """The float64 oracle, untuned, on a row sample of the same step."""
     import numpy as np
@@ -321,12 +236,6 @@ def main() -> int:
         return 1
     if args.copy_calibration:
         copy_calibration(args.copy_calibration)
-        return 0
-    if args.mfma_ceiling:
-        mfma_ceiling()
-        return 0
-    if args.valu_ceiling:
-        valu_ceiling()
         return 0
     if args.configs:
         configs_sweep(args.dtype)

@@ -9,10 +9,10 @@
  * Conventions shared by every entry point
  * ---------------------------------------
  *  * Pointers named x, phi, coef, base_w, packed, y are DEVICE pointers owned
- *    by the caller.  The library keeps no global state; calls are reentrant and
- *    thread-safe.  Only kan_layer_forward allocates (a temporary from the
- *    stream-ordered pool, see there); every other entry point allocates
- *    nothing.
+ *    by the caller.  No entry point allocates device or host memory; where a
+ *    call needs scratch memory the caller passes it (a workspace pointer with
+ *    a size query).  The library keeps no global state; calls are reentrant
+ *    and thread-safe.
  *  * Work is enqueued on `stream` (a hipStream_t passed as void*; NULL is the
  *    null stream) and returns before it finishes.  Results are visible after the
  *    caller synchronises that stream.  A device fault inside a kernel surfaces at
@@ -97,33 +97,47 @@ kan_status kan_basis_eval(const kan_grid* grid, kan_dtype dtype, const void* x,
  * coefficients (the layer has no separate spline scaler, Sec. 2 "Integration
  * with KAN layers").
  *
- *   x       [batch, in_features]              dtype storage
- *   coef    [out_features, in_features, G+3]  dtype storage
- *   base_w  [out_features, in_features]       dtype storage
- *   y       [batch, out_features]             dtype storage, fully overwritten
+ *   x          [batch, in_features]              dtype storage
+ *   coef       [out_features, in_features, G+3]  dtype storage
+ *   base_w     [out_features, in_features]       dtype storage
+ *   workspace  caller-owned device scratch of workspace_bytes >=
+ *              kan_layer_forward_workspace_bytes(...) bytes, 16-byte aligned,
+ *              overlapping no other argument; its contents are overwritten
+ *              (it receives the packed weights) and are of no use afterwards.
+ *              It must stay allocated until the enqueued work has finished.
+ *   y          [batch, out_features]             dtype storage, fully overwritten
  *
  * The contraction runs on the matrix cores over K = in_features * (G + 4)
  * columns (G + 3 basis values and one SiLU value per input feature); the basis
  * is generated in registers and never written to memory.  The call is
- * kan_layer_pack into a temporary buffer followed by kan_layer_forward_packed;
- * the temporary (kan_layer_packed_bytes bytes) comes from hipMallocAsync on
- * `stream` and is released with hipFreeAsync on `stream`, so the call stays
- * asynchronous.  Callers that must not allocate use the two calls below with a
- * buffer of their own.
+ * kan_layer_pack into the workspace followed by kan_layer_forward_packed,
+ * both enqueued on `stream`.
  *
  * y must not overlap any input.  Every pointer must be aligned to the dtype
  * size.  A NaN in x[b, :] makes y[b, :] NaN (through the SiLU branch).
  *
  * Returns KAN_OK, KAN_ERR_INVALID_ARG (grid == NULL, bad grid, batch < 0,
  * in_features < 1, out_features < 1, in_features * (G + 4) >= 2^31,
- * NULL/misaligned/overlapping pointers with batch > 0), KAN_ERR_UNSUPPORTED
- * (spline_order != 3, unknown dtype) or KAN_ERR_DEVICE (allocation or launch
- * rejected).
+ * in_features >= 2^24, NULL/misaligned/overlapping pointers or a short
+ * workspace with batch > 0), KAN_ERR_UNSUPPORTED (spline_order != 3, unknown
+ * dtype) or KAN_ERR_DEVICE (launch rejected).
  */
 kan_status kan_layer_forward(const kan_grid* grid, kan_dtype dtype, int64_t batch,
                              int32_t in_features, int32_t out_features,
                              const void* x, const void* coef, const void* base_w,
+                             void* workspace, size_t workspace_bytes,
                              void* y, void* stream);
+
+/*
+ * kan_layer_forward_workspace_bytes -- size in bytes of the workspace that
+ * kan_layer_forward needs for a layer (eq. kan_forward) of this grid, dtype,
+ * batch and shape (the packed weights; it does not grow with the batch).
+ * Writes *bytes.  Returns KAN_OK, KAN_ERR_INVALID_ARG (bytes == NULL, bad grid
+ * or sizes, batch < 0) or KAN_ERR_UNSUPPORTED.
+ */
+kan_status kan_layer_forward_workspace_bytes(const kan_grid* grid, kan_dtype dtype,
+                                             int64_t batch, int32_t in_features,
+                                             int32_t out_features, size_t* bytes);
 
 /*
  * kan_layer_packed_bytes -- size in bytes of the packed weights of a layer
@@ -141,10 +155,10 @@ kan_status kan_layer_packed_bytes(const kan_grid* grid, kan_dtype dtype, int32_t
  * columns, feature pair and block of columns, the weights of both features for
  * every output column, the SiLU weight before the G + 3 spline coefficients of
  * its feature and zeros in the padding (in bf16 with 5 <= G <= 12 a feature's
- * 16 columns are permuted for the structured-sparse matrix instruction).  The layout is private to this library
- * and depends only on (grid, dtype, in_features, out_features).  Weights that
- * do not change can be packed once and reused by any number of
- * kan_layer_forward_packed calls.
+ * 16 columns are permuted for the structured-sparse matrix instruction).  The
+ * layout is private to this library and depends only on (grid, dtype,
+ * in_features, out_features).  Weights that do not change can be packed once
+ * and reused by any number of kan_layer_forward_packed calls.
  *
  *   coef    [out_features, in_features, G+3]  dtype storage
  *   base_w  [out_features, in_features]       dtype storage
@@ -164,21 +178,30 @@ kan_status kan_layer_pack(const kan_grid* grid, kan_dtype dtype, int32_t in_feat
  *
  *   x       [batch, in_features]    dtype storage
  *   packed  output of kan_layer_pack, packed_bytes >= kan_layer_packed_bytes(...)
+ *   shape   NULL: the workgroup shape the library plans for this layer and
+ *           batch (what kan_layer_plan reports).  Otherwise four int32
+ *           {rf, wk, nw, cs} as in kan_layer_plan's plan[0..3], forcing that
+ *           shape (for testing and tuning; every valid shape gives the same
+ *           result up to the fp32 summation order); a shape that is not valid
+ *           for the layer is KAN_ERR_INVALID_ARG.
  *   y       [batch, out_features]   dtype storage, fully overwritten; must not
  *           overlap x or packed.
  *
- * Allocates nothing.  Returns as kan_layer_forward.
+ * Returns as kan_layer_forward.
  */
 kan_status kan_layer_forward_packed(const kan_grid* grid, kan_dtype dtype, int64_t batch,
                                     int32_t in_features, int32_t out_features, const void* x,
-                                    const void* packed, size_t packed_bytes, void* y,
-                                    void* stream);
+                                    const void* packed, size_t packed_bytes,
+                                    const int32_t* shape, void* y, void* stream);
 
 /*
  * kan_layer_plan -- the workgroup shape that kan_layer_forward_packed (and
  * kan_layer_forward) launches for a layer of this grid, dtype, shape and
  * batch.  Host only: no HIP call, nothing enqueued.  For testing and tuning.
  *
+ *   shape    NULL for the library's own choice, or a forced {rf, wk, nw, cs}
+ *            as accepted by kan_layer_forward_packed (validated here the same
+ *            way: an invalid one is KAN_ERR_INVALID_ARG)
  *   plan[0]  32-row MFMA tiles per wave (1 or 2)
  *   plan[1]  waves splitting the contraction (K) of a workgroup (1, 2 or 4)
  *   plan[2]  waves per workgroup (4 or 8)
@@ -186,14 +209,12 @@ kan_status kan_layer_forward_packed(const kan_grid* grid, kan_dtype dtype, int64
  *   plan[4]  1 if the layer runs on the structured-sparse matrix instruction
  *            (bf16, 5 <= G <= 12), else 0
  *
- * The environment variable KAN_LAYER_CFG="rf,wk[,nw[,cs]]", read at every
- * call, forces plan[0..3] when it is well formed and valid for the layer;
- * otherwise the library's own choice stands.  Writes plan[0..4].  Returns
- * KAN_OK, KAN_ERR_INVALID_ARG (plan == NULL, bad grid or sizes, batch < 1) or
- * KAN_ERR_UNSUPPORTED.
+ * Writes plan[0..4].  Returns KAN_OK, KAN_ERR_INVALID_ARG (plan == NULL, bad
+ * grid or sizes, batch < 1, an invalid forced shape) or KAN_ERR_UNSUPPORTED.
  */
 kan_status kan_layer_plan(const kan_grid* grid, kan_dtype dtype, int64_t batch,
-                          int32_t in_features, int32_t out_features, int32_t* plan);
+                          int32_t in_features, int32_t out_features, const int32_t* shape,
+                          int32_t* plan);
 
 /* Static, NUL-terminated description of a status code (never NULL). */
 const char* kan_status_string(kan_status status);
@@ -201,7 +222,7 @@ const char* kan_status_string(kan_status status);
 /* Version of this interface; bumped on any incompatible change. */
 int32_t kan_abi_version(void);
 
-#define KAN_ABI_VERSION 2
+#define KAN_ABI_VERSION 3
 
 #ifdef __cplusplus
 }

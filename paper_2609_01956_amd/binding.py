@@ -27,9 +27,12 @@ KAN_ERR_DEVICE = 3
 KAN_F32 = 0
 KAN_BF16 = 1
 
-EXPORTED_SYMBOLS = ("kan_basis_eval", "kan_layer_forward", "kan_layer_packed_bytes",
-                    "kan_layer_pack", "kan_layer_forward_packed", "kan_layer_plan",
-                    "kan_status_string", "kan_abi_version")
+EXPORTED_SYMBOLS = ("kan_basis_eval", "kan_layer_forward", "kan_layer_forward_workspace_bytes",
+                    "kan_layer_packed_bytes", "kan_layer_pack", "kan_layer_forward_packed",
+                    "kan_layer_plan", "kan_status_string", "kan_abi_version")
+
+_VP = ctypes.c_void_p
+_I32P = ctypes.POINTER(ctypes.c_int32)
 
 
 class kan_grid(ctypes.Structure):
@@ -58,28 +61,27 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
             lib.kan_basis_eval.argtypes = [ctypes.POINTER(kan_grid), ctypes.c_int, ctypes.c_void_p,
                                            ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p]
             lib.kan_basis_eval.restype = ctypes.c_int
-            lib.kan_layer_forward.argtypes = [ctypes.POINTER(kan_grid), ctypes.c_int, ctypes.c_int64,
-                                              ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
-                                              ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
-                                              ctypes.c_void_p]
+            g = ctypes.POINTER(kan_grid)
+            lib.kan_layer_forward.argtypes = [g, ctypes.c_int, ctypes.c_int64, ctypes.c_int32,
+                                              ctypes.c_int32, _VP, _VP, _VP, _VP, ctypes.c_size_t,
+                                              _VP, _VP]
             lib.kan_layer_forward.restype = ctypes.c_int
-            lib.kan_layer_packed_bytes.argtypes = [ctypes.POINTER(kan_grid), ctypes.c_int,
-                                                   ctypes.c_int32, ctypes.c_int32,
-                                                   ctypes.POINTER(ctypes.c_size_t)]
+            lib.kan_layer_forward_workspace_bytes.argtypes = [g, ctypes.c_int, ctypes.c_int64,
+                                                              ctypes.c_int32, ctypes.c_int32,
+                                                              ctypes.POINTER(ctypes.c_size_t)]
+            lib.kan_layer_forward_workspace_bytes.restype = ctypes.c_int
+            lib.kan_layer_packed_bytes.argtypes = [g, ctypes.c_int, ctypes.c_int32,
+                                                   ctypes.c_int32, ctypes.POINTER(ctypes.c_size_t)]
             lib.kan_layer_packed_bytes.restype = ctypes.c_int
-            lib.kan_layer_pack.argtypes = [ctypes.POINTER(kan_grid), ctypes.c_int, ctypes.c_int32,
-                                           ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
-                                           ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
+            lib.kan_layer_pack.argtypes = [g, ctypes.c_int, ctypes.c_int32, ctypes.c_int32, _VP,
+                                           _VP, _VP, ctypes.c_size_t, _VP]
             lib.kan_layer_pack.restype = ctypes.c_int
-            lib.kan_layer_forward_packed.argtypes = [ctypes.POINTER(kan_grid), ctypes.c_int,
-                                                     ctypes.c_int64, ctypes.c_int32,
-                                                     ctypes.c_int32, ctypes.c_void_p,
-                                                     ctypes.c_void_p, ctypes.c_size_t,
-                                                     ctypes.c_void_p, ctypes.c_void_p]
+            lib.kan_layer_forward_packed.argtypes = [g, ctypes.c_int, ctypes.c_int64,
+                                                     ctypes.c_int32, ctypes.c_int32, _VP, _VP,
+                                                     ctypes.c_size_t, _I32P, _VP, _VP]
             lib.kan_layer_forward_packed.restype = ctypes.c_int
-            lib.kan_layer_plan.argtypes = [ctypes.POINTER(kan_grid), ctypes.c_int,
-                                           ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
-                                           ctypes.POINTER(ctypes.c_int32)]
+            lib.kan_layer_plan.argtypes = [g, ctypes.c_int, ctypes.c_int64, ctypes.c_int32,
+                                           ctypes.c_int32, _I32P, _I32P]
             lib.kan_layer_plan.restype = ctypes.c_int
             lib.kan_status_string.argtypes = [ctypes.c_int]
             lib.kan_status_string.restype = ctypes.c_char_p
@@ -110,14 +112,37 @@ def kan_basis_eval(grid: kan_grid, dtype: int, x: int, n: int, phi: int, stream:
                                              int(n), ctypes.c_void_p(phi), ctypes.c_void_p(stream)))
 
 
+def _shape_arg(shape):
+    """None, or a forced workgroup shape (rf, wk, nw, cs) / "rf,wk[,nw[,cs]]"
+    as an int32[4] (nw defaults to 4, cs to 1)."""
+    if shape is None:
+        return None
+    if isinstance(shape, str):
+        shape = [int(t) for t in shape.split(",")]
+    v = list(shape) + [4, 1][len(shape) - 2:] if len(shape) < 4 else list(shape)
+    if len(v) != 4:
+        raise ValueError("a shape is (rf, wk[, nw[, cs]])")
+    return (ctypes.c_int32 * 4)(*[int(t) for t in v])
+
+
 def kan_layer_forward(grid: kan_grid, dtype: int, batch: int, in_features: int,
-                      out_features: int, x: int, coef: int, base_w: int, y: int,
-                      stream: int = 0) -> int:
+                      out_features: int, x: int, coef: int, base_w: int, workspace: int,
+                      workspace_bytes: int, y: int, stream: int = 0) -> int:
     """Raw call: device addresses as integers; returns the kan_status code."""
     return int(load_library().kan_layer_forward(
         ctypes.byref(grid), int(dtype), int(batch), int(in_features), int(out_features),
-        ctypes.c_void_p(x), ctypes.c_void_p(coef), ctypes.c_void_p(base_w), ctypes.c_void_p(y),
-        ctypes.c_void_p(stream)))
+        _VP(x), _VP(coef), _VP(base_w), _VP(workspace), ctypes.c_size_t(workspace_bytes),
+        _VP(y), _VP(stream)))
+
+
+def kan_layer_forward_workspace_bytes(grid: kan_grid, dtype: int, batch: int, in_features: int,
+                                      out_features: int) -> Tuple[int, int]:
+    """Raw call: returns (kan_status, bytes)."""
+    n = ctypes.c_size_t(0)
+    st = int(load_library().kan_layer_forward_workspace_bytes(
+        ctypes.byref(grid), int(dtype), int(batch), int(in_features), int(out_features),
+        ctypes.byref(n)))
+    return st, int(n.value)
 
 
 def kan_layer_packed_bytes(grid: kan_grid, dtype: int, in_features: int,
@@ -131,11 +156,13 @@ def kan_layer_packed_bytes(grid: kan_grid, dtype: int, in_features: int,
 
 
 def kan_layer_plan(grid: kan_grid, dtype: int, batch: int, in_features: int,
-                   out_features: int) -> Tuple[int, Tuple[int, ...]]:
-    """Raw call: returns (kan_status, (rf, wk, nw, cs, sparse))."""
+                   out_features: int, shape=None) -> Tuple[int, Tuple[int, ...]]:
+    """Raw call: returns (kan_status, (rf, wk, nw, cs, sparse)); `shape` forces
+    a workgroup shape (see _shape_arg), None takes the library's choice."""
     plan = (ctypes.c_int32 * 5)()
     st = int(load_library().kan_layer_plan(ctypes.byref(grid), int(dtype), int(batch),
-                                           int(in_features), int(out_features), plan))
+                                           int(in_features), int(out_features),
+                                           _shape_arg(shape), plan))
     return st, tuple(int(v) for v in plan)
 
 
@@ -143,19 +170,19 @@ def kan_layer_pack(grid: kan_grid, dtype: int, in_features: int, out_features: i
                    base_w: int, packed: int, packed_bytes: int, stream: int = 0) -> int:
     """Raw call: device addresses as integers; returns the kan_status code."""
     return int(load_library().kan_layer_pack(
-        ctypes.byref(grid), int(dtype), int(in_features), int(out_features), ctypes.c_void_p(coef),
-        ctypes.c_void_p(base_w), ctypes.c_void_p(packed), ctypes.c_size_t(packed_bytes),
-        ctypes.c_void_p(stream)))
+        ctypes.byref(grid), int(dtype), int(in_features), int(out_features), _VP(coef),
+        _VP(base_w), _VP(packed), ctypes.c_size_t(packed_bytes), _VP(stream)))
 
 
 def kan_layer_forward_packed(grid: kan_grid, dtype: int, batch: int, in_features: int,
                              out_features: int, x: int, packed: int, packed_bytes: int, y: int,
-                             stream: int = 0) -> int:
-    """Raw call: device addresses as integers; returns the kan_status code."""
+                             stream: int = 0, shape=None) -> int:
+    """Raw call: device addresses as integers; returns the kan_status code.
+    `shape` forces a workgroup shape (see _shape_arg)."""
     return int(load_library().kan_layer_forward_packed(
         ctypes.byref(grid), int(dtype), int(batch), int(in_features), int(out_features),
-        ctypes.c_void_p(x), ctypes.c_void_p(packed), ctypes.c_size_t(packed_bytes),
-        ctypes.c_void_p(y), ctypes.c_void_p(stream)))
+        _VP(x), _VP(packed), ctypes.c_size_t(packed_bytes), _shape_arg(shape), _VP(y),
+        _VP(stream)))
 
 
 def check(status: int) -> None:
@@ -260,14 +287,19 @@ def pack_layer(coef, base_w, grid_size: int, grid_lo: float = -1.0, grid_hi: flo
         out = PackedLayer(buf, grid_size, grid_lo, grid_hi, n_in, n_out, coef.dtype)
     elif out.nbytes < nbytes or out.buf.device != coef.device:
         raise ValueError("packed buffer too small or on another device")
+    else:
+        # the buffer now holds these weights: its geometry follows them
+        out.grid_size, out.grid_lo, out.grid_hi = int(grid_size), float(grid_lo), float(grid_hi)
+        out.n_in, out.n_out, out.dtype = int(n_in), int(n_out), coef.dtype
     with torch.cuda.device(coef.device):
         check(kan_layer_pack(g, dt, n_in, n_out, coef.data_ptr(), base_w.data_ptr(),
                              out.buf.data_ptr(), out.nbytes, _stream(coef.device)))
     return out
 
 
-def layer_forward_packed(x, packed: PackedLayer, out=None):
-    """kan_layer_forward_packed: x [B, in] with packed weights -> y [B, out]."""
+def layer_forward_packed(x, packed: PackedLayer, out=None, shape=None):
+    """kan_layer_forward_packed: x [B, in] with packed weights -> y [B, out].
+    `shape` forces a workgroup shape (rf, wk[, nw[, cs]]) for tests and tuning."""
     torch = _torch()
     _require_device(x)
     if x.dim() != 2 or x.shape[1] != packed.n_in:
@@ -285,16 +317,17 @@ def layer_forward_packed(x, packed: PackedLayer, out=None):
     with torch.cuda.device(x.device):
         check(kan_layer_forward_packed(g, _dtype_code(x), B, packed.n_in, packed.n_out,
                                        x.data_ptr(), packed.buf.data_ptr(), packed.nbytes,
-                                       out.data_ptr(), _stream(x.device)))
+                                       out.data_ptr(), _stream(x.device), shape=shape))
     return out
 
 
 def layer_forward(x, coef, base_w, grid_size: int, grid_lo: float = -1.0, grid_hi: float = 1.0,
-                  out=None, packed: Optional[PackedLayer] = None):
+                  out=None, packed: Optional[PackedLayer] = None, shape=None):
     """One KAN layer: x [B, in], coef [out, in, G + 3], base_w [out, in] -> y
     [B, out], all of one dtype on one device.  Packs the weights (kan_layer_pack,
     into `packed` if given, else a fresh buffer) and runs
-    kan_layer_forward_packed, both on torch's current stream."""
+    kan_layer_forward_packed, both on torch's current stream; `shape` forces a
+    workgroup shape."""
     _require_device(x)
     n_in, _ = _check_weights(coef, base_w, grid_size)
     if x.dim() != 2 or x.shape[1] != n_in:
@@ -302,7 +335,7 @@ def layer_forward(x, coef, base_w, grid_size: int, grid_lo: float = -1.0, grid_h
     if coef.dtype != x.dtype:
         raise ValueError("x, coef and base_w must share one dtype")
     p = pack_layer(coef, base_w, grid_size, grid_lo, grid_hi, out=packed)
-    return layer_forward_packed(x, p, out=out)
+    return layer_forward_packed(x, p, out=out, shape=shape)
 
 
 def mlp_forward(x, layers: Sequence[Tuple[object, object]], grid_size: int, grid_lo: float = -1.0,

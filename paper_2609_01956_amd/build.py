@@ -1,5 +1,4 @@
-"""Build libkan.so (HIP kernels + C ABI) for gfx950 with hipcc, in-tree,
-and libkan_probe.so (the MFMA-rate probe used by ``bench.py --mfma-ceiling``).
+"""Build libkan.so (HIP kernels + C ABI) for gfx950 with hipcc, in-tree.
 
     python -m paper_2609_01956_amd.build
 
@@ -20,8 +19,6 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libkan.so")
 SOURCES = ["kan_api.cpp", "kan_basis.hip", "kan_layer.hip", "kan_layer_bf16.hip",
            "kan_layer_f32.hip"]
-PROBE_LIB = os.path.join(HERE, "libkan_probe.so")
-PROBE_SOURCES = ["probe_mfma.hip"]
 ARCH = "gfx950"
 
 
@@ -76,9 +73,7 @@ def _compile(sources, out: str, verbose: bool) -> str:
 
 
 def build(verbose: bool = False) -> str:
-    """Compile libkan.so (the product) and libkan_probe.so (the MFMA-rate probe
-    that bench.py --mfma-ceiling runs); returns the path of libkan.so."""
-    _compile(PROBE_SOURCES, PROBE_LIB, verbose)
+    """Compile libkan.so from source; returns its path."""
     return _compile(SOURCES, LIB, verbose)
 
 

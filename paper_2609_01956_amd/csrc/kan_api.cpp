@@ -96,6 +96,9 @@ static kan_status check_layer(const kan_grid* grid, kan_dtype dtype, int32_t in_
     if (st != KAN_OK) return st;
     if (in_features < 1 || out_features < 1) return KAN_ERR_INVALID_ARG;
     if ((int64_t)in_features * (gc->nb + 1) >= 0x80000000LL) return KAN_ERR_INVALID_ARG;
+    // The fused kernel addresses x as a per-workgroup base plus 32-bit element
+    // offsets over at most kan::kLayerMaxRows rows.
+    if ((int64_t)kan::kLayerMaxRows * in_features >= 0x100000000LL) return KAN_ERR_INVALID_ARG;
     if ((int64_t)out_features * in_features * gc->nb >= (1LL << 40)) return KAN_ERR_INVALID_ARG;
     if (!kan::layer_geom(gc->nb, dtype == KAN_BF16, in_features, out_features, geom))
         return KAN_ERR_INVALID_ARG;
@@ -135,22 +138,14 @@ kan_status kan_layer_pack(const kan_grid* grid, kan_dtype dtype, int32_t in_feat
                                           static_cast<hipStream_t>(stream)));
 }
 
-kan_status kan_layer_forward_packed(const kan_grid* grid, kan_dtype dtype, int64_t batch,
-                                    int32_t in_features, int32_t out_features, const void* x,
-                                    const void* packed, size_t packed_bytes, void* y,
-                                    void* stream) {
-    kan::GridConst gc;
-    kan::LayerGeom geom;
-    const kan_status st = check_layer(grid, dtype, in_features, out_features, &gc, &geom);
-    if (st != KAN_OK) return st;
-    if (batch < 0) return KAN_ERR_INVALID_ARG;
-    if (batch == 0) return KAN_OK;
+// Validates the arguments of a packed forward (after check_layer).
+static kan_status check_forward_packed(const kan::LayerGeom& geom, kan_dtype dtype, int64_t batch,
+                                       int32_t in_features, int32_t out_features, const void* x,
+                                       const void* packed, size_t packed_bytes, const void* y) {
     if (x == nullptr || packed == nullptr || y == nullptr) return KAN_ERR_INVALID_ARG;
     const size_t es = dtype_size(dtype);
     if (!aligned(x, es) || !aligned(y, es) || !aligned(packed, 16)) return KAN_ERR_INVALID_ARG;
     if (packed_bytes < geom.packed_bytes) return KAN_ERR_INVALID_ARG;
-    // Row tiles of at least 32 rows go in blockIdx.x.
-    if (batch > (int64_t)0x7fffffff * 32) return KAN_ERR_INVALID_ARG;
     const uint64_t ub = (uint64_t)batch;
     if (ub > SIZE_MAX / es / (uint64_t)in_features || ub > SIZE_MAX / es / (uint64_t)out_features)
         return KAN_ERR_INVALID_ARG;
@@ -158,7 +153,28 @@ kan_status kan_layer_forward_packed(const kan_grid* grid, kan_dtype dtype, int64
     const size_t y_bytes = ub * (size_t)out_features * es;
     if (overlap(y, y_bytes, x, x_bytes) || overlap(y, y_bytes, packed, geom.packed_bytes))
         return KAN_ERR_INVALID_ARG;
+    return KAN_OK;
+}
 
+// The shape a forward launches: the planner's, or a forced one that must be
+// valid for the layer.
+static kan_status layer_shape(const kan::LayerGeom& geom, kan_dtype dtype, int64_t batch,
+                              const int32_t* shape, kan::LayerCfg* cfg) {
+    if (shape == nullptr) {
+        *cfg = kan::plan_layer(geom, dtype == KAN_BF16, batch);
+        return KAN_OK;
+    }
+    const kan::LayerCfg c{shape[0], shape[1], shape[2], shape[3]};
+    if (!kan::layer_cfg_valid(geom, c)) return KAN_ERR_INVALID_ARG;
+    *cfg = c;
+    return KAN_OK;
+}
+
+// Enqueues the fused kernel (arguments already validated).
+static kan_status launch_forward(const kan::GridConst& gc, const kan::LayerGeom& geom,
+                                 const kan::LayerCfg& cfg, kan_dtype dtype, int64_t batch,
+                                 int32_t in_features, int32_t out_features, const void* x,
+                                 const void* packed, void* y, hipStream_t s) {
     kan::LayerArgs a;
     a.x = x;
     a.wp = packed;
@@ -170,26 +186,48 @@ kan_status kan_layer_forward_packed(const kan_grid* grid, kan_dtype dtype, int64
     a.nsb = geom.nsb;
     a.npairs = geom.npairs;
     a.nblk = geom.nblk;
+    a.nblk_pad = geom.nblk_pad;
     a.nchunks = 0;  // set by the launcher (depends on the tile shape)
     a.inv_h = gc.inv_h;
     a.a_int = gc.a_int;
     a.a_frac = gc.a_frac;
-    kan::LayerCfg cfg = kan::plan_layer(geom, dtype == KAN_BF16, batch);
-    kan::parse_layer_cfg_override(geom, &cfg);
-    return device_status(kan::launch_layer(dtype == KAN_BF16, geom, cfg, a,
-                                           static_cast<hipStream_t>(stream)));
+    return device_status(kan::launch_layer(dtype == KAN_BF16, geom, cfg, a, s));
+}
+
+kan_status kan_layer_forward_packed(const kan_grid* grid, kan_dtype dtype, int64_t batch,
+                                    int32_t in_features, int32_t out_features, const void* x,
+                                    const void* packed, size_t packed_bytes,
+                                    const int32_t* shape, void* y, void* stream) {
+    kan::GridConst gc;
+    kan::LayerGeom geom;
+    kan_status st = check_layer(grid, dtype, in_features, out_features, &gc, &geom);
+    if (st != KAN_OK) return st;
+    if (batch < 0) return KAN_ERR_INVALID_ARG;
+    // Row tiles of at least 32 rows go in blockIdx.x.
+    if (batch > (int64_t)0x7fffffff * 32) return KAN_ERR_INVALID_ARG;
+    kan::LayerCfg cfg;
+    st = layer_shape(geom, dtype, batch < 1 ? 1 : batch, shape, &cfg);
+    if (st != KAN_OK) return st;
+    if (batch == 0) return KAN_OK;
+    st = check_forward_packed(geom, dtype, batch, in_features, out_features, x, packed,
+                              packed_bytes, y);
+    if (st != KAN_OK) return st;
+    return launch_forward(gc, geom, cfg, dtype, batch, in_features, out_features, x, packed, y,
+                          static_cast<hipStream_t>(stream));
 }
 
 kan_status kan_layer_plan(const kan_grid* grid, kan_dtype dtype, int64_t batch,
-                          int32_t in_features, int32_t out_features, int32_t* plan) {
+                          int32_t in_features, int32_t out_features, const int32_t* shape,
+                          int32_t* plan) {
     if (plan == nullptr) return KAN_ERR_INVALID_ARG;
     kan::GridConst gc;
     kan::LayerGeom geom;
-    const kan_status st = check_layer(grid, dtype, in_features, out_features, &gc, &geom);
+    kan_status st = check_layer(grid, dtype, in_features, out_features, &gc, &geom);
     if (st != KAN_OK) return st;
     if (batch < 1 || batch > (int64_t)0x7fffffff * 32) return KAN_ERR_INVALID_ARG;
-    kan::LayerCfg cfg = kan::plan_layer(geom, dtype == KAN_BF16, batch);
-    kan::parse_layer_cfg_override(geom, &cfg);
+    kan::LayerCfg cfg;
+    st = layer_shape(geom, dtype, batch, shape, &cfg);
+    if (st != KAN_OK) return st;
     plan[0] = cfg.rf;
     plan[1] = cfg.wk;
     plan[2] = cfg.nw;
@@ -198,15 +236,23 @@ kan_status kan_layer_plan(const kan_grid* grid, kan_dtype dtype, int64_t batch,
     return KAN_OK;
 }
 
-kan_status kan_layer_forward(const kan_grid* grid, kan_dtype dtype, int64_t batch,
-                             int32_t in_features, int32_t out_features, const void* x,
-                             const void* coef, const void* base_w, void* y, void* stream) {
+kan_status kan_layer_forward_workspace_bytes(const kan_grid* grid, kan_dtype dtype,
+                                             int64_t batch, int32_t in_features,
+                                             int32_t out_features, size_t* bytes) {
+    if (bytes == nullptr) return KAN_ERR_INVALID_ARG;
     kan::GridConst gc;
     kan::LayerGeom geom;
     const kan_status st = check_layer(grid, dtype, in_features, out_features, &gc, &geom);
     if (st != KAN_OK) return st;
     if (batch < 0) return KAN_ERR_INVALID_ARG;
-    if (batch == 0) return KAN_OK;
+    *bytes = geom.packed_bytes;
+    return KAN_OK;
+}
+
+// Validates kan_layer_forward's tensors (after check_layer, batch > 0).
+static kan_status check_forward(const kan::GridConst& gc, kan_dtype dtype, int64_t batch,
+                                int32_t in_features, int32_t out_features, const void* x,
+                                const void* coef, const void* base_w, const void* y) {
     if (x == nullptr || coef == nullptr || base_w == nullptr || y == nullptr)
         return KAN_ERR_INVALID_ARG;
     const size_t es = dtype_size(dtype);
@@ -223,22 +269,36 @@ kan_status kan_layer_forward(const kan_grid* grid, kan_dtype dtype, int64_t batc
     if (overlap(y, y_bytes, x, x_bytes) || overlap(y, y_bytes, coef, c_bytes) ||
         overlap(y, y_bytes, base_w, w_bytes))
         return KAN_ERR_INVALID_ARG;
+    return KAN_OK;
+}
 
-    // Temporary packed weights from the stream-ordered pool: allocated and
-    // released in stream order, so the call stays asynchronous.
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    void* packed = nullptr;
-    if (hipMallocAsync(&packed, geom.packed_bytes, s) != hipSuccess) {
-        (void)hipGetLastError();
-        return KAN_ERR_DEVICE;
-    }
-    kan_status r = kan_layer_pack(grid, dtype, in_features, out_features, coef, base_w, packed,
-                                  geom.packed_bytes, stream);
-    if (r == KAN_OK)
-        r = kan_layer_forward_packed(grid, dtype, batch, in_features, out_features, x, packed,
-                                     geom.packed_bytes, y, stream);
-    if (hipFreeAsync(packed, s) != hipSuccess && r == KAN_OK) r = KAN_ERR_DEVICE;
-    return r;
+kan_status kan_layer_forward(const kan_grid* grid, kan_dtype dtype, int64_t batch,
+                             int32_t in_features, int32_t out_features, const void* x,
+                             const void* coef, const void* base_w, void* workspace,
+                             size_t workspace_bytes, void* y, void* stream) {
+    kan::GridConst gc;
+    kan::LayerGeom geom;
+    kan_status st = check_layer(grid, dtype, in_features, out_features, &gc, &geom);
+    if (st != KAN_OK) return st;
+    if (batch < 0) return KAN_ERR_INVALID_ARG;
+    if (batch == 0) return KAN_OK;
+    st = check_forward(gc, dtype, batch, in_features, out_features, x, coef, base_w, y);
+    if (st != KAN_OK) return st;
+    if (workspace == nullptr || !aligned(workspace, 16) || workspace_bytes < geom.packed_bytes)
+        return KAN_ERR_INVALID_ARG;
+    const size_t es = dtype_size(dtype);
+    const uint64_t ub = (uint64_t)batch;
+    const size_t ws = geom.packed_bytes;
+    if (overlap(workspace, ws, x, ub * (size_t)in_features * es) ||
+        overlap(workspace, ws, coef, (size_t)out_features * in_features * gc.nb * es) ||
+        overlap(workspace, ws, base_w, (size_t)out_features * in_features * es) ||
+        overlap(workspace, ws, y, ub * (size_t)out_features * es))
+        return KAN_ERR_INVALID_ARG;
+    st = kan_layer_pack(grid, dtype, in_features, out_features, coef, base_w, workspace, ws,
+                        stream);
+    if (st != KAN_OK) return st;
+    return kan_layer_forward_packed(grid, dtype, batch, in_features, out_features, x, workspace,
+                                    ws, nullptr, y, stream);
 }
 
 }  // extern "C"

@@ -92,6 +92,9 @@ struct LayerCfg {
     int nw;  // waves per workgroup: 4, or 8 (wk = 1, cs = 1; rf = 2 sparse only)
     int cs;  // column slices per N tile: 1, 2 or 4 (rf = 1, nw = 4 only)
 };
+// Most rows any workgroup shape covers (x is addressed per workgroup with
+// 32-bit element offsets, so kLayerMaxRows * in must stay below 2^32).
+constexpr int kLayerMaxRows = 256;
 // Rows per workgroup of a shape.
 inline int64_t layer_cfg_rows(const LayerCfg& c) {
     return 32LL * c.rf * (c.nw / c.wk) / (c.rf == 2 && c.nw == 8 ? 2 : 1);
@@ -126,9 +129,8 @@ inline bool layer_x_words(const void* x, int64_t batch, int in) {
     return reinterpret_cast<uintptr_t>(x) % 4 == 0 && (batch * (int64_t)in) % 2 == 0;
 }
 LayerCfg plan_layer(const LayerGeom& g, bool bf16, int64_t batch);
-// KAN_LAYER_CFG="rf,wk[,nw[,cs]]" forces a configuration (testing and tuning);
-// ignored when malformed or not valid for the geometry.
-bool parse_layer_cfg_override(const LayerGeom& g, LayerCfg* c);
+// Whether a shape (planned or forced by the caller) is instantiated and valid
+// for the geometry.
 bool layer_cfg_valid(const LayerGeom& g, const LayerCfg& c);
 
 struct LayerArgs {

@@ -3,8 +3,6 @@
 // kan_layer_kernel.h.
 #include "kan_layer_kernel.h"
 
-#include <cstdio>
-#include <cstdlib>
 
 namespace kan {
 
@@ -192,17 +190,6 @@ LayerCfg plan_layer(const LayerGeom& g, bool bf16, int64_t batch) {
         if (w >= 256) return c;
     }
     return best;  // the most workgroups any shape gives
-}
-
-bool parse_layer_cfg_override(const LayerGeom& g, LayerCfg* c) {
-    const char* s = std::getenv("KAN_LAYER_CFG");
-    if (!s || !*s) return false;
-    LayerCfg t{0, 0, 4, 1};
-    const int n = std::sscanf(s, "%d,%d,%d,%d", &t.rf, &t.wk, &t.nw, &t.cs);
-    if (n < 2) return false;
-    if (!layer_cfg_valid(g, t)) return false;
-    *c = t;
-    return true;
 }
 
 // ------------------------------------------------------------------ launches

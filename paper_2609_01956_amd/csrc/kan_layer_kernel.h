@@ -271,7 +271,7 @@ void layer_kernel(LayerArgs a) {
         static_cast<const char*>(a.wp) + (size_t)nt * (size_t)a.nblk_pad * BLKBL;
 
     // x is addressed as a per-workgroup base plus 32-bit element offsets (the
-    // workgroup's rows span far less than 2^31 elements).  Rows past the
+    // host rejects layers with kLayerMaxRows * in >= 2^32).  Rows past the
     // batch read row batch - 1 (their results are not stored).
     const int64_t wg_row0 = (int64_t)blockIdx.x * BM;
     const T* __restrict__ xw = x + wg_row0 * (int64_t)a.in;
@@ -960,6 +960,7 @@ hipError_t launch_cfg(const LayerGeom& g, LayerArgs a, hipStream_t s) {
     // Eight waves of two row tiles: the sparse shared-A shape (layer_shape_ok)
     constexpr bool XA = RF == 2 && NW == 8;
     constexpr int BM = 32 * RF * (NW / WK) / (XA ? 2 : 1);
+    static_assert(BM <= kLayerMaxRows, "rows per workgroup (32-bit x offsets)");
     a.nblk_pad = g.nblk_pad;
     a.nchunks = g.nblk_pad / g.kb;
     const dim3 grid((unsigned)((a.batch + BM - 1) / BM), (unsigned)(g.ntiles * (NFL / NF)));

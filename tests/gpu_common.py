@@ -1,5 +1,4 @@
 """Shared helpers for the GPU parity tests (test code only)."""
-import os
 import sys
 
 import numpy as np
@@ -37,15 +36,6 @@ def normwise(y: np.ndarray, ref: np.ndarray) -> float:
     if scale == 0.0:
         return float(np.max(np.abs(y)))
     return float(np.max(np.abs(y - ref))) / scale
-
-
-def set_layer_cfg(spec):
-    """Force the fused layer's workgroup shape ("rows tiles per wave, waves
-    splitting K"); None restores the library's own choice."""
-    if spec is None:
-        os.environ.pop("KAN_LAYER_CFG", None)
-    else:
-        os.environ["KAN_LAYER_CFG"] = spec
 
 
 F32_LAYER_TOL = 1e-5

@@ -31,7 +31,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_abi_version_and_status_strings():
-    assert kb.kan_abi_version() == 2
+    assert kb.kan_abi_version() == 3
     for code in range(4):
         s = kb.kan_status_string(code)
         assert s.startswith(["KAN_OK", "KAN_ERR_INVALID_ARG", "KAN_ERR_UNSUPPORTED", "KAN_ERR_DEVICE"][code])
@@ -41,6 +41,7 @@ def test_abi_version_and_status_strings():
 # Fake, well-aligned, non-overlapping addresses: validation must reject every
 # case below on the host, so these are never dereferenced.
 X, PHI, C, W, Y = 0x100000, 0x200000000, 0x300000000, 0x400000000, 0x500000000
+WS, WSB = 0x700000000, 1 << 30  # a workspace large enough for every layer below
 
 
 @pytest.mark.parametrize("grid,code", [
@@ -57,13 +58,13 @@ X, PHI, C, W, Y = 0x100000, 0x200000000, 0x300000000, 0x400000000, 0x500000000
 ])
 def test_bad_grid(grid, code):
     assert kb.kan_basis_eval(grid, kb.KAN_F32, X, 16, PHI) == code
-    assert kb.kan_layer_forward(grid, kb.KAN_F32, 16, 4, 4, X, C, W, Y) == code
+    assert kb.kan_layer_forward(grid, kb.KAN_F32, 16, 4, 4, X, C, W, WS, WSB, Y) == code
 
 
 def test_null_grid_and_bad_dtype():
     lib = kb.load_library()
     assert lib.kan_basis_eval(None, 0, X, 16, PHI, None) == kb.KAN_ERR_INVALID_ARG
-    assert lib.kan_layer_forward(None, 0, 16, 4, 4, X, C, W, Y, None) == kb.KAN_ERR_INVALID_ARG
+    assert lib.kan_layer_forward(None, 0, 16, 4, 4, X, C, W, WS, WSB, Y, None) == kb.KAN_ERR_INVALID_ARG
     g = kb.make_grid(5)
     assert kb.kan_basis_eval(g, 2, X, 16, PHI) == kb.KAN_ERR_UNSUPPORTED
     assert kb.kan_basis_eval(g, -1, X, 16, PHI) == kb.KAN_ERR_UNSUPPORTED
@@ -92,22 +93,37 @@ def test_layer_argument_checks():
     g = kb.make_grid(10)
     f32 = kb.KAN_F32
     bad = kb.KAN_ERR_INVALID_ARG
-    assert kb.kan_layer_forward(g, f32, -1, 4, 4, X, C, W, Y) == bad
-    assert kb.kan_layer_forward(g, f32, 16, 0, 4, X, C, W, Y) == bad
-    assert kb.kan_layer_forward(g, f32, 16, 4, 0, X, C, W, Y) == bad
-    assert kb.kan_layer_forward(g, f32, 16, 2 ** 30, 4, X, C, W, Y) == bad  # in * (G + 4) >= 2^31
-    assert kb.kan_layer_forward(g, f32, 16, 4, 4, 0, C, W, Y) == bad
-    assert kb.kan_layer_forward(g, f32, 16, 4, 4, X, 0, W, Y) == bad
-    assert kb.kan_layer_forward(g, f32, 16, 4, 4, X, C, 0, Y) == bad
-    assert kb.kan_layer_forward(g, f32, 16, 4, 4, X, C, W, 0) == bad
-    assert kb.kan_layer_forward(g, f32, 16, 4, 4, X, C + 2, W, Y) == bad
-    assert kb.kan_layer_forward(g, f32, 16, 4, 4, X, C, W, Y + 2) == bad
+    assert kb.kan_layer_forward(g, f32, -1, 4, 4, X, C, W, WS, WSB, Y) == bad
+    assert kb.kan_layer_forward(g, f32, 16, 0, 4, X, C, W, WS, WSB, Y) == bad
+    assert kb.kan_layer_forward(g, f32, 16, 4, 0, X, C, W, WS, WSB, Y) == bad
+    assert kb.kan_layer_forward(g, f32, 16, 2 ** 30, 4, X, C, W, WS, WSB, Y) == bad  # in * (G + 4) >= 2^31
+    assert kb.kan_layer_forward(g, f32, 16, 4, 4, 0, C, W, WS, WSB, Y) == bad
+    assert kb.kan_layer_forward(g, f32, 16, 4, 4, X, 0, W, WS, WSB, Y) == bad
+    assert kb.kan_layer_forward(g, f32, 16, 4, 4, X, C, 0, WS, WSB, Y) == bad
+    assert kb.kan_layer_forward(g, f32, 16, 4, 4, X, C, W, WS, WSB, 0) == bad
+    assert kb.kan_layer_forward(g, f32, 16, 4, 4, X, C + 2, W, WS, WSB, Y) == bad
+    assert kb.kan_layer_forward(g, f32, 16, 4, 4, X, C, W, WS, WSB, Y + 2) == bad
     # y overlapping each input
-    assert kb.kan_layer_forward(g, f32, 16, 4, 4, X, C, W, X + 8) == bad
-    assert kb.kan_layer_forward(g, f32, 16, 4, 4, X, C, W, C + 8) == bad
-    assert kb.kan_layer_forward(g, f32, 16, 4, 4, X, C, W, W) == bad
+    assert kb.kan_layer_forward(g, f32, 16, 4, 4, X, C, W, WS, WSB, X + 8) == bad
+    assert kb.kan_layer_forward(g, f32, 16, 4, 4, X, C, W, WS, WSB, C + 8) == bad
+    assert kb.kan_layer_forward(g, f32, 16, 4, 4, X, C, W, WS, WSB, W) == bad
+    # x offsets of a workgroup are 32-bit: 256 rows x in must stay below 2^32
+    g1 = kb.make_grid(1)
+    assert kb.kan_layer_forward(g1, f32, 16, 2 ** 24, 1, X, C, W, WS, WSB, Y) == bad
+    assert kb.kan_layer_forward_packed(g1, f32, 16, 2 ** 24, 1, X, C, WSB, Y) == bad
+    assert kb.kan_layer_plan(g1, f32, 16, 2 ** 24, 1)[0] == bad
+    assert kb.kan_layer_packed_bytes(g1, f32, 2 ** 24, 1)[0] == bad
+    assert kb.kan_layer_packed_bytes(g1, f32, 2 ** 24 - 1, 1)[0] == kb.KAN_OK
+    # workspace: null, misaligned (16 bytes), short, overlapping any tensor
+    need = kb.kan_layer_forward_workspace_bytes(g, f32, 16, 4, 4)[1]
+    assert need == kb.kan_layer_packed_bytes(g, f32, 4, 4)[1]
+    assert kb.kan_layer_forward(g, f32, 16, 4, 4, X, C, W, 0, need, Y) == bad
+    assert kb.kan_layer_forward(g, f32, 16, 4, 4, X, C, W, WS + 8, need, Y) == bad
+    assert kb.kan_layer_forward(g, f32, 16, 4, 4, X, C, W, WS, need - 1, Y) == bad
+    for p in (X, C, W, Y):
+        assert kb.kan_layer_forward(g, f32, 16, 4, 4, X, C, W, p - 16, need, Y) == bad
     # empty batch: OK without launching
-    assert kb.kan_layer_forward(g, f32, 0, 4, 4, 0, 0, 0, 0) == kb.KAN_OK
+    assert kb.kan_layer_forward(g, f32, 0, 4, 4, 0, 0, 0, 0, 0, 0) == kb.KAN_OK
 
 
 def _expected_packed_bytes(G, bf16, n_in, n_out):
@@ -139,6 +155,21 @@ def test_packed_bytes(G, n_in, n_out, bf16):
     # 784 -> 256, G = 10 in bf16: 392 pairs x 2 blocks x 8 KiB
     if (G, n_in, n_out, bf16) == (10, 784, 256, True):
         assert n == 392 * 2 * 8192
+
+
+def test_workspace_bytes_checks():
+    g = kb.make_grid(10)
+    bad = kb.KAN_ERR_INVALID_ARG
+    lib = kb.load_library()
+    assert lib.kan_layer_forward_workspace_bytes(ctypes.byref(g), 0, 16, 4, 4, None) == bad
+    assert kb.kan_layer_forward_workspace_bytes(g, kb.KAN_F32, -1, 4, 4)[0] == bad
+    assert kb.kan_layer_forward_workspace_bytes(g, kb.KAN_F32, 16, 0, 4)[0] == bad
+    assert kb.kan_layer_forward_workspace_bytes(kb.make_grid(10, spline_order=2), kb.KAN_F32,
+                                                16, 4, 4)[0] == kb.KAN_ERR_UNSUPPORTED
+    # the packed weights, whatever the batch
+    for B in (0, 1, 65536):
+        st, n = kb.kan_layer_forward_workspace_bytes(g, kb.KAN_BF16, B, 784, 256)
+        assert st == kb.KAN_OK and n == 392 * 2 * 8192
 
 
 def test_packed_entry_point_checks():

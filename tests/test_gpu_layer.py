@@ -8,8 +8,8 @@ import pytest
 import oracle
 from paper_2609_01956_amd import binding as kb
 from paper_2609_01956_amd import workloads as wl
-from gpu_common import (BF16_LAYER_TOL, F32_LAYER_TOL, device, normwise, say, set_layer_cfg,
-                        to_dev, to_host64, torch)
+from gpu_common import (BF16_LAYER_TOL, F32_LAYER_TOL, device, normwise, say, to_dev,
+                        to_host64, torch)
 
 pytestmark = pytest.mark.gpu
 
@@ -32,9 +32,9 @@ def _inputs(B, n_in, n_out, G, seed, off=0.0, dtype_name="f32"):
     return x, C, Wb
 
 
-def _gpu_layer(x, C, Wb, G, dtype_name):
+def _gpu_layer(x, C, Wb, G, dtype_name, shape=None):
     dt = _dtype(dtype_name)
-    y = kb.layer_forward(to_dev(x, dt), to_dev(C, dt), to_dev(Wb, dt), G)
+    y = kb.layer_forward(to_dev(x, dt), to_dev(C, dt), to_dev(Wb, dt), G, shape=shape)
     torch.cuda.synchronize()
     return to_host64(y)
 
@@ -90,11 +90,7 @@ def test_layer_every_workgroup_shape(cfg, dtype_name, G):
     if dtype_name == "bf16":
         ref = oracle.round_bf16(ref)
     say(f"layer cfg={cfg} {dtype_name}")
-    set_layer_cfg(cfg)
-    try:
-        y = _gpu_layer(x, C, Wb, G, dtype_name)
-    finally:
-        set_layer_cfg(None)
+    y = _gpu_layer(x, C, Wb, G, dtype_name, shape=cfg)
     assert normwise(y, ref) <= _tol(dtype_name)
 
 
@@ -143,11 +139,7 @@ def test_layer_wide_tiles(dtype_name, B, n_in, n_out, G, cfg):
     if dtype_name == "bf16":
         ref = oracle.round_bf16(ref)
     say(f"layer wide {dtype_name} B={B} in={n_in} out={n_out} G={G} cfg={cfg}")
-    set_layer_cfg(cfg)
-    try:
-        y = _gpu_layer(x, C, Wb, G, dtype_name)
-    finally:
-        set_layer_cfg(None)
+    y = _gpu_layer(x, C, Wb, G, dtype_name, shape=cfg)
     assert normwise(y, ref) <= _tol(dtype_name)
 
 
@@ -175,11 +167,7 @@ def test_layer_bf16_sparse_mfma_256_column_shapes(cfg):
     x, C, Wb = _inputs(B, n_in, n_out, G, seed=5, off=0.2, dtype_name="bf16")
     ref = oracle.round_bf16(oracle.layer(x, C, Wb, G))
     say(f"layer bf16 sparse 256 columns cfg={cfg}")
-    set_layer_cfg(cfg)
-    try:
-        y = _gpu_layer(x, C, Wb, G, "bf16")
-    finally:
-        set_layer_cfg(None)
+    y = _gpu_layer(x, C, Wb, G, "bf16", shape=cfg)
     assert normwise(y, ref) <= BF16_LAYER_TOL, normwise(y, ref)
 
 
@@ -204,11 +192,7 @@ def test_layer_bf16_sparse_k_split(B, n_in, n_out, G, cfg):
     x, C, Wb = _inputs(B, n_in, n_out, G, seed=B + n_in + G, off=0.2, dtype_name="bf16")
     ref = oracle.round_bf16(oracle.layer(x, C, Wb, G))
     say(f"layer bf16 sparse K split B={B} in={n_in} out={n_out} G={G} cfg={cfg}")
-    set_layer_cfg(cfg)
-    try:
-        y = _gpu_layer(x, C, Wb, G, "bf16")
-    finally:
-        set_layer_cfg(None)
+    y = _gpu_layer(x, C, Wb, G, "bf16", shape=cfg)
     assert normwise(y, ref) <= BF16_LAYER_TOL, normwise(y, ref)
 
 
@@ -245,37 +229,42 @@ def test_layer_bf16_x_word_reads_and_their_fallbacks(case, cfg):
     else:
         xd = to_dev(x, dt)
     say(f"layer bf16 x reads {case} cfg={cfg}")
-    set_layer_cfg(cfg)
-    try:
-        y = kb.layer_forward(xd, to_dev(C, dt), to_dev(Wb, dt), G)
-        torch.cuda.synchronize()
-    finally:
-        set_layer_cfg(None)
+    y = kb.layer_forward(xd, to_dev(C, dt), to_dev(Wb, dt), G, shape=cfg)
+    torch.cuda.synchronize()
     assert normwise(to_host64(y), ref) <= BF16_LAYER_TOL
 
 
 @pytest.mark.parametrize("dtype_name", ["f32", "bf16"])
-def test_c_layer_forward_allocating_entry_point(dtype_name):
-    """kan_layer_forward (packs into a stream-ordered temporary) called through
-    the raw C entry point gives the same bits as pack + forward_packed."""
-    B, n_in, n_out, G = 513, 31, 70, 10
-    x, C, Wb = _inputs(B, n_in, n_out, G, seed=9, off=0.1, dtype_name=dtype_name)
-    dt = _dtype(dtype_name)
-    xt, Ct, Wt = to_dev(x, dt), to_dev(C, dt), to_dev(Wb, dt)
-    y = torch.empty((B, n_out), dtype=dt, device=device())
+def test_c_layer_forward_workspace_entry_point(dtype_name):
+    """kan_layer_forward (packs into the caller's workspace, then the packed
+    forward) called through the raw C entry point gives the same bits as pack +
+    forward_packed, and a second call reusing the workspace for a smaller
+    layer is right too."""
     code = kb.KAN_F32 if dtype_name == "f32" else kb.KAN_BF16
-    say(f"layer C entry point {dtype_name}")
-    st = kb.kan_layer_forward(kb.make_grid(G), code, B, n_in, n_out, xt.data_ptr(), Ct.data_ptr(),
-                              Wt.data_ptr(), y.data_ptr(),
-                              int(torch.cuda.current_stream().cuda_stream))
-    assert st == kb.KAN_OK
-    y2 = kb.layer_forward(xt, Ct, Wt, G)
-    torch.cuda.synchronize()
-    assert torch.equal(y, y2)
-    ref = oracle.layer(x, C, Wb, G)
-    if dtype_name == "bf16":
-        ref = oracle.round_bf16(ref)
-    assert normwise(to_host64(y), ref) <= _tol(dtype_name)
+    dt = _dtype(dtype_name)
+    stream = int(torch.cuda.current_stream().cuda_stream)
+    ws = None
+    for B, n_in, n_out, G in [(513, 31, 70, 10), (77, 9, 20, 5)]:
+        x, C, Wb = _inputs(B, n_in, n_out, G, seed=9, off=0.1, dtype_name=dtype_name)
+        xt, Ct, Wt = to_dev(x, dt), to_dev(C, dt), to_dev(Wb, dt)
+        y = torch.empty((B, n_out), dtype=dt, device=device())
+        st, need = kb.kan_layer_forward_workspace_bytes(kb.make_grid(G), code, B, n_in, n_out)
+        assert st == kb.KAN_OK and need > 0
+        if ws is None:
+            ws = torch.empty(need, dtype=torch.uint8, device=device())
+        assert ws.numel() >= need
+        say(f"layer C entry point {dtype_name} B={B} in={n_in} out={n_out} G={G}")
+        st = kb.kan_layer_forward(kb.make_grid(G), code, B, n_in, n_out, xt.data_ptr(),
+                                  Ct.data_ptr(), Wt.data_ptr(), ws.data_ptr(), ws.numel(),
+                                  y.data_ptr(), stream)
+        assert st == kb.KAN_OK
+        y2 = kb.layer_forward(xt, Ct, Wt, G)
+        torch.cuda.synchronize()
+        assert torch.equal(y, y2)
+        ref = oracle.layer(x, C, Wb, G)
+        if dtype_name == "bf16":
+            ref = oracle.round_bf16(ref)
+        assert normwise(to_host64(y), ref) <= _tol(dtype_name)
 
 
 def test_packed_weights_reused_across_batches():
@@ -344,11 +333,7 @@ def test_layer_bf16_sparse_nan_row(n_out, cfg):
     x, C, Wb = _inputs(B, n_in, n_out, G, seed=9, off=0.2, dtype_name="bf16")
     x[17, 3] = np.nan
     say(f"layer bf16 sparse nan row out={n_out} cfg={cfg}")
-    set_layer_cfg(cfg)
-    try:
-        y = _gpu_layer(x, C, Wb, G, "bf16")
-    finally:
-        set_layer_cfg(None)
+    y = _gpu_layer(x, C, Wb, G, "bf16", shape=cfg)
     assert np.all(np.isnan(y[17]))
     ok = np.ones(B, bool)
     ok[17] = False

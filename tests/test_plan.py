@@ -1,8 +1,8 @@
 """Host-side shape planning of the fused layer through kan_layer_plan (no GPU):
 the shapes chosen for the layers of the 784-256-256-10 MLP, which grids run
 on the structured-sparse matrix instruction, that every shape the GPU parity
-tests force is the one that runs (an invalid KAN_LAYER_CFG would silently
-fall back to the library's choice), and argument checks."""
+tests force is valid and is the one that runs, that invalid forced shapes are
+rejected, and argument checks."""
 import pytest
 
 from paper_2609_01956_amd import binding as kb
@@ -12,14 +12,15 @@ import test_gpu_layer as gl
 DT = {"f32": kb.KAN_F32, "bf16": kb.KAN_BF16}
 
 
-def _plan(monkeypatch, G, dtype_name, B, n_in, n_out, cfg=None):
-    if cfg is None:
-        monkeypatch.delenv("KAN_LAYER_CFG", raising=False)
-    else:
-        monkeypatch.setenv("KAN_LAYER_CFG", cfg)
-    st, plan = kb.kan_layer_plan(kb.make_grid(G), DT[dtype_name], B, n_in, n_out)
+def _plan(G, dtype_name, B, n_in, n_out, cfg=None):
+    st, plan = kb.kan_layer_plan(kb.make_grid(G), DT[dtype_name], B, n_in, n_out, cfg)
     assert st == kb.KAN_OK
     return plan
+
+
+def _rejected(G, dtype_name, B, n_in, n_out, cfg):
+    st, _ = kb.kan_layer_plan(kb.make_grid(G), DT[dtype_name], B, n_in, n_out, cfg)
+    return st == kb.KAN_ERR_INVALID_ARG
 
 
 def _shape(cfg):
@@ -39,8 +40,8 @@ def _shape(cfg):
     ("f32", 256, 256, (2, 1, 4, 1, 0)),
     ("f32", 256, 10, (1, 2, 4, 1, 0)),
 ])
-def test_mlp_layers_planned_shapes(monkeypatch, dtype_name, n_in, n_out, want):
-    assert _plan(monkeypatch, 10, dtype_name, 65536, n_in, n_out) == want
+def test_mlp_layers_planned_shapes(dtype_name, n_in, n_out, want):
+    assert _plan(10, dtype_name, 65536, n_in, n_out) == want
 
 
 @pytest.mark.parametrize("B,n_out,want", [
@@ -52,41 +53,43 @@ def test_mlp_layers_planned_shapes(monkeypatch, dtype_name, n_in, n_out, want):
     # four fragments: no K split on the sparse layout's wider tiles
     (65536, 100, (1, 1, 8, 1, 1)),
 ])
-def test_narrow_sparse_layers_planned_shapes(monkeypatch, B, n_out, want):
-    assert _plan(monkeypatch, 10, "bf16", B, 256, n_out) == want
+def test_narrow_sparse_layers_planned_shapes(B, n_out, want):
+    assert _plan(10, "bf16", B, 256, n_out) == want
 
 
 @pytest.mark.parametrize("G,sparse", [(1, 0), (4, 0), (5, 1), (10, 1), (12, 1), (13, 0),
                                       (200, 0)])
-def test_sparse_instruction_for_two_blocks_per_feature(monkeypatch, G, sparse):
+def test_sparse_instruction_for_two_blocks_per_feature(G, sparse):
     # bf16 blocks hold 8 of a feature's G + 4 columns: two blocks for 5..12
-    assert _plan(monkeypatch, G, "bf16", 4096, 64, 64)[4] == sparse
-    assert _plan(monkeypatch, G, "f32", 4096, 64, 64)[4] == 0
+    assert _plan(G, "bf16", 4096, 64, 64)[4] == sparse
+    assert _plan(G, "f32", 4096, 64, 64)[4] == 0
 
 
-def test_shared_a_shape_only_on_sparse_256_column_tiles(monkeypatch):
-    assert _plan(monkeypatch, 10, "bf16", 65536, 784, 256, "2,1,8") == (2, 1, 8, 1, 1)
-    # dense bf16, fp32 and narrower sparse tiles keep the library's choice
+def test_shared_a_shape_only_on_sparse_256_column_tiles():
+    assert _plan(10, "bf16", 65536, 784, 256, "2,1,8") == (2, 1, 8, 1, 1)
+    # dense bf16, fp32 and narrower sparse tiles reject it
     for G, dt, n_out in [(20, "bf16", 256), (10, "f32", 256), (10, "bf16", 45)]:
-        own = _plan(monkeypatch, G, dt, 65536, 784, n_out)
-        assert _plan(monkeypatch, G, dt, 65536, 784, n_out, "2,1,8") == own
+        assert _rejected(G, dt, 65536, 784, n_out, "2,1,8")
 
 
-def test_sparse_k_split_only_on_narrow_tiles(monkeypatch):
+def test_sparse_k_split_only_on_narrow_tiles():
     # waves splitting K on the sparse layout: tiles of one or two fragments;
     # eight-wave K splits are not shapes of the dense kernel
-    assert _plan(monkeypatch, 10, "bf16", 65536, 256, 10, "1,4,8") == (1, 4, 8, 1, 1)
-    assert _plan(monkeypatch, 10, "bf16", 65536, 256, 64, "1,2") == (1, 2, 4, 1, 1)
+    assert _plan(10, "bf16", 65536, 256, 10, "1,4,8") == (1, 4, 8, 1, 1)
+    assert _plan(10, "bf16", 65536, 256, 64, "1,2") == (1, 2, 4, 1, 1)
     for G, dt, n_out, cfg in [(10, "bf16", 256, "1,2"), (10, "bf16", 100, "1,4"),
                               (20, "bf16", 10, "1,4,8"), (10, "f32", 10, "1,2,8")]:
-        own = _plan(monkeypatch, G, dt, 65536, 256, n_out)
-        assert _plan(monkeypatch, G, dt, 65536, 256, n_out, cfg) == own
+        assert _rejected(G, dt, 65536, 256, n_out, cfg)
 
 
-def test_malformed_override_is_ignored(monkeypatch):
-    own = _plan(monkeypatch, 10, "bf16", 65536, 784, 256)
-    for cfg in ["", "x", "3", "3,1", "1,3", "1,1,6", "1,1,4,3", "1,2,8"]:
-        assert _plan(monkeypatch, 10, "bf16", 65536, 784, 256, cfg) == own
+@pytest.mark.parametrize("cfg", ["3,1", "1,3", "1,1,6", "1,1,4,3", "0,1", "1,2,8"])
+def test_invalid_forced_shape_is_rejected(cfg):
+    assert _rejected(10, "bf16", 65536, 784, 256, cfg)
+    g = kb.make_grid(10)
+    # the forward rejects it on the host too (fake addresses are never touched)
+    st, need = kb.kan_layer_packed_bytes(g, kb.KAN_BF16, 784, 256)
+    assert kb.kan_layer_forward_packed(g, kb.KAN_BF16, 16, 784, 256, 0x100000, 0x200000000,
+                                       need, 0x400000000, shape=cfg) == kb.KAN_ERR_INVALID_ARG
 
 
 def _forced_cases():
@@ -108,9 +111,9 @@ def _forced_cases():
 
 
 @pytest.mark.parametrize("dtype_name,G,B,n_in,n_out,cfg", list(_forced_cases()))
-def test_every_shape_the_gpu_tests_force_is_the_one_that_runs(monkeypatch, dtype_name, G, B,
+def test_every_shape_the_gpu_tests_force_is_the_one_that_runs(dtype_name, G, B,
                                                               n_in, n_out, cfg):
-    assert _plan(monkeypatch, G, dtype_name, B, n_in, n_out, cfg)[:4] == _shape(cfg)
+    assert _plan(G, dtype_name, B, n_in, n_out, cfg)[:4] == _shape(cfg)
 
 
 def test_plan_argument_checks():
@@ -122,5 +125,5 @@ def test_plan_argument_checks():
     assert kb.kan_layer_plan(g, kb.KAN_BF16, 16, 4, 0)[0] == bad
     assert kb.kan_layer_plan(g, 2, 16, 4, 4)[0] == kb.KAN_ERR_UNSUPPORTED
     lib = kb.load_library()
-    assert lib.kan_layer_plan(None, 0, 16, 4, 4, None) == bad
-    assert lib.kan_layer_plan(g, 0, 16, 4, 4, None) == bad
+    assert lib.kan_layer_plan(None, 0, 16, 4, 4, None, None) == bad
+    assert lib.kan_layer_plan(g, 0, 16, 4, 4, None, None) == bad
