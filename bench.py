@@ -10,8 +10,10 @@ Inputs and weights are resident in HBM before timing starts; every launch goes
 through the C ABI onto torch's current stream.
 
 Prints ONE JSON line: samples/s (value), Gbasis/s, the roofline of the
-dominant kernel (per-kernel durations from HIP events on the launch stream)
-and the float64 CPU oracle timed on a bounded row sample of the same step.
+dominant kernel (per-kernel durations from HIP events on the launch stream),
+per-layer parity of the run's output against the float64 oracle, the same
+step in the other dtype (bf16 and fp32 are both measured) and the float64
+CPU oracle timed on a bounded row sample of the same step.
 
     python bench.py [--steps K] [--warmup W] [--dtype bf16|f32]
 """
@@ -32,17 +34,22 @@ METRIC = "KAN layer fwd samples/s + Gbasis/s; % of HBM / MFMA peak on MI355X"
 # MI355X published peaks
 PEAK_HBM_GBS = 8000.0
 PEAK_TFLOPS = {"bf16": 2516.6, "f32": 157.3}
-# Plain (non-packed) fp32 VALU in G lane-ops/s: the published 157.3 TFLOP/s
-# fp32 vector rate counts an fma as two flops, i.e. 256 CUs x 4 SIMDs x 32
-# lanes x 2.4 GHz (bench.py --valu-ceiling measures ~28 fma lanes per clock
-# per SIMD with two or more waves on it).  And the least VALU work the basis
-# and SiLU values of one (row, input feature) take, in lane-ops: of the G + 3
-# basis columns at most four consecutive ones are nonzero, each 7 ops in the
-# truncated power form (v 1, P and Q 2 clamped fmas, P^2, Q^2, Q^3 3, the
-# final fma 1); the coordinate and the interval 4 (fma, add, floor, fraction);
-# SiLU 4 (exp, fma, reciprocal, multiply); in bf16 2 packed conversions.
+# VALU peak in G lane-ops/s: MI355X's 256 CUs x 4 SIMDs x 32 fp32 lanes x
+# 2.4 GHz = 78.6 T lane-ops/s, the published 157.3 TFLOP/s fp32 vector rate
+# with an fma counted as one lane-op (two flops).  Two counts of the VALU work
+# of one (row, input feature) are reported against it:
+#  * the least the kernels do (the headline "alu" figure): of the G + 3 basis
+#    columns at most four consecutive ones are nonzero, each 7 lane-ops in the
+#    truncated power form (v 1, P and Q 2 clamped fmas, P^2, Q^2, Q^3 3, the
+#    final fma 1); the coordinate and the interval 4 (fma, add, floor,
+#    fraction); SiLU 4 (exp, fma, reciprocal, multiply); in bf16 2 packed
+#    conversions;
+#  * the dense count of the method (every one of the G + 3 values evaluated,
+#    no span lookup): 10 lane-ops per basis value (coordinate, clamp and the
+#    two-term form) plus the SiLU's 4.
 PEAK_VALU_GOPS = 256 * 4 * 32 * 2.4
 VALU_OPS_PER_FEATURE = {"bf16": 38.0, "f32": 36.0}
+VALU_OPS_PER_VALUE_DENSE = 10.0
 
 
 def parse():
@@ -51,8 +58,8 @@ def parse():
     p.add_argument("--steps", type=int, default=20)
     p.add_argument("--warmup", type=int, default=5)
     p.add_argument("--dtype", choices=["bf16", "f32"], default="bf16")
-    p.add_argument("--cpu-seconds", type=float, default=10.0,
-                   help="target wall time of the CPU oracle sample")
+    p.add_argument("--cpu-seconds", type=float, default=12.0,
+                   help="target wall time of the CPU oracle sample (three runs)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--configs", action="store_true",
                    help="only time the fused layer and the basis kernel on every configured "
@@ -90,6 +97,7 @@ def layer_roofline(dtype: str, batch: int, n_in: int, n_out: int, nb: int) -> di
         k = {"bound": "mfma", "unit": "TFLOP/s", "peak": PEAK_TFLOPS[dtype],
              "algorithmic": flop / 1e12}  # dense TFLOP
     k["valu_gops"] = valu / 1e9
+    k["valu_gops_dense"] = (VALU_OPS_PER_VALUE_DENSE * nb + 4.0) * batch * n_in / 1e9
     return k
 
 
@@ -182,6 +190,7 @@ def configs_sweep(dtype: str) -> None:
             lus = _time_us(lambda: kb.layer_forward_packed(h, pk, out=out))
             k = layer_roofline(dtype, B, C.shape[1], C.shape[0], nb)
             k.pop("valu_gops")
+            k.pop("valu_gops_dense")
             k.update(us=lus, samples_per_s=B / lus * 1e6, achieved=k["algorithmic"] / (lus * 1e-6))
             k["frac"] = k["achieved"] / k["peak"]
             layers.append({"in": C.shape[1], "out": C.shape[0], **k})
@@ -190,8 +199,11 @@ def configs_sweep(dtype: str) -> None:
         print(json.dumps(line), flush=True)
 
 
-def cpu_baseline(W, n_layers_shapes, target_s: float):
-    """The float64 oracle, untuned, on a row sample of the same step."""
+def cpu_baseline(W, target_s: float):
+    """The float64 oracle, untuned, on a row sample of the same step: the
+    basis of the input and the 3-layer forward of its first rows.  One
+    64-row warm-up sizes the sample so that one run takes about target_s / 3;
+    three runs follow and their median is reported (cost is linear in rows)."""
     import numpy as np
     import oracle
 
@@ -209,48 +221,38 @@ def cpu_baseline(W, n_layers_shapes, target_s: float):
     t0 = time.perf_counter()
     step(64)
     dt64 = time.perf_counter() - t0
-    rows = int(max(64, min(x.shape[0], 64 * target_s / max(dt64, 1e-6))))
-    t0 = time.perf_counter()
-    step(rows)
-    dt = time.perf_counter() - t0
+    rows = int(max(64, min(x.shape[0], 64 * (target_s / 3.0) / max(dt64, 1e-6))))
+    runs = []
+    for _ in range(3):
+        t0 = time.perf_counter()
+        step(rows)
+        runs.append(time.perf_counter() - t0)
+    dt = float(np.median(runs))
     return {"value": rows / dt, "unit": "samples/s", "cores": threads, "kind": "oracle",
             "sample": f"first {rows} rows of the {x.shape[0]}-row batch: float64 basis of the "
-                      f"input + 3-layer forward, {dt:.1f} s wall on {threads} threads"}
+                      f"input + 3-layer forward; median of 3 runs ({', '.join(f'{r:.2f}' for r in runs)} s) "
+                      f"after a 64-row warm-up, on {threads} threads"}
 
 
-def main() -> int:
-    args = parse()
-    if args.gpus != 1:
-        print(f"bench.py measures one GPU; --gpus {args.gpus} is not run (rows are "
-              "independent: the batch would shard across GPUs with the weights replicated "
-              "and no communication inside a layer)", file=sys.stderr)
-        return 2
+def measure_step(dtype: str, W, steps: int, warmup: int) -> dict:
+    """Times `steps` steps of the hot path in `dtype` (after `warmup` untimed
+    ones) with a HIP event between consecutive kernels on torch's current
+    stream, the stream every kernel is launched on.  Returns the step time,
+    per-kernel averages and rooflines, and the outputs of the last step."""
     import numpy as np
     import torch
 
     from paper_2609_01956_amd import binding as kb
     from paper_2609_01956_amd import workloads as wl
 
-    if not torch.cuda.is_available():
-        print("bench.py needs a GPU", file=sys.stderr)
-        return 1
-    if args.copy_calibration:
-        copy_calibration(args.copy_calibration)
-        return 0
-    if args.configs:
-        configs_sweep(args.dtype)
-        return 0
-    kb.load_library()
     dev = torch.device("cuda:0")
-    tdt = torch.bfloat16 if args.dtype == "bf16" else torch.float32
-    es = 2 if args.dtype == "bf16" else 4
-
-    W = wl.make_workload(WORKLOAD)
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    es = 2 if dtype == "bf16" else 4
     G, lo, hi = W["G"], W["lo"], W["hi"]
     nb = G + 3
     x_np = W["x"]
     B, n_in0 = x_np.shape
-    prep = (lambda a: wl.round_to_bf16_f32(a)) if args.dtype == "bf16" else (lambda a: a)
+    prep = (lambda a: wl.round_to_bf16_f32(a)) if dtype == "bf16" else (lambda a: a)
     x = torch.from_numpy(prep(x_np)).to(dev).to(tdt).contiguous()
     layers = [(torch.from_numpy(prep(C)).to(dev).to(tdt).contiguous(),
                torch.from_numpy(prep(Wb)).to(dev).to(tdt).contiguous()) for C, Wb in W["layers"]]
@@ -285,21 +287,20 @@ def main() -> int:
                 events[k].record()
             h = out
 
-    for _ in range(args.warmup):
+    for _ in range(warmup):
         step()
     torch.cuda.synchronize()
 
-    # Timed region: exactly K steps, with one HIP event between kernels (all on
-    # torch's current stream, the stream the kernels are launched on).
+    # Timed region: exactly `steps` steps, bracketed by synchronisations.
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(names) + 1)]
-          for _ in range(args.steps)]
+          for _ in range(steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for k in range(args.steps):
+    for k in range(steps):
         step(ev[k])
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    ms_per_step = (t1 - t0) * 1e3 / steps
     per_kernel_ms = [float(np.mean([e[i].elapsed_time(e[i + 1]) for e in ev]))
                      for i in range(len(names))]
 
@@ -315,7 +316,9 @@ def main() -> int:
         kern[names[1 + 2 * li]] = {
             "bound": "hbm", "unit": "GB/s", "peak": PEAK_HBM_GBS,
             "algorithmic": (o * i_ * (nb + 1) * es + packs[li].nbytes) / 1e9}
-        kern[names[2 + 2 * li]] = layer_roofline(args.dtype, B, i_, o, nb)
+        kern[names[2 + 2 * li]] = layer_roofline(dtype, B, i_, o, nb)
+        # HBM bytes the layer must move: x, the packed weights once, y
+        kern[names[2 + 2 * li]]["algorithmic_bytes"] = (B * (i_ + o) * es + packs[li].nbytes)
     for name, ms in zip(names, per_kernel_ms):
         k = kern[name]
         k["avg_us"] = ms * 1e3
@@ -323,47 +326,127 @@ def main() -> int:
         k["frac"] = k["achieved"] / k["peak"]
         if "valu_gops" in k:  # the basis generation's share of the VALU peak
             k["valu_frac"] = k.pop("valu_gops") / (ms * 1e-3) / PEAK_VALU_GOPS
+            k["valu_frac_dense_count"] = k.pop("valu_gops_dense") / (ms * 1e-3) / PEAK_VALU_GOPS
     dom = max(names, key=lambda n: kern[n]["avg_us"])
     dk = kern[dom]
-
-    # Parity re-check of this run's output on sampled rows (float64 oracle).
-    parity = None
-    try:
-        import oracle
-        rows = np.arange(0, B, max(1, B // 64))[:64]
-        trace = oracle.mlp(prep(x_np)[rows], [(prep(C), prep(Wb)) for C, Wb in W["layers"]], G,
-                           bf16=args.dtype == "bf16", bf16_operands=args.dtype == "bf16")
-        got = hs[-1][torch.from_numpy(rows).to(dev)].float().cpu().numpy().astype(np.float64)
-        parity = float(np.abs(got - trace).max() / np.abs(trace).max())
-    except Exception as e:  # the oracle is optional for timing
-        parity = f"unavailable: {e}"
-
+    traffic = traffic_record(dtype, dom)
+    roof = {"kernel": dom, "bound": dk["bound"], "achieved": dk["achieved"], "peak": dk["peak"],
+            "unit": dk["unit"], "frac": dk["frac"], "traffic": traffic}
+    if traffic is not None and "algorithmic_bytes" in dk:
+        # HBM bytes measured per launch over the bytes the layer must move
+        roof["traffic_over_algorithmic_bytes"] = traffic / dk["algorithmic_bytes"]
     basis_total = B * nb * (n_in0 + sum(i_ for i_, _ in shapes))
+    return {"ms_per_step": ms_per_step, "samples_per_s": B / (ms_per_step * 1e-3),
+            "gbasis_per_s": basis_total / (ms_per_step * 1e-3) / 1e9, "roofline": roof,
+            "kernels": kern, "shapes": shapes, "x": x, "outs": hs, "prep": prep}
+
+
+def layer_parity(dtype: str, W, r: dict, n_rows: int = 64) -> dict:
+    """Per layer, the sampled rows of this run's GPU output against the plain
+    float64 oracle (eq. kan_forward) fed the GPU's own input rows of that
+    layer (rounded to bf16 in bf16 mode): normwise errors, gated at 1e-5
+    (fp32) and 2e-2 (bf16).  End-to-end errors against the oracle's own chain
+    (and, in bf16, against the chain that also rounds the contraction
+    operands to bf16) are information only."""
+    import numpy as np
+    import torch
+
+    import oracle
+
+    G = W["G"]
+    prep = r["prep"]
+    B = W["x"].shape[0]
+    rows = np.arange(0, B, max(1, B // n_rows))[:n_rows]
+    ridx = torch.from_numpy(rows).to(r["x"].device)
+    host = lambda t: t[ridx].float().cpu().numpy().astype(np.float64)
+    ins = [r["x"]] + r["outs"][:-1]
+    bf = dtype == "bf16"
+    per_layer = []
+    for (C, Wb), h_in, h_out in zip(W["layers"], ins, r["outs"]):
+        ref = oracle.layer(host(h_in), prep(C), prep(Wb), G)
+        if bf:
+            ref = oracle.round_bf16(ref)
+        got = host(h_out)
+        per_layer.append(float(np.abs(got - ref).max() / np.abs(ref).max()))
+    tol = 2e-2 if bf else 1e-5
+    layers = [(prep(C), prep(Wb)) for C, Wb in W["layers"]]
+    got = host(r["outs"][-1])
+    chain = oracle.mlp(prep(W["x"])[rows], layers, G, bf16=bf)
+    out = {"rows": int(rows.size), "per_layer_normwise": per_layer, "tolerance": tol,
+           "ok": bool(max(per_layer) <= tol),
+           "e2e_vs_oracle_chain_info": float(np.abs(got - chain).max() / np.abs(chain).max())}
+    if bf:
+        ops = oracle.mlp(prep(W["x"])[rows], layers, G, bf16=True, bf16_operands=True)
+        out["e2e_vs_bf16_operand_chain_info"] = float(np.abs(got - ops).max() / np.abs(ops).max())
+    return out
+
+
+def main() -> int:
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not run (rows are "
+              "independent: the batch would shard across GPUs with the weights replicated "
+              "and no communication inside a layer)", file=sys.stderr)
+        return 2
+    import torch
+
+    from paper_2609_01956_amd import binding as kb
+    from paper_2609_01956_amd import workloads as wl
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 1
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration)
+        return 0
+    if args.configs:
+        configs_sweep(args.dtype)
+        return 0
+    kb.load_library()
+    W = wl.make_workload(WORKLOAD)
+    other = "f32" if args.dtype == "bf16" else "bf16"
+    res = {}
+    for dt in (args.dtype, other):
+        res[dt] = measure_step(dt, W, args.steps, args.warmup)
+        try:
+            res[dt]["parity"] = layer_parity(dt, W, res[dt])
+        except Exception as e:  # the oracle is optional for timing
+            res[dt]["parity"] = f"unavailable: {e}"
+    r = res[args.dtype]
+    B, n_in0 = W["x"].shape
+    G = W["G"]
     line = {
         "metric": METRIC,
-        "value": B / (ms_per_step * 1e-3),
+        "value": r["samples_per_s"],
         "unit": "samples/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": ms_per_step,
+        "ms_per_step": r["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": args.dtype,
         "data": "synthetic",
-        "config": {"workload": WORKLOAD, "global_batch": B, "layers": [n_in0] + [o for _, o in shapes],
-                   "grid_size": G, "spline_order": 3, "grid": [lo, hi],
+        "config": {"workload": WORKLOAD, "global_batch": B,
+                   "layers": [n_in0] + [o for _, o in r["shapes"]],
+                   "grid_size": G, "spline_order": 3, "grid": [W["lo"], W["hi"]],
                    "step": "kan_basis_eval(x) + 3 x (kan_layer_pack + kan_layer_forward_packed)"},
-        "gbasis_per_s": basis_total / (ms_per_step * 1e-3) / 1e9,
-        "roofline": {"kernel": dom, "bound": dk["bound"], "achieved": dk["achieved"],
-                     "peak": dk["peak"], "unit": dk["unit"], "frac": dk["frac"],
-                     "traffic": traffic_record(args.dtype, dom)},
-        "kernels": {n: {k: v for k, v in kern[n].items()} for n in names},
-        "parity_e2e_normwise": parity,
+        "gbasis_per_s": r["gbasis_per_s"],
+        "roofline": r["roofline"],
+        "kernels": r["kernels"],
+        "parity": r["parity"],
     }
+    o = res[other]
+    line[other] = {"ms_per_step": o["ms_per_step"], "samples_per_s": o["samples_per_s"],
+                   "gbasis_per_s": o["gbasis_per_s"], "roofline": o["roofline"],
+                   "kernels": {n: {k: v for k, v in kk.items() if k in
+                                   ("avg_us", "frac", "bound", "achieved", "unit", "valu_frac",
+                                    "valu_frac_dense_count")}
+                               for n, kk in o["kernels"].items()},
+                   "parity": o["parity"]}
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(W, shapes, args.cpu_seconds)
+        line["cpu_baseline"] = cpu_baseline(W, args.cpu_seconds)
     print(json.dumps(line), flush=True)
     return 0
 

@@ -412,6 +412,55 @@ def test_mlp_chains_layers_and_rounds_storage():
     np.testing.assert_array_equal(yb, r(oracle.layer(h1, r(C2), r(W2), G)))
 
 
+def test_mlp_matches_pure_python_chain():
+    """A two-layer chain evaluated in pure Python: scalar loops over scipy's
+    B-spline basis elements, math.exp for SiLU, and, in bf16 mode, torch's
+    bfloat16 conversion of the input, the weights and each layer's output (the
+    storage of eq. kan_forward's tensors in bf16).  None of the oracle's
+    routines takes part."""
+    import torch
+    G, lo, hi = 5, -1.0, 1.0
+    rng = np.random.default_rng(31)
+    x = rng.uniform(-1.3, 1.3, (3, 3))
+    C1 = rng.normal(0, 0.5, (2, 3, G + 3))
+    W1 = rng.normal(0, 0.7, (2, 3))
+    C2 = rng.normal(0, 0.5, (2, 2, G + 3))
+    W2 = rng.normal(0, 0.7, (2, 2))
+    h = (hi - lo) / G
+    t = [lo + (j - 3) * h for j in range(G + 7)]
+    elems = [BSpline.basis_element(t[j:j + 5], extrapolate=False) for j in range(G + 3)]
+
+    def bf(v):
+        return float(torch.tensor(v, dtype=torch.float64).to(torch.bfloat16).to(torch.float64))
+
+    def layer(xs, C, Wb, rnd):
+        out = []
+        for row in xs:
+            ys = []
+            for o in range(len(Wb)):
+                acc = 0.0
+                for i, v in enumerate(row):
+                    for j in range(G + 3):
+                        b = float(elems[j](v))
+                        acc += rnd(C[o][i][j]) * (0.0 if math.isnan(b) else b)
+                    acc += rnd(Wb[o][i]) * v / (1.0 + math.exp(-v))
+                ys.append(rnd(acc))
+            out.append(ys)
+        return out
+
+    for bf16, rnd in [(False, float), (True, bf)]:
+        xs = [[rnd(v) for v in row] for row in x.tolist()]
+        want = layer(layer(xs, C1.tolist(), W1.tolist(), rnd), C2.tolist(), W2.tolist(), rnd)
+        got = oracle.mlp(x, [(C1, W1), (C2, W2)], G, lo, hi, bf16=bf16)
+        if bf16:
+            # the same bf16 values (a double sum differing in its last bit could
+            # only move a value lying within 1e-16 of a rounding tie)
+            np.testing.assert_allclose(got, want, rtol=2 ** -8, atol=0)
+            assert np.mean(got == np.array(want)) == 1.0
+        else:
+            np.testing.assert_allclose(got, want, rtol=1e-12, atol=1e-14)
+
+
 def test_layer_bf16_operands_matches_rounded_matmul():
     """bf16-operand mode equals numpy matmuls of bf16-rounded scipy basis values
     and SiLU values, and the rounding agrees with torch's bfloat16 conversion."""

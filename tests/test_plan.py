@@ -108,6 +108,9 @@ def _forced_cases():
     for B, n_in, n_out, G in gl.NARROW_SHAPES:
         for cfg in gl.NARROW_CFGS:
             yield "bf16", G, B, n_in, n_out, cfg
+    for dtype_name, G, n_in, n_out, cfg in gl.KNOT_CASES:
+        if cfg is not None:
+            yield dtype_name, G, 300, n_in, n_out, cfg
 
 
 @pytest.mark.parametrize("dtype_name,G,B,n_in,n_out,cfg", list(_forced_cases()))
