@@ -55,7 +55,9 @@ typedef enum kan_status {
     KAN_OK = 0,
     KAN_ERR_INVALID_ARG = 1, /* bad size, range, pointer, alignment or overlap   */
     KAN_ERR_UNSUPPORTED = 2, /* spline_order != 3 or an unknown dtype           */
-    KAN_ERR_DEVICE = 3       /* the HIP runtime rejected a launch               */
+    KAN_ERR_DEVICE = 3,      /* the HIP runtime rejected a launch               */
+    KAN_ERR_SCRATCH_LIMIT = 4 /* kan_layer_forward_noalloc: the layer's packed
+                                 weights exceed KAN_NOALLOC_SCRATCH_BYTES       */
 } kan_status;
 
 typedef enum kan_dtype {
@@ -215,6 +217,39 @@ kan_status kan_layer_forward_packed(const kan_grid* grid, kan_dtype dtype, int64
 kan_status kan_layer_plan(const kan_grid* grid, kan_dtype dtype, int64_t batch,
                           int32_t in_features, int32_t out_features, const int32_t* shape,
                           int32_t* plan);
+
+/*
+ * kan_layer_forward_noalloc -- kan_layer_forward without a workspace argument,
+ * for callers that cannot allocate device memory (work under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc).  The
+ * packed weights go to a fixed scratch array of KAN_NOALLOC_SCRATCH_BYTES
+ * bytes that the library holds in device memory on every GPU it runs on,
+ * until the process ends; nothing is allocated or freed by the call.
+ *
+ *   x, coef, base_w, y   as kan_layer_forward (caller-owned device memory)
+ *
+ * Every call on one GPU uses that GPU's one scratch array: calls that overlap
+ * in time on one GPU (on different streams, or from different host threads
+ * without ordering between their streams) race on it and may return wrong
+ * results.  Calls ordered on one stream are safe.  The scratch is fully
+ * rewritten by each call before it is read, so nothing carries over from an
+ * earlier call.  The first call on a device looks up that device's scratch
+ * address (hipGetSymbolAddress) and caches it, for the device current at the
+ * call.
+ *
+ * Returns as kan_layer_forward, plus KAN_ERR_SCRATCH_LIMIT when the layer's
+ * packed weights (kan_layer_packed_bytes) exceed KAN_NOALLOC_SCRATCH_BYTES;
+ * that check runs on the host before any HIP call.
+ */
+kan_status kan_layer_forward_noalloc(const kan_grid* grid, kan_dtype dtype, int64_t batch,
+                                     int32_t in_features, int32_t out_features,
+                                     const void* x, const void* coef, const void* base_w,
+                                     void* y, void* stream);
+
+/* Size of the per-device scratch array of kan_layer_forward_noalloc: 16 MiB,
+ * enough for the packed weights of a 784 -> 256 layer with G = 10 in fp32
+ * (11.2 MB) or of a 128 -> 128 layer with G = 200 in fp32 (13.4 MB). */
+#define KAN_NOALLOC_SCRATCH_BYTES (16u << 20)
 
 /* Static, NUL-terminated description of a status code (never NULL). */
 const char* kan_status_string(kan_status status);

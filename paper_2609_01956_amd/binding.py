@@ -23,13 +23,16 @@ KAN_OK = 0
 KAN_ERR_INVALID_ARG = 1
 KAN_ERR_UNSUPPORTED = 2
 KAN_ERR_DEVICE = 3
+KAN_ERR_SCRATCH_LIMIT = 4
+KAN_NOALLOC_SCRATCH_BYTES = 16 << 20
 
 KAN_F32 = 0
 KAN_BF16 = 1
 
 EXPORTED_SYMBOLS = ("kan_basis_eval", "kan_layer_forward", "kan_layer_forward_workspace_bytes",
                     "kan_layer_packed_bytes", "kan_layer_pack", "kan_layer_forward_packed",
-                    "kan_layer_plan", "kan_status_string", "kan_abi_version")
+                    "kan_layer_plan", "kan_layer_forward_noalloc", "kan_status_string",
+                    "kan_abi_version")
 
 _VP = ctypes.c_void_p
 _I32P = ctypes.POINTER(ctypes.c_int32)
@@ -83,6 +86,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
             lib.kan_layer_plan.argtypes = [g, ctypes.c_int, ctypes.c_int64, ctypes.c_int32,
                                            ctypes.c_int32, _I32P, _I32P]
             lib.kan_layer_plan.restype = ctypes.c_int
+            lib.kan_layer_forward_noalloc.argtypes = [g, ctypes.c_int, ctypes.c_int64,
+                                                      ctypes.c_int32, ctypes.c_int32, _VP, _VP,
+                                                      _VP, _VP, _VP]
+            lib.kan_layer_forward_noalloc.restype = ctypes.c_int
             lib.kan_status_string.argtypes = [ctypes.c_int]
             lib.kan_status_string.restype = ctypes.c_char_p
             lib.kan_abi_version.argtypes = []
@@ -133,6 +140,15 @@ def kan_layer_forward(grid: kan_grid, dtype: int, batch: int, in_features: int,
         ctypes.byref(grid), int(dtype), int(batch), int(in_features), int(out_features),
         _VP(x), _VP(coef), _VP(base_w), _VP(workspace), ctypes.c_size_t(workspace_bytes),
         _VP(y), _VP(stream)))
+
+
+def kan_layer_forward_noalloc(grid: kan_grid, dtype: int, batch: int, in_features: int,
+                              out_features: int, x: int, coef: int, base_w: int, y: int,
+                              stream: int = 0) -> int:
+    """Raw call: device addresses as integers; returns the kan_status code."""
+    return int(load_library().kan_layer_forward_noalloc(
+        ctypes.byref(grid), int(dtype), int(batch), int(in_features), int(out_features),
+        _VP(x), _VP(coef), _VP(base_w), _VP(y), _VP(stream)))
 
 
 def kan_layer_forward_workspace_bytes(grid: kan_grid, dtype: int, batch: int, in_features: int,
@@ -190,7 +206,7 @@ def check(status: int) -> None:
     if status == KAN_OK:
         return
     msg = kan_status_string(status)
-    if status == KAN_ERR_INVALID_ARG:
+    if status in (KAN_ERR_INVALID_ARG, KAN_ERR_SCRATCH_LIMIT):
         raise ValueError(msg)
     if status == KAN_ERR_UNSUPPORTED:
         raise NotImplementedError(msg)

@@ -60,6 +60,9 @@ const char* kan_status_string(kan_status status) {
         case KAN_ERR_INVALID_ARG: return "KAN_ERR_INVALID_ARG: invalid size, range, pointer, alignment or overlap";
         case KAN_ERR_UNSUPPORTED: return "KAN_ERR_UNSUPPORTED: only cubic splines (spline_order 3) and f32/bf16 are implemented";
         case KAN_ERR_DEVICE: return "KAN_ERR_DEVICE: the HIP runtime rejected a kernel launch";
+        case KAN_ERR_SCRATCH_LIMIT:
+            return "KAN_ERR_SCRATCH_LIMIT: the layer's packed weights exceed the 16 MiB scratch of "
+                   "kan_layer_forward_noalloc (use kan_layer_forward with a workspace)";
     }
     return "unknown kan_status";
 }
@@ -299,6 +302,31 @@ kan_status kan_layer_forward(const kan_grid* grid, kan_dtype dtype, int64_t batc
     if (st != KAN_OK) return st;
     return kan_layer_forward_packed(grid, dtype, batch, in_features, out_features, x, workspace,
                                     ws, nullptr, y, stream);
+}
+
+kan_status kan_layer_forward_noalloc(const kan_grid* grid, kan_dtype dtype, int64_t batch,
+                                     int32_t in_features, int32_t out_features, const void* x,
+                                     const void* coef, const void* base_w, void* y,
+                                     void* stream) {
+    kan::GridConst gc;
+    kan::LayerGeom geom;
+    kan_status st = check_layer(grid, dtype, in_features, out_features, &gc, &geom);
+    if (st != KAN_OK) return st;
+    if (batch < 0) return KAN_ERR_INVALID_ARG;
+    if (geom.packed_bytes > (size_t)KAN_NOALLOC_SCRATCH_BYTES) return KAN_ERR_SCRATCH_LIMIT;
+    if (batch == 0) return KAN_OK;
+    st = check_forward(gc, dtype, batch, in_features, out_features, x, coef, base_w, y);
+    if (st != KAN_OK) return st;
+    void* ws = nullptr;
+    size_t ws_bytes = 0;
+    if (kan::noalloc_scratch(&ws, &ws_bytes) != hipSuccess) return KAN_ERR_DEVICE;
+    // (the scratch is the library's own device array: it overlaps no caller
+    // tensor)
+    st = kan_layer_pack(grid, dtype, in_features, out_features, coef, base_w, ws, ws_bytes,
+                        stream);
+    if (st != KAN_OK) return st;
+    return kan_layer_forward_packed(grid, dtype, batch, in_features, out_features, x, ws,
+                                    ws_bytes, nullptr, y, stream);
 }
 
 }  // extern "C"

@@ -151,6 +151,11 @@ struct LayerArgs {
     float a_frac;
 };
 
+// Device address and size of the calling thread's current device's copy of
+// the fixed scratch array used by kan_layer_forward_noalloc (looked up once
+// per device, then cached).
+hipError_t noalloc_scratch(void** ptr, size_t* bytes);
+
 hipError_t launch_pack(bool bf16, const LayerGeom& g, int in, int out, const void* coef,
                        const void* base_w, void* packed, hipStream_t s);
 hipError_t launch_layer(bool bf16, const LayerGeom& g, const LayerCfg& c, LayerArgs a,

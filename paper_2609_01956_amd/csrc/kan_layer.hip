@@ -3,6 +3,10 @@
 // kan_layer_kernel.h.
 #include "kan_layer_kernel.h"
 
+#include <mutex>
+
+#include "kan.h"
+
 
 namespace kan {
 
@@ -190,6 +194,40 @@ LayerCfg plan_layer(const LayerGeom& g, bool bf16, int64_t batch) {
         if (w >= 256) return c;
     }
     return best;  // the most workgroups any shape gives
+}
+
+// ----------------------------------------------------- no-allocation scratch
+
+namespace {
+
+// Packed weights of kan_layer_forward_noalloc.  Each GPU the library runs on
+// holds its own copy for the life of the process.  In host code `scratch`
+// names a host-side stand-in, not device memory: kernels only ever receive
+// the device address from hipGetSymbolAddress below.
+static __device__ __align__(256) unsigned char scratch[KAN_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex scratch_mu;
+void* scratch_addr[kMaxDevices];
+
+}  // namespace
+
+hipError_t noalloc_scratch(void** ptr, size_t* bytes) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(scratch_mu);
+    if (scratch_addr[dev] == nullptr) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (p == nullptr) return hipErrorInvalidSymbol;
+        scratch_addr[dev] = p;
+    }
+    *ptr = scratch_addr[dev];
+    *bytes = KAN_NOALLOC_SCRATCH_BYTES;
+    return hipSuccess;
 }
 
 // ------------------------------------------------------------------ launches

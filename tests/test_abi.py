@@ -32,9 +32,10 @@ def test_library_exports_every_declared_symbol():
 
 def test_abi_version_and_status_strings():
     assert kb.kan_abi_version() == 3
-    for code in range(4):
-        s = kb.kan_status_string(code)
-        assert s.startswith(["KAN_OK", "KAN_ERR_INVALID_ARG", "KAN_ERR_UNSUPPORTED", "KAN_ERR_DEVICE"][code])
+    names = ["KAN_OK", "KAN_ERR_INVALID_ARG", "KAN_ERR_UNSUPPORTED", "KAN_ERR_DEVICE",
+             "KAN_ERR_SCRATCH_LIMIT"]
+    for code, name in enumerate(names):
+        assert kb.kan_status_string(code).startswith(name)
     assert kb.kan_status_string(99) == "unknown kan_status"
 
 
@@ -230,3 +231,29 @@ def test_product_path_does_not_touch_the_oracle():
             if fn.endswith((".py", ".hip", ".cpp", ".h")):
                 text = open(os.path.join(dirpath, fn)).read()
                 assert "oracle" not in text.lower(), os.path.join(dirpath, fn)
+
+
+def test_noalloc_entry_point_host_checks():
+    """kan_layer_forward_noalloc rejects, on the host and before any HIP call,
+    the same invalid arguments as kan_layer_forward, and a layer whose packed
+    weights exceed its fixed 16 MiB scratch with KAN_ERR_SCRATCH_LIMIT."""
+    f32, bad = kb.KAN_F32, kb.KAN_ERR_INVALID_ARG
+    g = kb.make_grid(10)
+    assert kb.kan_layer_forward_noalloc(g, f32, -1, 4, 4, X, C, W, Y) == bad
+    assert kb.kan_layer_forward_noalloc(g, f32, 16, 4, 4, 0, C, W, Y) == bad
+    assert kb.kan_layer_forward_noalloc(g, f32, 16, 4, 4, X, C, W, X + 8) == bad
+    assert kb.kan_layer_forward_noalloc(kb.make_grid(10, spline_order=2), f32, 16, 4, 4, X, C, W,
+                                        Y) == kb.KAN_ERR_UNSUPPORTED
+    assert kb.kan_layer_forward_noalloc(g, f32, 0, 4, 4, 0, 0, 0, 0) == kb.KAN_OK
+    # 256 -> 128 at G = 200 in fp32: 26.7 MB of packed weights
+    g200 = kb.make_grid(200)
+    assert kb.kan_layer_packed_bytes(g200, f32, 256, 128)[1] > kb.KAN_NOALLOC_SCRATCH_BYTES
+    assert kb.kan_layer_forward_noalloc(g200, f32, 16, 256, 128, X, C, W, Y) == \
+        kb.KAN_ERR_SCRATCH_LIMIT
+    # the largest configured layers fit: 784 -> 256 at G = 10, 128 -> 128 at G = 200
+    for G, n_in, n_out in [(10, 784, 256), (200, 128, 128)]:
+        for dt in (kb.KAN_F32, kb.KAN_BF16):
+            assert kb.kan_layer_packed_bytes(kb.make_grid(G), dt, n_in, n_out)[1] <= \
+                kb.KAN_NOALLOC_SCRATCH_BYTES
+    with pytest.raises(ValueError):
+        kb.check(kb.KAN_ERR_SCRATCH_LIMIT)
