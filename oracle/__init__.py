@@ -21,6 +21,12 @@ follows:
 * ``mlp``          -- layers applied in sequence, optionally with bf16 storage
                       rounding of every tensor (round-to-nearest-even).
 * ``round_bf16``   -- double -> nearest bfloat16 value, ties to even.
+* ``basis_tp_deriv`` -- dN_j/dx of the clamped form (eq. general_truncated
+                      differentiated, times the derivative of eq. bounded's
+                      clamp).
+* ``silu_deriv``   -- sigma'(x) = s + x s (1 - s), s = 1 / (1 + exp(-x)).
+* ``layer_backward`` -- gradients of eq. kan_forward for an upstream dy:
+                      (dx, dC, dWb).
 
 Pins (``tests/test_oracle_*.py``): closed forms printed by the paper, the
 paper's M_B-spline matrix, scipy's B-spline basis elements, the three routes
@@ -77,6 +83,13 @@ def _load():
                                              ctypes.c_int, ctypes.c_int, ctypes.c_double,
                                              ctypes.c_double, ctypes.c_int, ctypes.c_int, _D]
             lib.kan_oracle_round_bf16.argtypes = [_D, _I64, _D]
+            lib.kan_oracle_basis_tp_deriv.argtypes = [_D, _I64, ctypes.c_int, ctypes.c_int,
+                                                      ctypes.c_double, ctypes.c_double, _D]
+            lib.kan_oracle_silu_deriv.argtypes = [_D, _I64, _D]
+            lib.kan_oracle_layer_backward.argtypes = [_D, _I64, ctypes.c_int, ctypes.c_int, _D,
+                                                      _D, _D, ctypes.c_int, ctypes.c_int,
+                                                      ctypes.c_double, ctypes.c_double, _D, _D,
+                                                      _D]
             lib.kan_oracle_num_threads.restype = ctypes.c_int
             lib.kan_oracle_set_threads.argtypes = [ctypes.c_int]
             _lib = lib
@@ -210,3 +223,41 @@ def mlp(x, layers, G: int, lo: float = -1.0, hi: float = 1.0, k: int = 3,
         trace.append((h, y))
         h = y
     return trace if return_all else h
+
+
+def basis_tp_deriv(x, G: int, lo: float = -1.0, hi: float = 1.0, k: int = 3) -> np.ndarray:
+    """dN_j/dx of the clamped truncated-power basis, shape x.shape + (G + k,):
+    eq. general_truncated differentiated in x, times the derivative of the
+    clamp of eq. bounded (1 for 0 < u < k + 1, else 0)."""
+    _check_grid(G, k, lo, hi)
+    xa = _f64(x)
+    out = np.empty(xa.shape + (G + k,), dtype=np.float64)
+    _load().kan_oracle_basis_tp_deriv(_p(xa), xa.size, G, k, lo, hi, _p(out))
+    return out
+
+
+def silu_deriv(x) -> np.ndarray:
+    """sigma'(x) for sigma(x) = x / (1 + exp(-x))."""
+    xa = _f64(x)
+    out = np.empty_like(xa)
+    _load().kan_oracle_silu_deriv(_p(xa), xa.size, _p(out))
+    return out
+
+
+def layer_backward(x, C, Wb, dy, G: int, lo: float = -1.0, hi: float = 1.0, k: int = 3):
+    """Gradients of sum(dy * y) for y = layer(x, C, Wb) (eq. kan_forward):
+    returns (dx [B, in], dC [out, in, G + k], dWb [out, in]), float64."""
+    _check_grid(G, k, lo, hi)
+    xa, Ca, Wa, ga = _f64(x), _f64(C), _f64(Wb), _f64(dy)
+    if xa.ndim != 2:
+        raise ValueError("x must be [B, in]")
+    B, n_in = xa.shape
+    n_out = Wa.shape[0]
+    if Ca.shape != (n_out, n_in, G + k) or Wa.shape != (n_out, n_in) or ga.shape != (B, n_out):
+        raise ValueError("shapes of C, Wb and dy do not match x and the grid")
+    dx = np.empty((B, n_in))
+    dC = np.empty((n_out, n_in, G + k))
+    dW = np.empty((n_out, n_in))
+    _load().kan_oracle_layer_backward(_p(xa), B, n_in, n_out, _p(Ca), _p(Wa), _p(ga), G, k, lo,
+                                      hi, _p(dx), _p(dC), _p(dW))
+    return dx, dC, dW

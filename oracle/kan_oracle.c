@@ -25,6 +25,16 @@
  *                       branch sigma(x) = x / (1 + exp(-x)).
  *   round_bf16       -- round-to-nearest-even to bfloat16 (8 significant
  *                       bits), used to mirror bf16 storage between layers.
+ *   basis_tp_deriv   -- d N_{j,k} / dx of the clamped truncated-power form:
+ *                       eq. general_truncated differentiated term by term
+ *                       (power k - 1, factor k), times the derivative of the
+ *                       clamp of eq. bounded (1 inside (0, k+1), else 0).
+ *   layer_backward   -- gradients of eq. kan_forward for an upstream gradient
+ *                       dy: dC = dy^T Phi(x), dWb = dy^T sigma(x), and
+ *                       dx = sum_o dy (sum_j C N_j'(x) + Wb sigma'(x)).  The
+ *                       paper times the forward only (Sec. 5 lists backward
+ *                       timing as future work); these are the chain rule
+ *                       applied to its forward.
  *
  * Build: gcc -O2 -fopenmp -fPIC -shared (no -ffast-math; the rounding of every
  * double operation must be IEEE).
@@ -282,5 +292,115 @@ void kan_oracle_round_bf16(const double* v, int64_t n, double* out) {
         double res = ldexp(r, q);
         if (fabs(res) > 3.3895313892515355e38) res = a > 0 ? INFINITY : -INFINITY;
         out[e] = res;
+    }
+}
+
+/* ------------------------------------------------------------ backward */
+
+/* d/dx of the clamped basis N_j at x.  Differentiating eq. general_truncated
+ * in x gives (1 / ((k-1)! h^k)) sum_m (-1)^m C(k+1, m) (x - t_{j+m})_+^{k-1},
+ * i.e. (1/h) (1/(k-1)!) sum_m (-1)^m C(k+1, m) (u - m)_+^{k-1} in u; with
+ * the clamp of eq. bounded the form is N(ubar(u)), whose derivative is that
+ * sum at ubar times dubar/du = [0 < u < k+1].  (z)_+^0 is read as [z > 0].
+ * A NaN input gives NaN. */
+static void tp_deriv_row(double xv, int G, int k, double lo, double hi, double* row) {
+    const int nb = G + k;
+    const double h = (hi - lo) / (double)G;
+    const double inv_fact = 1.0 / factorial(k - 1);
+    for (int j = 0; j < nb; ++j) {
+        if (isnan(xv)) { row[j] = xv; continue; }
+        const double tj = lo + (double)(j - k) * h;
+        const double u = (xv - tj) / h;
+        if (!(u > 0.0 && u < (double)(k + 1))) { row[j] = 0.0; continue; }
+        double s = 0.0;
+        for (int m = 0; m <= k + 1; ++m) {
+            const double z = u - (double)m;
+            const double zp = (k - 1 == 0) ? (z > 0.0 ? 1.0 : 0.0) : ipow(z > 0.0 ? z : 0.0, k - 1);
+            const double term = binom(k + 1, m) * zp;
+            s += (m & 1) ? -term : term;
+        }
+        row[j] = s * inv_fact / h;
+    }
+}
+
+void kan_oracle_basis_tp_deriv(const double* x, int64_t n, int G, int k, double lo,
+                               double hi, double* dphi) {
+    const int nb = G + k;
+    #pragma omp parallel for schedule(static)
+    for (int64_t e = 0; e < n; ++e)
+        tp_deriv_row(x[e], G, k, lo, hi, &dphi[e * nb]);
+}
+
+/* sigma'(x) for sigma(x) = x / (1 + exp(-x)): with s = 1 / (1 + exp(-x)),
+ * d(x s)/dx = s + x s (1 - s). */
+static double silu_deriv_one(double v) {
+    const double s = 1.0 / (1.0 + exp(-v));
+    return s + v * s * (1.0 - s);
+}
+
+void kan_oracle_silu_deriv(const double* x, int64_t n, double* out) {
+    #pragma omp parallel for schedule(static)
+    for (int64_t e = 0; e < n; ++e) out[e] = silu_deriv_one(x[e]);
+}
+
+/* Gradients of L = sum_{b,o} dy[b, o] y[b, o] with y from eq. kan_forward:
+ *   dx[b, i]  = sum_o dy[b, o] ( sum_j C[o, i, j] N_j'(x[b, i]) + Wb[o, i] sigma'(x[b, i]) )
+ *   dC[o,i,j] = sum_b dy[b, o] N_j(x[b, i])
+ *   dWb[o, i] = sum_b dy[b, o] sigma(x[b, i])
+ * x [B, in], C [out, in, G + k], Wb [out, in], dy [B, out]; outputs dx
+ * [B, in], dC [out, in, G + k], dWb [out, in].  Plain loops in double, each
+ * sum in index order (o, then j; b ascending). */
+void kan_oracle_layer_backward(const double* x, int64_t B, int in, int out,
+                               const double* C, const double* Wb, const double* dy,
+                               int G, int k, double lo, double hi,
+                               double* dx, double* dC, double* dWb) {
+    const int nb = G + k;
+    /* dx: rows are independent */
+    #pragma omp parallel
+    {
+        double* dn = (double*)malloc(sizeof(double) * (size_t)nb);
+        #pragma omp for schedule(dynamic, 4)
+        for (int64_t b = 0; b < B; ++b) {
+            for (int i = 0; i < in; ++i) {
+                const double xv = x[b * (int64_t)in + i];
+                tp_deriv_row(xv, G, k, lo, hi, dn);
+                const double sd = silu_deriv_one(xv);
+                double s = 0.0;
+                for (int o = 0; o < out; ++o) {
+                    const double g = dy[b * (int64_t)out + o];
+                    const double* c = &C[((int64_t)o * in + i) * nb];
+                    double t = 0.0;
+                    for (int j = 0; j < nb; ++j) t += c[j] * dn[j];
+                    t += Wb[(int64_t)o * in + i] * sd;
+                    s += g * t;
+                }
+                dx[b * (int64_t)in + i] = s;
+            }
+        }
+        free(dn);
+    }
+    /* dC, dWb: one (o, i) pair per iteration, the sum over b in order */
+    #pragma omp parallel
+    {
+        double* nrow = (double*)malloc(sizeof(double) * (size_t)nb);
+        double* acc = (double*)malloc(sizeof(double) * (size_t)nb);
+        #pragma omp for schedule(dynamic, 1) collapse(2)
+        for (int o = 0; o < out; ++o) {
+            for (int i = 0; i < in; ++i) {
+                double accw = 0.0;
+                for (int j = 0; j < nb; ++j) acc[j] = 0.0;
+                for (int64_t b = 0; b < B; ++b) {
+                    const double g = dy[b * (int64_t)out + o];
+                    const double xv = x[b * (int64_t)in + i];
+                    tp_row(xv, G, k, lo, hi, 1, nrow);
+                    for (int j = 0; j < nb; ++j) acc[j] += g * nrow[j];
+                    accw += g * silu_one(xv);
+                }
+                for (int j = 0; j < nb; ++j) dC[((int64_t)o * in + i) * nb + j] = acc[j];
+                dWb[(int64_t)o * in + i] = accw;
+            }
+        }
+        free(acc);
+        free(nrow);
     }
 }
