@@ -219,6 +219,61 @@ kan_status kan_layer_plan(const kan_grid* grid, kan_dtype dtype, int64_t batch,
                           int32_t* plan);
 
 /*
+ * kan_layer_backward -- gradients of one KAN layer (eq. kan_forward) for an
+ * upstream gradient dy = dL/dy:
+ *
+ *   dx[b, i]       = sum_o dy[b, o] ( sum_j coef[o, i, j] N_j'(x[b, i])
+ *                                     + base_w[o, i] silu'(x[b, i]) )
+ *   dcoef[o, i, j] = sum_b dy[b, o] N_j(x[b, i])
+ *   dbase_w[o, i]  = sum_b dy[b, o] silu(x[b, i])
+ *
+ * N_j' is the derivative in x of the clamped truncated-power basis
+ * (eq. general_truncated differentiated: (1/h) (1/2) sum_m (-1)^m C(4, m)
+ * (u - m)_+^2 at the clamped coordinate of eq. bounded, 0 off the support).
+ * The paper reports forward timing only and lists backward timing as future
+ * work (Sec. 5); these are the chain rule applied to its forward.
+ *
+ *   x        [batch, in_features]              dtype storage
+ *   coef     [out_features, in_features, G+3]  dtype storage (read only for dx)
+ *   base_w   [out_features, in_features]       dtype storage (read only for dx)
+ *   dy       [batch, out_features]             dtype storage
+ *   dx       [batch, in_features]              output, or NULL to skip it
+ *   dcoef    [out_features, in_features, G+3]  output, or NULL to skip the
+ *   dbase_w  [out_features, in_features]         weight gradients (both NULL
+ *                                                or both non-NULL)
+ *   workspace  caller-owned device scratch of workspace_bytes >=
+ *              kan_layer_backward_workspace_bytes(...), 16-byte aligned,
+ *              overlapping no other argument; overwritten.
+ *
+ * Both contractions run on the matrix cores with fp32 accumulation; the
+ * basis values are regenerated in registers, never stored.  The weight
+ * gradients sum the batch in a fixed order (deterministic).  Outputs are
+ * fully overwritten; with batch == 0 the weight gradients are written as 0.
+ * Outputs must not overlap each other, any input or the workspace.
+ *
+ * Returns KAN_OK, KAN_ERR_INVALID_ARG (as kan_layer_forward, plus a NULL dy,
+ * no output requested, only one of dcoef / dbase_w, a short or misaligned
+ * workspace), KAN_ERR_UNSUPPORTED or KAN_ERR_DEVICE.
+ */
+kan_status kan_layer_backward(const kan_grid* grid, kan_dtype dtype, int64_t batch,
+                              int32_t in_features, int32_t out_features, const void* x,
+                              const void* coef, const void* base_w, const void* dy, void* dx,
+                              void* dcoef, void* dbase_w, void* workspace,
+                              size_t workspace_bytes, void* stream);
+
+/*
+ * kan_layer_backward_workspace_bytes -- size in bytes of the workspace
+ * kan_layer_backward needs for this grid, dtype, batch and shape (the packed
+ * weights of the dx contraction, dy transposed, and the fp32 partial weight
+ * gradients of the batch splits).  Writes *bytes.  Returns KAN_OK,
+ * KAN_ERR_INVALID_ARG (bytes == NULL, bad grid or sizes, batch < 0) or
+ * KAN_ERR_UNSUPPORTED.
+ */
+kan_status kan_layer_backward_workspace_bytes(const kan_grid* grid, kan_dtype dtype,
+                                              int64_t batch, int32_t in_features,
+                                              int32_t out_features, size_t* bytes);
+
+/*
  * kan_layer_forward_noalloc -- kan_layer_forward without a workspace argument,
  * for callers that cannot allocate device memory (work under HIP graph
  * capture, tight serving loops, harnesses that forbid hipMalloc).  The

@@ -31,7 +31,8 @@ KAN_BF16 = 1
 
 EXPORTED_SYMBOLS = ("kan_basis_eval", "kan_layer_forward", "kan_layer_forward_workspace_bytes",
                     "kan_layer_packed_bytes", "kan_layer_pack", "kan_layer_forward_packed",
-                    "kan_layer_plan", "kan_layer_forward_noalloc", "kan_status_string",
+                    "kan_layer_plan", "kan_layer_forward_noalloc", "kan_layer_backward",
+                    "kan_layer_backward_workspace_bytes", "kan_status_string",
                     "kan_abi_version")
 
 _VP = ctypes.c_void_p
@@ -90,6 +91,14 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                                       ctypes.c_int32, ctypes.c_int32, _VP, _VP,
                                                       _VP, _VP, _VP]
             lib.kan_layer_forward_noalloc.restype = ctypes.c_int
+            lib.kan_layer_backward.argtypes = [g, ctypes.c_int, ctypes.c_int64, ctypes.c_int32,
+                                               ctypes.c_int32, _VP, _VP, _VP, _VP, _VP, _VP, _VP,
+                                               _VP, ctypes.c_size_t, _VP]
+            lib.kan_layer_backward.restype = ctypes.c_int
+            lib.kan_layer_backward_workspace_bytes.argtypes = [g, ctypes.c_int, ctypes.c_int64,
+                                                               ctypes.c_int32, ctypes.c_int32,
+                                                               ctypes.POINTER(ctypes.c_size_t)]
+            lib.kan_layer_backward_workspace_bytes.restype = ctypes.c_int
             lib.kan_status_string.argtypes = [ctypes.c_int]
             lib.kan_status_string.restype = ctypes.c_char_p
             lib.kan_abi_version.argtypes = []
@@ -149,6 +158,27 @@ def kan_layer_forward_noalloc(grid: kan_grid, dtype: int, batch: int, in_feature
     return int(load_library().kan_layer_forward_noalloc(
         ctypes.byref(grid), int(dtype), int(batch), int(in_features), int(out_features),
         _VP(x), _VP(coef), _VP(base_w), _VP(y), _VP(stream)))
+
+
+def kan_layer_backward(grid: kan_grid, dtype: int, batch: int, in_features: int,
+                       out_features: int, x: int, coef: int, base_w: int, dy: int, dx: int,
+                       dcoef: int, dbase_w: int, workspace: int, workspace_bytes: int,
+                       stream: int = 0) -> int:
+    """Raw call: device addresses as integers (0 for NULL); returns the kan_status code."""
+    return int(load_library().kan_layer_backward(
+        ctypes.byref(grid), int(dtype), int(batch), int(in_features), int(out_features),
+        _VP(x), _VP(coef), _VP(base_w), _VP(dy), _VP(dx), _VP(dcoef), _VP(dbase_w),
+        _VP(workspace), ctypes.c_size_t(workspace_bytes), _VP(stream)))
+
+
+def kan_layer_backward_workspace_bytes(grid: kan_grid, dtype: int, batch: int, in_features: int,
+                                       out_features: int) -> Tuple[int, int]:
+    """Raw call: returns (kan_status, bytes)."""
+    n = ctypes.c_size_t(0)
+    st = int(load_library().kan_layer_backward_workspace_bytes(
+        ctypes.byref(grid), int(dtype), int(batch), int(in_features), int(out_features),
+        ctypes.byref(n)))
+    return st, int(n.value)
 
 
 def kan_layer_forward_workspace_bytes(grid: kan_grid, dtype: int, batch: int, in_features: int,
@@ -364,3 +394,38 @@ def mlp_forward(x, layers: Sequence[Tuple[object, object]], grid_size: int, grid
         h = layer_forward(h, coef, base_w, grid_size, grid_lo, grid_hi)
         outs.append(h)
     return outs if return_all else h
+
+
+def layer_backward(x, coef, base_w, dy, grid_size: int, grid_lo: float = -1.0,
+                   grid_hi: float = 1.0, need_dx: bool = True, need_dw: bool = True,
+                   workspace=None):
+    """Gradients of one KAN layer (kan_layer_backward): x [B, in], coef [out,
+    in, G + 3], base_w [out, in], dy [B, out], all of one dtype on one device
+    -> (dx [B, in] or None, dcoef or None, dbase_w or None), enqueued on
+    torch's current stream.  `workspace` (a uint8 device tensor) is used when
+    large enough, else a fresh one is taken from torch's allocator."""
+    torch = _torch()
+    _require_device(x, dy)
+    n_in, n_out = _check_weights(coef, base_w, grid_size)
+    if x.dim() != 2 or x.shape[1] != n_in or dy.shape != (x.shape[0], n_out):
+        raise ValueError("x must be [B, in] and dy [B, out] for the weights' in and out")
+    if not (x.dtype == dy.dtype == coef.dtype):
+        raise ValueError("x, dy and the weights must share one dtype")
+    if not (need_dx or need_dw):
+        raise ValueError("nothing to compute")
+    B = x.shape[0]
+    dt = _dtype_code(x)
+    g = make_grid(grid_size, grid_lo, grid_hi)
+    st, nbytes = kan_layer_backward_workspace_bytes(g, dt, B, n_in, n_out)
+    check(st)
+    if workspace is None or workspace.numel() < nbytes or workspace.device != x.device:
+        workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=x.device)
+    dx = torch.empty_like(x) if need_dx else None
+    dC = torch.empty_like(coef) if need_dw else None
+    dW = torch.empty_like(base_w) if need_dw else None
+    ptr = lambda t: 0 if t is None else t.data_ptr()
+    with torch.cuda.device(x.device):
+        check(kan_layer_backward(g, dt, B, n_in, n_out, x.data_ptr(), coef.data_ptr(),
+                                 base_w.data_ptr(), dy.data_ptr(), ptr(dx), ptr(dC), ptr(dW),
+                                 workspace.data_ptr(), workspace.numel(), _stream(x.device)))
+    return dx, dC, dW

@@ -329,4 +329,91 @@ kan_status kan_layer_forward_noalloc(const kan_grid* grid, kan_dtype dtype, int6
                                     ws_bytes, nullptr, y, stream);
 }
 
+// Backward geometry (after check_layer): the batch must fit the kernels' grids.
+static kan_status backward_geom(const kan::GridConst& gc, kan_dtype dtype, int64_t batch,
+                                int32_t in_features, int32_t out_features, kan::BwdGeom* bg) {
+    if (batch < 0 || batch > (int64_t)0x7fffffff * 32) return KAN_ERR_INVALID_ARG;
+    if (!kan::bwd_geom(gc.nb, dtype == KAN_BF16, batch, in_features, out_features, bg))
+        return KAN_ERR_INVALID_ARG;
+    return KAN_OK;
+}
+
+kan_status kan_layer_backward_workspace_bytes(const kan_grid* grid, kan_dtype dtype,
+                                              int64_t batch, int32_t in_features,
+                                              int32_t out_features, size_t* bytes) {
+    if (bytes == nullptr) return KAN_ERR_INVALID_ARG;
+    kan::GridConst gc;
+    kan::LayerGeom geom;
+    kan_status st = check_layer(grid, dtype, in_features, out_features, &gc, &geom);
+    if (st != KAN_OK) return st;
+    kan::BwdGeom bg;
+    st = backward_geom(gc, dtype, batch, in_features, out_features, &bg);
+    if (st != KAN_OK) return st;
+    *bytes = bg.bytes;
+    return KAN_OK;
+}
+
+kan_status kan_layer_backward(const kan_grid* grid, kan_dtype dtype, int64_t batch,
+                              int32_t in_features, int32_t out_features, const void* x,
+                              const void* coef, const void* base_w, const void* dy, void* dx,
+                              void* dcoef, void* dbase_w, void* workspace,
+                              size_t workspace_bytes, void* stream) {
+    kan::GridConst gc;
+    kan::LayerGeom geom;
+    kan_status st = check_layer(grid, dtype, in_features, out_features, &gc, &geom);
+    if (st != KAN_OK) return st;
+    kan::BwdGeom bg;
+    st = backward_geom(gc, dtype, batch, in_features, out_features, &bg);
+    if (st != KAN_OK) return st;
+    if ((dcoef == nullptr) != (dbase_w == nullptr)) return KAN_ERR_INVALID_ARG;
+    if (dx == nullptr && dcoef == nullptr) return KAN_ERR_INVALID_ARG;
+    const bool need_x = batch > 0;
+    if (need_x && (x == nullptr || dy == nullptr)) return KAN_ERR_INVALID_ARG;
+    if (dx != nullptr && need_x && (coef == nullptr || base_w == nullptr))
+        return KAN_ERR_INVALID_ARG;
+    if (workspace == nullptr || !aligned(workspace, 16) || workspace_bytes < bg.bytes)
+        return KAN_ERR_INVALID_ARG;
+    const size_t es = dtype_size(dtype);
+    const uint64_t ub = (uint64_t)batch;
+    if (ub > SIZE_MAX / es / (uint64_t)in_features || ub > SIZE_MAX / es / (uint64_t)out_features)
+        return KAN_ERR_INVALID_ARG;
+    struct Buf { const void* p; size_t n; };
+    const size_t x_b = ub * (size_t)in_features * es;
+    const size_t y_b = ub * (size_t)out_features * es;
+    const size_t c_b = (size_t)out_features * in_features * gc.nb * es;
+    const size_t w_b = (size_t)out_features * in_features * es;
+    const Buf ins[] = {{need_x ? x : nullptr, x_b}, {dx ? coef : nullptr, c_b},
+                       {dx ? base_w : nullptr, w_b}, {need_x ? dy : nullptr, y_b}};
+    const Buf outs[] = {{dx, x_b}, {dcoef, c_b}, {dbase_w, w_b}, {workspace, bg.bytes}};
+    for (const Buf& o : outs) {
+        if (o.p == nullptr || o.n == 0) continue;
+        if (!aligned(o.p, es)) return KAN_ERR_INVALID_ARG;
+        for (const Buf& i : ins)
+            if (i.p != nullptr && i.n > 0 && overlap(o.p, o.n, i.p, i.n)) return KAN_ERR_INVALID_ARG;
+        for (const Buf& q : outs)
+            if (&q != &o && q.p != nullptr && q.n > 0 && overlap(o.p, o.n, q.p, q.n))
+                return KAN_ERR_INVALID_ARG;
+    }
+    for (const Buf& i : ins)
+        if (i.p != nullptr && !aligned(i.p, es)) return KAN_ERR_INVALID_ARG;
+    if (batch == 0 && dx != nullptr && dcoef == nullptr) return KAN_OK;
+    kan::BwdArgs a;
+    a.x = x;
+    a.coef = coef;
+    a.bw = base_w;
+    a.dy = dy;
+    a.dx = batch > 0 ? dx : nullptr;
+    a.dcoef = dcoef;
+    a.dbw = dbase_w;
+    a.ws = workspace;
+    a.batch = batch;
+    a.in = in_features;
+    a.out = out_features;
+    a.inv_h = gc.inv_h;
+    a.a_int = gc.a_int;
+    a.a_frac = gc.a_frac;
+    return device_status(kan::launch_backward(dtype == KAN_BF16, bg, a,
+                                              static_cast<hipStream_t>(stream)));
+}
+
 }  // extern "C"

@@ -166,4 +166,53 @@ hipError_t launch_layer_bf16(const LayerGeom& g, const LayerCfg& c, const LayerA
 hipError_t launch_layer_f32(const LayerGeom& g, const LayerCfg& c, const LayerArgs& a,
                             hipStream_t s);
 
+// ------------------------------------------------------------- backward
+//
+// Gradients of the layer for an upstream gradient dy [batch, out]:
+//   dx[b, i]  = sum_o dy[b, o] (sum_j C[o, i, j] N_j'(x[b, i]) + Wb[o, i] silu'(x[b, i]))
+//   dC[o,i,j] = sum_b dy[b, o] N_j(x[b, i]),   dWb[o, i] = sum_b dy[b, o] silu(x[b, i])
+// Both contractions run over "K rows": feature f owns rows [f cp, (f+1) cp),
+// row f cp + c holding column c of the feature (0: SiLU, 1..nb: basis c - 1,
+// beyond: zero padding).  cp is 16 when a feature's nb + 1 columns fit in 16,
+// else a multiple of 32; rows are cut into tiles of 32 (two features each
+// when cp = 16, part of one feature otherwise).
+struct BwdGeom {
+    int nb;         // G + 3
+    int cp;         // K rows per feature
+    int ntiles;     // 32-row K tiles
+    int kr;         // 32 ntiles
+    int out32;      // out rounded up to 32 (rows of the transposed dy)
+    int groups;     // dx: k-step groups over all outputs (16 outputs bf16, 8 fp32)
+    int gmax;       // dx: groups per output chunk held in registers (256 outputs)
+    int nchunk;     // dx: output chunks (partial dx summed by a reduce when > 1)
+    int oh, nfw;    // dW: waves across outputs, 32-output fragments per wave
+    int kt;         // dW: K rows per workgroup
+    int ktiles;     // dW: K tiles of kt rows
+    int otiles;     // dW: output tiles of 32 oh nfw columns
+    int split;      // dW: batch splits (partials summed by the reduce kernel)
+    int rows_per_split;  // multiple of 32
+    int64_t bpad;   // batch rounded up to 32 (columns of the transposed dy)
+    size_t off_wt, off_dyt, off_p, off_dxp, bytes;  // workspace layout
+};
+
+// Returns false when the sizes do not fit the kernels' index types.
+bool bwd_geom(int nb, bool bf16, int64_t batch, int in, int out, BwdGeom* g);
+
+struct BwdArgs {
+    const void* x;     // [batch, in]
+    const void* coef;  // [out, in, nb]
+    const void* bw;    // [out, in]
+    const void* dy;    // [batch, out]
+    void* dx;          // [batch, in] or null
+    void* dcoef;       // [out, in, nb] or null (then dbw is null too)
+    void* dbw;         // [out, in]
+    void* ws;          // workspace of BwdGeom::bytes
+    int64_t batch;
+    int in;
+    int out;
+    float inv_h, a_int, a_frac;
+};
+
+hipError_t launch_backward(bool bf16, const BwdGeom& g, const BwdArgs& a, hipStream_t s);
+
 }  // namespace kan

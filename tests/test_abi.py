@@ -257,3 +257,55 @@ def test_noalloc_entry_point_host_checks():
                 kb.KAN_NOALLOC_SCRATCH_BYTES
     with pytest.raises(ValueError):
         kb.check(kb.KAN_ERR_SCRATCH_LIMIT)
+
+
+def test_backward_host_checks():
+    """kan_layer_backward rejects invalid arguments on the host, before any
+    HIP call (fake addresses, never dereferenced)."""
+    g = kb.make_grid(10)
+    f32, bad = kb.KAN_F32, kb.KAN_ERR_INVALID_ARG
+    DY, DX, DC, DW = 0x800000000, 0x900000000, 0xA00000000, 0xB00000000
+    st, need = kb.kan_layer_backward_workspace_bytes(g, f32, 16, 4, 4)
+    assert st == kb.KAN_OK and need > 0
+    call = lambda *a: kb.kan_layer_backward(g, f32, 16, 4, 4, *a)
+    assert call(X, C, W, 0, DX, DC, DW, WS, need) == bad               # no dy
+    assert call(X, C, W, DY, DX, DC, 0, WS, need) == bad               # one weight gradient only
+    assert call(X, C, W, DY, DX, 0, DW, WS, need) == bad
+    assert call(X, C, W, DY, 0, 0, 0, WS, need) == bad                 # nothing requested
+    assert call(X, 0, W, DY, DX, DC, DW, WS, need) == bad              # dx needs the weights
+    assert call(X, C, W, DY, DX, DC, DW, WS, need - 1) == bad          # short workspace
+    assert call(X, C, W, DY, DX, DC, DW, WS + 8, need) == bad          # misaligned workspace
+    assert call(X, C, W, DY, DX + 2, DC, DW, WS, need) == bad          # misaligned dx
+    assert call(X, C, W, DY, X + 16, DC, DW, WS, need) == bad          # dx over x
+    assert call(X, C, W, DY, DX, DY, DW, WS, need) == bad              # dcoef over dy
+    assert call(X, C, W, DY, DX, DC, DC + 16, WS, need) == bad         # outputs overlapping
+    assert call(X, C, W, DY, DX, DC, DW, DX - 16, need) == bad         # workspace over dx
+    assert kb.kan_layer_backward(g, f32, -1, 4, 4, X, C, W, DY, DX, DC, DW, WS, need) == bad
+    assert kb.kan_layer_backward(kb.make_grid(10, spline_order=2), f32, 16, 4, 4, X, C, W, DY,
+                                 DX, DC, DW, WS, need) == kb.KAN_ERR_UNSUPPORTED
+    # an empty batch needing only dx: nothing to do
+    assert kb.kan_layer_backward(g, f32, 0, 4, 4, 0, C, W, 0, DX, 0, 0, WS, need) == kb.KAN_OK
+    lib = kb.load_library()
+    assert lib.kan_layer_backward_workspace_bytes(ctypes.byref(g), 0, 16, 4, 4, None) == bad
+    assert kb.kan_layer_backward_workspace_bytes(g, f32, -1, 4, 4)[0] == bad
+
+
+@pytest.mark.parametrize("G,n_in,n_out,B,bf16", [(10, 784, 256, 65536, True),
+                                                 (10, 784, 256, 65536, False),
+                                                 (200, 128, 128, 8192, False),
+                                                 (5, 2, 5, 1024, False)])
+def test_backward_workspace_bytes(G, n_in, n_out, B, bf16):
+    """The workspace holds the packed weights of the dx contraction, dy
+    transposed (padded to 32 outputs and 32 rows) and the fp32 partial weight
+    gradients of at most 256 batch splits' worth of workgroups."""
+    dt = kb.KAN_BF16 if bf16 else kb.KAN_F32
+    st, n = kb.kan_layer_backward_workspace_bytes(kb.make_grid(G), dt, B, n_in, n_out)
+    assert st == kb.KAN_OK
+    es = 2 if bf16 else 4
+    out32 = -(-n_out // 32) * 32
+    bpad = -(-B // 32) * 32
+    assert n >= out32 * bpad * es
+    cp = 16 if G + 4 <= 16 else 32 * -(-(G + 4) // 32)
+    kr = 32 * ((n_in + 1) // 2 if cp == 16 else n_in * cp // 32)
+    assert n >= kr * n_out * es  # packed weights
+    assert n < out32 * bpad * es + 300 * out32 * kr * 4 + kr * 256 * 4 + (1 << 20)
