@@ -81,35 +81,37 @@ __host__ __device__ constexpr int dx_local_row(int i) {
     return 16 * ((i / 4) % 2) + 4 * (i / 8) + i % 4;
 }
 
-// ------------------------------------------------------------ dy transpose
+// -------------------------------------------------------------- transposes
 
-// dyt[o][pos(b)] = dy[b][o], zero-padded to out32 rows and bpad columns.  fp32
-// keeps each 32-row chunk of the batch as its even rows then its odd rows
-// (position 16 (b % 2) + b / 2 in the chunk): a 32x32x2 k-step takes rows 2 j
-// and 2 j + 1 in its two lane halves, so a lane's rows of a chunk are then
-// consecutive.
-template <typename T>
-__global__ __launch_bounds__(256) void transpose_kernel(const T* __restrict__ dy,
-                                                        T* __restrict__ dyt, int64_t batch,
-                                                        int out, int64_t bpad) {
+// dst[c][pos(b)] = src[b][c] for a row-major src [rows, cols], zero-padded to
+// ceil(cols / 32) * 32 rows and rpad columns (rpad a multiple of 32).  With
+// PERM each 32-row chunk of b is stored as its even rows then its odd rows
+// (position 16 (b % 2) + b / 2 in the chunk): a 32x32x2 fp32 k-step takes rows
+// 2 j and 2 j + 1 in its two lane halves, so a lane's rows of a chunk are then
+// consecutive.  Used for dy (the B operand of dW) and x (read per feature for
+// 32 consecutive batch rows by both backward kernels).
+template <typename T, bool PERM>
+__global__ __launch_bounds__(256) void transpose_kernel(const T* __restrict__ src,
+                                                        T* __restrict__ dst, int64_t rows,
+                                                        int cols, int64_t rpad) {
     __shared__ T tile[32][33];
     const int64_t b0 = (int64_t)blockIdx.x * 32;
-    const int o0 = blockIdx.y * 32;
+    const int c0 = blockIdx.y * 32;
     const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;  // 8 rows of 32
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
         const int bl = ty + 8 * k;
         const int64_t b = b0 + bl;
-        const int o = o0 + tx;
-        tile[bl][tx] = (b < batch && o < out) ? dy[b * out + o] : T(0);
+        const int c = c0 + tx;
+        tile[bl][tx] = (b < rows && c < cols) ? src[b * cols + c] : T(0);
     }
     __syncthreads();
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
-        const int ol = ty + 8 * k;
+        const int cl = ty + 8 * k;
         const int bl = tx;
-        const int pos = sizeof(T) == 4 ? 16 * (bl & 1) + (bl >> 1) : bl;
-        dyt[(int64_t)(o0 + ol) * bpad + b0 + pos] = tile[bl][ol];
+        const int pos = PERM ? 16 * (bl & 1) + (bl >> 1) : bl;
+        dst[(int64_t)(c0 + cl) * rpad + b0 + pos] = tile[bl][cl];
     }
 }
 
@@ -156,134 +158,224 @@ __global__ __launch_bounds__(256) void pack_dx_kernel(const T* __restrict__ coef
 
 template <typename T>
 struct DxArgs {
-    const T* x;
+    const T* xt;       // x transposed: [in][bpad]
+    int64_t bpad;
     const T* dy;
     const u32x4* wtp;  // packed weights, 16-byte units
     T* dx;
     float* dxp;        // per-chunk partials when the outputs take several chunks
     int64_t batch;
     int in, out, nb, cp, ntiles, groups, gmax;
+    int tiles_per_split;  // K tiles of a workgroup (blockIdx.z), whole features
     float inv_h, a_int, a_frac;
 };
 
-// One workgroup: 256 batch rows (eight waves of 32) against every K tile, for
-// output chunk blockIdx.y (up to gmax k-step groups, 256 outputs).  SM is
-// the compile-time bound on the groups of a chunk.
-template <typename T, int SM>
-__global__ __launch_bounds__(kThreads) void dx_kernel(DxArgs<T> a) {
+// One workgroup: 8 RF 32 batch rows (eight waves of RF 32-row tiles) against
+// the K tiles of split blockIdx.z, for output chunk blockIdx.y (up to gmax
+// k-step groups, 256 outputs).  SM bounds the groups of a chunk at compile
+// time.  Every A fragment read from LDS feeds RF MFMAs.
+//
+// Pipeline (two LDS stages, two register sets, loop unrolled by two so the
+// sets are compile-time choices): LDS stage t % 2 holds tile t; during tile t
+// the MFMAs and the epilogue run, then the loads of tile t + 2 (weights, and
+// x of the lane's rows for its epilogue) go into register set t % 2 and
+// register set (t + 1) % 2, loaded a whole tile earlier, is stored to stage
+// (t + 1) % 2 before the barrier.
+template <typename T, int SM, int RF, int NW>
+__global__ __launch_bounds__(64 * NW) void dx_kernel(DxArgs<T> a) {
     constexpr bool BF = sizeof(T) == 2;
-    constexpr int UPT = (SM * 64 + kThreads - 1) / kThreads;  // 16-byte units per thread per tile
+    constexpr int NT = 64 * NW;
+    constexpr int UPT = (SM * 64 + NT - 1) / NT;  // 16-byte units per thread per tile
     __shared__ u32x4 lds[2][SM * 64];
+    // per wave: one lane's 16 accumulators at a time (stride 80 bytes, so the
+    // 16-byte writes of 16 lanes fall in distinct banks), read back at the
+    // four columns the clamped derivative can make nonzero
+    __shared__ u32x4 gat[NW][64 * 5];
 
     const int tid = threadIdx.x;
     const int wave = tid >> 6, lane = tid & 63, r = lane & 31, h = lane >> 5;
-    const int64_t row = (int64_t)blockIdx.x * 256 + wave * 32 + r;
-    const int64_t rowc = row < a.batch ? row : a.batch - 1;
+    const int64_t row0 = (int64_t)blockIdx.x * (NW * 32 * RF) + wave * (32 * RF) + r;
+    int64_t rowc[RF];
+#pragma unroll
+    for (int rf = 0; rf < RF; ++rf) {
+        const int64_t row = row0 + 32 * rf;
+        rowc[rf] = row < a.batch ? row : a.batch - 1;
+    }
     const int ch = blockIdx.y;
     const int g0 = ch * a.gmax;
     const int S = min(a.gmax, a.groups - g0);
+    const int t_begin = blockIdx.z * a.tiles_per_split;
+    const int t_end = min(t_begin + a.tiles_per_split, a.ntiles);
 
-    // B operand: the lane's batch row of dy for every k-step group of the chunk
-    u32x4 dyr[SM];
-    const T* dyrow = a.dy + rowc * a.out;
+    // B operands: the lane's batch rows of dy for every k-step group of the chunk
+    u32x4 dyr[RF][SM];
 #pragma unroll
-    for (int s = 0; s < SM; ++s) {
-        float v[B<T>::E];
+    for (int rf = 0; rf < RF; ++rf) {
+        const T* dyrow = a.dy + rowc[rf] * a.out;
 #pragma unroll
-        for (int e = 0; e < B<T>::E; ++e) {
-            const int o = BF ? (g0 + s) * 16 + 8 * h + e : (g0 + s) * 8 + 2 * e + h;
-            v[e] = (s < S && o < a.out) ? B<T>::ld(dyrow + o) : 0.0f;
+        for (int s = 0; s < SM; ++s) {
+            float v[B<T>::E];
+#pragma unroll
+            for (int e = 0; e < B<T>::E; ++e) {
+                const int o = BF ? (g0 + s) * 16 + 8 * h + e : (g0 + s) * 8 + 2 * e + h;
+                v[e] = (s < S && o < a.out) ? B<T>::ld(dyrow + o) : 0.0f;
+            }
+            if constexpr (BF)
+                dyr[rf][s] = u32x4{pack2_bf16(v[0], v[1]), pack2_bf16(v[2], v[3]),
+                                   pack2_bf16(v[4], v[5]), pack2_bf16(v[6], v[7])};
+            else
+                dyr[rf][s] = u32x4{__float_as_uint(v[0]), __float_as_uint(v[1]),
+                                   __float_as_uint(v[2]), __float_as_uint(v[3])};
         }
-        if constexpr (BF)
-            dyr[s] = u32x4{pack2_bf16(v[0], v[1]), pack2_bf16(v[2], v[3]), pack2_bf16(v[4], v[5]),
-                           pack2_bf16(v[6], v[7])};
-        else
-            dyr[s] = u32x4{__float_as_uint(v[0]), __float_as_uint(v[1]), __float_as_uint(v[2]),
-                           __float_as_uint(v[3])};
     }
 
-    u32x4 stg[UPT];
-    auto load_tile = [&](int t) {
-        const u32x4* src = a.wtp + ((int64_t)t * a.groups + g0) * 64;
+    typedef u32x4 WSet[UPT];
+    typedef T XSet[RF];
+    WSet wq[2];
+    XSet xq[2];
+    // Loads of tile t: unconditional (tiles past the split's last, units past
+    // the chunk's and features past `in` re-read valid addresses; their
+    // values are not used), so the compiler's wait before a register set is
+    // used counts only the loads issued after it.  x comes from its
+    // transpose: a lane half reads 32 consecutive rows of one feature.
+    auto issue = [&](int t, WSet& w, XSet& xs) {
+        const int tc = min(t, t_end - 1);
+        const u32x4* src = a.wtp + ((int64_t)tc * a.groups + g0) * 64;
+#pragma unroll
+        for (int k = 0; k < UPT; ++k) w[k] = src[min(tid + k * NT, S * 64 - 1)];
+        const int f = min((32 * tc + 16 * h) / a.cp, a.in - 1);
+#pragma unroll
+        for (int rf = 0; rf < RF; ++rf) xs[rf] = a.xt[(int64_t)f * a.bpad + rowc[rf]];
+    };
+    auto put = [&](int buf, const WSet& w) {
 #pragma unroll
         for (int k = 0; k < UPT; ++k) {
-            const int u = tid + k * kThreads;
-            if (u < S * 64) stg[k] = src[u];
+            const int u = tid + k * NT;
+            if (u < S * 64) lds[buf][u] = w[k];
         }
     };
-    auto store_tile = [&](int buf) {
-#pragma unroll
-        for (int k = 0; k < UPT; ++k) {
-            const int u = tid + k * kThreads;
-            if (u < S * 64) lds[buf][u] = stg[k];
+    auto to_f = [&](T v) -> float {
+        if constexpr (BF) return bf16_to_f32(v);
+        else return v;
+    };
+    auto store_dx = [&](int rf, int f, float v) {
+        const int64_t row = row0 + 32 * rf;
+        if (row < a.batch && f < a.in) {
+            if (a.dxp != nullptr)
+                a.dxp[((int64_t)ch * a.batch + row) * a.in + f] = v;
+            else
+                B<T>::st(a.dx + row * a.in + f, v);
         }
     };
-
-    load_tile(0);
-    store_tile(0);
-    __syncthreads();
 
     const int tpf = a.cp / 32;  // tiles per feature (cp >= 32)
-    float dxacc = 0.0f;
-    for (int t = 0; t < a.ntiles; ++t) {
-        if (t + 1 < a.ntiles) load_tile(t + 1);
-        const int R0 = 32 * t + 16 * h;
-        const int f = R0 / a.cp;
-        const int c0 = R0 - f * a.cp;
-        const float xv = f < a.in ? B<T>::ld(a.x + rowc * a.in + f) : 0.0f;
-
-        floatx16 acc;
+    float dxacc[RF];
 #pragma unroll
-        for (int q = 0; q < 16; ++q) acc[q] = 0.0f;
-        const u32x4* st = lds[t & 1];
+    for (int rf = 0; rf < RF; ++rf) dxacc[rf] = 0.0f;
+
+    // Tile t from LDS stage `buf`, with the x of its epilogue in xs.
+    auto tile = [&](int t, int buf, const XSet& xs) {
+        floatx16 acc[RF];
+#pragma unroll
+        for (int rf = 0; rf < RF; ++rf)
+#pragma unroll
+            for (int q = 0; q < 16; ++q) acc[rf][q] = 0.0f;
+        const u32x4* st = lds[buf];
 #pragma unroll
         for (int s = 0; s < SM; ++s) {
             if (s < S) {
                 const u32x4 w = st[s * 64 + lane];
-                if constexpr (BF) {
-                    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                        __builtin_bit_cast(bf16x8, w), __builtin_bit_cast(bf16x8, dyr[s]), acc, 0,
-                        0, 0);
-                } else {
 #pragma unroll
-                    for (int j = 0; j < 4; ++j)
-                        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(
-                            __uint_as_float(w[j]), __uint_as_float(dyr[s][j]), acc, 0, 0, 0);
+                for (int rf = 0; rf < RF; ++rf) {
+                    if constexpr (BF) {
+                        acc[rf] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                            __builtin_bit_cast(bf16x8, w), __builtin_bit_cast(bf16x8, dyr[rf][s]),
+                            acc[rf], 0, 0, 0);
+                    } else {
+#pragma unroll
+                        for (int j = 0; j < 4; ++j)
+                            acc[rf] = __builtin_amdgcn_mfma_f32_32x32x2f32(
+                                __uint_as_float(w[j]), __uint_as_float(dyr[rf][s][j]), acc[rf], 0,
+                                0, 0);
+                    }
                 }
             }
         }
-
-        // acc[q] = Gm[row][feature f, column c0 + q].  v of column c0 in one
-        // rounding at the magnitude of the group's own coordinates (the
-        // column offset is folded into the fma's exact integer addend), then
-        // v - q exactly where the derivative is nonzero.
-        const float s0 = __builtin_fmaf(xv, a.inv_h, a.a_int + 1.0f - (float)c0) + a.a_frac;
-        float sb = 0.0f;
+        // acc[rf][q] = Gm[row][feature f, column c0 + q].  Of the basis
+        // columns only the four with |v| < 2 have a nonzero derivative: with
+        // s the coordinate of column 0 of the feature, tau = s - floor(s) and
+        // clo = floor(s) - 1, column clo + k has u = tau + 3 - k, where the
+        // derivative of the cubic (its segment form on the span) is
+        //   k = 0: -(1 - tau)^2 / 2      k = 1: (3 tau^2 - 4 tau) / 2
+        //   k = 2: (1 + 2 tau - 3 tau^2) / 2   k = 3: tau^2 / 2.
+        // Column 0 carries the SiLU derivative.  The four accumulators are read
+        // back from a wave-private LDS copy (their index differs per lane).
+        const int R0 = 32 * t + 16 * h;
+        const int f = R0 / a.cp;
+        const int c0 = R0 - f * a.cp;
+        char* gl = reinterpret_cast<char*>(gat[wave]) + lane * 80;
 #pragma unroll
-        for (int q = 1; q < 16; ++q) sb = __builtin_fmaf(acc[q], dbasis(s0 - (float)q), sb);
-        const float d0 = c0 == 0 ? silu_deriv(xv) : a.inv_h * dbasis(s0);
-        const float sum = __builtin_fmaf(acc[0], d0, a.inv_h * sb);
-        auto put = [&](float v) {
-            if (row < a.batch && f < a.in) {
-                if (a.dxp != nullptr)
-                    a.dxp[((int64_t)ch * a.batch + row) * a.in + f] = v;
-                else
-                    B<T>::st(a.dx + row * a.in + f, v);
+        for (int rf = 0; rf < RF; ++rf) {
+            const float xv = f < a.in ? to_f(xs[rf]) : 0.0f;
+            // coordinate of column c0 (its integer offset folded into the fma),
+            // clamped to keep the window index small for far-out inputs; +-Inf
+            // lands outside every column, NaN is carried by the SiLU term
+            const float sc = __builtin_amdgcn_fmed3f(
+                __builtin_fmaf(xv, a.inv_h, a.a_int + 1.0f - (float)c0) + a.a_frac, -8.0f, 24.0f);
+            const float fl = __builtin_floorf(sc);
+            const float tau = sc - fl;
+            const int qlo = (int)fl - 1;  // first window column, relative to c0
+            const float t2 = tau * tau;
+            float d[4];
+            d[0] = -0.5f * (1.0f - tau) * (1.0f - tau);
+            d[1] = __builtin_fmaf(1.5f, t2, -2.0f * tau);
+            d[2] = __builtin_fmaf(-1.5f, t2, __builtin_fmaf(tau, 1.0f, 0.5f));
+            d[3] = 0.5f * t2;
+#pragma unroll
+            for (int m = 0; m < 4; ++m)
+                *reinterpret_cast<floatx4*>(gl + 16 * m) =
+                    floatx4{acc[rf][4 * m], acc[rf][4 * m + 1], acc[rf][4 * m + 2], acc[rf][4 * m + 3]};
+            float sb = 0.0f;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const int q = qlo + k;
+                const int c = c0 + q;
+                const bool ok = q >= 0 && q < 16 && c >= 1 && c <= a.nb;
+                const float g = *reinterpret_cast<const float*>(gl + 4 * min(max(q, 0), 15));
+                sb = __builtin_fmaf(ok ? g : 0.0f, d[k], sb);
             }
-        };
-        if (a.cp == 16) {
-            put(sum);
-        } else {
-            dxacc += sum;
-            if ((t + 1) % tpf == 0) {  // the feature's last tile: add the two lane halves
-                const float tot = dxacc + __shfl_xor(dxacc, 32);
-                if (h == 0) put(tot);
-                dxacc = 0.0f;
+            const float sum = __builtin_fmaf(c0 == 0 ? acc[rf][0] : 0.0f, silu_deriv(xv), a.inv_h * sb);
+            if (a.cp == 16) {
+                store_dx(rf, f, sum);
+            } else {
+                dxacc[rf] += sum;
             }
         }
+        if (a.cp != 16 && (t + 1) % tpf == 0) {  // the feature's last tile: add the two halves
+#pragma unroll
+            for (int rf = 0; rf < RF; ++rf) {
+                const float tot = dxacc[rf] + __shfl_xor(dxacc[rf], 32);
+                if (h == 0) store_dx(rf, f, tot);
+                dxacc[rf] = 0.0f;
+            }
+        }
+    };
 
-        if (t + 1 < a.ntiles) store_tile((t + 1) & 1);
+    issue(t_begin, wq[0], xq[0]);
+    issue(t_begin + 1, wq[1], xq[1]);
+    put(0, wq[0]);
+    __syncthreads();
+    for (int t = t_begin; t < t_end; t += 2) {
+        tile(t, 0, xq[0]);
+        issue(t + 2, wq[0], xq[0]);
+        if (t + 1 < t_end) put(1, wq[1]);
         __syncthreads();
+        if (t + 1 < t_end) {
+            tile(t + 1, 1, xq[1]);
+            issue(t + 3, wq[1], xq[1]);
+            if (t + 2 < t_end) put(0, wq[0]);
+            __syncthreads();
+        }
     }
 }
 
@@ -303,7 +395,7 @@ __global__ __launch_bounds__(256) void dx_reduce_kernel(const float* __restrict_
 
 template <typename T>
 struct DwArgs {
-    const T* x;
+    const T* xt;    // x transposed: [in][bpad]
     const T* dyt;   // [out32][bpad]
     float* P;       // [split][out32][kr] partial sums of dW^T / 2
     int64_t batch, bpad;
@@ -311,39 +403,44 @@ struct DwArgs {
     float inv_h, a_int, a_frac;
 };
 
-// Workgroup: K rows [kt0, kt0 + KT) x outputs [ot0, ot0 + OT) over the batch
-// rows of split blockIdx.y.  Wave (kg, oh) holds two 32-row K tiles (RF = 2)
-// by NFW 32-output fragments, so every B fragment read from LDS feeds two
-// MFMAs and every generated A element NFW.  Per chunk of 32 batch rows the
-// workgroup stages the transposed dy of its outputs (plain copies of
-// contiguous runs) and x / silu(x) / 2 of its features (fp32, transposed to
-// batch-fastest) in LDS, double-buffered; each lane generates its A rows'
-// values N_c(x) / 2 (or silu / 2) at its batch rows.
+// Workgroup: the 256 K rows [kt0, kt0 + 256) x outputs [ot0, ot0 + OT) over
+// the batch rows of split blockIdx.y.  Wave (kg, oh) holds RF = OH 32-row K
+// tiles by NFW 32-output fragments (8 / OH K groups of RF tiles: 256 rows).
+//
+// Per chunk of 32 batch rows the workgroup stages in LDS, double-buffered:
+//   * the transposed dy of its outputs (plain copies of contiguous runs);
+//   * the chunk of the A operand (K rows x 32 batch rows: N_c(x) / 2 and
+//     silu(x) / 2), built once per workgroup: each thread owns (batch row,
+//     feature) pairs and writes only the four columns the clamped form can
+//     make nonzero (c = floor(s) - 1 .. floor(s) + 2, s the coordinate of
+//     column 0) and the SiLU column, after clearing the four it wrote two
+//     chunks earlier in the same stage.  Every other entry stays 0 (the
+//     stages start cleared), which is the value of the clamped form there.
+// Each wave then reads its A and B fragments from LDS: every A fragment
+// feeds NFW MFMAs and every B fragment RF.
 template <typename T, int OH, int NFW>
 __global__ __launch_bounds__(kThreads) void dw_kernel(DwArgs<T> a) {
     constexpr bool BF = sizeof(T) == 2;
-    constexpr int RF = 2;
+    constexpr int RF = OH;
     constexpr int KG = 8 / OH;
-    constexpr int KT = KG * RF * 32;
+    constexpr int KT = KG * RF * 32;            // 256
     constexpr int OT = OH * NFW * 32;
     constexpr int NFEAT = KT / 16 + 2;          // features a workgroup's K rows touch, at most
-    constexpr int UR = BF ? 4 : 8;              // 16-byte units of a chunk's dy run per output
+    constexpr int UR = BF ? 4 : 8;              // 16-byte units of a chunk's 32 batch values
     constexpr int ROWU = UR + 1;                // LDS row stride in units (one unit of padding)
-    constexpr int DU = (OT * UR + kThreads - 1) / kThreads;    // dy units per thread
-    constexpr int XU = (32 * NFEAT + kThreads - 1) / kThreads;  // x values per thread
+    constexpr int ES = sizeof(T);
+    constexpr int DU = (OT * UR + kThreads - 1) / kThreads;     // dy units per thread
+    constexpr int XU = (32 * NFEAT + kThreads - 1) / kThreads;  // (row, feature) pairs per thread
+    static_assert(KT == 256, "K rows per workgroup");
     __shared__ u32x4 dys[2][OT * ROWU];
-    __shared__ __attribute__((aligned(16))) float xs[2][NFEAT][32];
-    __shared__ __attribute__((aligned(16))) float ss[2][NFEAT][32];
+    __shared__ u32x4 as[2][KT * ROWU];
     // features with a NaN input in this workgroup's rows: their basis
-    // gradients are NaN (N_j(NaN) is NaN; the clamp in half_basis would
-    // otherwise swallow it)
+    // gradients are NaN (N_j(NaN) is NaN; the clamped form would give 0)
     __shared__ int nanf[NFEAT];
 
     const int tid = threadIdx.x;
     const int wave = tid >> 6, lane = tid & 63, r = lane & 31, h = lane >> 5;
     const int kg = wave / OH, oh = wave % OH;
-    for (int i = tid; i < NFEAT; i += kThreads) nanf[i] = 0;
-    __syncthreads();
     const int kt0 = blockIdx.x * KT;
     const int ot0 = blockIdx.z * OT;
     const int F0 = kt0 / a.cp;
@@ -353,61 +450,95 @@ __global__ __launch_bounds__(kThreads) void dw_kernel(DwArgs<T> a) {
     const int64_t b_end = min(b_begin + a.rows_per_split, a.bpad);
     const int nchunks = (int)((b_end - b_begin) / 32);
 
-    // the lane's A rows: K row R = kt0 + 32 (kg RF + rt) + r
-    int fl[RF];
-    float cj[RF];
-    bool sil[RF];
-#pragma unroll
-    for (int rt = 0; rt < RF; ++rt) {
-        const int R = kt0 + 32 * (kg * RF + rt) + r;
-        const int f = R / a.cp;
-        const int c = R - f * a.cp;
-        fl[rt] = min(max(f - F0, 0), NFEAT - 1);
-        cj[rt] = a.a_int + 1.0f - (float)c;
-        sil[rt] = c == 0;
-    }
+    for (int i = tid; i < NFEAT; i += kThreads) nanf[i] = 0;
+    for (int i = tid; i < 2 * KT * ROWU; i += kThreads) (&as[0][0])[i] = u32x4{0u, 0u, 0u, 0u};
 
-    u32x4 dreg[DU];
-    float xreg[XU];
-    auto load_chunk = [&](int64_t b0) {
+    typedef u32x4 DSet[DU];
+    typedef T XSet[XU];
+    DSet dq[2];
+    XSet xq[2];
+    int prev[2][XU];  // first window column written two chunks ago in each stage (or -8)
+#pragma unroll
+    for (int k = 0; k < XU; ++k) prev[0][k] = prev[1][k] = -8;
+
+    // Loads of chunk ck: unconditional (chunks past the split's last, units
+    // past the tile's and features past `in` re-read valid addresses; their
+    // values are not used or are replaced), so the compiler's wait before a
+    // register set is used counts only the loads issued after it.  Rows past
+    // the batch are zero in both transposes.
+    auto issue = [&](int ck, DSet& d, XSet& xs) {
+        const int64_t b0 = b_begin + 32 * (int64_t)min(ck, nchunks - 1);
 #pragma unroll
         for (int k = 0; k < DU; ++k) {
-            const int u = tid + k * kThreads;
-            const int o = u / UR, w = u % UR;
-            u32x4 v = {0u, 0u, 0u, 0u};
-            if (u < OT * UR && ot0 + o < a.out32)
-                v = *reinterpret_cast<const u32x4*>(
-                    reinterpret_cast<const char*>(a.dyt + (int64_t)(ot0 + o) * a.bpad + b0) +
-                    16 * w);
-            dreg[k] = v;
+            const int u = min(tid + k * kThreads, OT * UR - 1);
+            const int o = min(ot0 + u / UR, a.out32 - 1), w = u % UR;
+            d[k] = *reinterpret_cast<const u32x4*>(
+                reinterpret_cast<const char*>(a.dyt + (int64_t)o * a.bpad + b0) + 16 * w);
         }
 #pragma unroll
         for (int k = 0; k < XU; ++k) {
-            const int idx = tid + k * kThreads;
-            float v = 0.0f;
-            if (idx < 32 * nfeat) {
-                const int bl = idx / nfeat, f = F0 + idx % nfeat;
-                const int64_t b = b0 + bl;
-                if (b < a.batch && f < a.in) v = B<T>::ld(a.x + b * a.in + f);
-            }
-            xreg[k] = v;
+            const int idx = min(tid + k * kThreads, 32 * nfeat - 1);
+            const int bl = idx % 32, f = min(F0 + idx / 32, a.in - 1);
+            xs[k] = a.xt[(int64_t)f * a.bpad + b0 + bl];
         }
     };
-    auto store_chunk = [&](int buf) {
+    // one A entry: K row R (absolute), batch row bl of the chunk
+    auto put_a = [&](int buf, int R, int bl, float v) {
+        const int lr = R - kt0;
+        if (lr >= 0 && lr < KT) {
+            const int pos = BF ? bl : 16 * (bl & 1) + (bl >> 1);
+            char* p = reinterpret_cast<char*>(&as[buf][lr * ROWU]) + pos * ES;
+            if constexpr (BF)
+                *reinterpret_cast<uint16_t*>(p) = f32_to_bf16(v);
+            else
+                *reinterpret_cast<float*>(p) = v;
+        }
+    };
+    auto stage = [&](int buf, const DSet& d, const XSet& xs, int (&pv)[XU]) {
 #pragma unroll
         for (int k = 0; k < DU; ++k) {
             const int u = tid + k * kThreads;
-            if (u < OT * UR) dys[buf][(u / UR) * ROWU + u % UR] = dreg[k];
+            if (u < OT * UR) dys[buf][(u / UR) * ROWU + u % UR] = d[k];
         }
 #pragma unroll
         for (int k = 0; k < XU; ++k) {
             const int idx = tid + k * kThreads;
             if (idx < 32 * nfeat) {
-                const int bl = idx / nfeat, f = idx % nfeat;
-                const int pos = BF ? bl : 16 * (bl & 1) + (bl >> 1);
-                xs[buf][f][pos] = xreg[k];
-                ss[buf][f][pos] = half_silu_b(xreg[k]);
-                if (xreg[k] != xreg[k]) nanf[f] = 1;
+                const int bl = idx % 32, fl = idx / 32;
+                const int Rf = (F0 + fl) * a.cp;  // K row of the feature's column 0
+                float xv;
+                if constexpr (BF) xv = bf16_to_f32(xs[k]);
+                else xv = xs[k];
+                if (F0 + fl >= a.in) xv = 0.0f;  // (a padding feature)
+                // clear the window written two chunks ago in this stage
+#pragma unroll
+                for (int m = 0; m < 4; ++m) {
+                    const int c = pv[k] + m;
+                    if (c >= 1 && c <= a.nb) put_a(buf, Rf + c, bl, 0.0f);
+                }
+                put_a(buf, Rf, bl, half_silu_b(xv));
+                if (xv != xv) {
+                    nanf[fl] = 1;
+                    pv[k] = -8;
+                    continue;
+                }
+                // coordinate of column 0 (clamped so that the column index
+                // stays small for far-out or infinite inputs), the window's
+                // first column, then each value with its column folded into
+                // the fma's exact integer addend
+                const float s0 = __builtin_amdgcn_fmed3f(
+                    __builtin_fmaf(xv, a.inv_h, a.a_int + 1.0f) + a.a_frac, -8.0f,
+                    (float)(a.nb + 8));
+                const int clo = (int)__builtin_floorf(s0) - 1;
+                pv[k] = clo;
+#pragma unroll
+                for (int m = 0; m < 4; ++m) {
+                    const int c = clo + m;
+                    if (c >= 1 && c <= a.nb) {
+                        const float v = __builtin_fmaf(xv, a.inv_h, a.a_int + 1.0f - (float)c) + a.a_frac;
+                        put_a(buf, Rf + c, bl, half_basis(v));
+                    }
+                }
             }
         }
     };
@@ -420,43 +551,24 @@ __global__ __launch_bounds__(kThreads) void dw_kernel(DwArgs<T> a) {
 #pragma unroll
             for (int q = 0; q < 16; ++q) acc[rt][nf][q] = 0.0f;
 
-    if (nchunks > 0) {
-        load_chunk(b_begin);
-        store_chunk(0);
-    }
-    __syncthreads();
-    for (int ck = 0; ck < nchunks; ++ck) {
-        const int buf = ck & 1;
-        if (ck + 1 < nchunks) load_chunk(b_begin + 32 * (int64_t)(ck + 1));
+    auto chunk = [&](int buf) {
         const char* dl = reinterpret_cast<const char*>(dys[buf]);
+        const char* al = reinterpret_cast<const char*>(as[buf]);
         if constexpr (BF) {
 #pragma unroll
             for (int s = 0; s < 2; ++s) {  // k-steps of 16 batch rows
                 bf16x8 A[RF];
 #pragma unroll
                 for (int rt = 0; rt < RF; ++rt) {
-                    const floatx4* xp = reinterpret_cast<const floatx4*>(&xs[buf][fl[rt]][16 * s + 8 * h]);
-                    const floatx4* sp = reinterpret_cast<const floatx4*>(&ss[buf][fl[rt]][16 * s + 8 * h]);
-                    float v[8];
-#pragma unroll
-                    for (int m = 0; m < 2; ++m) {
-                        const floatx4 xv = xp[m], sv = sp[m];
-#pragma unroll
-                        for (int e = 0; e < 4; ++e) {
-                            const float bv = half_basis(
-                                __builtin_fmaf(xv[e], a.inv_h, cj[rt]) + a.a_frac);
-                            v[4 * m + e] = sil[rt] ? sv[e] : bv;
-                        }
-                    }
+                    const int lr = 32 * (kg * RF + rt) + r;
                     A[rt] = __builtin_bit_cast(
-                        bf16x8, u32x4{pack2_bf16(v[0], v[1]), pack2_bf16(v[2], v[3]),
-                                      pack2_bf16(v[4], v[5]), pack2_bf16(v[6], v[7])});
+                        bf16x8, *reinterpret_cast<const u32x4*>(al + lr * ROWU * 16 + 32 * s + 16 * h));
                 }
 #pragma unroll
                 for (int nf = 0; nf < NFW; ++nf) {
                     const int o = (oh * NFW + nf) * 32 + r;
                     const bf16x8 Bv = __builtin_bit_cast(
-                        bf16x8, *reinterpret_cast<const u32x4*>(dl + (o * ROWU) * 16 + 32 * s + 16 * h));
+                        bf16x8, *reinterpret_cast<const u32x4*>(dl + o * ROWU * 16 + 32 * s + 16 * h));
 #pragma unroll
                     for (int rt = 0; rt < RF; ++rt)
                         acc[rt][nf] =
@@ -469,19 +581,14 @@ __global__ __launch_bounds__(kThreads) void dw_kernel(DwArgs<T> a) {
                 floatx4 A[RF];
 #pragma unroll
                 for (int rt = 0; rt < RF; ++rt) {
-                    const floatx4 xv = *reinterpret_cast<const floatx4*>(&xs[buf][fl[rt]][16 * h + 4 * jg]);
-                    const floatx4 sv = *reinterpret_cast<const floatx4*>(&ss[buf][fl[rt]][16 * h + 4 * jg]);
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const float bv = half_basis(__builtin_fmaf(xv[e], a.inv_h, cj[rt]) + a.a_frac);
-                        A[rt][e] = sil[rt] ? sv[e] : bv;
-                    }
+                    const int lr = 32 * (kg * RF + rt) + r;
+                    A[rt] = *reinterpret_cast<const floatx4*>(al + lr * ROWU * 16 + 64 * h + 16 * jg);
                 }
 #pragma unroll
                 for (int nf = 0; nf < NFW; ++nf) {
                     const int o = (oh * NFW + nf) * 32 + r;
-                    const floatx4 Bv = *reinterpret_cast<const floatx4*>(
-                        dl + (o * ROWU) * 16 + 64 * h + 16 * jg);
+                    const floatx4 Bv =
+                        *reinterpret_cast<const floatx4*>(dl + o * ROWU * 16 + 64 * h + 16 * jg);
 #pragma unroll
                     for (int e = 0; e < 4; ++e)
 #pragma unroll
@@ -491,14 +598,30 @@ __global__ __launch_bounds__(kThreads) void dw_kernel(DwArgs<T> a) {
                 }
             }
         }
-        if (ck + 1 < nchunks) store_chunk(buf ^ 1);
+    };
+
+    // Pipeline: stage ck % 2 holds chunk ck; register set ck % 2 is loaded two
+    // chunks ahead (loop unrolled by two so the sets are compile-time
+    // choices), staged one chunk before its use.
+    __syncthreads();  // (stages cleared, flags reset)
+    issue(0, dq[0], xq[0]);
+    issue(1, dq[1], xq[1]);
+    if (nchunks > 0) stage(0, dq[0], xq[0], prev[0]);
+    __syncthreads();
+    for (int ck = 0; ck < nchunks; ck += 2) {
+        chunk(0);
+        issue(ck + 2, dq[0], xq[0]);
+        if (ck + 1 < nchunks) stage(1, dq[1], xq[1], prev[1]);
         __syncthreads();
+        if (ck + 1 < nchunks) {
+            chunk(1);
+            issue(ck + 3, dq[1], xq[1]);
+            if (ck + 2 < nchunks) stage(0, dq[0], xq[0], prev[0]);
+            __syncthreads();
+        }
     }
 
     // acc[rt][nf][q] = (dW^T / 2)[K row kt0 + 32 (kg RF + rt) + 8 (q / 4) + 4 h + q % 4][output o]
-    // (the lane's A row of tile rt is K row kt0 + 32 (kg RF + rt) + r, but the
-    // accumulator rows are the output rows above: their features are looked
-    // up for the NaN flags)
 #pragma unroll
     for (int rt = 0; rt < RF; ++rt) {
 #pragma unroll
@@ -556,23 +679,29 @@ __global__ __launch_bounds__(256) void dw_reduce_kernel(const float* __restrict_
 
 // ---------------------------------------------------------------- launches
 
-template <typename T, int SM>
+template <typename T, int SM, int RF, int NW = 8>
 hipError_t launch_dx_sm(const BwdGeom& g, const DxArgs<T>& d, hipStream_t s) {
-    const dim3 grid((unsigned)((d.batch + 255) / 256), (unsigned)g.nchunk);
-    hipLaunchKernelGGL((dx_kernel<T, SM>), grid, dim3(kThreads), 0, s, d);
+    constexpr int BM = NW * 32 * RF;
+    const dim3 grid((unsigned)((d.batch + BM - 1) / BM), (unsigned)g.nchunk,
+                    (unsigned)g.dx_ksplit);
+    hipLaunchKernelGGL((dx_kernel<T, SM, RF, NW>), grid, dim3(64 * NW), 0, s, d);
     return hipGetLastError();
 }
 
 template <typename T>
 hipError_t launch_dx(const BwdGeom& g, const DxArgs<T>& d, hipStream_t s) {
     const int sm = min(g.groups, g.gmax);  // groups of the largest chunk
-    if (sm <= 1) return launch_dx_sm<T, 1>(g, d, s);
-    if (sm <= 2) return launch_dx_sm<T, 2>(g, d, s);
-    if (sm <= 4) return launch_dx_sm<T, 4>(g, d, s);
-    if (sm <= 8) return launch_dx_sm<T, 8>(g, d, s);
-    if (sm <= 16) return launch_dx_sm<T, 16>(g, d, s);
+    // two row tiles per wave while their dy registers stay within 64
+    if (g.dx_rf == 2) {
+        if (sm <= 1) return launch_dx_sm<T, 1, 2>(g, d, s);
+        if (sm <= 2) return launch_dx_sm<T, 2, 2>(g, d, s);
+        if (sm <= 4) return launch_dx_sm<T, 4, 2>(g, d, s);
+        if (sm <= 8) return launch_dx_sm<T, 8, 2>(g, d, s);
+        return hipErrorInvalidValue;
+    }
+    if (sm <= 16) return launch_dx_sm<T, 16, 1>(g, d, s);
     if constexpr (sizeof(T) == 4) {
-        if (sm <= 32) return launch_dx_sm<T, 32>(g, d, s);
+        if (sm <= 32) return launch_dx_sm<T, 32, 1>(g, d, s);
     }
     return hipErrorInvalidValue;
 }
@@ -598,6 +727,14 @@ hipError_t backward_t(const BwdGeom& g, const BwdArgs& a, hipStream_t s) {
     char* ws = static_cast<char*>(a.ws);
     const T* x = static_cast<const T*>(a.x);
     hipError_t e = hipSuccess;
+    T* xt = reinterpret_cast<T*>(ws + g.off_xt);
+    if (a.batch > 0) {
+        // x transposed for both kernels (natural row order), dy for dW
+        hipLaunchKernelGGL((transpose_kernel<T, false>),
+                           dim3((unsigned)(g.bpad / 32), (unsigned)((a.in + 31) / 32)), dim3(256), 0,
+                           s, x, xt, a.batch, a.in, g.bpad);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
     if (a.dx != nullptr && a.batch > 0) {
         T* wtp = reinterpret_cast<T*>(ws + g.off_wt);
         const int64_t units = (int64_t)g.ntiles * g.groups * 64;
@@ -606,7 +743,8 @@ hipError_t backward_t(const BwdGeom& g, const BwdArgs& a, hipStream_t s) {
                            a.in, a.out, g.nb, g.cp, g.groups, units);
         if ((e = hipGetLastError()) != hipSuccess) return e;
         DxArgs<T> d;
-        d.x = x;
+        d.xt = xt;
+        d.bpad = g.bpad;
         d.dy = static_cast<const T*>(a.dy);
         d.wtp = reinterpret_cast<const u32x4*>(wtp);
         d.dx = static_cast<T*>(a.dx);
@@ -619,6 +757,7 @@ hipError_t backward_t(const BwdGeom& g, const BwdArgs& a, hipStream_t s) {
         d.ntiles = g.ntiles;
         d.groups = g.groups;
         d.gmax = g.gmax;
+        d.tiles_per_split = g.dx_tiles_per_split;
         d.inv_h = a.inv_h;
         d.a_int = a.a_int;
         d.a_frac = a.a_frac;
@@ -635,13 +774,12 @@ hipError_t backward_t(const BwdGeom& g, const BwdArgs& a, hipStream_t s) {
         int split = 0;
         if (a.batch > 0) {
             T* dyt = reinterpret_cast<T*>(ws + g.off_dyt);
-            hipLaunchKernelGGL(transpose_kernel<T>, dim3((unsigned)(g.bpad / 32),
-                                                         (unsigned)(g.out32 / 32)),
-                               dim3(256), 0, s, static_cast<const T*>(a.dy), dyt, a.batch, a.out,
-                               g.bpad);
+            hipLaunchKernelGGL((transpose_kernel<T, sizeof(T) == 4>),
+                               dim3((unsigned)(g.bpad / 32), (unsigned)(g.out32 / 32)), dim3(256),
+                               0, s, static_cast<const T*>(a.dy), dyt, a.batch, a.out, g.bpad);
             if ((e = hipGetLastError()) != hipSuccess) return e;
             DwArgs<T> d;
-            d.x = x;
+            d.xt = xt;
             d.dyt = dyt;
             d.P = P;
             d.batch = a.batch;
@@ -687,11 +825,30 @@ bool bwd_geom(int nb, bool bf16, int64_t batch, int in, int out, BwdGeom* g) {
     else if (g->out32 <= 64) { g->oh = 2; g->nfw = 1; }
     else if (g->out32 <= 128) { g->oh = 2; g->nfw = 2; }
     else { g->oh = 2; g->nfw = 4; }
-    g->kt = (8 / g->oh) * 2 * 32;
+    g->kt = 256;
     g->ktiles = (g->kr + g->kt - 1) / g->kt;
     const int ot = g->oh * g->nfw * 32;
     g->otiles = (g->out32 + ot - 1) / ot;
     if (g->otiles > 65535) return false;
+    // dx: two 32-row tiles per wave while their dy registers stay within 64
+    // (up to 8 k-step groups: 128 outputs bf16, 64 fp32), and the K tiles split over
+    // workgroups (whole features each) until the grid fills the chip
+    g->dx_rf = (g->groups < g->gmax ? g->groups : g->gmax) <= 8 ? 2 : 1;
+    {
+        const int tpf = g->cp == 16 ? 1 : g->cp / 32;
+        g->dx_bm = 32 * g->dx_rf * 8;  // rows per workgroup (eight waves)
+        const int64_t rblocks = (batch + g->dx_bm - 1) / g->dx_bm;
+        int64_t ks = rblocks * g->nchunk >= 256 ? 1 : (256 + rblocks * g->nchunk - 1) /
+                                                     (rblocks * g->nchunk > 0 ? rblocks * g->nchunk : 1);
+        const int64_t nfe = g->ntiles / tpf;  // features' tile groups
+        if (ks > nfe) ks = nfe > 0 ? nfe : 1;
+        if (ks < 1) ks = 1;
+        int64_t tps = (g->ntiles + ks - 1) / ks;
+        tps = (tps + tpf - 1) / tpf * tpf;
+        g->dx_tiles_per_split = (int)tps;
+        g->dx_ksplit = (int)((g->ntiles + tps - 1) / tps);
+        if (g->dx_ksplit > 65535 || rblocks > 0x7fffffffLL) return false;
+    }
     g->bpad = (batch + 31) / 32 * 32;
     const int64_t nck = g->bpad / 32;
     int64_t split = 256 / ((int64_t)g->ktiles * g->otiles);
@@ -708,6 +865,8 @@ bool bwd_geom(int nb, bool bf16, int64_t batch, int in, int out, BwdGeom* g) {
     off = align256(off + (size_t)g->ntiles * g->groups * 1024);
     g->off_dyt = off;
     off = align256(off + (size_t)g->out32 * (size_t)g->bpad * es);
+    g->off_xt = off;
+    off = align256(off + (size_t)((in + 31) / 32 * 32) * (size_t)g->bpad * es);
     g->off_p = off;
     off = align256(off + (size_t)(g->split > 0 ? g->split : 1) * g->out32 * (size_t)g->kr * 4);
     g->off_dxp = off;

@@ -185,14 +185,18 @@ struct BwdGeom {
     int groups;     // dx: k-step groups over all outputs (16 outputs bf16, 8 fp32)
     int gmax;       // dx: groups per output chunk held in registers (256 outputs)
     int nchunk;     // dx: output chunks (partial dx summed by a reduce when > 1)
+    int dx_rf;      // dx: 32-row batch tiles per wave
+    int dx_bm;      // dx: batch rows per workgroup
+    int dx_ksplit;  // dx: workgroups splitting the K tiles of a row block
+    int dx_tiles_per_split;  // dx: K tiles per such workgroup (whole features)
     int oh, nfw;    // dW: waves across outputs, 32-output fragments per wave
-    int kt;         // dW: K rows per workgroup
+    int kt;         // dW: K rows per workgroup (256)
     int ktiles;     // dW: K tiles of kt rows
     int otiles;     // dW: output tiles of 32 oh nfw columns
     int split;      // dW: batch splits (partials summed by the reduce kernel)
     int rows_per_split;  // multiple of 32
     int64_t bpad;   // batch rounded up to 32 (columns of the transposed dy)
-    size_t off_wt, off_dyt, off_p, off_dxp, bytes;  // workspace layout
+    size_t off_wt, off_dyt, off_xt, off_p, off_dxp, bytes;  // workspace layout
 };
 
 // Returns false when the sizes do not fit the kernels' index types.
