@@ -275,19 +275,21 @@ def _stream(device) -> int:
     return int(_torch().cuda.current_stream(device).cuda_stream)
 
 
-def basis(x, grid_size: int, grid_lo: float = -1.0, grid_hi: float = 1.0, out=None):
-    """phi[..., j] = N_j(x[...]) for j < grid_size + 3 (kan_basis_eval)."""
+def basis(x, grid_size: int, grid_lo: float = -1.0, grid_hi: float = 1.0, out=None,
+          spline_order: int = 3):
+    """phi[..., j] = N_j(x[...]) for j < grid_size + spline_order (kan_basis_eval)."""
     torch = _torch()
     _require_device(x)
-    nb = int(grid_size) + 3
+    nb = int(grid_size) + int(spline_order)
     if out is None:
         out = torch.empty(tuple(x.shape) + (nb,), dtype=x.dtype, device=x.device)
     else:
         _require_device(x, out)
         if out.dtype != x.dtype or tuple(out.shape) != tuple(x.shape) + (nb,):
-            raise ValueError("out must have shape x.shape + (G + 3,) and x's dtype")
+            raise ValueError("out must have shape x.shape + (G + k,) and x's dtype")
     with torch.cuda.device(x.device):
-        check(kan_basis_eval(make_grid(grid_size, grid_lo, grid_hi), _dtype_code(x), x.data_ptr(),
+        check(kan_basis_eval(make_grid(grid_size, grid_lo, grid_hi, spline_order), _dtype_code(x),
+                             x.data_ptr(),
                              x.numel(), out.data_ptr(), _stream(x.device)))
     return out
 
@@ -295,8 +297,9 @@ def basis(x, grid_size: int, grid_lo: float = -1.0, grid_hi: float = 1.0, out=No
 class PackedLayer:
     """Weights of one layer packed by kan_layer_pack (device buffer + shape)."""
 
-    def __init__(self, buf, grid_size, grid_lo, grid_hi, n_in, n_out, dtype):
+    def __init__(self, buf, grid_size, grid_lo, grid_hi, n_in, n_out, dtype, spline_order=3):
         self.buf = buf
+        self.spline_order = int(spline_order)
         self.grid_size, self.grid_lo, self.grid_hi = int(grid_size), float(grid_lo), float(grid_hi)
         self.n_in, self.n_out = int(n_in), int(n_out)
         self.dtype = dtype
@@ -306,12 +309,12 @@ class PackedLayer:
         return int(self.buf.numel())
 
 
-def _check_weights(coef, base_w, grid_size):
+def _check_weights(coef, base_w, grid_size, spline_order=3):
     _require_device(coef, base_w)
     if base_w.dim() != 2 or coef.dim() != 3:
         raise ValueError("expected coef [out, in, G+3], base_w [out, in]")
     n_out, n_in = base_w.shape
-    if tuple(coef.shape) != (n_out, n_in, int(grid_size) + 3):
+    if tuple(coef.shape) != (n_out, n_in, int(grid_size) + int(spline_order)):
         raise ValueError("coef / base_w shapes do not match each other and the grid")
     if coef.dtype != base_w.dtype:
         raise ValueError("coef and base_w must share one dtype")
@@ -319,24 +322,25 @@ def _check_weights(coef, base_w, grid_size):
 
 
 def pack_layer(coef, base_w, grid_size: int, grid_lo: float = -1.0, grid_hi: float = 1.0,
-               out: Optional[PackedLayer] = None) -> PackedLayer:
+               out: Optional[PackedLayer] = None, spline_order: int = 3) -> PackedLayer:
     """kan_layer_pack: coef [out, in, G + 3], base_w [out, in] -> PackedLayer
     (device buffer from torch's allocator, filled on torch's current stream)."""
     torch = _torch()
-    n_in, n_out = _check_weights(coef, base_w, grid_size)
+    n_in, n_out = _check_weights(coef, base_w, grid_size, spline_order)
     dt = _dtype_code(coef)
-    g = make_grid(grid_size, grid_lo, grid_hi)
+    g = make_grid(grid_size, grid_lo, grid_hi, spline_order)
     st, nbytes = kan_layer_packed_bytes(g, dt, n_in, n_out)
     check(st)
     if out is None:
         buf = torch.empty(nbytes, dtype=torch.uint8, device=coef.device)
-        out = PackedLayer(buf, grid_size, grid_lo, grid_hi, n_in, n_out, coef.dtype)
+        out = PackedLayer(buf, grid_size, grid_lo, grid_hi, n_in, n_out, coef.dtype, spline_order)
     elif out.nbytes < nbytes or out.buf.device != coef.device:
         raise ValueError("packed buffer too small or on another device")
     else:
         # the buffer now holds these weights: its geometry follows them
         out.grid_size, out.grid_lo, out.grid_hi = int(grid_size), float(grid_lo), float(grid_hi)
         out.n_in, out.n_out, out.dtype = int(n_in), int(n_out), coef.dtype
+        out.spline_order = int(spline_order)
     with torch.cuda.device(coef.device):
         check(kan_layer_pack(g, dt, n_in, n_out, coef.data_ptr(), base_w.data_ptr(),
                              out.buf.data_ptr(), out.nbytes, _stream(coef.device)))
@@ -359,7 +363,7 @@ def layer_forward_packed(x, packed: PackedLayer, out=None, shape=None):
         _require_device(x, out)
         if out.dtype != x.dtype or tuple(out.shape) != (B, packed.n_out):
             raise ValueError("out must be [B, out] with x's dtype")
-    g = make_grid(packed.grid_size, packed.grid_lo, packed.grid_hi)
+    g = make_grid(packed.grid_size, packed.grid_lo, packed.grid_hi, packed.spline_order)
     with torch.cuda.device(x.device):
         check(kan_layer_forward_packed(g, _dtype_code(x), B, packed.n_in, packed.n_out,
                                        x.data_ptr(), packed.buf.data_ptr(), packed.nbytes,
@@ -368,30 +372,33 @@ def layer_forward_packed(x, packed: PackedLayer, out=None, shape=None):
 
 
 def layer_forward(x, coef, base_w, grid_size: int, grid_lo: float = -1.0, grid_hi: float = 1.0,
-                  out=None, packed: Optional[PackedLayer] = None, shape=None):
+                  out=None, packed: Optional[PackedLayer] = None, shape=None,
+                  spline_order: int = 3):
     """One KAN layer: x [B, in], coef [out, in, G + 3], base_w [out, in] -> y
     [B, out], all of one dtype on one device.  Packs the weights (kan_layer_pack,
     into `packed` if given, else a fresh buffer) and runs
     kan_layer_forward_packed, both on torch's current stream; `shape` forces a
     workgroup shape."""
     _require_device(x)
-    n_in, _ = _check_weights(coef, base_w, grid_size)
+    n_in, _ = _check_weights(coef, base_w, grid_size, spline_order)
     if x.dim() != 2 or x.shape[1] != n_in:
         raise ValueError("x must be [B, in] with coef's in")
     if coef.dtype != x.dtype:
         raise ValueError("x, coef and base_w must share one dtype")
-    p = pack_layer(coef, base_w, grid_size, grid_lo, grid_hi, out=packed)
+    p = pack_layer(coef, base_w, grid_size, grid_lo, grid_hi, out=packed,
+                   spline_order=spline_order)
     return layer_forward_packed(x, p, out=out, shape=shape)
 
 
 def mlp_forward(x, layers: Sequence[Tuple[object, object]], grid_size: int, grid_lo: float = -1.0,
-                grid_hi: float = 1.0, return_all: bool = False):
+                grid_hi: float = 1.0, return_all: bool = False, spline_order: int = 3):
     """Stacked KAN layers; each output feeds the next layer unchanged (values
     off the grid are handled by the clamp of the basis)."""
     h = x
     outs = []
     for coef, base_w in layers:
-        h = layer_forward(h, coef, base_w, grid_size, grid_lo, grid_hi)
+        h = layer_forward(h, coef, base_w, grid_size, grid_lo, grid_hi,
+                          spline_order=spline_order)
         outs.append(h)
     return outs if return_all else h
 

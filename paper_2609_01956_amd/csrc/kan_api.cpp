@@ -22,29 +22,45 @@ bool overlap(const void* p, size_t n, const void* q, size_t m) {
     return a < b + m && b < a + n;
 }
 
-// Validates the grid and dtype and fills the grid constants:
-//   nb = G + 3, inv_h = G / (hi - lo), a_int + a_frac = 1 - lo / h, so that
-//   v_j = u_j - 2 = x * inv_h + (a_int - j) + a_frac  (see kan_device.h).
+constexpr int32_t kMaxDegree = 7;
+
+// Validates the grid and dtype and fills the grid constants (kan_device.h):
+//   nb = G + k; inv_h + inv_lo = G / (hi - lo); a_int + a_frac = (k - 1) / 2 -
+//   lo / h, so that v_j = u_j - (k + 1) / 2 = fma(x, inv_h, a_int - j) +
+//   (x inv_lo + a_frac).
 kan_status check_grid(const kan_grid* grid, kan_dtype dtype, kan::GridConst* gc) {
     if (grid == nullptr) return KAN_ERR_INVALID_ARG;
-    if (grid->spline_order != 3) return KAN_ERR_UNSUPPORTED;
+    const int32_t k = grid->spline_order;
+    if (k < 1 || k > kMaxDegree) return KAN_ERR_UNSUPPORTED;
     if (dtype != KAN_F32 && dtype != KAN_BF16) return KAN_ERR_UNSUPPORTED;
     const int32_t G = grid->grid_size;
     if (G < 1 || G > kMaxGrid) return KAN_ERR_INVALID_ARG;
     const double lo = grid->grid_lo, hi = grid->grid_hi;
     if (!std::isfinite(lo) || !std::isfinite(hi) || !(lo < hi)) return KAN_ERR_INVALID_ARG;
     const double inv_h = (double)G / (hi - lo);
-    if (!std::isfinite(inv_h)) return KAN_ERR_INVALID_ARG;
+    if (!std::isfinite(inv_h) || !std::isfinite((double)(float)inv_h) || (float)inv_h == 0.0f)
+        return KAN_ERR_INVALID_ARG;
     // Keep a_int - j (and x * inv_h near the support) inside fp32's exact
     // integer range.
     const double lim = 4194304.0;  // 2^22
     if (std::fabs(lo) * inv_h > lim || std::fabs(hi) * inv_h > lim) return KAN_ERR_INVALID_ARG;
-    const double A = 1.0 - lo * inv_h;
+    const double A = 0.5 * (k - 1) - lo * inv_h;
     const double ai = std::nearbyint(A);
-    gc->nb = G + 3;
-    gc->inv_h = (float)inv_h;
+    const float ih = (float)inv_h;
+    gc->nb = G + k;
+    gc->k = k;
+    gc->inv_h = ih;
+    gc->inv_lo = (float)(inv_h - (double)ih);
     gc->a_int = (float)ai;
     gc->a_frac = (float)(A - ai);
+    gc->xlim = (float)(std::fmax(std::fabs(lo), std::fabs(hi)) + (k + 2) * (hi - lo) / G);
+    gc->hw = 0.5f * (float)(k + 1);
+    double kf = 1.0, binom = 1.0;
+    for (int i = 2; i <= k; ++i) kf *= i;
+    for (int m = 0; m < 4; ++m) {
+        gc->hc[m] = (float)((m & 1 ? -binom : binom) / (2.0 * kf));
+        binom = binom * (double)(k + 1 - m) / (double)(m + 1);
+    }
     return KAN_OK;
 }
 
@@ -58,7 +74,9 @@ const char* kan_status_string(kan_status status) {
     switch (status) {
         case KAN_OK: return "KAN_OK: success";
         case KAN_ERR_INVALID_ARG: return "KAN_ERR_INVALID_ARG: invalid size, range, pointer, alignment or overlap";
-        case KAN_ERR_UNSUPPORTED: return "KAN_ERR_UNSUPPORTED: only cubic splines (spline_order 3) and f32/bf16 are implemented";
+        case KAN_ERR_UNSUPPORTED:
+            return "KAN_ERR_UNSUPPORTED: spline_order outside 1..7 (the backward: other than 3), or "
+                   "a dtype other than f32/bf16";
         case KAN_ERR_DEVICE: return "KAN_ERR_DEVICE: the HIP runtime rejected a kernel launch";
         case KAN_ERR_SCRATCH_LIMIT:
             return "KAN_ERR_SCRATCH_LIMIT: the layer's packed weights exceed the 16 MiB scratch of "
@@ -103,7 +121,7 @@ static kan_status check_layer(const kan_grid* grid, kan_dtype dtype, int32_t in_
     // offsets over at most kan::kLayerMaxRows rows.
     if ((int64_t)kan::kLayerMaxRows * in_features >= 0x100000000LL) return KAN_ERR_INVALID_ARG;
     if ((int64_t)out_features * in_features * gc->nb >= (1LL << 40)) return KAN_ERR_INVALID_ARG;
-    if (!kan::layer_geom(gc->nb, dtype == KAN_BF16, in_features, out_features, geom))
+    if (!kan::layer_geom(gc->nb, gc->k, dtype == KAN_BF16, in_features, out_features, geom))
         return KAN_ERR_INVALID_ARG;
     return KAN_OK;
 }
@@ -192,8 +210,13 @@ static kan_status launch_forward(const kan::GridConst& gc, const kan::LayerGeom&
     a.nblk_pad = geom.nblk_pad;
     a.nchunks = 0;  // set by the launcher (depends on the tile shape)
     a.inv_h = gc.inv_h;
+    a.inv_lo = gc.inv_lo;
+    a.xlim = gc.xlim;
     a.a_int = gc.a_int;
     a.a_frac = gc.a_frac;
+    a.kdeg = gc.k;
+    a.hw = gc.hw;
+    for (int m = 0; m < 4; ++m) a.hc[m] = gc.hc[m];
     return device_status(kan::launch_layer(dtype == KAN_BF16, geom, cfg, a, s));
 }
 
@@ -346,6 +369,7 @@ kan_status kan_layer_backward_workspace_bytes(const kan_grid* grid, kan_dtype dt
     kan::LayerGeom geom;
     kan_status st = check_layer(grid, dtype, in_features, out_features, &gc, &geom);
     if (st != KAN_OK) return st;
+    if (gc.k != 3) return KAN_ERR_UNSUPPORTED;
     kan::BwdGeom bg;
     st = backward_geom(gc, dtype, batch, in_features, out_features, &bg);
     if (st != KAN_OK) return st;
@@ -362,6 +386,7 @@ kan_status kan_layer_backward(const kan_grid* grid, kan_dtype dtype, int64_t bat
     kan::LayerGeom geom;
     kan_status st = check_layer(grid, dtype, in_features, out_features, &gc, &geom);
     if (st != KAN_OK) return st;
+    if (gc.k != 3) return KAN_ERR_UNSUPPORTED;  // (the backward kernels are cubic)
     kan::BwdGeom bg;
     st = backward_geom(gc, dtype, batch, in_features, out_features, &bg);
     if (st != KAN_OK) return st;
@@ -410,6 +435,8 @@ kan_status kan_layer_backward(const kan_grid* grid, kan_dtype dtype, int64_t bat
     a.in = in_features;
     a.out = out_features;
     a.inv_h = gc.inv_h;
+    a.inv_lo = gc.inv_lo;
+    a.xlim = gc.xlim;
     a.a_int = gc.a_int;
     a.a_frac = gc.a_frac;
     return device_status(kan::launch_backward(dtype == KAN_BF16, bg, a,

@@ -167,7 +167,7 @@ struct DxArgs {
     int64_t batch;
     int in, out, nb, cp, ntiles, groups, gmax;
     int tiles_per_split;  // K tiles of a workgroup (blockIdx.z), whole features
-    float inv_h, a_int, a_frac;
+    float inv_h, inv_lo, xlim, a_int, a_frac;
 };
 
 // One workgroup: 8 RF 32 batch rows (eight waves of RF 32-row tiles) against
@@ -321,7 +321,9 @@ __global__ __launch_bounds__(64 * NW) void dx_kernel(DxArgs<T> a) {
             // clamped to keep the window index small for far-out inputs; +-Inf
             // lands outside every column, NaN is carried by the SiLU term
             const float sc = __builtin_amdgcn_fmed3f(
-                __builtin_fmaf(xv, a.inv_h, a.a_int + 1.0f - (float)c0) + a.a_frac, -8.0f, 24.0f);
+                __builtin_fmaf(xv, a.inv_h, a.a_int + 1.0f - (float)c0) +
+                    coord_lo(xv, a.xlim, a.inv_lo, a.a_frac),
+                -8.0f, 24.0f);
             const float fl = __builtin_floorf(sc);
             const float tau = sc - fl;
             const int qlo = (int)fl - 1;  // first window column, relative to c0
@@ -400,7 +402,7 @@ struct DwArgs {
     float* P;       // [split][out32][kr] partial sums of dW^T / 2
     int64_t batch, bpad;
     int in, out32, nb, cp, kr, rows_per_split;
-    float inv_h, a_int, a_frac;
+    float inv_h, inv_lo, xlim, a_int, a_frac;
 };
 
 // Workgroup: the 256 K rows [kt0, kt0 + 256) x outputs [ot0, ot0 + OT) over
@@ -526,16 +528,16 @@ __global__ __launch_bounds__(kThreads) void dw_kernel(DwArgs<T> a) {
                 // stays small for far-out or infinite inputs), the window's
                 // first column, then each value with its column folded into
                 // the fma's exact integer addend
+                const float lot = coord_lo(xv, a.xlim, a.inv_lo, a.a_frac);
                 const float s0 = __builtin_amdgcn_fmed3f(
-                    __builtin_fmaf(xv, a.inv_h, a.a_int + 1.0f) + a.a_frac, -8.0f,
-                    (float)(a.nb + 8));
+                    __builtin_fmaf(xv, a.inv_h, a.a_int + 1.0f) + lot, -8.0f, (float)(a.nb + 8));
                 const int clo = (int)__builtin_floorf(s0) - 1;
                 pv[k] = clo;
 #pragma unroll
                 for (int m = 0; m < 4; ++m) {
                     const int c = clo + m;
                     if (c >= 1 && c <= a.nb) {
-                        const float v = __builtin_fmaf(xv, a.inv_h, a.a_int + 1.0f - (float)c) + a.a_frac;
+                        const float v = __builtin_fmaf(xv, a.inv_h, a.a_int + 1.0f - (float)c) + lot;
                         put_a(buf, Rf + c, bl, half_basis(v));
                     }
                 }
@@ -759,6 +761,8 @@ hipError_t backward_t(const BwdGeom& g, const BwdArgs& a, hipStream_t s) {
         d.gmax = g.gmax;
         d.tiles_per_split = g.dx_tiles_per_split;
         d.inv_h = a.inv_h;
+        d.inv_lo = a.inv_lo;
+        d.xlim = a.xlim;
         d.a_int = a.a_int;
         d.a_frac = a.a_frac;
         if ((e = launch_dx<T>(g, d, s)) != hipSuccess) return e;
@@ -791,6 +795,8 @@ hipError_t backward_t(const BwdGeom& g, const BwdArgs& a, hipStream_t s) {
             d.kr = g.kr;
             d.rows_per_split = g.rows_per_split;
             d.inv_h = a.inv_h;
+            d.inv_lo = a.inv_lo;
+            d.xlim = a.xlim;
             d.a_int = a.a_int;
             d.a_frac = a.a_frac;
             if ((e = launch_dw<T>(g, d, s)) != hipSuccess) return e;

@@ -1,17 +1,19 @@
 // kan_basis.hip -- basis-only kernel: phi[e, j] = N_j(x[e]) for every input
-// element and every basis j (eq. truncated with the clamp of eq. bounded).
+// element and every basis j (eq. truncated with the clamp of eq. bounded; for
+// degrees other than 3, eq. general_truncated with the clamp to [0, k + 1]).
 //
 // The kernel is bound by HBM writes (nb outputs per input read).  Each
 // 256-thread workgroup owns xb consecutive inputs, i.e. one contiguous
 // xb * nb run of the output:
 //   phase 1  tpx threads per input evaluate its nb values in registers (the
-//            coordinate, then 6 VALU ops for N / 2 and one scale, no span
-//            lookup, no data-dependent branches) and write them to LDS in
-//            output order;
+//            coordinate, then for the cubic 6 VALU ops for N / 2 and one
+//            scale, no span lookup, no data-dependent branches) and write them
+//            to LDS in output order;
 //   phase 2  the workgroup streams the run from LDS to HBM with 16-byte
 //            non-temporal stores, so every store instruction of a wave covers
 //            1 KiB of consecutive output.
-// NaN inputs give NaN outputs: the scale 2 is replaced by the NaN itself.
+// NaN inputs give NaN outputs: the final scale (2 for the cubic's N / 2, else
+// 1) is replaced by the NaN itself.
 #include "kan_internal.h"
 
 namespace kan {
@@ -41,7 +43,17 @@ __device__ __forceinline__ void store_vec<uint16_t>(uint16_t* dst, const float* 
     __builtin_nontemporal_store(v, reinterpret_cast<u16x8*>(dst));
 }
 
-template <typename T>
+// A basis at v = u - (K + 1) / 2, up to the factor kScale<K>: the cubic's
+// two-term form N / 2 (kan_device.h) for K = 3, the reflected general form
+// otherwise.
+template <int K>
+__device__ __forceinline__ float basis_value(float v) {
+    if constexpr (K == 3) return half_basis(v);
+    else return basis_deg<K>(v);
+}
+template <int K> constexpr float kScale = K == 3 ? 2.0f : 1.0f;
+
+template <typename T, int K>
 __global__ __launch_bounds__(kThreads) void basis_kernel(const T* __restrict__ x, int64_t n,
                                                          T* __restrict__ phi, GridConst g,
                                                          int tpx, int jc, int vec) {
@@ -58,21 +70,22 @@ __global__ __launch_bounds__(kThreads) void basis_kernel(const T* __restrict__ x
     const int je = min(jb + jc, nb);
     if (el < cnt) {
         const float xv = Storage<T>::load(x + e0 + el);
-        const float scale = (xv != xv) ? xv : 2.0f;  // half_basis gives N / 2
+        const float scale = (xv != xv) ? xv : kScale<K>;  // a NaN input gives NaN values
         float cj = g.a_int - (float)jb;
         float* dst = stage + el * nb;
-        if (tpx == 1 && g.a_frac == 0.0f) {
-            // (uniform trip count; on grids whose lo / h is an integer the
-            // coordinate is the fma alone)
+        if (tpx == 1 && g.a_frac == 0.0f && g.inv_lo == 0.0f) {
+            // (uniform trip count; on grids whose 1 / h and lo / h are exact
+            // the coordinate is the fma alone)
 #pragma unroll 4
             for (int j = 0; j < nb; ++j) {
-                dst[j] = half_basis(__builtin_fmaf(xv, g.inv_h, cj)) * scale;
+                dst[j] = basis_value<K>(__builtin_fmaf(xv, g.inv_h, cj)) * scale;
                 cj -= 1.0f;
             }
         } else {
+            const float lo = coord_lo(xv, g.xlim, g.inv_lo, g.a_frac);
 #pragma unroll 4
             for (int j = jb; j < je; ++j) {
-                dst[j] = half_basis(coord(xv, g, cj)) * scale;
+                dst[j] = basis_value<K>(__builtin_fmaf(xv, g.inv_h, cj) + lo) * scale;
                 cj -= 1.0f;
             }
         }
@@ -114,12 +127,27 @@ BasisLaunch plan_basis(int64_t n, int nb, const void* phi) {
     return L;
 }
 
+template <typename T, int K>
+static hipError_t launch_k(const T* x, int64_t n, T* phi, const GridConst& g,
+                           const BasisLaunch& L, hipStream_t s) {
+    hipLaunchKernelGGL((basis_kernel<T, K>), dim3((unsigned)L.blocks), dim3(kThreads), L.lds, s,
+                       x, n, phi, g, L.tpx, L.jc, L.vec ? 1 : 0);
+    return hipGetLastError();
+}
+
 template <typename T>
 static hipError_t launch(const T* x, int64_t n, T* phi, const GridConst& g, const BasisLaunch& L,
                          hipStream_t s) {
-    hipLaunchKernelGGL(basis_kernel<T>, dim3((unsigned)L.blocks), dim3(kThreads), L.lds, s, x, n,
-                       phi, g, L.tpx, L.jc, L.vec ? 1 : 0);
-    return hipGetLastError();
+    switch (g.k) {
+        case 1: return launch_k<T, 1>(x, n, phi, g, L, s);
+        case 2: return launch_k<T, 2>(x, n, phi, g, L, s);
+        case 3: return launch_k<T, 3>(x, n, phi, g, L, s);
+        case 4: return launch_k<T, 4>(x, n, phi, g, L, s);
+        case 5: return launch_k<T, 5>(x, n, phi, g, L, s);
+        case 6: return launch_k<T, 6>(x, n, phi, g, L, s);
+        case 7: return launch_k<T, 7>(x, n, phi, g, L, s);
+        default: return hipErrorInvalidValue;
+    }
 }
 
 hipError_t launch_basis_f32(const float* x, int64_t n, float* phi, const GridConst& g,

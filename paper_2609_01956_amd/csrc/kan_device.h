@@ -41,12 +41,67 @@ typedef __bf16 bf16x16 __attribute__((ext_vector_type(16)));
 typedef uint16_t u16x8 __attribute__((ext_vector_type(8)));
 
 // Grid constants shared by all kernels (computed on the host in double).
+// For degree k the coordinate of basis j relative to the centre of its
+// support is v_j = u_j - (k + 1) / 2 = x / h - lo / h + (k - 1) / 2 - j, formed as
+//     v_j = fma(x, inv_h, a_int - j) + (x' inv_lo + a_frac),
+// with inv_h + inv_lo = 1 / h (inv_lo the fp32 rounding residual of 1 / h,
+// 0 when 1 / h is exact) and a_int + a_frac = (k - 1) / 2 - lo / h, and x'
+// the input clamped to [-xlim, xlim] (a range past every support: the
+// correction stays finite for infinite inputs, whose basis is 0 anyway).
 struct GridConst {
-    int nb;        // G + 3 basis functions per input
+    int nb;        // G + k basis functions per input
+    int k;         // spline degree, 1 .. 7
     float inv_h;   // G / (hi - lo), rounded to fp32
-    float a_int;   // nearest integer to 1 - lo / h
-    float a_frac;  // (1 - lo / h) - a_int, rounded to fp32
+    float inv_lo;  // G / (hi - lo) - inv_h, rounded to fp32
+    float a_int;   // nearest integer to (k - 1) / 2 - lo / h
+    float a_frac;  // ((k - 1) / 2 - lo / h) - a_int, rounded to fp32
+    float xlim;    // max(|lo|, |hi|) + (k + 2) h
+    float hw;      // (k + 1) / 2, the half width of a support
+    float hc[4];   // (-1)^m C(k + 1, m) / (2 k!), m = 0 .. 3
 };
+
+// x' inv_lo + a_frac (see GridConst).
+__device__ __forceinline__ float coord_lo(float x, float xlim, float inv_lo, float a_frac) {
+    return __builtin_fmaf(__builtin_amdgcn_fmed3f(x, -xlim, xlim), inv_lo, a_frac);
+}
+
+// N_k(u) / 2 at v = u - (k + 1) / 2 for a degree k known at run time
+// (eq. general_truncated with the clamp of eq. bounded, at the reflected
+// coordinate w = hw - min(|v|, hw), where only the terms m < w survive:
+// N / 2 = sum_m hc[m] (w - m)_+^k).
+__device__ __forceinline__ float half_basis_deg(float v, int k, float hw, const float (&hc)[4]) {
+    const float w = hw - __builtin_fminf(__builtin_fabsf(v), hw);
+    float s = 0.0f;
+#pragma unroll
+    for (int m = 0; m < 4; ++m) {
+        const float z = __builtin_fmaxf(w - (float)m, 0.0f);
+        float p = z;
+        for (int i = 1; i < k; ++i) p *= z;
+        s = __builtin_fmaf(hc[m], p, s);
+    }
+    return s;
+}
+
+// N_K(u) at v = u - (K + 1) / 2 for a compile-time degree K, the same form.
+template <int K>
+__device__ __forceinline__ float basis_deg(float v) {
+    constexpr float hw = 0.5f * (K + 1);
+    constexpr int M = (K + 1) / 2;  // terms m < hw
+    const float w = hw - __builtin_fminf(__builtin_fabsf(v), hw);
+    float kf = 1.0f;
+    for (int i = 2; i <= K; ++i) kf *= (float)i;
+    float s = 0.0f, binom = 1.0f;
+#pragma unroll
+    for (int m = 0; m < M + (K % 2 == 0 ? 1 : 0) && m < 4; ++m) {
+        const float z = __builtin_fmaxf(w - (float)m, 0.0f);
+        float p = z;
+#pragma unroll
+        for (int i = 1; i < K; ++i) p *= z;
+        s = __builtin_fmaf((m & 1 ? -binom : binom) / kf, p, s);
+        binom = binom * (float)(K + 1 - m) / (float)(m + 1);
+    }
+    return s;
+}
 
 constexpr float kCbrtTwoThirds = 0.87358046473629571f;  // (2/3)^(1/3)
 constexpr float kCbrtOneThird = 0.69336127435063470f;   // (1/3)^(1/3)
@@ -61,9 +116,9 @@ __device__ __forceinline__ float half_basis(float v) {
     return __builtin_fmaf(P * P, P, -(Q * Q * Q));
 }
 
-// v_j = u_j - 2 for basis j, given cj = a_int - j.
+// v_j = u_j - (k + 1) / 2 for basis j, given cj = a_int - j.
 __device__ __forceinline__ float coord(float x, const GridConst& g, float cj) {
-    return __builtin_fmaf(x, g.inv_h, cj) + g.a_frac;
+    return __builtin_fmaf(x, g.inv_h, cj) + coord_lo(x, g.xlim, g.inv_lo, g.a_frac);
 }
 
 // silu(x) = x / (1 + exp(-x)).

@@ -57,7 +57,8 @@ __host__ __device__ constexpr int layer_chunk_blocks(bool bf16, int nf) {
 }
 
 struct LayerGeom {
-    int nb;       // G + 3
+    int nb;       // G + k
+    int kdeg;     // spline degree k
     int kj;       // columns per block (8 bf16, 2 fp32)
     int nsb;      // blocks per feature pair, ceil((nb + 1) / kj)
     int npairs;   // ceil(in / 2)
@@ -76,7 +77,7 @@ struct LayerGeom {
 };
 
 // Returns false when the sizes do not fit the index types of the kernels.
-bool layer_geom(int nb, bool bf16, int in, int out, LayerGeom* g);
+bool layer_geom(int nb, int kdeg, bool bf16, int in, int out, LayerGeom* g);
 
 // Workgroup shape of the fused kernel: nw waves, each holding rf 32-row MFMA
 // tiles of nf / cs 32-column fragments; wk waves split the blocks (K) of a
@@ -147,8 +148,13 @@ struct LayerArgs {
     int nblk_pad;     // blocks per N tile in the packed buffer
     int nchunks;      // nblk_pad / blocks-per-chunk
     float inv_h;      // see GridConst
+    float inv_lo;
+    float xlim;
     float a_int;
     float a_frac;
+    int kdeg;         // spline degree (3: the cubic kernels; else the run-time degree form)
+    float hw;
+    float hc[4];
 };
 
 // Device address and size of the calling thread's current device's copy of
@@ -214,7 +220,7 @@ struct BwdArgs {
     int64_t batch;
     int in;
     int out;
-    float inv_h, a_int, a_frac;
+    float inv_h, inv_lo, xlim, a_int, a_frac;
 };
 
 hipError_t launch_backward(bool bf16, const BwdGeom& g, const BwdArgs& a, hipStream_t s);

@@ -88,8 +88,9 @@ __global__ __launch_bounds__(kThreads) void pack_kernel(const T* __restrict__ co
 
 // ------------------------------------------------------------------ planning
 
-bool layer_geom(int nb, bool bf16, int in, int out, LayerGeom* g) {
+bool layer_geom(int nb, int kdeg, bool bf16, int in, int out, LayerGeom* g) {
     g->nb = nb;
+    g->kdeg = kdeg;
     g->kj = bf16 ? 8 : 2;
     g->nsb = (nb + 1 + g->kj - 1) / g->kj;
     g->npairs = (in + 1) / 2;
@@ -110,12 +111,16 @@ bool layer_geom(int nb, bool bf16, int in, int out, LayerGeom* g) {
     g->nblk = (int)nblk;
     g->nblk_pad = (int)nblk_pad;
     g->kb = kb;
-    g->sparse = bf16 && g->nsb == 2;
+    // (the structured-sparse operand holds the four nonzero cubic columns)
+    g->sparse = bf16 && g->nsb == 2 && kdeg == 3;
     g->packed_bytes = (size_t)g->ntiles * (size_t)nblk_pad * (size_t)blk_bytes;
     return true;
 }
 
 bool layer_cfg_valid(const LayerGeom& g, const LayerCfg& c) {
+    // other degrees: the run-time degree build of one shape (one row tile per
+    // wave, four waves, whole K and N tile)
+    if (g.kdeg != 3) return c.rf == 1 && c.wk == 1 && c.nw == 4 && c.cs == 1;
     // sparse: one row tile per wave, where 256-column tiles take
     // four-wave workgroups only on column slices (the whole 256 columns with
     // four waves' larger share of the weight staging exceed 256 registers
@@ -135,6 +140,7 @@ bool layer_cfg_valid(const LayerGeom& g, const LayerCfg& c) {
 }
 
 LayerCfg plan_layer(const LayerGeom& g, bool bf16, int64_t batch) {
+    if (g.kdeg != 3) return LayerCfg{1, 1, 4, 1};
     auto wgs = [&](const LayerCfg& c) {
         const int64_t bm = layer_cfg_rows(c);
         return ((batch + bm - 1) / bm) * g.ntiles * c.cs;

@@ -181,8 +181,10 @@ struct Occ {
 // take the two column halves of the tile, and each generates the A of one of
 // the group's two row tiles and passes it to the other through LDS (half the
 // LDS bytes of B per MFMA of one-row-tile waves, still two waves per SIMD).
+// GD: a spline degree other than 3, evaluated with the run-time degree form
+// (half_basis_deg) instead of the cubic's two-term form.
 template <typename T, int RF, int NFL, int NF, int WK, int NW, int NSBC = 0, bool XP = false,
-          bool SP = false, bool XA = false>
+          bool SP = false, bool XA = false, bool GD = false>
 __global__ __launch_bounds__(64 * NW)
 __attribute__((amdgpu_waves_per_eu(Occ<RF, XA ? NF / 2 : NF>::waves)))
 void layer_kernel(LayerArgs a) {
@@ -252,6 +254,12 @@ void layer_kernel(LayerArgs a) {
 
     const T* __restrict__ x = static_cast<const T*>(a.x);
     T* __restrict__ y = static_cast<T*>(a.y);
+    static_assert(!GD || (!SP && !XA), "the structured-sparse operand is cubic");
+    // a basis value N / 2 at v = u - (k + 1) / 2
+    auto hb = [&](float v) -> float {
+        if constexpr (GD) return half_basis_deg(v, a.kdeg, a.hw, a.hc);
+        else return half_basis(v);
+    };
 
     const int tid = threadIdx.x;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
@@ -426,14 +434,15 @@ void layer_kernel(LayerArgs a) {
         float s[RF];
         const float c = a.a_int + 1.0f - (float)(KJ * pg.bsub);
 #pragma unroll
-        for (int rf = 0; rf < RF; ++rf) s[rf] = __builtin_fmaf(xv[rf], a.inv_h, c) + a.a_frac;
+        for (int rf = 0; rf < RF; ++rf)
+            s[rf] = __builtin_fmaf(xv[rf], a.inv_h, c) + coord_lo(xv[rf], a.xlim, a.inv_lo, a.a_frac);
         // (xv: x values of block pg, already converted)
         const bool first = pg.bsub == 0;
         float v[RF][KJ];
         auto gen_elem = [&](int k) {
             const int rf = k / KJ;
             const int e = k % KJ;
-            const float bv = half_basis(s[rf] - (float)e);
+            const float bv = hb(s[rf] - (float)e);
             v[rf][e] = (e == 0 && first) ? slv[rf] : bv;
             if constexpr (BF16) {
                 if (e & 1) {
@@ -496,7 +505,7 @@ void layer_kernel(LayerArgs a) {
       if constexpr (GEN_SPLIT) {
         auto basis = [&](int rf, int e0, int e1) {
 #pragma unroll
-            for (int e = e0; e < e1; ++e) An.a[rf][e] = (__bf16)half_basis(sc[rf] - (float)e);
+            for (int e = e0; e < e1; ++e) An.a[rf][e] = (__bf16)hb(sc[rf] - (float)e);
         };
         auto zero = [&](int rf, int e0) {
 #pragma unroll
@@ -506,7 +515,8 @@ void layer_kernel(LayerArgs a) {
 #pragma unroll
             for (int rf = 0; rf < RF; ++rf) {
                 const float xv = x_value(pg, xr[rf], rf);
-                sc[rf] = __builtin_fmaf(xv, a.inv_h, a.a_int + 1.0f) + a.a_frac;
+                sc[rf] = __builtin_fmaf(xv, a.inv_h, a.a_int + 1.0f) +
+                         coord_lo(xv, a.xlim, a.inv_lo, a.a_frac);
                 // keep the coordinate itself for the feature's later blocks
                 // (recomputing it there from x would hold the raw x register,
                 // and a copy of it could wait on a load still in flight)
@@ -519,8 +529,10 @@ void layer_kernel(LayerArgs a) {
         if constexpr (DIRECT) {
             const float c = a.a_int + 1.0f - (float)(KJ * pg.bsub);
 #pragma unroll
-            for (int rf = 0; rf < RF; ++rf)
-                sc[rf] = __builtin_fmaf(x_value(pg, xr[rf], rf), a.inv_h, c) + a.a_frac;
+            for (int rf = 0; rf < RF; ++rf) {
+                const float xv = x_value(pg, xr[rf], rf);
+                sc[rf] = __builtin_fmaf(xv, a.inv_h, c) + coord_lo(xv, a.xlim, a.inv_lo, a.a_frac);
+            }
         } else {
 #pragma unroll
             for (int rf = 0; rf < RF; ++rf) sc[rf] -= (float)KJ;
@@ -563,7 +575,8 @@ void layer_kernel(LayerArgs a) {
       if constexpr (SP) {
 #pragma unroll
         for (int rf = 0; rf < GRF; ++rf) {
-            const float sv = __builtin_fmaf(xf[rf], a.inv_h, a.a_int + 1.0f) + a.a_frac;
+            const float sv = __builtin_fmaf(xf[rf], a.inv_h, a.a_int + 1.0f) +
+                             coord_lo(xf[rf], a.xlim, a.inv_lo, a.a_frac);
             // c0 + 1 = floor(s) within [2, 13] (a NaN coordinate gives c0 = 1
             // and NaN values, as it should)
             const float f1 = __builtin_amdgcn_fmed3f(__builtin_floorf(sv), 2.0f, 13.0f);
@@ -704,10 +717,11 @@ void layer_kernel(LayerArgs a) {
         const float c0 = a.a_int + 1.0f - (float)(KJ * pos_c.bsub);
 #pragma unroll
         for (int rf = 0; rf < RF; ++rf) {
-            const float s0 = __builtin_fmaf(x0[rf], a.inv_h, c0) + a.a_frac;
+            const float s0 = __builtin_fmaf(x0[rf], a.inv_h, c0) +
+                             coord_lo(x0[rf], a.xlim, a.inv_lo, a.a_frac);
 #pragma unroll
             for (int e = 0; e < KJ; ++e) {
-                const float bv = half_basis(s0 - (float)e);
+                const float bv = hb(s0 - (float)e);
                 const float v = (e == 0 && pos_c.bsub == 0) ? sl[rf] : bv;
                 if constexpr (BF16) A_cur.a[rf][e] = (__bf16)v;
                 else A_cur.a[rf][e] = v;
@@ -991,6 +1005,17 @@ hipError_t launch_cfg(const LayerGeom& g, LayerArgs a, hipStream_t s) {
     if constexpr (XA || (NW == 8 && WK > 1)) {  // (sparse-only shapes)
         return hipErrorInvalidValue;
     } else {
+        if (g.kdeg != 3) {
+            // other degrees: one shape, the run-time degree form
+            if constexpr (RF == 1 && WK == 1 && NW == 4 && NF == NFL) {
+                hipLaunchKernelGGL(
+                    (layer_kernel<T, RF, NFL, NF, WK, NW, 0, false, false, false, true>), grid,
+                    dim3(64 * NW), 0, s, a);
+                return hipGetLastError();
+            } else {
+                return hipErrorInvalidValue;
+            }
+        }
         hipLaunchKernelGGL((layer_kernel<T, RF, NFL, NF, WK, NW>), grid, dim3(64 * NW), 0, s, a);
         return hipGetLastError();
     }

@@ -46,8 +46,9 @@ WS, WSB = 0x700000000, 1 << 30  # a workspace large enough for every layer below
 
 
 @pytest.mark.parametrize("grid,code", [
-    (kb.make_grid(5, spline_order=2), kb.KAN_ERR_UNSUPPORTED),
-    (kb.make_grid(5, spline_order=4), kb.KAN_ERR_UNSUPPORTED),
+    (kb.make_grid(5, spline_order=0), kb.KAN_ERR_UNSUPPORTED),
+    (kb.make_grid(5, spline_order=8), kb.KAN_ERR_UNSUPPORTED),
+    (kb.make_grid(5, spline_order=-1), kb.KAN_ERR_UNSUPPORTED),
     (kb.make_grid(0), kb.KAN_ERR_INVALID_ARG),
     (kb.make_grid(-3), kb.KAN_ERR_INVALID_ARG),
     (kb.make_grid(4001), kb.KAN_ERR_INVALID_ARG),
@@ -165,7 +166,7 @@ def test_workspace_bytes_checks():
     assert lib.kan_layer_forward_workspace_bytes(ctypes.byref(g), 0, 16, 4, 4, None) == bad
     assert kb.kan_layer_forward_workspace_bytes(g, kb.KAN_F32, -1, 4, 4)[0] == bad
     assert kb.kan_layer_forward_workspace_bytes(g, kb.KAN_F32, 16, 0, 4)[0] == bad
-    assert kb.kan_layer_forward_workspace_bytes(kb.make_grid(10, spline_order=2), kb.KAN_F32,
+    assert kb.kan_layer_forward_workspace_bytes(kb.make_grid(10, spline_order=8), kb.KAN_F32,
                                                 16, 4, 4)[0] == kb.KAN_ERR_UNSUPPORTED
     # the packed weights, whatever the batch
     for B in (0, 1, 65536):
@@ -181,7 +182,7 @@ def test_packed_entry_point_checks():
     assert lib.kan_layer_packed_bytes(ctypes.byref(g), f32, 4, 4, None) == bad
     assert kb.kan_layer_packed_bytes(g, f32, 0, 4)[0] == bad
     assert kb.kan_layer_packed_bytes(g, f32, 4, 0)[0] == bad
-    assert kb.kan_layer_packed_bytes(kb.make_grid(10, spline_order=2), f32, 4, 4)[0] == \
+    assert kb.kan_layer_packed_bytes(kb.make_grid(10, spline_order=9), f32, 4, 4)[0] == \
         kb.KAN_ERR_UNSUPPORTED
     need = kb.kan_layer_packed_bytes(g, f32, 4, 4)[1]
     # pack: null, misaligned (16 bytes for the packed buffer), short, overlapping
@@ -242,7 +243,7 @@ def test_noalloc_entry_point_host_checks():
     assert kb.kan_layer_forward_noalloc(g, f32, -1, 4, 4, X, C, W, Y) == bad
     assert kb.kan_layer_forward_noalloc(g, f32, 16, 4, 4, 0, C, W, Y) == bad
     assert kb.kan_layer_forward_noalloc(g, f32, 16, 4, 4, X, C, W, X + 8) == bad
-    assert kb.kan_layer_forward_noalloc(kb.make_grid(10, spline_order=2), f32, 16, 4, 4, X, C, W,
+    assert kb.kan_layer_forward_noalloc(kb.make_grid(10, spline_order=0), f32, 16, 4, 4, X, C, W,
                                         Y) == kb.KAN_ERR_UNSUPPORTED
     assert kb.kan_layer_forward_noalloc(g, f32, 0, 4, 4, 0, 0, 0, 0) == kb.KAN_OK
     # 256 -> 128 at G = 200 in fp32: 26.7 MB of packed weights
@@ -281,8 +282,12 @@ def test_backward_host_checks():
     assert call(X, C, W, DY, DX, DC, DC + 16, WS, need) == bad         # outputs overlapping
     assert call(X, C, W, DY, DX, DC, DW, DX - 16, need) == bad         # workspace over dx
     assert kb.kan_layer_backward(g, f32, -1, 4, 4, X, C, W, DY, DX, DC, DW, WS, need) == bad
-    assert kb.kan_layer_backward(kb.make_grid(10, spline_order=2), f32, 16, 4, 4, X, C, W, DY,
-                                 DX, DC, DW, WS, need) == kb.KAN_ERR_UNSUPPORTED
+    # the backward is cubic only
+    for k in (1, 2, 4, 7):
+        assert kb.kan_layer_backward(kb.make_grid(10, spline_order=k), f32, 16, 4, 4, X, C, W, DY,
+                                     DX, DC, DW, WS, need) == kb.KAN_ERR_UNSUPPORTED
+        assert kb.kan_layer_backward_workspace_bytes(kb.make_grid(10, spline_order=k), f32, 16,
+                                                     4, 4)[0] == kb.KAN_ERR_UNSUPPORTED
     # an empty batch needing only dx: nothing to do
     assert kb.kan_layer_backward(g, f32, 0, 4, 4, 0, C, W, 0, DX, 0, 0, WS, need) == kb.KAN_OK
     lib = kb.load_library()
@@ -309,3 +314,20 @@ def test_backward_workspace_bytes(G, n_in, n_out, B, bf16):
     kr = 32 * ((n_in + 1) // 2 if cp == 16 else n_in * cp // 32)
     assert n >= kr * n_out * es  # packed weights
     assert n < out32 * bpad * es + 300 * out32 * kr * 4 + kr * 256 * 4 + (1 << 20)
+
+
+@pytest.mark.parametrize("k", [1, 2, 4, 5, 6, 7])
+def test_other_degrees_accepted(k):
+    """Degrees 1..7 (eq. general_truncated): G + k bases; the fused layer runs
+    one workgroup shape (the run-time degree build), never the structured-sparse
+    instruction, and a forced other shape is rejected."""
+    g = kb.make_grid(10, spline_order=k)
+    assert kb.kan_basis_eval(g, kb.KAN_F32, X, 0, PHI) == kb.KAN_OK
+    for dt in (kb.KAN_F32, kb.KAN_BF16):
+        st, plan = kb.kan_layer_plan(g, dt, 65536, 784, 256)
+        assert st == kb.KAN_OK and plan == (1, 1, 4, 1, 0)
+        assert kb.kan_layer_plan(g, dt, 65536, 784, 256, "2,1")[0] == kb.KAN_ERR_INVALID_ARG
+        st, n = kb.kan_layer_packed_bytes(g, dt, 5, 7)
+        assert st == kb.KAN_OK
+        kj = 8 if dt == kb.KAN_BF16 else 2
+        assert n % (2 * 32 * kj * (2 if dt == kb.KAN_BF16 else 4)) == 0
