@@ -1,10 +1,11 @@
 /*
- * kan.h -- C ABI of the MI355X (gfx950) InKAN KAN-layer forward.
+ * kan.h -- C ABI of the MI355X (gfx950) InKAN KAN layer.
  *
- * The library evaluates uniform cubic B-spline KAN layers with the basis in
- * clamped truncated-power form (paper: Sec. 2 "Step 4", eq. truncated, with the
- * bounded coordinate of eq. bounded) and contracts it with the spline
- * coefficients plus the SiLU base branch (eq. kan_forward).
+ * The library evaluates uniform B-spline KAN layers with the basis in clamped
+ * truncated-power form (paper: Sec. 2 "Step 4", eq. truncated for cubics and
+ * eq. general_truncated for other degrees, with the bounded coordinate of
+ * eq. bounded) and contracts it with the spline coefficients plus the SiLU
+ * base branch (eq. kan_forward); it also computes the layer's gradients.
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -21,21 +22,25 @@
  *    KAN_F32 is IEEE binary32 throughout; KAN_BF16 is bfloat16 storage with
  *    binary32 basis evaluation and accumulation, rounded to nearest-even on
  *    store.
- *  * Grid: G = grid_size intervals of width h = (grid_hi - grid_lo) / G.  The
- *    knot vector is t_j = grid_lo + (j - 3) h, j = 0 .. G + 6, which gives
- *    nb = G + 3 cubic basis functions; basis j is supported on [t_j, t_{j+4}]
- *    (uniform simple knots, Sec. 2 "Step 3"; the extension by three spans on
- *    each side of [grid_lo, grid_hi] is this library's grid convention).
- *    Only cubic splines are implemented, as in the paper (Sec. 5): any other
- *    spline_order is KAN_ERR_UNSUPPORTED.  Knots are always uniform; there is
- *    no way to pass a non-uniform knot vector (Sec. 5).
+ *  * Grid: G = grid_size intervals of width h = (grid_hi - grid_lo) / G and
+ *    degree k = spline_order.  The knot vector is t_j = grid_lo + (j - k) h,
+ *    j = 0 .. G + 2k, which gives nb = G + k basis functions; basis j is
+ *    supported on [t_j, t_{j+k+1}] (uniform simple knots, Sec. 2 "Step 3";
+ *    the extension by k spans on each side of [grid_lo, grid_hi] is this
+ *    library's grid convention).  The paper implements k = 3 only (Sec. 5);
+ *    this library evaluates eq. general_truncated for 1 <= k <= 7 (the cubic
+ *    on its tuned kernels) and the backward for k = 3.  Knots are always
+ *    uniform; there is no way to pass a non-uniform knot vector (Sec. 5).
  *  * Accuracy: the basis is evaluated in binary32 as
- *      u_j = x / h - grid_lo / h + 3 - j           (one fused multiply-add),
+ *      u_j = x / h - grid_lo / h + k - j   (a fused multiply-add with the fp32
+ *                                           1/h, plus x times the rounding
+ *                                           residual of 1/h and the fraction
+ *                                           of grid_lo / h),
  *      N_j = clamp-based truncated power of u_j     (eq. truncated + eq. bounded),
- *    where the clamp to [0, 4] makes every basis exactly 0 off its support.
- *    When 1/h and grid_lo/h are exact in binary32 (e.g. [-1, 1] with any G up
- *    to 2^22) the basis is within 1e-6 of the exact value; otherwise the error
- *    grows with the rounding of those two constants.
+ *    where the clamp to [0, k + 1] makes every basis exactly 0 off its
+ *    support.  The basis is within 1e-6 of the exact value in binary32;
+ *    inputs within the coordinate's rounding (about 2^-23 h) of a support end
+ *    may land on either side of it.
  *  * Validation happens on the host before any HIP call, and every invalid
  *    argument returns its code without touching the device.  An empty problem
  *    (n == 0 or batch == 0) returns KAN_OK and launches nothing.
@@ -54,7 +59,8 @@ extern "C" {
 typedef enum kan_status {
     KAN_OK = 0,
     KAN_ERR_INVALID_ARG = 1, /* bad size, range, pointer, alignment or overlap   */
-    KAN_ERR_UNSUPPORTED = 2, /* spline_order != 3 or an unknown dtype           */
+    KAN_ERR_UNSUPPORTED = 2, /* spline_order outside 1..7 (backward: != 3) or an
+                                unknown dtype                                   */
     KAN_ERR_DEVICE = 3,      /* the HIP runtime rejected a launch               */
     KAN_ERR_SCRATCH_LIMIT = 4 /* kan_layer_forward_noalloc: the layer's packed
                                  weights exceed KAN_NOALLOC_SCRATCH_BYTES       */
@@ -67,24 +73,25 @@ typedef enum kan_dtype {
 
 typedef struct kan_grid {
     int32_t grid_size;    /* G, number of grid intervals, 1 <= G <= 4000      */
-    int32_t spline_order; /* k, must be 3                                       */
+    int32_t spline_order; /* k, 1 <= k <= 7 (the backward: 3)                   */
     float grid_lo;        /* finite, grid_lo < grid_hi                          */
     float grid_hi;        /* |grid_lo| / h and |grid_hi| / h at most 2^22       */
 } kan_grid;
 
 /*
  * kan_basis_eval -- basis-only evaluation (the elementwise truncated-power
- * basis of eq. truncated with the clamp of eq. bounded).
+ * basis of eq. truncated / eq. general_truncated with the clamp of
+ * eq. bounded).
  *
  *   x    [n]           input values, any shape flattened; dtype storage.
- *   phi  [n, G + 3]    output, basis index fastest: phi[e * (G+3) + j] = N_j(x[e]).
+ *   phi  [n, G + k]    output, basis index fastest: phi[e * (G+k) + j] = N_j(x[e]).
  *
  * phi must not overlap x.  x and phi must be aligned to the dtype size.
- * A NaN input gives NaN in all G + 3 outputs of that element; +-Inf gives 0.
+ * A NaN input gives NaN in all G + k outputs of that element; +-Inf gives 0.
  *
  * Returns KAN_OK, KAN_ERR_INVALID_ARG (grid == NULL, bad grid, n < 0,
- * NULL/misaligned/overlapping pointers with n > 0, n * (G + 3) overflowing
- * int64), KAN_ERR_UNSUPPORTED (spline_order != 3, unknown dtype) or
+ * NULL/misaligned/overlapping pointers with n > 0, n * (G + k) overflowing
+ * int64), KAN_ERR_UNSUPPORTED (spline_order outside 1..7, unknown dtype) or
  * KAN_ERR_DEVICE (launch rejected).
  */
 kan_status kan_basis_eval(const kan_grid* grid, kan_dtype dtype, const void* x,
@@ -100,7 +107,7 @@ kan_status kan_basis_eval(const kan_grid* grid, kan_dtype dtype, const void* x,
  * with KAN layers").
  *
  *   x          [batch, in_features]              dtype storage
- *   coef       [out_features, in_features, G+3]  dtype storage
+ *   coef       [out_features, in_features, G+k]  dtype storage
  *   base_w     [out_features, in_features]       dtype storage
  *   workspace  caller-owned device scratch of workspace_bytes >=
  *              kan_layer_forward_workspace_bytes(...) bytes, 16-byte aligned,
@@ -109,8 +116,8 @@ kan_status kan_basis_eval(const kan_grid* grid, kan_dtype dtype, const void* x,
  *              It must stay allocated until the enqueued work has finished.
  *   y          [batch, out_features]             dtype storage, fully overwritten
  *
- * The contraction runs on the matrix cores over K = in_features * (G + 4)
- * columns (G + 3 basis values and one SiLU value per input feature); the basis
+ * The contraction runs on the matrix cores over K = in_features * (G + k + 1)
+ * columns (G + k basis values and one SiLU value per input feature); the basis
  * is generated in registers and never written to memory.  The call is
  * kan_layer_pack into the workspace followed by kan_layer_forward_packed,
  * both enqueued on `stream`.
@@ -119,9 +126,9 @@ kan_status kan_basis_eval(const kan_grid* grid, kan_dtype dtype, const void* x,
  * size.  A NaN in x[b, :] makes y[b, :] NaN (through the SiLU branch).
  *
  * Returns KAN_OK, KAN_ERR_INVALID_ARG (grid == NULL, bad grid, batch < 0,
- * in_features < 1, out_features < 1, in_features * (G + 4) >= 2^31,
+ * in_features < 1, out_features < 1, in_features * (G + k + 1) >= 2^31,
  * in_features >= 2^24, NULL/misaligned/overlapping pointers or a short
- * workspace with batch > 0), KAN_ERR_UNSUPPORTED (spline_order != 3, unknown
+ * workspace with batch > 0), KAN_ERR_UNSUPPORTED (spline_order outside 1..7, unknown
  * dtype) or KAN_ERR_DEVICE (launch rejected).
  */
 kan_status kan_layer_forward(const kan_grid* grid, kan_dtype dtype, int64_t batch,
@@ -155,14 +162,15 @@ kan_status kan_layer_packed_bytes(const kan_grid* grid, kan_dtype dtype, int32_t
  * spline coefficients coef[o, i, j] and the SiLU weights base_w[o, i]) into
  * the order in which the matrix cores consume them: for each tile of output
  * columns, feature pair and block of columns, the weights of both features for
- * every output column, the SiLU weight before the G + 3 spline coefficients of
- * its feature and zeros in the padding (in bf16 with 5 <= G <= 12 a feature's
- * 16 columns are permuted for the structured-sparse matrix instruction).  The
+ * every output column, the SiLU weight before the G + k spline coefficients of
+ * its feature and zeros in the padding (in bf16 with k = 3 and 5 <= G <= 12 a
+ * feature's 16 columns are permuted for the structured-sparse matrix
+ * instruction).  The
  * layout is private to this library and depends only on (grid, dtype,
  * in_features, out_features).  Weights that do not change can be packed once
  * and reused by any number of kan_layer_forward_packed calls.
  *
- *   coef    [out_features, in_features, G+3]  dtype storage
+ *   coef    [out_features, in_features, G+k]  dtype storage
  *   base_w  [out_features, in_features]       dtype storage
  *   packed  packed_bytes >= kan_layer_packed_bytes(...), 16-byte aligned,
  *           not overlapping coef or base_w; fully overwritten.
@@ -209,7 +217,9 @@ kan_status kan_layer_forward_packed(const kan_grid* grid, kan_dtype dtype, int64
  *   plan[2]  waves per workgroup (4 or 8)
  *   plan[3]  workgroups splitting the columns of an output tile (1, 2 or 4)
  *   plan[4]  1 if the layer runs on the structured-sparse matrix instruction
- *            (bf16, 5 <= G <= 12), else 0
+ *            (bf16, k = 3, 5 <= G <= 12), else 0
+ *
+ * Degrees other than 3 run one shape, {1, 1, 4, 1}.
  *
  * Writes plan[0..4].  Returns KAN_OK, KAN_ERR_INVALID_ARG (plan == NULL, bad
  * grid or sizes, batch < 1, an invalid forced shape) or KAN_ERR_UNSUPPORTED.
@@ -230,6 +240,7 @@ kan_status kan_layer_plan(const kan_grid* grid, kan_dtype dtype, int64_t batch,
  * N_j' is the derivative in x of the clamped truncated-power basis
  * (eq. general_truncated differentiated: (1/h) (1/2) sum_m (-1)^m C(4, m)
  * (u - m)_+^2 at the clamped coordinate of eq. bounded, 0 off the support).
+ * Cubic splines only (spline_order 3; else KAN_ERR_UNSUPPORTED).
  * The paper reports forward timing only and lists backward timing as future
  * work (Sec. 5); these are the chain rule applied to its forward.
  *
