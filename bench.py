@@ -341,6 +341,33 @@ def measure_step(dtype: str, W, steps: int, warmup: int) -> dict:
             "kernels": kern, "shapes": shapes, "x": x, "outs": hs, "prep": prep}
 
 
+def cdb_context() -> dict:
+    """The truncated-power basis kernel against our Cox-de Boor kernel (the
+    recursion over every knot interval that the paper measures against), fp32
+    storage, on the inputs of: the MLP's first layer (65536 x 784, G = 10), the
+    paper's basis-timing layer (256 x 784, G = 5), and the grid-size sweep's
+    largest grid (8192 x 128, G = 200).  Context, not a target: both kernels
+    write the same basis tensor, so on large inputs both are bound by its HBM
+    write and the ratio stays near 1."""
+    import numpy as np
+    import torch
+
+    from paper_2609_01956_amd import binding as kb
+
+    out = {}
+    rng = np.random.default_rng(7)
+    for name, (B, n, G) in {"mlp_layer1_65536x784_g10": (65536, 784, 10),
+                            "basis_timing_layer_256x784_g5": (256, 784, 5),
+                            "grid_sweep_8192x128_g200": (8192, 128, 200)}.items():
+        x = torch.from_numpy(rng.uniform(-1, 1, (B, n)).astype(np.float32)).to("cuda")
+        phi = torch.empty((B, n, G + 3), dtype=torch.float32, device="cuda")
+        tp = _time_us(lambda: kb.basis(x, G, out=phi))
+        cdb = _time_us(lambda: kb.basis(x, G, out=phi, method="cdb"))
+        out[name] = {"tp_us": tp, "cdb_us": cdb, "cdb_over_tp": cdb / tp,
+                     "tp_gbasis_per_s": B * n * (G + 3) / tp / 1e3}
+    return out
+
+
 def layer_parity(dtype: str, W, r: dict, n_rows: int = 64) -> dict:
     """Per layer, the sampled rows of this run's GPU output against the plain
     float64 oracle (eq. kan_forward) fed the GPU's own input rows of that
@@ -445,6 +472,7 @@ def main() -> int:
                                     "valu_frac_dense_count")}
                                for n, kk in o["kernels"].items()},
                    "parity": o["parity"]}
+    line["cox_de_boor_context"] = cdb_context()
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(W, args.cpu_seconds)
     print(json.dumps(line), flush=True)

@@ -98,6 +98,20 @@ kan_status kan_basis_eval(const kan_grid* grid, kan_dtype dtype, const void* x,
                           int64_t n, void* phi, void* stream);
 
 /*
+ * kan_basis_eval_cdb -- the same basis-only evaluation as kan_basis_eval, by
+ * the Cox-de Boor recursion (eq. cdb0, eq. cdbk) over all G + 2k knot
+ * intervals (no span lookup), the evaluation the paper compares its
+ * truncated-power form against (Sec. 4, Tables 1 and 3).  For measuring that
+ * comparison on this hardware; results equal kan_basis_eval's up to the
+ * rounding of the recursion (half-open intervals: an input exactly on the last
+ * knot gives 0, as the clamped form).
+ *
+ * Arguments, layout, NaN/Inf behaviour and return codes as kan_basis_eval.
+ */
+kan_status kan_basis_eval_cdb(const kan_grid* grid, kan_dtype dtype, const void* x,
+                              int64_t n, void* phi, void* stream);
+
+/*
  * kan_layer_forward -- one KAN layer (eq. kan_forward):
  *
  *   y[b, o] = sum_i ( sum_j coef[o, i, j] N_j(x[b, i])  +  base_w[o, i] silu(x[b, i]) )

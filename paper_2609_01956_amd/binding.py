@@ -29,7 +29,7 @@ KAN_NOALLOC_SCRATCH_BYTES = 16 << 20
 KAN_F32 = 0
 KAN_BF16 = 1
 
-EXPORTED_SYMBOLS = ("kan_basis_eval", "kan_layer_forward", "kan_layer_forward_workspace_bytes",
+EXPORTED_SYMBOLS = ("kan_basis_eval", "kan_basis_eval_cdb", "kan_layer_forward", "kan_layer_forward_workspace_bytes",
                     "kan_layer_packed_bytes", "kan_layer_pack", "kan_layer_forward_packed",
                     "kan_layer_plan", "kan_layer_forward_noalloc", "kan_layer_backward",
                     "kan_layer_backward_workspace_bytes", "kan_status_string",
@@ -65,6 +65,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
             lib.kan_basis_eval.argtypes = [ctypes.POINTER(kan_grid), ctypes.c_int, ctypes.c_void_p,
                                            ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p]
             lib.kan_basis_eval.restype = ctypes.c_int
+            lib.kan_basis_eval_cdb.argtypes = lib.kan_basis_eval.argtypes
+            lib.kan_basis_eval_cdb.restype = ctypes.c_int
             g = ctypes.POINTER(kan_grid)
             lib.kan_layer_forward.argtypes = [g, ctypes.c_int, ctypes.c_int64, ctypes.c_int32,
                                               ctypes.c_int32, _VP, _VP, _VP, _VP, ctypes.c_size_t,
@@ -139,6 +141,13 @@ def _shape_arg(shape):
     if len(v) != 4:
         raise ValueError("a shape is (rf, wk[, nw[, cs]])")
     return (ctypes.c_int32 * 4)(*[int(t) for t in v])
+
+
+def kan_basis_eval_cdb(grid: kan_grid, dtype: int, x: int, n: int, phi: int,
+                       stream: int = 0) -> int:
+    """Raw call: device addresses as integers; returns the kan_status code."""
+    return int(load_library().kan_basis_eval_cdb(ctypes.byref(grid), int(dtype), _VP(x), int(n),
+                                                 _VP(phi), _VP(stream)))
 
 
 def kan_layer_forward(grid: kan_grid, dtype: int, batch: int, in_features: int,
@@ -276,8 +285,12 @@ def _stream(device) -> int:
 
 
 def basis(x, grid_size: int, grid_lo: float = -1.0, grid_hi: float = 1.0, out=None,
-          spline_order: int = 3):
-    """phi[..., j] = N_j(x[...]) for j < grid_size + spline_order (kan_basis_eval)."""
+          spline_order: int = 3, method: str = "tp"):
+    """phi[..., j] = N_j(x[...]) for j < grid_size + spline_order: the
+    truncated-power form (kan_basis_eval, method "tp") or the Cox-de Boor
+    recursion (kan_basis_eval_cdb, method "cdb")."""
+    if method not in ("tp", "cdb"):
+        raise ValueError("method is 'tp' or 'cdb'")
     torch = _torch()
     _require_device(x)
     nb = int(grid_size) + int(spline_order)
@@ -288,7 +301,8 @@ def basis(x, grid_size: int, grid_lo: float = -1.0, grid_hi: float = 1.0, out=No
         if out.dtype != x.dtype or tuple(out.shape) != tuple(x.shape) + (nb,):
             raise ValueError("out must have shape x.shape + (G + k,) and x's dtype")
     with torch.cuda.device(x.device):
-        check(kan_basis_eval(make_grid(grid_size, grid_lo, grid_hi, spline_order), _dtype_code(x),
+        fn = kan_basis_eval if method == "tp" else kan_basis_eval_cdb
+        check(fn(make_grid(grid_size, grid_lo, grid_hi, spline_order), _dtype_code(x),
                              x.data_ptr(),
                              x.numel(), out.data_ptr(), _stream(x.device)))
     return out

@@ -87,6 +87,36 @@ const char* kan_status_string(kan_status status) {
 
 int32_t kan_abi_version(void) { return KAN_ABI_VERSION; }
 
+// Shared validation of the basis-only entry points.
+static kan_status check_basis(const kan_grid* grid, kan_dtype dtype, const void* x, int64_t n,
+                              const void* phi, kan::GridConst* gc) {
+    const kan_status st = check_grid(grid, dtype, gc);
+    if (st != KAN_OK) return st;
+    if (n < 0) return KAN_ERR_INVALID_ARG;
+    if (n == 0) return KAN_OK;
+    if (n > INT64_MAX / gc->nb) return KAN_ERR_INVALID_ARG;
+    const size_t es = dtype_size(dtype);
+    if (x == nullptr || phi == nullptr) return KAN_ERR_INVALID_ARG;
+    if (!aligned(x, es) || !aligned(phi, es)) return KAN_ERR_INVALID_ARG;
+    if ((uint64_t)n > (uint64_t)(SIZE_MAX / es / gc->nb)) return KAN_ERR_INVALID_ARG;
+    if (overlap(x, (size_t)n * es, phi, (size_t)n * gc->nb * es)) return KAN_ERR_INVALID_ARG;
+    if ((n + 255) / 256 > 0x7fffffffLL) return KAN_ERR_INVALID_ARG;
+    return KAN_OK;
+}
+
+kan_status kan_basis_eval_cdb(const kan_grid* grid, kan_dtype dtype, const void* x, int64_t n,
+                              void* phi, void* stream) {
+    kan::GridConst gc;
+    const kan_status st = check_basis(grid, dtype, x, n, phi, &gc);
+    if (st != KAN_OK || n == 0) return st;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (dtype == KAN_F32)
+        return device_status(kan::launch_basis_cdb_f32(static_cast<const float*>(x), n,
+                                                       static_cast<float*>(phi), gc, s));
+    return device_status(kan::launch_basis_cdb_bf16(static_cast<const uint16_t*>(x), n,
+                                                    static_cast<uint16_t*>(phi), gc, s));
+}
+
 kan_status kan_basis_eval(const kan_grid* grid, kan_dtype dtype, const void* x, int64_t n,
                           void* phi, void* stream) {
     kan::GridConst gc;

@@ -53,6 +53,22 @@ __device__ __forceinline__ float basis_value(float v) {
 }
 template <int K> constexpr float kScale = K == 3 ? 2.0f : 1.0f;
 
+// Phase 2 of the basis kernels: stream the contiguous run of `total` staged
+// values to `out`.
+template <typename T>
+__device__ __forceinline__ void stream_out(const float* stage, T* out, int total, int vec) {
+    int done = 0;
+    if (vec && (reinterpret_cast<uintptr_t>(out) % 16) == 0) {
+        constexpr int V = 16 / sizeof(T);
+        const int nvec = total / V;
+        for (int q = threadIdx.x; q < nvec; q += kThreads)
+            store_vec<T>(out + q * V, stage + q * V);
+        done = nvec * V;
+    }
+    for (int q = done + threadIdx.x; q < total; q += kThreads)
+        Storage<T>::store(out + q, stage[q]);
+}
+
 template <typename T, int K>
 __global__ __launch_bounds__(kThreads) void basis_kernel(const T* __restrict__ x, int64_t n,
                                                          T* __restrict__ phi, GridConst g,
@@ -91,20 +107,109 @@ __global__ __launch_bounds__(kThreads) void basis_kernel(const T* __restrict__ x
         }
     }
     __syncthreads();
+    stream_out<T>(stage, phi + e0 * nb, cnt * nb, vec);
+}
 
-    // Phase 2: stream the contiguous run [e0 * nb, (e0 + cnt) * nb) out.
-    const int total = cnt * nb;
-    T* out = phi + e0 * nb;
-    int done = 0;
-    if (vec && (reinterpret_cast<uintptr_t>(out) % 16) == 0) {
-        constexpr int V = 16 / sizeof(T);
-        const int nvec = total / V;
-        for (int q = threadIdx.x; q < nvec; q += kThreads)
-            store_vec<T>(out + q * V, stage + q * V);
-        done = nvec * V;
+// ------------------------------------------------------------ Cox-de Boor
+//
+// The same basis by the recursion of eq. cdb0 / eq. cdbk over every knot
+// interval, as a B-spline layer without span lookup evaluates it (the
+// evaluation the paper measures its truncated-power form against).  With
+// uniform knots t_j = lo + (j - K) h the recursion's weights are
+// (x - t_j) / (t_{j+p} - t_j) = u_j / p and (t_{j+p+1} - x) / (t_{j+p+1} -
+// t_{j+1}) = (p + 1 - u_j) / p, u_j = (x - t_j) / h, so for p = 1 .. K
+//   N_{j,p} = (u_j N_{j,p-1} + (p + 1 - u_j) N_{j+1,p-1}) / p,
+// starting from N_{j,0} = [0 <= u_j < 1] for the W = G + 2K intervals (the
+// half-open indicator of eq. cdb0), set from floor(u_0) so that exactly one
+// interval holds x.  Each weight's u_j is one fma at its own magnitude (plus
+// the 1/h residual term).  A NaN input gives NaN values
+// (its indicators are all 0, so the NaN is added back explicitly).
+//
+// basis_cdb_kernel: one thread per input, the W values of a level in
+// registers (MW >= W at compile time).
+template <typename T, int K, int MW>
+__global__ __launch_bounds__(kThreads) void basis_cdb_kernel(const T* __restrict__ x, int64_t n,
+                                                             T* __restrict__ phi, GridConst g,
+                                                             int vec) {
+    extern __shared__ float stage[];
+    const int nb = g.nb;
+    const int W = nb + K;
+    const int64_t e0 = (int64_t)blockIdx.x * kThreads;
+    const int64_t left = n - e0;
+    const int cnt = left < kThreads ? (int)left : kThreads;
+    const int el = threadIdx.x;
+    if (el < cnt) {
+        const float xv = Storage<T>::load(x + e0 + el);
+        // (an input clamped to +-xlim, past every knot, gives the same zeros
+        // and keeps the weights u_j finite for infinite inputs)
+        const float xc = __builtin_amdgcn_fmed3f(xv, -g.xlim, g.xlim);
+        const float lo = coord_lo(xc, g.xlim, g.inv_lo, g.a_frac);
+        const float c0 = g.a_int + g.hw;  // u_j = x / h - lo / h + K - j
+        // the interval holding x, from one coordinate (so that exactly one
+        // indicator is set, however the u_j below round)
+        const float span = __builtin_floorf(__builtin_fmaf(xc, g.inv_h, c0) + lo);
+        float u[MW], w[MW];
+#pragma unroll
+        for (int j = 0; j < MW; ++j) {
+            u[j] = __builtin_fmaf(xc, g.inv_h, c0 - (float)j) + lo;
+            w[j] = (j < W && span == (float)j) ? 1.0f : 0.0f;
+        }
+#pragma unroll
+        for (int p = 1; p <= K; ++p) {
+            const float ip = 1.0f / (float)p;
+#pragma unroll
+            for (int j = 0; j + p < MW; ++j)
+                w[j] = (u[j] * w[j] + ((float)(p + 1) - u[j]) * w[j + 1]) * ip;
+        }
+        const float nanv = xv != xv ? xv : 0.0f;
+        float* dst = stage + el * nb;
+#pragma unroll
+        for (int j = 0; j + K < MW; ++j)
+            if (j < nb) dst[j] = w[j] + nanv;
     }
-    for (int q = done + threadIdx.x; q < total; q += kThreads)
-        Storage<T>::store(out + q, stage[q]);
+    __syncthreads();
+    stream_out<T>(stage, phi + e0 * nb, cnt * nb, vec);
+}
+
+// basis_cdb_lds_kernel: wider grids, each thread's level in an LDS row of
+// wp >= W floats (tpb threads per workgroup); the rows' first nb values are
+// the output.
+template <typename T, int K>
+__global__ __launch_bounds__(64) void basis_cdb_lds_kernel(const T* __restrict__ x, int64_t n,
+                                                           T* __restrict__ phi, GridConst g,
+                                                           int wp, int tpb) {
+    extern __shared__ float work[];
+    const int nb = g.nb;
+    const int W = nb + K;
+    const int64_t e0 = (int64_t)blockIdx.x * tpb;
+    const int64_t left = n - e0;
+    const int cnt = left < tpb ? (int)left : tpb;
+    const int el = threadIdx.x;
+    if (el < cnt) {
+        const float xv = Storage<T>::load(x + e0 + el);
+        const float xc = __builtin_amdgcn_fmed3f(xv, -g.xlim, g.xlim);
+        const float lo = coord_lo(xc, g.xlim, g.inv_lo, g.a_frac);
+        const float c0 = g.a_int + g.hw;
+        const float span = __builtin_floorf(__builtin_fmaf(xc, g.inv_h, c0) + lo);
+        float* w = work + el * wp;
+        for (int j = 0; j < W; ++j) w[j] = span == (float)j ? 1.0f : 0.0f;
+        for (int p = 1; p <= K; ++p) {
+            const float ip = 1.0f / (float)p;
+            float next = w[0];
+            for (int j = 0; j + p < W; ++j) {
+                const float u = __builtin_fmaf(xc, g.inv_h, c0 - (float)j) + lo;
+                const float cur = next;
+                next = w[j + 1];
+                w[j] = (u * cur + ((float)(p + 1) - u) * next) * ip;
+            }
+        }
+        if (xv != xv)
+            for (int j = 0; j < nb; ++j) w[j] = xv;
+    }
+    __syncthreads();
+    T* out = phi + e0 * nb;
+    for (int q = threadIdx.x; q < cnt * nb; q += blockDim.x)
+        Storage<T>::store(out + q, work[(q / nb) * wp + q % nb]);
 }
 
 }  // namespace
@@ -158,6 +263,64 @@ hipError_t launch_basis_f32(const float* x, int64_t n, float* phi, const GridCon
 hipError_t launch_basis_bf16(const uint16_t* x, int64_t n, uint16_t* phi, const GridConst& g,
                              const BasisLaunch& L, hipStream_t s) {
     return launch<uint16_t>(x, n, phi, g, L, s);
+}
+
+}  // namespace kan
+
+namespace kan {
+
+namespace {
+
+template <typename T, int K>
+hipError_t launch_cdb_k(const T* x, int64_t n, T* phi, const GridConst& g, hipStream_t s) {
+    const int W = g.nb + K;
+    const int vec = (reinterpret_cast<uintptr_t>(phi) % 16) == 0 ? 1 : 0;
+    const unsigned blocks = (unsigned)((n + kThreads - 1) / kThreads);
+    const size_t lds = (size_t)kThreads * g.nb * 4;
+    if (W <= 16) {
+        hipLaunchKernelGGL((basis_cdb_kernel<T, K, 16>), dim3(blocks), dim3(kThreads), lds, s, x,
+                           n, phi, g, vec);
+    } else if (W <= 32) {
+        hipLaunchKernelGGL((basis_cdb_kernel<T, K, 32>), dim3(blocks), dim3(kThreads), lds, s, x,
+                           n, phi, g, vec);
+    } else {
+        // rows of an odd number of floats (no bank conflicts between the
+        // threads' rows), as many threads as fit 64 KiB of LDS
+        const int wp = W | 1;
+        int tpb = 64;
+        while (tpb > 1 && (size_t)tpb * wp * 4 > 65536) tpb /= 2;
+        const int64_t nblk = (n + tpb - 1) / tpb;
+        if (nblk > 0x7fffffffLL) return hipErrorInvalidValue;
+        hipLaunchKernelGGL((basis_cdb_lds_kernel<T, K>), dim3((unsigned)nblk), dim3(tpb),
+                           (size_t)tpb * wp * 4, s, x, n, phi, g, wp, tpb);
+    }
+    return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_cdb(const T* x, int64_t n, T* phi, const GridConst& g, hipStream_t s) {
+    switch (g.k) {
+        case 1: return launch_cdb_k<T, 1>(x, n, phi, g, s);
+        case 2: return launch_cdb_k<T, 2>(x, n, phi, g, s);
+        case 3: return launch_cdb_k<T, 3>(x, n, phi, g, s);
+        case 4: return launch_cdb_k<T, 4>(x, n, phi, g, s);
+        case 5: return launch_cdb_k<T, 5>(x, n, phi, g, s);
+        case 6: return launch_cdb_k<T, 6>(x, n, phi, g, s);
+        case 7: return launch_cdb_k<T, 7>(x, n, phi, g, s);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace
+
+hipError_t launch_basis_cdb_f32(const float* x, int64_t n, float* phi, const GridConst& g,
+                                hipStream_t s) {
+    return launch_cdb<float>(x, n, phi, g, s);
+}
+
+hipError_t launch_basis_cdb_bf16(const uint16_t* x, int64_t n, uint16_t* phi, const GridConst& g,
+                                 hipStream_t s) {
+    return launch_cdb<uint16_t>(x, n, phi, g, s);
 }
 
 }  // namespace kan

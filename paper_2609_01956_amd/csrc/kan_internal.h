@@ -29,6 +29,11 @@ hipError_t launch_basis_f32(const float* x, int64_t n, float* phi, const GridCon
                             const BasisLaunch& L, hipStream_t s);
 hipError_t launch_basis_bf16(const uint16_t* x, int64_t n, uint16_t* phi, const GridConst& g,
                              const BasisLaunch& L, hipStream_t s);
+// The same basis by the Cox-de Boor recursion over every knot interval.
+hipError_t launch_basis_cdb_f32(const float* x, int64_t n, float* phi, const GridConst& g,
+                                hipStream_t s);
+hipError_t launch_basis_cdb_bf16(const uint16_t* x, int64_t n, uint16_t* phi, const GridConst& g,
+                                 hipStream_t s);
 
 // ---------------------------------------------------------------- fused layer
 //

@@ -331,3 +331,15 @@ def test_other_degrees_accepted(k):
         assert st == kb.KAN_OK
         kj = 8 if dt == kb.KAN_BF16 else 2
         assert n % (2 * 32 * kj * (2 if dt == kb.KAN_BF16 else 4)) == 0
+
+
+def test_cdb_basis_host_checks():
+    g = kb.make_grid(10)
+    f32, bad = kb.KAN_F32, kb.KAN_ERR_INVALID_ARG
+    assert kb.kan_basis_eval_cdb(g, f32, X, -1, PHI) == bad
+    assert kb.kan_basis_eval_cdb(g, f32, 0, 16, PHI) == bad
+    assert kb.kan_basis_eval_cdb(g, f32, X + 2, 16, PHI) == bad
+    assert kb.kan_basis_eval_cdb(g, f32, X, 16, X + 32) == bad
+    assert kb.kan_basis_eval_cdb(kb.make_grid(10, spline_order=8), f32, X, 16, PHI) == \
+        kb.KAN_ERR_UNSUPPORTED
+    assert kb.kan_basis_eval_cdb(g, f32, 0, 0, 0) == kb.KAN_OK
