@@ -299,6 +299,39 @@ kan_status kan_layer_backward_workspace_bytes(const kan_grid* grid, kan_dtype dt
                                               int32_t out_features, size_t* bytes);
 
 /*
+ * kan_layer_forward_span -- the layer of kan_layer_forward (eq. kan_forward)
+ * restricted to its nonzero terms: of each input's G + k basis values only
+ * the k + 1 whose support holds the input can be nonzero (the clamp of
+ * eq. bounded makes every other one exactly 0), so each (row, feature) adds
+ * k + 1 coefficient rows and the SiLU weight row, on the vector ALUs, instead
+ * of the G + k + 1 columns of the dense contraction.  Each basis value is
+ * still the closed clamped form (no recursion); the result equals
+ * kan_layer_forward's up to the fp32 summation order.  For large grids,
+ * where the dense contraction multiplies mostly zeros (G = 200: 4 of 203).
+ * This goes beyond the paper, whose method evaluates every basis.
+ *
+ *   x, coef, base_w, y   as kan_layer_forward
+ *   workspace            caller-owned, workspace_bytes >=
+ *                        kan_layer_forward_span_workspace_bytes(...), 16-byte
+ *                        aligned, overlapping no other argument (the weights
+ *                        transposed to fp32 [in][G + k + 1][out tile], and
+ *                        fp32 partial sums when the features are split over
+ *                        workgroups, added in a fixed order).
+ *
+ * Returns as kan_layer_forward, plus KAN_ERR_UNSUPPORTED for grids too wide
+ * for one feature's weight tile in LDS (G + k + 1 > 512).
+ */
+kan_status kan_layer_forward_span(const kan_grid* grid, kan_dtype dtype, int64_t batch,
+                                  int32_t in_features, int32_t out_features, const void* x,
+                                  const void* coef, const void* base_w, void* workspace,
+                                  size_t workspace_bytes, void* y, void* stream);
+
+/* Size in bytes of kan_layer_forward_span's workspace for this layer and batch. */
+kan_status kan_layer_forward_span_workspace_bytes(const kan_grid* grid, kan_dtype dtype,
+                                                  int64_t batch, int32_t in_features,
+                                                  int32_t out_features, size_t* bytes);
+
+/*
  * kan_layer_forward_noalloc -- kan_layer_forward without a workspace argument,
  * for callers that cannot allocate device memory (work under HIP graph
  * capture, tight serving loops, harnesses that forbid hipMalloc).  The

@@ -32,7 +32,8 @@ KAN_BF16 = 1
 EXPORTED_SYMBOLS = ("kan_basis_eval", "kan_basis_eval_cdb", "kan_layer_forward", "kan_layer_forward_workspace_bytes",
                     "kan_layer_packed_bytes", "kan_layer_pack", "kan_layer_forward_packed",
                     "kan_layer_plan", "kan_layer_forward_noalloc", "kan_layer_backward",
-                    "kan_layer_backward_workspace_bytes", "kan_status_string",
+                    "kan_layer_backward_workspace_bytes", "kan_layer_forward_span",
+                    "kan_layer_forward_span_workspace_bytes", "kan_status_string",
                     "kan_abi_version")
 
 _VP = ctypes.c_void_p
@@ -101,6 +102,11 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                                                ctypes.c_int32, ctypes.c_int32,
                                                                ctypes.POINTER(ctypes.c_size_t)]
             lib.kan_layer_backward_workspace_bytes.restype = ctypes.c_int
+            lib.kan_layer_forward_span.argtypes = lib.kan_layer_forward.argtypes
+            lib.kan_layer_forward_span.restype = ctypes.c_int
+            lib.kan_layer_forward_span_workspace_bytes.argtypes = \
+                lib.kan_layer_forward_workspace_bytes.argtypes
+            lib.kan_layer_forward_span_workspace_bytes.restype = ctypes.c_int
             lib.kan_status_string.argtypes = [ctypes.c_int]
             lib.kan_status_string.restype = ctypes.c_char_p
             lib.kan_abi_version.argtypes = []
@@ -178,6 +184,26 @@ def kan_layer_backward(grid: kan_grid, dtype: int, batch: int, in_features: int,
         ctypes.byref(grid), int(dtype), int(batch), int(in_features), int(out_features),
         _VP(x), _VP(coef), _VP(base_w), _VP(dy), _VP(dx), _VP(dcoef), _VP(dbase_w),
         _VP(workspace), ctypes.c_size_t(workspace_bytes), _VP(stream)))
+
+
+def kan_layer_forward_span(grid: kan_grid, dtype: int, batch: int, in_features: int,
+                           out_features: int, x: int, coef: int, base_w: int, workspace: int,
+                           workspace_bytes: int, y: int, stream: int = 0) -> int:
+    """Raw call: device addresses as integers; returns the kan_status code."""
+    return int(load_library().kan_layer_forward_span(
+        ctypes.byref(grid), int(dtype), int(batch), int(in_features), int(out_features),
+        _VP(x), _VP(coef), _VP(base_w), _VP(workspace), ctypes.c_size_t(workspace_bytes),
+        _VP(y), _VP(stream)))
+
+
+def kan_layer_forward_span_workspace_bytes(grid: kan_grid, dtype: int, batch: int,
+                                           in_features: int, out_features: int) -> Tuple[int, int]:
+    """Raw call: returns (kan_status, bytes)."""
+    n = ctypes.c_size_t(0)
+    st = int(load_library().kan_layer_forward_span_workspace_bytes(
+        ctypes.byref(grid), int(dtype), int(batch), int(in_features), int(out_features),
+        ctypes.byref(n)))
+    return st, int(n.value)
 
 
 def kan_layer_backward_workspace_bytes(grid: kan_grid, dtype: int, batch: int, in_features: int,
@@ -450,3 +476,29 @@ def layer_backward(x, coef, base_w, dy, grid_size: int, grid_lo: float = -1.0,
                                  base_w.data_ptr(), dy.data_ptr(), ptr(dx), ptr(dC), ptr(dW),
                                  workspace.data_ptr(), workspace.numel(), _stream(x.device)))
     return dx, dC, dW
+
+
+def layer_forward_span(x, coef, base_w, grid_size: int, grid_lo: float = -1.0,
+                       grid_hi: float = 1.0, out=None, spline_order: int = 3, workspace=None):
+    """kan_layer_forward_span: the layer on its nonzero terms only (the k + 1
+    bases whose support holds each input, and SiLU); x [B, in], coef [out, in,
+    G + k], base_w [out, in] -> y [B, out], on torch's current stream."""
+    torch = _torch()
+    _require_device(x)
+    n_in, n_out = _check_weights(coef, base_w, grid_size, spline_order)
+    if x.dim() != 2 or x.shape[1] != n_in or x.dtype != coef.dtype:
+        raise ValueError("x must be [B, in] with the weights' in and dtype")
+    B = x.shape[0]
+    dt = _dtype_code(x)
+    g = make_grid(grid_size, grid_lo, grid_hi, spline_order)
+    st, nbytes = kan_layer_forward_span_workspace_bytes(g, dt, B, n_in, n_out)
+    check(st)
+    if workspace is None or workspace.numel() < nbytes or workspace.device != x.device:
+        workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=x.device)
+    if out is None:
+        out = torch.empty((B, n_out), dtype=x.dtype, device=x.device)
+    with torch.cuda.device(x.device):
+        check(kan_layer_forward_span(g, dt, B, n_in, n_out, x.data_ptr(), coef.data_ptr(),
+                                     base_w.data_ptr(), workspace.data_ptr(), workspace.numel(),
+                                     out.data_ptr(), _stream(x.device)))
+    return out

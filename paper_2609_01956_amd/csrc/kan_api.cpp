@@ -473,4 +473,76 @@ kan_status kan_layer_backward(const kan_grid* grid, kan_dtype dtype, int64_t bat
                                               static_cast<hipStream_t>(stream)));
 }
 
+// Span-sparse geometry (after check_layer).
+static kan_status span_geom_of(const kan::GridConst& gc, int64_t batch, int32_t in_features,
+                               int32_t out_features, kan::SpanGeom* sg) {
+    if (batch < 0 || batch > (int64_t)0x7fffffff * 256) return KAN_ERR_INVALID_ARG;
+    if (!kan::span_geom(gc.nb, batch, in_features, out_features, sg)) return KAN_ERR_UNSUPPORTED;
+    return KAN_OK;
+}
+
+kan_status kan_layer_forward_span_workspace_bytes(const kan_grid* grid, kan_dtype dtype,
+                                                  int64_t batch, int32_t in_features,
+                                                  int32_t out_features, size_t* bytes) {
+    if (bytes == nullptr) return KAN_ERR_INVALID_ARG;
+    kan::GridConst gc;
+    kan::LayerGeom geom;
+    kan_status st = check_layer(grid, dtype, in_features, out_features, &gc, &geom);
+    if (st != KAN_OK) return st;
+    kan::SpanGeom sg;
+    st = span_geom_of(gc, batch, in_features, out_features, &sg);
+    if (st != KAN_OK) return st;
+    *bytes = sg.bytes;
+    return KAN_OK;
+}
+
+kan_status kan_layer_forward_span(const kan_grid* grid, kan_dtype dtype, int64_t batch,
+                                  int32_t in_features, int32_t out_features, const void* x,
+                                  const void* coef, const void* base_w, void* workspace,
+                                  size_t workspace_bytes, void* y, void* stream) {
+    kan::GridConst gc;
+    kan::LayerGeom geom;
+    kan_status st = check_layer(grid, dtype, in_features, out_features, &gc, &geom);
+    if (st != KAN_OK) return st;
+    kan::SpanGeom sg;
+    st = span_geom_of(gc, batch, in_features, out_features, &sg);
+    if (st != KAN_OK) return st;
+    if (batch == 0) return KAN_OK;
+    st = check_forward(gc, dtype, batch, in_features, out_features, x, coef, base_w, y);
+    if (st != KAN_OK) return st;
+    if (workspace == nullptr || !aligned(workspace, 16) || workspace_bytes < sg.bytes)
+        return KAN_ERR_INVALID_ARG;
+    const size_t es = dtype_size(dtype);
+    const uint64_t ub = (uint64_t)batch;
+    const size_t ws = sg.bytes;
+    if (overlap(workspace, ws, x, ub * (size_t)in_features * es) ||
+        overlap(workspace, ws, coef, (size_t)out_features * in_features * gc.nb * es) ||
+        overlap(workspace, ws, base_w, (size_t)out_features * in_features * es) ||
+        overlap(workspace, ws, y, ub * (size_t)out_features * es))
+        return KAN_ERR_INVALID_ARG;
+    kan::SpanArgs a;
+    a.x = x;
+    a.wt = nullptr;
+    a.y = y;
+    a.ws = workspace;
+    a.off_p = sg.off_p;
+    a.batch = batch;
+    a.in = in_features;
+    a.out = out_features;
+    a.nb = gc.nb;
+    a.outp = sg.outp;
+    a.fs = sg.fs;
+    a.fpf = sg.fpf;
+    a.inv_h = gc.inv_h;
+    a.inv_lo = gc.inv_lo;
+    a.xlim = gc.xlim;
+    a.a_int = gc.a_int;
+    a.a_frac = gc.a_frac;
+    a.kdeg = gc.k;
+    a.hw = gc.hw;
+    for (int m = 0; m < 4; ++m) a.hc[m] = gc.hc[m];
+    return device_status(kan::launch_span(dtype == KAN_BF16, sg, a, coef, base_w,
+                                          static_cast<hipStream_t>(stream)));
+}
+
 }  // extern "C"

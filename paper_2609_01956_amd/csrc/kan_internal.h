@@ -230,4 +230,35 @@ struct BwdArgs {
 
 hipError_t launch_backward(bool bf16, const BwdGeom& g, const BwdArgs& a, hipStream_t s);
 
+// ------------------------------------------------------------ span-sparse
+//
+// The layer forward restricted to the k + 1 bases whose support holds each
+// input (and the SiLU term), on the vector ALUs with one feature's weights
+// staged in LDS at a time (kan_span.hip).
+struct SpanGeom {
+    int opt, ng;     // outputs per thread, output groups per workgroup
+    int otiles;      // output tiles of opt * ng columns
+    int outp;        // out padded to whole tiles (columns of the transposed weights)
+    int fs, fpf;     // feature splits (partials summed when > 1), features per split
+    int64_t rblocks; // 256-row blocks
+    size_t off_w, off_p, bytes;  // workspace: transposed fp32 weights, partial sums
+};
+bool span_geom(int nb, int64_t batch, int in, int out, SpanGeom* g);
+
+struct SpanArgs {
+    const void* x;    // [batch, in]
+    const float* wt;  // transposed weights [in][nb + 1][outp] (set by the launcher)
+    void* y;          // [batch, out]
+    void* ws;         // workspace of SpanGeom::bytes
+    size_t off_p;
+    int64_t batch;
+    int in, out, nb, outp, fs, fpf;
+    float inv_h, inv_lo, xlim, a_int, a_frac;
+    int kdeg;
+    float hw;
+    float hc[4];
+};
+hipError_t launch_span(bool bf16, const SpanGeom& g, const SpanArgs& a, const void* coef,
+                       const void* bw, hipStream_t s);
+
 }  // namespace kan

@@ -343,3 +343,46 @@ def test_cdb_basis_host_checks():
     assert kb.kan_basis_eval_cdb(kb.make_grid(10, spline_order=8), f32, X, 16, PHI) == \
         kb.KAN_ERR_UNSUPPORTED
     assert kb.kan_basis_eval_cdb(g, f32, 0, 0, 0) == kb.KAN_OK
+
+
+def test_span_forward_host_checks():
+    """kan_layer_forward_span rejects invalid arguments on the host (fake
+    addresses, never dereferenced) and grids too wide for its LDS tile."""
+    g = kb.make_grid(100)
+    f32, bad = kb.KAN_F32, kb.KAN_ERR_INVALID_ARG
+    WS = 0xC00000000
+    st, need = kb.kan_layer_forward_span_workspace_bytes(g, f32, 300, 13, 45)
+    assert st == kb.KAN_OK and need > 0
+    call = lambda *a: kb.kan_layer_forward_span(g, f32, 300, 13, 45, *a)
+    assert call(X, C, W, WS, need - 1, Y) == bad            # short workspace
+    assert call(X, C, W, 0, need, Y) == bad                 # no workspace
+    assert call(X, C, W, WS + 8, need, Y) == bad            # misaligned workspace
+    assert call(X, C, W, Y - 16, need, Y) == bad            # workspace over y
+    assert call(X, C, W, WS, need, X + 16) == bad           # y over x
+    assert call(X, 0, W, WS, need, Y) == bad                # no coefficients
+    assert call(X + 2, C, W, WS, need, Y) == bad            # misaligned x
+    assert kb.kan_layer_forward_span(g, f32, -1, 13, 45, X, C, W, WS, need, Y) == bad
+    assert kb.kan_layer_forward_span(g, f32, 0, 13, 45, 0, 0, 0, 0, 0, 0) == kb.KAN_OK
+    # G + k + 1 = 512 columns fit one feature's weight tile, 513 do not
+    assert kb.kan_layer_forward_span_workspace_bytes(kb.make_grid(508), f32, 16, 3, 40)[0] == \
+        kb.KAN_OK
+    wide = kb.make_grid(509)
+    assert kb.kan_layer_forward_span_workspace_bytes(wide, f32, 16, 3, 40)[0] == \
+        kb.KAN_ERR_UNSUPPORTED
+    assert kb.kan_layer_forward_span(wide, f32, 16, 3, 40, X, C, W, WS, 1 << 30, Y) == \
+        kb.KAN_ERR_UNSUPPORTED
+    assert kb.kan_layer_forward_span_workspace_bytes(kb.make_grid(10, spline_order=7), f32, 16,
+                                                     3, 40)[0] == kb.KAN_OK
+
+
+@pytest.mark.parametrize("G,n_in,n_out,B", [(50, 128, 128, 8192), (200, 128, 128, 8192),
+                                            (100, 13, 45, 300), (5, 2, 5, 1024)])
+def test_span_workspace_bytes(G, n_in, n_out, B):
+    """The workspace holds the fp32 weights transposed per feature and padded
+    to the output tile (16, 32 or 64), plus fp32 partial sums for at most 256
+    feature splits when the row blocks do not fill the chip."""
+    for dt in (kb.KAN_F32, kb.KAN_BF16):
+        st, n = kb.kan_layer_forward_span_workspace_bytes(kb.make_grid(G), dt, B, n_in, n_out)
+        assert st == kb.KAN_OK
+        w = n_in * (G + 4) * n_out * 4
+        assert w <= n <= n_in * (G + 4) * (n_out + 63) * 4 + 256 * B * n_out * 4 + 512
