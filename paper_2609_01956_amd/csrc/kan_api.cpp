@@ -533,6 +533,7 @@ kan_status kan_layer_forward_span(const kan_grid* grid, kan_dtype dtype, int64_t
     a.outp = sg.outp;
     a.fs = sg.fs;
     a.fpf = sg.fpf;
+    a.cs = sg.cs;
     a.inv_h = gc.inv_h;
     a.inv_lo = gc.inv_lo;
     a.xlim = gc.xlim;

@@ -236,11 +236,12 @@ hipError_t launch_backward(bool bf16, const BwdGeom& g, const BwdArgs& a, hipStr
 // input (and the SiLU term), on the vector ALUs with one feature's weights
 // staged in LDS at a time (kan_span.hip).
 struct SpanGeom {
-    int opt, ng;     // outputs per thread, output groups per workgroup
+    int opt, ng, nr; // outputs per thread, output groups per workgroup, rows per thread
     int otiles;      // output tiles of opt * ng columns
     int outp;        // out padded to whole tiles (columns of the transposed weights)
     int fs, fpf;     // feature splits (partials summed when > 1), features per split
-    int64_t rblocks; // 256-row blocks
+    int cs;          // LDS stride of one weight column in floats (tile width, padded)
+    int64_t rblocks; // row blocks of 256 nr / ng rows
     size_t off_w, off_p, bytes;  // workspace: transposed fp32 weights, partial sums
 };
 bool span_geom(int nb, int64_t batch, int in, int out, SpanGeom* g);
@@ -252,7 +253,7 @@ struct SpanArgs {
     void* ws;         // workspace of SpanGeom::bytes
     size_t off_p;
     int64_t batch;
-    int in, out, nb, outp, fs, fpf;
+    int in, out, nb, outp, fs, fpf, cs;
     float inv_h, inv_lo, xlim, a_int, a_frac;
     int kdeg;
     float hw;

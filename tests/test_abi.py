@@ -379,10 +379,10 @@ def test_span_forward_host_checks():
                                             (100, 13, 45, 300), (5, 2, 5, 1024)])
 def test_span_workspace_bytes(G, n_in, n_out, B):
     """The workspace holds the fp32 weights transposed per feature and padded
-    to the output tile (16, 32 or 64), plus fp32 partial sums for at most 256
+    to the output tile (16, 32 or 64), plus fp32 partial sums for at most 512
     feature splits when the row blocks do not fill the chip."""
     for dt in (kb.KAN_F32, kb.KAN_BF16):
         st, n = kb.kan_layer_forward_span_workspace_bytes(kb.make_grid(G), dt, B, n_in, n_out)
         assert st == kb.KAN_OK
         w = n_in * (G + 4) * n_out * 4
-        assert w <= n <= n_in * (G + 4) * (n_out + 63) * 4 + 256 * B * n_out * 4 + 512
+        assert w <= n <= n_in * (G + 4) * (n_out + 63) * 4 + 512 * B * n_out * 4 + 512
