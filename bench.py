@@ -154,7 +154,9 @@ def configs_sweep(dtype: str) -> None:
     """Every configured workload, one JSON line each: the fused layer (packed
     weights, per layer of the MLP) against its roofline, the basis-only kernel
     of its input, and for the grid-size sweep the partition-of-unity error of
-    the basis kernel on the same x plus 2001 points spread over the grid."""
+    the basis kernel on the same x plus 2001 points spread over the grid and
+    the span-sparse layer (kan_layer_forward_span, weight transposition
+    included) beside the dense one."""
     import numpy as np
     import torch
 
@@ -196,6 +198,21 @@ def configs_sweep(dtype: str) -> None:
             layers.append({"in": C.shape[1], "out": C.shape[0], **k})
             h = out
         line["layers"] = layers
+        if name in SPAN_GRIDS:
+            (C, Wb), = W["layers"]
+            Ct = torch.from_numpy(prep(C)).to("cuda").to(tdt).contiguous()
+            Wt = torch.from_numpy(prep(Wb)).to("cuda").to(tdt).contiguous()
+            n_out, n_in = Wb.shape
+            st, nbytes = kb.kan_layer_forward_span_workspace_bytes(
+                kb.make_grid(G, lo, hi), kb.KAN_BF16 if dtype == "bf16" else kb.KAN_F32, B,
+                n_in, n_out)
+            kb.check(st)
+            ws = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+            y = torch.empty((B, n_out), dtype=tdt, device="cuda")
+            sus = _time_us(lambda: kb.layer_forward_span(x, Ct, Wt, G, lo, hi, out=y, workspace=ws))
+            line["span_sparse_layer"] = {
+                "us": sus, "samples_per_s": B / sus * 1e6,
+                "valu_frac": B * n_in * (5.0 * n_out + 38.0) / (sus * 1e-6) / 1e9 / PEAK_VALU_GOPS}
         print(json.dumps(line), flush=True)
 
 
@@ -341,6 +358,101 @@ def measure_step(dtype: str, W, steps: int, warmup: int) -> dict:
             "kernels": kern, "shapes": shapes, "x": x, "outs": hs, "prep": prep}
 
 
+def backward_block(dtype: str, W, r: dict, reps: int = 10) -> dict:
+    """kan_layer_backward of each MLP layer (dx, dcoef and dbase_w) on that
+    layer's own input from the timed forward and a seeded N(0, 1) dy, timed
+    with HIP events on torch's current stream.  Work: the two contractions
+    dx = dy W^T and [dcoef dbase_w] = A^T dy over all G + 4 columns of the
+    layer (A: SiLU and basis values of x), 2 B out in (G + 4) dense flops
+    each, against the MFMA peak of the dtype."""
+    import torch
+
+    from paper_2609_01956_amd import binding as kb
+
+    G, lo, hi = W["G"], W["lo"], W["hi"]
+    nb = G + 3
+    tdt = r["x"].dtype
+    prep = r["prep"]
+    ins = [r["x"]] + r["outs"][:-1]
+    gen = torch.Generator(device=r["x"].device).manual_seed(11)
+    layers = {}
+    total = 0.0
+    for li, ((C, Wb), h) in enumerate(zip(W["layers"], ins)):
+        Ct = torch.from_numpy(prep(C)).to(h.device).to(tdt).contiguous()
+        Wt = torch.from_numpy(prep(Wb)).to(h.device).to(tdt).contiguous()
+        B, n_in = h.shape
+        n_out = C.shape[0]
+        dy = torch.randn((B, n_out), generator=gen, device=h.device).to(tdt)
+        st, nbytes = kb.kan_layer_backward_workspace_bytes(
+            kb.make_grid(G, lo, hi), kb.KAN_BF16 if dtype == "bf16" else kb.KAN_F32, B, n_in,
+            n_out)
+        kb.check(st)
+        ws = torch.empty(nbytes, dtype=torch.uint8, device=h.device)
+        outs = (torch.empty_like(h), torch.empty_like(Ct), torch.empty_like(Wt))
+        us = _time_us(lambda: kb.layer_backward(h, Ct, Wt, dy, G, lo, hi, workspace=ws, out=outs),
+                      warmup=2, reps=reps)
+        flop = 2 * 2.0 * B * n_out * n_in * (nb + 1)
+        layers[f"layer{li + 1}_{n_in}x{n_out}"] = {
+            "avg_us": us, "bound": "mfma", "unit": "TFLOP/s", "peak": PEAK_TFLOPS[dtype],
+            "achieved": flop / (us * 1e-6) / 1e12,
+            "frac": flop / (us * 1e-6) / 1e12 / PEAK_TFLOPS[dtype]}
+        total += us
+    return {"ms_all_layers": total * 1e-3, "layers": layers,
+            "step": "kan_layer_backward (dx, dcoef, dbase_w) per layer"}
+
+
+SPAN_GRIDS = ("c4_layer_128x128_g50", "c4_layer_128x128_g100", "c4_layer_128x128_g200")
+
+
+def grid_sweep_block(dtype: str = "f32") -> dict:
+    """The grid-size sweep layer (batch 8192, 128 -> 128, G = 50, 100, 200)
+    through both forward paths: the dense fused layer (kan_layer_forward_packed,
+    MFMA over all G + 4 columns) and the span-sparse one (kan_layer_forward_span,
+    its weight transposition included: only the k + 1 nonzero bases and SiLU
+    per input, on the vector ALUs), with the partition-of-unity error of the
+    basis kernel on the same inputs.  Dense work against the MFMA peak; the
+    span path's multiply-adds (B in out (k + 2)) and its least basis work (38
+    lane-ops per input) against the VALU peak."""
+    import numpy as np
+    import torch
+
+    from paper_2609_01956_amd import binding as kb
+    from paper_2609_01956_amd import workloads as wl
+
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    prep = (lambda a: wl.round_to_bf16_f32(a)) if dtype == "bf16" else (lambda a: a)
+    out = {}
+    for name in SPAN_GRIDS:
+        W = wl.make_workload(name)
+        G, lo, hi = W["G"], W["lo"], W["hi"]
+        (C, Wb), = W["layers"]
+        x = torch.from_numpy(prep(W["x"])).to("cuda").to(tdt).contiguous()
+        Ct = torch.from_numpy(prep(C)).to("cuda").to(tdt).contiguous()
+        Wt = torch.from_numpy(prep(Wb)).to("cuda").to(tdt).contiguous()
+        B, n_in = x.shape
+        n_out = C.shape[0]
+        y = torch.empty((B, n_out), dtype=tdt, device="cuda")
+        pk = kb.pack_layer(Ct, Wt, G, lo, hi)
+        dense = _time_us(lambda: kb.layer_forward_packed(x, pk, out=y))
+        st, nbytes = kb.kan_layer_forward_span_workspace_bytes(
+            kb.make_grid(G, lo, hi), kb.KAN_BF16 if dtype == "bf16" else kb.KAN_F32, B, n_in,
+            n_out)
+        kb.check(st)
+        ws = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+        span = _time_us(lambda: kb.layer_forward_span(x, Ct, Wt, G, lo, hi, out=y, workspace=ws))
+        xs = torch.from_numpy(np.concatenate([W["x"].reshape(-1),
+                                              np.linspace(lo, hi, 2001)]).astype(np.float32))
+        pu = kb.basis(xs.to("cuda"), G, lo, hi).double().sum(dim=1)
+        flop = 2.0 * B * n_out * n_in * (G + 4)
+        lane_ops = B * n_in * (5.0 * n_out + 38.0)
+        out[name] = {"grid_size": G, "dense_us": dense, "span_us": span,
+                     "samples_per_s": B / (min(dense, span) * 1e-6),
+                     "dense_mfma_frac": flop / (dense * 1e-6) / 1e12 / PEAK_TFLOPS[dtype],
+                     "span_valu_frac": lane_ops / (span * 1e-6) / 1e9 / PEAK_VALU_GOPS,
+                     "pu_max_err": float((pu - 1.0).abs().max())}
+    return {"dtype": dtype, "grids": out}
+
+
 def cdb_context() -> dict:
     """The truncated-power basis kernel against our Cox-de Boor kernel (the
     recursion over every knot interval that the paper measures against), fp32
@@ -472,6 +584,9 @@ def main() -> int:
                                     "valu_frac_dense_count")}
                                for n, kk in o["kernels"].items()},
                    "parity": o["parity"]}
+    line["backward"] = backward_block(args.dtype, W, r)
+    line[other]["backward"] = backward_block(other, W, o)
+    line["grid_sweep"] = grid_sweep_block("f32")
     line["cox_de_boor_context"] = cdb_context()
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(W, args.cpu_seconds)

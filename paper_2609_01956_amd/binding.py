@@ -445,12 +445,14 @@ def mlp_forward(x, layers: Sequence[Tuple[object, object]], grid_size: int, grid
 
 def layer_backward(x, coef, base_w, dy, grid_size: int, grid_lo: float = -1.0,
                    grid_hi: float = 1.0, need_dx: bool = True, need_dw: bool = True,
-                   workspace=None):
+                   workspace=None, out=None):
     """Gradients of one KAN layer (kan_layer_backward): x [B, in], coef [out,
     in, G + 3], base_w [out, in], dy [B, out], all of one dtype on one device
     -> (dx [B, in] or None, dcoef or None, dbase_w or None), enqueued on
     torch's current stream.  `workspace` (a uint8 device tensor) is used when
-    large enough, else a fresh one is taken from torch's allocator."""
+    large enough, else a fresh one is taken from torch's allocator; `out`, a
+    (dx, dcoef, dbase_w) tuple of tensors shaped like x, coef and base_w,
+    receives the gradients instead of fresh tensors."""
     torch = _torch()
     _require_device(x, dy)
     n_in, n_out = _check_weights(coef, base_w, grid_size)
@@ -467,9 +469,18 @@ def layer_backward(x, coef, base_w, dy, grid_size: int, grid_lo: float = -1.0,
     check(st)
     if workspace is None or workspace.numel() < nbytes or workspace.device != x.device:
         workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=x.device)
-    dx = torch.empty_like(x) if need_dx else None
-    dC = torch.empty_like(coef) if need_dw else None
-    dW = torch.empty_like(base_w) if need_dw else None
+    if out is not None:
+        dx, dC, dW = out
+        for t, like in ((dx, x), (dC, coef), (dW, base_w)):
+            if t is not None and (t.shape != like.shape or t.dtype != like.dtype or
+                                  t.device != like.device or not t.is_contiguous()):
+                raise ValueError("out tensors must match x, coef and base_w")
+        dx = dx if need_dx else None
+        dC, dW = (dC, dW) if need_dw else (None, None)
+    else:
+        dx = torch.empty_like(x) if need_dx else None
+        dC = torch.empty_like(coef) if need_dw else None
+        dW = torch.empty_like(base_w) if need_dw else None
     ptr = lambda t: 0 if t is None else t.data_ptr()
     with torch.cuda.device(x.device):
         check(kan_layer_backward(g, dt, B, n_in, n_out, x.data_ptr(), coef.data_ptr(),
