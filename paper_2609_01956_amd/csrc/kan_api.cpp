@@ -147,12 +147,14 @@ static kan_status check_layer(const kan_grid* grid, kan_dtype dtype, int32_t in_
     if (st != KAN_OK) return st;
     if (in_features < 1 || out_features < 1) return KAN_ERR_INVALID_ARG;
     if ((int64_t)in_features * (gc->nb + 1) >= 0x80000000LL) return KAN_ERR_INVALID_ARG;
-    // The fused kernel addresses x as a per-workgroup base plus 32-bit element
-    // offsets over at most kan::kLayerMaxRows rows.
-    if ((int64_t)kan::kLayerMaxRows * in_features >= 0x100000000LL) return KAN_ERR_INVALID_ARG;
+    // The fused kernel reads x through a per-workgroup buffer resource with
+    // 32-bit byte offsets over at most kan::kLayerMaxRows rows (of elements of
+    // at most 4 bytes), and each N tile of the packed weights likewise.
+    if ((int64_t)kan::kLayerMaxRows * in_features * 4 >= 0x100000000LL) return KAN_ERR_INVALID_ARG;
     if ((int64_t)out_features * in_features * gc->nb >= (1LL << 40)) return KAN_ERR_INVALID_ARG;
     if (!kan::layer_geom(gc->nb, gc->k, dtype == KAN_BF16, in_features, out_features, geom))
         return KAN_ERR_INVALID_ARG;
+    if (geom->packed_bytes / (size_t)geom->ntiles >= 0x100000000ULL) return KAN_ERR_INVALID_ARG;
     return KAN_OK;
 }
 

@@ -35,6 +35,10 @@ namespace kan {
 typedef float floatx2 __attribute__((ext_vector_type(2)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+// Fourth word of a raw buffer resource (stride 0) on CDNA GPUs: 32-bit data
+// format, no swizzling; reads past the resource's byte count return 0.
+constexpr int kBufferWord3 = 0x00020000;
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x16 __attribute__((ext_vector_type(16)));

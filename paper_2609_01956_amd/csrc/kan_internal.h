@@ -99,7 +99,7 @@ struct LayerCfg {
     int cs;  // column slices per N tile: 1, 2 or 4 (rf = 1, nw = 4 only)
 };
 // Most rows any workgroup shape covers (x is addressed per workgroup with
-// 32-bit element offsets, so kLayerMaxRows * in must stay below 2^32).
+// 32-bit byte offsets, so kLayerMaxRows * in * 4 must stay below 2^32).
 constexpr int kLayerMaxRows = 256;
 // Rows per workgroup of a shape.
 inline int64_t layer_cfg_rows(const LayerCfg& c) {

@@ -278,11 +278,19 @@ void layer_kernel(LayerArgs a) {
     const char* __restrict__ wpt =
         static_cast<const char*>(a.wp) + (size_t)nt * (size_t)a.nblk_pad * BLKBL;
 
-    // x is addressed as a per-workgroup base plus 32-bit element offsets (the
-    // host rejects layers with kLayerMaxRows * in >= 2^32).  Rows past the
-    // batch read row batch - 1 (their results are not stored).
+    // x and the N tile's packed weights are read through buffer resources
+    // with 32-bit byte offsets: x from a per-workgroup base (the host rejects
+    // layers with kLayerMaxRows * in * 4 >= 2^32, and N tiles of 2^32 packed
+    // bytes or more).  Each lane's offset within a pair or chunk is fixed, so
+    // it is computed once here; the pair's or chunk's offset is wave-uniform
+    // and goes in the scalar operand.  Rows past the batch read row batch - 1
+    // (their results are not stored).
     const int64_t wg_row0 = (int64_t)blockIdx.x * BM;
     const T* __restrict__ xw = x + wg_row0 * (int64_t)a.in;
+    const uint64_t x_left = (uint64_t)(a.batch - wg_row0) * (uint64_t)a.in * sizeof(T);
+    const __amdgpu_buffer_rsrc_t xrs = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<T*>(xw), (short)0, (int)(x_left < 0xffffffffull ? x_left : 0xffffffffull),
+        kBufferWord3);
     uint32_t xoff[GRF];  // element offset of (row, feature h of pair 0)
 #pragma unroll
     for (int rf = 0; rf < GRF; ++rf) {
@@ -300,6 +308,21 @@ void layer_kernel(LayerArgs a) {
     uint32_t xsel[GRF];
 #pragma unroll
     for (int rf = 0; rf < GRF; ++rf) xsel[rf] = (xoff[rf] & 1u) ? 0x03020c0cu : 0x01000c0cu;
+    // Byte offsets of the lane's x at pair 0 (XP: of the aligned word holding
+    // it), and at the last pair of an odd feature count, where the phantom
+    // lanes step back one feature; pair p adds 2 p elements (XP: p words).
+    uint32_t xvo[GRF], xvo_odd[GRF];
+#pragma unroll
+    for (int rf = 0; rf < GRF; ++rf) {
+        const uint32_t eb = xoff[rf] - (uint32_t)h;
+        if constexpr (XP) {
+            xvo[rf] = (xoff[rf] >> 1) * 4u;
+            xvo_odd[rf] = (eb >> 1) * 4u;
+        } else {
+            xvo[rf] = xoff[rf] * (uint32_t)sizeof(T);
+            xvo_odd[rf] = eb * (uint32_t)sizeof(T);
+        }
+    }
 
     // ---- loads of chunk c into register set j, for the wave's blocks from
     // position p on: first the x of each block and row tile (per lane: the
@@ -317,6 +340,9 @@ void layer_kernel(LayerArgs a) {
     constexpr bool X_FIRST_ONLY = ALIGNED && BF16 && (SP || Occ<RF, NF>::waves == 2);
     typedef u32x4 WSet[DPW];
     const uint32_t wlane = (uint32_t)(wave * 1024 + lane * 16);
+    const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<char*>(wpt), (short)0, (int)((uint32_t)a.nblk_pad * (uint32_t)BLKBL),
+        kBufferWord3);
     uint32_t goff[CS == 1 ? 1 : DPW];
     if constexpr (CS > 1) {
 #pragma unroll
@@ -333,16 +359,20 @@ void layer_kernel(LayerArgs a) {
             int pr = p.pair;
             if constexpr (SPK) pr = c * PPC + wk + WK * (t / 2);
             pr = pr < a.npairs ? pr : a.npairs - 1;
-            const uint32_t back = (pr == last_pair_odd) ? (uint32_t)h : 0u;
+            const bool odd = pr == last_pair_odd;  // wave-uniform
             // The split generation reads x only at a feature's first block.
             if (!(X_FIRST_ONLY && t % NSBC != 0)) {
 #pragma unroll
                 for (int rf = 0; rf < GRF; ++rf) {
-                    const uint32_t off = xoff[rf] + (uint32_t)(2 * pr) - back;
+                    const uint32_t vo = odd ? xvo_odd[rf] : xvo[rf];
                     if constexpr (XP)
-                        xs[t][rf] = reinterpret_cast<const uint32_t*>(xw)[off >> 1];
+                        xs[t][rf] = __builtin_amdgcn_raw_buffer_load_b32(xrs, vo, 4 * pr, 0);
+                    else if constexpr (sizeof(T) == 4)
+                        xs[t][rf] = __builtin_amdgcn_raw_buffer_load_b32(
+                            xrs, vo, 2 * (int)sizeof(T) * pr, 0);
                     else
-                        xs[t][rf] = Tr<T>::raw(xw + off);
+                        xs[t][rf] = __builtin_amdgcn_raw_buffer_load_b16(
+                            xrs, vo, 2 * (int)sizeof(T) * pr, 0);
                 }
             } else {
 #pragma unroll
@@ -351,13 +381,11 @@ void layer_kernel(LayerArgs a) {
             p = advance<WK>(p, nsb);
         }
         const int cc = c < a.nchunks ? c : a.nchunks - 1;
-        const char* g = wpt + (size_t)cc * (KB * BLKBL);  // wave-uniform
+        const int cofs = (int)((uint32_t)cc * (uint32_t)(KB * BLKBL));  // the chunk's bytes
 #pragma unroll
         for (int i = 0; i < DPW; ++i) {
-            if constexpr (CS == 1)
-                ws[i] = *reinterpret_cast<const u32x4*>(g + (wlane + (uint32_t)(i * 1024 * NW)));
-            else
-                ws[i] = *reinterpret_cast<const u32x4*>(g + goff[i]);
+            const uint32_t vo = CS == 1 ? wlane + (uint32_t)(i * 1024 * NW) : goff[i];
+            ws[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(wrs, vo, cofs, 0));
         }
     };
     // Register set -> LDS stage kk (the same byte offsets as in the chunk).
@@ -375,8 +403,9 @@ void layer_kernel(LayerArgs a) {
             v = __uint_as_float(__builtin_amdgcn_perm(raw, raw, xsel[rf]));
         else
             v = Tr<T>::value(raw);
-        if (p.pair == last_pair_odd) return h ? 0.0f : v;
-        return v;
+        // (one condition: the wave-uniform pair test and the lane's half
+        // combine into one lane mask, so this is a single select)
+        return (p.pair == last_pair_odd && h != 0) ? 0.0f : v;
     };
 
     // acc[rf]: row tile rf ^ ch of the wave's row group (XA: the tile whose A
@@ -974,7 +1003,7 @@ hipError_t launch_cfg(const LayerGeom& g, LayerArgs a, hipStream_t s) {
     // Eight waves of two row tiles: the sparse shared-A shape (layer_shape_ok)
     constexpr bool XA = RF == 2 && NW == 8;
     constexpr int BM = 32 * RF * (NW / WK) / (XA ? 2 : 1);
-    static_assert(BM <= kLayerMaxRows, "rows per workgroup (32-bit x offsets)");
+    static_assert(BM <= kLayerMaxRows, "rows per workgroup (32-bit x byte offsets)");
     a.nblk_pad = g.nblk_pad;
     a.nchunks = g.nblk_pad / g.kb;
     const dim3 grid((unsigned)((a.batch + BM - 1) / BM), (unsigned)(g.ntiles * (NFL / NF)));

@@ -109,13 +109,15 @@ def test_layer_argument_checks():
     assert kb.kan_layer_forward(g, f32, 16, 4, 4, X, C, W, WS, WSB, X + 8) == bad
     assert kb.kan_layer_forward(g, f32, 16, 4, 4, X, C, W, WS, WSB, C + 8) == bad
     assert kb.kan_layer_forward(g, f32, 16, 4, 4, X, C, W, WS, WSB, W) == bad
-    # x offsets of a workgroup are 32-bit: 256 rows x in must stay below 2^32
+    # x byte offsets of a workgroup are 32-bit: 256 rows x in x 4 bytes must
+    # stay below 2^32 (in both dtypes)
     g1 = kb.make_grid(1)
-    assert kb.kan_layer_forward(g1, f32, 16, 2 ** 24, 1, X, C, W, WS, WSB, Y) == bad
-    assert kb.kan_layer_forward_packed(g1, f32, 16, 2 ** 24, 1, X, C, WSB, Y) == bad
-    assert kb.kan_layer_plan(g1, f32, 16, 2 ** 24, 1)[0] == bad
-    assert kb.kan_layer_packed_bytes(g1, f32, 2 ** 24, 1)[0] == bad
-    assert kb.kan_layer_packed_bytes(g1, f32, 2 ** 24 - 1, 1)[0] == kb.KAN_OK
+    for dt in (f32, kb.KAN_BF16):
+        assert kb.kan_layer_forward(g1, dt, 16, 2 ** 22, 1, X, C, W, WS, WSB, Y) == bad
+        assert kb.kan_layer_forward_packed(g1, dt, 16, 2 ** 22, 1, X, C, WSB, Y) == bad
+        assert kb.kan_layer_plan(g1, dt, 16, 2 ** 22, 1)[0] == bad
+        assert kb.kan_layer_packed_bytes(g1, dt, 2 ** 22, 1)[0] == bad
+        assert kb.kan_layer_packed_bytes(g1, dt, 2 ** 22 - 1, 1)[0] == kb.KAN_OK
     # workspace: null, misaligned (16 bytes), short, overlapping any tensor
     need = kb.kan_layer_forward_workspace_bytes(g, f32, 16, 4, 4)[1]
     assert need == kb.kan_layer_packed_bytes(g, f32, 4, 4)[1]
