@@ -231,8 +231,13 @@ __global__ __launch_bounds__(64 * NW) void dx_kernel(DxArgs<T> a) {
 
     typedef u32x4 WSet[UPT];
     typedef T XSet[RF];
-    WSet wq[2];
-    XSet xq[2];
+    // Register sets: tile t's loads go to set t % L, issued L tiles before
+    // the tile and stored to LDS one tile before it, so each store waits for
+    // loads issued L - 1 tiles earlier (a tile is short: with one tile of
+    // distance the stores wait on most of a memory round trip).
+    constexpr int L = SM >= 32 ? 2 : 4;  // (32 k-steps of fp32 dy already fill the registers)
+    WSet wq[L];
+    XSet xq[L];
     // Loads of tile t: unconditional (tiles past the split's last, units past
     // the chunk's and features past `in` re-read valid addresses; their
     // values are not used), so the compiler's wait before a register set is
@@ -363,21 +368,27 @@ __global__ __launch_bounds__(64 * NW) void dx_kernel(DxArgs<T> a) {
         }
     };
 
-    issue(t_begin, wq[0], xq[0]);
-    issue(t_begin + 1, wq[1], xq[1]);
+#pragma unroll
+    for (int j = 0; j < L; ++j) issue(t_begin + j, wq[j], xq[j]);
     put(0, wq[0]);
     __syncthreads();
-    for (int t = t_begin; t < t_end; t += 2) {
-        tile(t, 0, xq[0]);
-        issue(t + 2, wq[0], xq[0]);
-        if (t + 1 < t_end) put(1, wq[1]);
-        __syncthreads();
-        if (t + 1 < t_end) {
-            tile(t + 1, 1, xq[1]);
-            issue(t + 3, wq[1], xq[1]);
-            if (t + 2 < t_end) put(0, wq[0]);
+    // tile t = t_begin + L i + j: LDS stage j % 2, register set j
+#pragma unroll 1
+    for (int tb = t_begin; tb < t_end; tb += L) {
+        bool done = false;
+        StaticFor<0, L>::run([&](auto jj) {
+            constexpr int j = decltype(jj)::value;
+            const int t = tb + j;
+            if (done || t >= t_end) {
+                done = true;
+                return;
+            }
+            tile(t, j & 1, xq[j]);
+            issue(t + L, wq[j], xq[j]);
+            if (t + 1 < t_end) put((j + 1) & 1, wq[(j + 1) % L]);
             __syncthreads();
-        }
+            __builtin_amdgcn_sched_barrier(0);  // (tiles are not interleaved)
+        });
     }
 }
 

@@ -30,6 +30,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 namespace kan {
 
 typedef float floatx2 __attribute__((ext_vector_type(2)));
@@ -148,6 +150,21 @@ template <> struct Storage<float> {
 template <> struct Storage<uint16_t> {
     static __device__ __forceinline__ float load(const uint16_t* p) { return bf16_to_f32(*p); }
     static __device__ __forceinline__ void store(uint16_t* p, float v) { *p = f32_to_bf16(v); }
+};
+
+// Compile-time loop: f(std::integral_constant<int, I>) for I = 0 .. N - 1.
+template <int I, int N>
+struct StaticFor {
+    template <typename F>
+    __device__ __forceinline__ static void run(F&& f) {
+        f(std::integral_constant<int, I>{});
+        StaticFor<I + 1, N>::run(f);
+    }
+};
+template <int N>
+struct StaticFor<N, N> {
+    template <typename F>
+    __device__ __forceinline__ static void run(F&&) {}
 };
 
 }  // namespace kan

@@ -109,21 +109,6 @@ __device__ __forceinline__ void zero_frag(AFrag<float, RF>& A, int rf) {
     A.a[rf][1] = 0.0f;
 }
 
-// Compile-time loop: f(std::integral_constant<int, I>) for I = 0 .. N - 1.
-template <int I, int N>
-struct StaticFor {
-    template <typename F>
-    __device__ __forceinline__ static void run(F& f) {
-        f(std::integral_constant<int, I>{});
-        StaticFor<I + 1, N>::run(f);
-    }
-};
-template <int N>
-struct StaticFor<N, N> {
-    template <typename F>
-    __device__ __forceinline__ static void run(F&) {}
-};
-
 // Position of a wave's block: global block index, feature pair and block
 // within the pair.  A wave visits blocks wk, wk + WK, wk + 2 WK, ...
 struct Pos {
