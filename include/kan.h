@@ -134,7 +134,8 @@ kan_status kan_basis_eval_cdb(const kan_grid* grid, kan_dtype dtype, const void*
  * columns (G + k basis values and one SiLU value per input feature); the basis
  * is generated in registers and never written to memory.  The call is
  * kan_layer_pack into the workspace followed by kan_layer_forward_packed,
- * both enqueued on `stream`.
+ * both enqueued on `stream`; the workspace past the packed weights (from the
+ * next 256-byte boundary) is the packed forward's workspace.
  *
  * y must not overlap any input.  Every pointer must be aligned to the dtype
  * size.  A NaN in x[b, :] makes y[b, :] NaN (through the SiLU branch).
@@ -153,8 +154,12 @@ kan_status kan_layer_forward(const kan_grid* grid, kan_dtype dtype, int64_t batc
 
 /*
  * kan_layer_forward_workspace_bytes -- size in bytes of the workspace that
- * kan_layer_forward needs for a layer (eq. kan_forward) of this grid, dtype,
- * batch and shape (the packed weights; it does not grow with the batch).
+ * kan_layer_forward uses for a layer (eq. kan_forward) of this grid, dtype,
+ * batch and shape: the packed weights (kan_layer_packed_bytes, the least
+ * kan_layer_forward accepts) and, for batches too small to fill the GPU, the
+ * fp32 partial sums of the split contraction from the next 256-byte boundary
+ * (kan_layer_forward_packed_workspace_bytes).  With only the packed weights'
+ * size the layer runs unsplit.
  * Writes *bytes.  Returns KAN_OK, KAN_ERR_INVALID_ARG (bytes == NULL, bad grid
  * or sizes, batch < 0) or KAN_ERR_UNSUPPORTED.
  */
@@ -208,6 +213,15 @@ kan_status kan_layer_pack(const kan_grid* grid, kan_dtype dtype, int32_t in_feat
  *           shape (for testing and tuning; every valid shape gives the same
  *           result up to the fp32 summation order); a shape that is not valid
  *           for the layer is KAN_ERR_INVALID_ARG.
+ *   workspace  NULL, or caller-owned device memory of workspace_bytes bytes.
+ *           For batches too small to fill the GPU (kan_layer_plan's plan[5]
+ *           > 1) the contraction over K is split across workgroups, each
+ *           writing fp32 partial sums here, which are then added in a fixed
+ *           order (deterministic); that needs workspace_bytes >=
+ *           kan_layer_forward_packed_workspace_bytes(...), a 16-byte aligned
+ *           workspace overlapping no other argument.  A NULL or smaller
+ *           workspace runs the layer unsplit (same result up to the fp32
+ *           summation order).
  *   y       [batch, out_features]   dtype storage, fully overwritten; must not
  *           overlap x or packed.
  *
@@ -216,7 +230,21 @@ kan_status kan_layer_pack(const kan_grid* grid, kan_dtype dtype, int32_t in_feat
 kan_status kan_layer_forward_packed(const kan_grid* grid, kan_dtype dtype, int64_t batch,
                                     int32_t in_features, int32_t out_features, const void* x,
                                     const void* packed, size_t packed_bytes,
-                                    const int32_t* shape, void* y, void* stream);
+                                    const int32_t* shape, void* workspace,
+                                    size_t workspace_bytes, void* y, void* stream);
+
+/*
+ * kan_layer_forward_packed_workspace_bytes -- size in bytes of the partial
+ * sums kan_layer_forward_packed writes when it splits the contraction for
+ * this layer, batch and shape (NULL: the planned shape), 0 when it does not
+ * split.  Writes *bytes.  Returns KAN_OK, KAN_ERR_INVALID_ARG (bytes == NULL,
+ * bad grid or sizes, batch < 0, an invalid forced shape) or
+ * KAN_ERR_UNSUPPORTED.
+ */
+kan_status kan_layer_forward_packed_workspace_bytes(const kan_grid* grid, kan_dtype dtype,
+                                                    int64_t batch, int32_t in_features,
+                                                    int32_t out_features, const int32_t* shape,
+                                                    size_t* bytes);
 
 /*
  * kan_layer_plan -- the workgroup shape that kan_layer_forward_packed (and
@@ -232,10 +260,15 @@ kan_status kan_layer_forward_packed(const kan_grid* grid, kan_dtype dtype, int64
  *   plan[3]  workgroups splitting the columns of an output tile (1, 2 or 4)
  *   plan[4]  1 if the layer runs on the structured-sparse matrix instruction
  *            (bf16, k = 3, 5 <= G <= 12), else 0
+ *   plan[5]  workgroups splitting the contraction (K) of each output tile when
+ *            the caller gives kan_layer_forward_packed its workspace (1: no
+ *            split).  Only batches that give fewer than 512 workgroups split,
+ *            only layers with a long contraction, and into at most as many
+ *            splits as keep the fp32 partial sums within 16 MiB.
  *
  * Degrees other than 3 run one shape, {1, 1, 4, 1}.
  *
- * Writes plan[0..4].  Returns KAN_OK, KAN_ERR_INVALID_ARG (plan == NULL, bad
+ * Writes plan[0..5].  Returns KAN_OK, KAN_ERR_INVALID_ARG (plan == NULL, bad
  * grid or sizes, batch < 1, an invalid forced shape) or KAN_ERR_UNSUPPORTED.
  */
 kan_status kan_layer_plan(const kan_grid* grid, kan_dtype dtype, int64_t batch,
@@ -337,7 +370,9 @@ kan_status kan_layer_forward_span_workspace_bytes(const kan_grid* grid, kan_dtyp
  * capture, tight serving loops, harnesses that forbid hipMalloc).  The
  * packed weights go to a fixed scratch array of KAN_NOALLOC_SCRATCH_BYTES
  * bytes that the library holds in device memory on every GPU it runs on,
- * until the process ends; nothing is allocated or freed by the call.
+ * until the process ends, followed (from the next 256-byte boundary) by the
+ * partial sums of a split contraction when they fit there (else the layer
+ * runs unsplit); nothing is allocated or freed by the call.
  *
  *   x, coef, base_w, y   as kan_layer_forward (caller-owned device memory)
  *
@@ -370,7 +405,7 @@ const char* kan_status_string(kan_status status);
 /* Version of this interface; bumped on any incompatible change. */
 int32_t kan_abi_version(void);
 
-#define KAN_ABI_VERSION 3
+#define KAN_ABI_VERSION 4
 
 #ifdef __cplusplus
 }

@@ -31,6 +31,7 @@ KAN_BF16 = 1
 
 EXPORTED_SYMBOLS = ("kan_basis_eval", "kan_basis_eval_cdb", "kan_layer_forward", "kan_layer_forward_workspace_bytes",
                     "kan_layer_packed_bytes", "kan_layer_pack", "kan_layer_forward_packed",
+                    "kan_layer_forward_packed_workspace_bytes",
                     "kan_layer_plan", "kan_layer_forward_noalloc", "kan_layer_backward",
                     "kan_layer_backward_workspace_bytes", "kan_layer_forward_span",
                     "kan_layer_forward_span_workspace_bytes", "kan_status_string",
@@ -85,8 +86,13 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
             lib.kan_layer_pack.restype = ctypes.c_int
             lib.kan_layer_forward_packed.argtypes = [g, ctypes.c_int, ctypes.c_int64,
                                                      ctypes.c_int32, ctypes.c_int32, _VP, _VP,
-                                                     ctypes.c_size_t, _I32P, _VP, _VP]
+                                                     ctypes.c_size_t, _I32P, _VP,
+                                                     ctypes.c_size_t, _VP, _VP]
             lib.kan_layer_forward_packed.restype = ctypes.c_int
+            lib.kan_layer_forward_packed_workspace_bytes.argtypes = [
+                g, ctypes.c_int, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, _I32P,
+                ctypes.POINTER(ctypes.c_size_t)]
+            lib.kan_layer_forward_packed_workspace_bytes.restype = ctypes.c_int
             lib.kan_layer_plan.argtypes = [g, ctypes.c_int, ctypes.c_int64, ctypes.c_int32,
                                            ctypes.c_int32, _I32P, _I32P]
             lib.kan_layer_plan.restype = ctypes.c_int
@@ -238,9 +244,10 @@ def kan_layer_packed_bytes(grid: kan_grid, dtype: int, in_features: int,
 
 def kan_layer_plan(grid: kan_grid, dtype: int, batch: int, in_features: int,
                    out_features: int, shape=None) -> Tuple[int, Tuple[int, ...]]:
-    """Raw call: returns (kan_status, (rf, wk, nw, cs, sparse)); `shape` forces
-    a workgroup shape (see _shape_arg), None takes the library's choice."""
-    plan = (ctypes.c_int32 * 5)()
+    """Raw call: returns (kan_status, (rf, wk, nw, cs, sparse, k_splits));
+    `shape` forces a workgroup shape (see _shape_arg), None takes the
+    library's choice."""
+    plan = (ctypes.c_int32 * 6)()
     st = int(load_library().kan_layer_plan(ctypes.byref(grid), int(dtype), int(batch),
                                            int(in_features), int(out_features),
                                            _shape_arg(shape), plan))
@@ -257,13 +264,26 @@ def kan_layer_pack(grid: kan_grid, dtype: int, in_features: int, out_features: i
 
 def kan_layer_forward_packed(grid: kan_grid, dtype: int, batch: int, in_features: int,
                              out_features: int, x: int, packed: int, packed_bytes: int, y: int,
-                             stream: int = 0, shape=None) -> int:
+                             stream: int = 0, shape=None, workspace: int = 0,
+                             workspace_bytes: int = 0) -> int:
     """Raw call: device addresses as integers; returns the kan_status code.
-    `shape` forces a workgroup shape (see _shape_arg)."""
+    `shape` forces a workgroup shape (see _shape_arg); `workspace` (0: none)
+    holds the partial sums of a split contraction."""
     return int(load_library().kan_layer_forward_packed(
         ctypes.byref(grid), int(dtype), int(batch), int(in_features), int(out_features),
-        _VP(x), _VP(packed), ctypes.c_size_t(packed_bytes), _shape_arg(shape), _VP(y),
-        _VP(stream)))
+        _VP(x), _VP(packed), ctypes.c_size_t(packed_bytes), _shape_arg(shape), _VP(workspace),
+        ctypes.c_size_t(workspace_bytes), _VP(y), _VP(stream)))
+
+
+def kan_layer_forward_packed_workspace_bytes(grid: kan_grid, dtype: int, batch: int,
+                                             in_features: int, out_features: int,
+                                             shape=None) -> Tuple[int, int]:
+    """Raw call: returns (kan_status, bytes)."""
+    n = ctypes.c_size_t(0)
+    st = int(load_library().kan_layer_forward_packed_workspace_bytes(
+        ctypes.byref(grid), int(dtype), int(batch), int(in_features), int(out_features),
+        _shape_arg(shape), ctypes.byref(n)))
+    return st, int(n.value)
 
 
 def check(status: int) -> None:
@@ -387,9 +407,14 @@ def pack_layer(coef, base_w, grid_size: int, grid_lo: float = -1.0, grid_hi: flo
     return out
 
 
-def layer_forward_packed(x, packed: PackedLayer, out=None, shape=None):
+def layer_forward_packed(x, packed: PackedLayer, out=None, shape=None, workspace=None,
+                         split: bool = True):
     """kan_layer_forward_packed: x [B, in] with packed weights -> y [B, out].
-    `shape` forces a workgroup shape (rf, wk[, nw[, cs]]) for tests and tuning."""
+    `shape` forces a workgroup shape (rf, wk[, nw[, cs]]) for tests and tuning.
+    For batches too small to fill the GPU the contraction is split across
+    workgroups; its partial sums go to `workspace` (a uint8 device tensor)
+    when large enough, else to a fresh one from torch's allocator; split=False
+    runs the layer unsplit."""
     torch = _torch()
     _require_device(x)
     if x.dim() != 2 or x.shape[1] != packed.n_in:
@@ -404,10 +429,21 @@ def layer_forward_packed(x, packed: PackedLayer, out=None, shape=None):
         if out.dtype != x.dtype or tuple(out.shape) != (B, packed.n_out):
             raise ValueError("out must be [B, out] with x's dtype")
     g = make_grid(packed.grid_size, packed.grid_lo, packed.grid_hi, packed.spline_order)
+    dt = _dtype_code(x)
+    ws_ptr, ws_bytes = 0, 0
+    if split:
+        st, need = kan_layer_forward_packed_workspace_bytes(g, dt, B, packed.n_in, packed.n_out,
+                                                            shape)
+        check(st)
+        if need > 0:
+            if workspace is None or workspace.numel() < need or workspace.device != x.device:
+                workspace = torch.empty(need, dtype=torch.uint8, device=x.device)
+            ws_ptr, ws_bytes = workspace.data_ptr(), workspace.numel()
     with torch.cuda.device(x.device):
-        check(kan_layer_forward_packed(g, _dtype_code(x), B, packed.n_in, packed.n_out,
-                                       x.data_ptr(), packed.buf.data_ptr(), packed.nbytes,
-                                       out.data_ptr(), _stream(x.device), shape=shape))
+        check(kan_layer_forward_packed(g, dt, B, packed.n_in, packed.n_out, x.data_ptr(),
+                                       packed.buf.data_ptr(), packed.nbytes, out.data_ptr(),
+                                       _stream(x.device), shape=shape, workspace=ws_ptr,
+                                       workspace_bytes=ws_bytes))
     return out
 
 

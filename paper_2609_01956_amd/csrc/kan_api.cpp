@@ -15,6 +15,7 @@ constexpr int32_t kMaxGrid = 4000;
 size_t dtype_size(kan_dtype dt) { return dt == KAN_BF16 ? 2 : 4; }
 
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 
 // [p, p + n) and [q, q + m) (bytes) intersect?
 bool overlap(const void* p, size_t n, const void* q, size_t m) {
@@ -227,7 +228,8 @@ static kan_status layer_shape(const kan::LayerGeom& geom, kan_dtype dtype, int64
 static kan_status launch_forward(const kan::GridConst& gc, const kan::LayerGeom& geom,
                                  const kan::LayerCfg& cfg, kan_dtype dtype, int64_t batch,
                                  int32_t in_features, int32_t out_features, const void* x,
-                                 const void* packed, void* y, hipStream_t s) {
+                                 const void* packed, int ks, void* partial, void* y,
+                                 hipStream_t s) {
     kan::LayerArgs a;
     a.x = x;
     a.wp = packed;
@@ -241,6 +243,8 @@ static kan_status launch_forward(const kan::GridConst& gc, const kan::LayerGeom&
     a.nblk = geom.nblk;
     a.nblk_pad = geom.nblk_pad;
     a.nchunks = 0;  // set by the launcher (depends on the tile shape)
+    a.cps = 0;      // set by the launcher (from ks)
+    a.P = nullptr;
     a.inv_h = gc.inv_h;
     a.inv_lo = gc.inv_lo;
     a.xlim = gc.xlim;
@@ -249,13 +253,14 @@ static kan_status launch_forward(const kan::GridConst& gc, const kan::LayerGeom&
     a.kdeg = gc.k;
     a.hw = gc.hw;
     for (int m = 0; m < 4; ++m) a.hc[m] = gc.hc[m];
-    return device_status(kan::launch_layer(dtype == KAN_BF16, geom, cfg, a, s));
+    return device_status(kan::launch_layer(dtype == KAN_BF16, geom, cfg, a, ks, partial, s));
 }
 
 kan_status kan_layer_forward_packed(const kan_grid* grid, kan_dtype dtype, int64_t batch,
                                     int32_t in_features, int32_t out_features, const void* x,
                                     const void* packed, size_t packed_bytes,
-                                    const int32_t* shape, void* y, void* stream) {
+                                    const int32_t* shape, void* workspace,
+                                    size_t workspace_bytes, void* y, void* stream) {
     kan::GridConst gc;
     kan::LayerGeom geom;
     kan_status st = check_layer(grid, dtype, in_features, out_features, &gc, &geom);
@@ -270,8 +275,40 @@ kan_status kan_layer_forward_packed(const kan_grid* grid, kan_dtype dtype, int64
     st = check_forward_packed(geom, dtype, batch, in_features, out_features, x, packed,
                               packed_bytes, y);
     if (st != KAN_OK) return st;
-    return launch_forward(gc, geom, cfg, dtype, batch, in_features, out_features, x, packed, y,
-                          static_cast<hipStream_t>(stream));
+    // The K split of small batches runs when the workspace holds its partial
+    // sums; without one the layer runs unsplit (same result up to the fp32
+    // summation order).
+    int ks = kan::layer_k_splits(geom, cfg, batch, out_features);
+    const size_t pbytes = kan::layer_partial_bytes(geom, cfg, batch, out_features);
+    if (ks > 1 && (workspace == nullptr || workspace_bytes < pbytes)) ks = 1;
+    if (ks > 1) {
+        const size_t es = dtype_size(dtype);
+        const uint64_t ub = (uint64_t)batch;
+        if (!aligned(workspace, 16) ||
+            overlap(workspace, pbytes, x, ub * (size_t)in_features * es) ||
+            overlap(workspace, pbytes, packed, geom.packed_bytes) ||
+            overlap(workspace, pbytes, y, ub * (size_t)out_features * es))
+            return KAN_ERR_INVALID_ARG;
+    }
+    return launch_forward(gc, geom, cfg, dtype, batch, in_features, out_features, x, packed, ks,
+                          ks > 1 ? workspace : nullptr, y, static_cast<hipStream_t>(stream));
+}
+
+kan_status kan_layer_forward_packed_workspace_bytes(const kan_grid* grid, kan_dtype dtype,
+                                                    int64_t batch, int32_t in_features,
+                                                    int32_t out_features, const int32_t* shape,
+                                                    size_t* bytes) {
+    if (bytes == nullptr) return KAN_ERR_INVALID_ARG;
+    kan::GridConst gc;
+    kan::LayerGeom geom;
+    kan_status st = check_layer(grid, dtype, in_features, out_features, &gc, &geom);
+    if (st != KAN_OK) return st;
+    if (batch < 0 || batch > (int64_t)0x7fffffff * 32) return KAN_ERR_INVALID_ARG;
+    kan::LayerCfg cfg;
+    st = layer_shape(geom, dtype, batch < 1 ? 1 : batch, shape, &cfg);
+    if (st != KAN_OK) return st;
+    *bytes = batch == 0 ? 0 : kan::layer_partial_bytes(geom, cfg, batch, out_features);
+    return KAN_OK;
 }
 
 kan_status kan_layer_plan(const kan_grid* grid, kan_dtype dtype, int64_t batch,
@@ -291,6 +328,7 @@ kan_status kan_layer_plan(const kan_grid* grid, kan_dtype dtype, int64_t batch,
     plan[2] = cfg.nw;
     plan[3] = cfg.cs;
     plan[4] = geom.sparse ? 1 : 0;
+    plan[5] = kan::layer_k_splits(geom, cfg, batch, out_features);
     return KAN_OK;
 }
 
@@ -302,8 +340,12 @@ kan_status kan_layer_forward_workspace_bytes(const kan_grid* grid, kan_dtype dty
     kan::LayerGeom geom;
     const kan_status st = check_layer(grid, dtype, in_features, out_features, &gc, &geom);
     if (st != KAN_OK) return st;
-    if (batch < 0) return KAN_ERR_INVALID_ARG;
-    *bytes = geom.packed_bytes;
+    if (batch < 0 || batch > (int64_t)0x7fffffff * 32) return KAN_ERR_INVALID_ARG;
+    // the packed weights, then (small batches) the K split's partial sums
+    const kan::LayerCfg cfg = kan::plan_layer(geom, dtype == KAN_BF16, batch < 1 ? 1 : batch);
+    const size_t pbytes =
+        batch == 0 ? 0 : kan::layer_partial_bytes(geom, cfg, batch, out_features);
+    *bytes = pbytes == 0 ? geom.packed_bytes : align256(geom.packed_bytes) + pbytes;
     return KAN_OK;
 }
 
@@ -347,16 +389,21 @@ kan_status kan_layer_forward(const kan_grid* grid, kan_dtype dtype, int64_t batc
     const size_t es = dtype_size(dtype);
     const uint64_t ub = (uint64_t)batch;
     const size_t ws = geom.packed_bytes;
-    if (overlap(workspace, ws, x, ub * (size_t)in_features * es) ||
-        overlap(workspace, ws, coef, (size_t)out_features * in_features * gc.nb * es) ||
-        overlap(workspace, ws, base_w, (size_t)out_features * in_features * es) ||
-        overlap(workspace, ws, y, ub * (size_t)out_features * es))
+    // (the whole workspace: past the packed weights it may hold partial sums)
+    if (overlap(workspace, workspace_bytes, x, ub * (size_t)in_features * es) ||
+        overlap(workspace, workspace_bytes, coef, (size_t)out_features * in_features * gc.nb * es) ||
+        overlap(workspace, workspace_bytes, base_w, (size_t)out_features * in_features * es) ||
+        overlap(workspace, workspace_bytes, y, ub * (size_t)out_features * es))
         return KAN_ERR_INVALID_ARG;
     st = kan_layer_pack(grid, dtype, in_features, out_features, coef, base_w, workspace, ws,
                         stream);
     if (st != KAN_OK) return st;
+    // the rest of the workspace, past the packed weights, for the K split
+    const size_t off = align256(ws);
+    void* rest = workspace_bytes > off ? static_cast<char*>(workspace) + off : nullptr;
+    const size_t rest_bytes = workspace_bytes > off ? workspace_bytes - off : 0;
     return kan_layer_forward_packed(grid, dtype, batch, in_features, out_features, x, workspace,
-                                    ws, nullptr, y, stream);
+                                    ws, nullptr, rest, rest_bytes, y, stream);
 }
 
 kan_status kan_layer_forward_noalloc(const kan_grid* grid, kan_dtype dtype, int64_t batch,
@@ -377,11 +424,16 @@ kan_status kan_layer_forward_noalloc(const kan_grid* grid, kan_dtype dtype, int6
     if (kan::noalloc_scratch(&ws, &ws_bytes) != hipSuccess) return KAN_ERR_DEVICE;
     // (the scratch is the library's own device array: it overlaps no caller
     // tensor)
-    st = kan_layer_pack(grid, dtype, in_features, out_features, coef, base_w, ws, ws_bytes,
-                        stream);
+    st = kan_layer_pack(grid, dtype, in_features, out_features, coef, base_w, ws,
+                        geom.packed_bytes, stream);
     if (st != KAN_OK) return st;
+    // the scratch past the packed weights holds the K split's partial sums
+    // when they fit (else the layer runs unsplit)
+    const size_t off = align256(geom.packed_bytes);
+    void* rest = ws_bytes > off ? static_cast<char*>(ws) + off : nullptr;
+    const size_t rest_bytes = ws_bytes > off ? ws_bytes - off : 0;
     return kan_layer_forward_packed(grid, dtype, batch, in_features, out_features, x, ws,
-                                    ws_bytes, nullptr, y, stream);
+                                    geom.packed_bytes, nullptr, rest, rest_bytes, y, stream);
 }
 
 // Backward geometry (after check_layer): the batch must fit the kernels' grids.

@@ -152,6 +152,8 @@ struct LayerArgs {
     int nblk;         // blocks holding data
     int nblk_pad;     // blocks per N tile in the packed buffer
     int nchunks;      // nblk_pad / blocks-per-chunk
+    int cps;          // chunks per K split (workgroup z takes chunks [z cps, (z + 1) cps))
+    float* P;         // K splits > 1: fp32 partial sums [split][batch][out] (else null)
     float inv_h;      // see GridConst
     float inv_lo;
     float xlim;
@@ -169,8 +171,17 @@ hipError_t noalloc_scratch(void** ptr, size_t* bytes);
 
 hipError_t launch_pack(bool bf16, const LayerGeom& g, int in, int out, const void* coef,
                        const void* base_w, void* packed, hipStream_t s);
-hipError_t launch_layer(bool bf16, const LayerGeom& g, const LayerCfg& c, LayerArgs a,
-                        hipStream_t s);
+// K splits across workgroups for a shape and batch: small batches give too
+// few workgroups to fill the chip, so each of ks workgroups per output tile
+// takes a range of the K chunks and writes fp32 partial sums, which a second
+// kernel adds in a fixed order (1: no split).
+int layer_k_splits(const LayerGeom& g, const LayerCfg& c, int64_t batch, int out);
+// Bytes of those partial sums (0 for one split).
+size_t layer_partial_bytes(const LayerGeom& g, const LayerCfg& c, int64_t batch, int out);
+// The fused forward; ks > 1 needs `partial` of layer_partial_bytes bytes
+// (16-byte aligned), else it may be null.
+hipError_t launch_layer(bool bf16, const LayerGeom& g, const LayerCfg& c, LayerArgs a, int ks,
+                        void* partial, hipStream_t s);
 // Per-dtype kernel launches (one translation unit each).
 hipError_t launch_layer_bf16(const LayerGeom& g, const LayerCfg& c, const LayerArgs& a,
                              hipStream_t s);

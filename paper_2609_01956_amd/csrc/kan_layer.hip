@@ -3,6 +3,7 @@
 // kan_layer_kernel.h.
 #include "kan_layer_kernel.h"
 
+#include <algorithm>
 #include <mutex>
 
 #include "kan.h"
@@ -190,7 +191,8 @@ LayerCfg plan_layer(const LayerGeom& g, bool bf16, int64_t batch) {
         if (!layer_cfg_valid(g, c)) continue;
         const int64_t w = wgs(c);
         if (w >= want) return c;
-        if (w > best_wgs) { best = c; best_wgs = w; }
+        // (on a tie, the later shape: fewer rows per workgroup, more waves on K)
+        if (w >= best_wgs) { best = c; best_wgs = w; }
     }
     if (best_wgs >= 256) return best;
     for (const LayerCfg& c : sliced) {
@@ -260,10 +262,87 @@ hipError_t launch_pack(bool bf16, const LayerGeom& g, int in, int out, const voi
     return hipGetLastError();
 }
 
-hipError_t launch_layer(bool bf16, const LayerGeom& g, const LayerCfg& c, LayerArgs a,
-                        hipStream_t s) {
+namespace {
+
+// y = sum over the K splits of the partial sums, in split order.  The loads
+// go out 16 at a time before their adds, so a small batch (one workgroup
+// reading many splits) waits on one memory round trip per 16 splits rather
+// than one per split.  The +0 that stands in for a split past the last one
+// leaves the sum bitwise unchanged (the sum starts at +0 and never becomes
+// -0).
+template <typename T>
+__global__ __launch_bounds__(256) void split_reduce_kernel(const float* __restrict__ P,
+                                                           T* __restrict__ y, int64_t n, int ks) {
+    constexpr int kBatch = 16;
+    const int64_t u = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (u >= n) return;
+    float v = 0.0f;
+    for (int z0 = 0; z0 < ks; z0 += kBatch) {
+        float t[kBatch];
+#pragma unroll
+        for (int i = 0; i < kBatch; ++i)
+            t[i] = z0 + i < ks ? P[(int64_t)(z0 + i) * n + u] : 0.0f;
+#pragma unroll
+        for (int i = 0; i < kBatch; ++i) v += t[i];
+    }
+    if constexpr (sizeof(T) == 2) y[u] = f32_to_bf16(v);
+    else y[u] = v;
+}
+
+int layer_chunks(const LayerGeom& g) { return g.nblk_pad / g.kb; }
+
+}  // namespace
+
+int layer_k_splits(const LayerGeom& g, const LayerCfg& c, int64_t batch, int out) {
+    // Split only where the workgroups give fewer than two per CU, towards
+    // kSplitTargetWgs workgroups (fp32 shapes hold fewer registers and more
+    // workgroups per CU than bf16 ones), never into splits of fewer than 4
+    // chunks and 16 blocks (pipeline fill and drain; the 256-column bf16
+    // tiles have 2 blocks per chunk, the others 8), and with at most
+    // kSplitMaxPartialBytes of partial sums (written and read back once
+    // more).  Measured on MI355X at batches 1 to 4096 of 784 -> 64, 784 ->
+    // 256, 256 -> 256 and 256 -> 10 layers in both dtypes.
+    constexpr int64_t kSplitBelowWgs = 512;
+    const int64_t kSplitTargetWgs = g.kj == 8 ? 512 : 2048;
+    const int kSplitMinChunks = std::max(4, 16 / g.kb);
+    constexpr int64_t kSplitMaxPartialBytes = (int64_t)16 << 20;
+    const int64_t bm = layer_cfg_rows(c);
+    const int64_t wgs = ((batch + bm - 1) / bm) * g.ntiles * c.cs;
+    const int nch = layer_chunks(g);
+    if (nch < 2 * kSplitMinChunks || wgs >= kSplitBelowWgs) return 1;
+    int64_t ks = (kSplitTargetWgs + wgs - 1) / wgs;
+    ks = std::min<int64_t>(ks, nch / kSplitMinChunks);
+    ks = std::min<int64_t>(ks, kSplitMaxPartialBytes / (batch * (int64_t)out * 4));
+    if (ks <= 1) return 1;
+    const int cps = (int)((nch + ks - 1) / ks);
+    return (nch + cps - 1) / cps;
+}
+
+size_t layer_partial_bytes(const LayerGeom& g, const LayerCfg& c, int64_t batch, int out) {
+    const int ks = layer_k_splits(g, c, batch, out);
+    if (ks <= 1) return 0;
+    return ((size_t)ks * (size_t)batch * (size_t)out * 4 + 255) & ~(size_t)255;
+}
+
+hipError_t launch_layer(bool bf16, const LayerGeom& g, const LayerCfg& c, LayerArgs a, int ks,
+                        void* partial, hipStream_t s) {
     if (!layer_cfg_valid(g, c)) return hipErrorInvalidValue;
-    return bf16 ? launch_layer_bf16(g, c, a, s) : launch_layer_f32(g, c, a, s);
+    const int nch = layer_chunks(g);
+    if (ks < 1 || ks > nch || (ks > 1 && partial == nullptr)) return hipErrorInvalidValue;
+    a.cps = (nch + ks - 1) / ks;
+    ks = (nch + a.cps - 1) / a.cps;
+    a.P = ks > 1 ? static_cast<float*>(partial) : nullptr;
+    hipError_t e = bf16 ? launch_layer_bf16(g, c, a, s) : launch_layer_f32(g, c, a, s);
+    if (e != hipSuccess || ks == 1) return e;
+    const int64_t n = a.batch * (int64_t)a.out;
+    const unsigned blocks = (unsigned)((n + 255) / 256);
+    if (bf16)
+        hipLaunchKernelGGL(split_reduce_kernel<uint16_t>, dim3(blocks), dim3(256), 0, s,
+                           a.P, static_cast<uint16_t*>(a.y), n, ks);
+    else
+        hipLaunchKernelGGL(split_reduce_kernel<float>, dim3(blocks), dim3(256), 0, s, a.P,
+                           static_cast<float*>(a.y), n, ks);
+    return hipGetLastError();
 }
 
 }  // namespace kan

@@ -259,9 +259,15 @@ void layer_kernel(LayerArgs a) {
     const int64_t row0 = (int64_t)blockIdx.x * BM + wm * 32 * RF;
     const int nt = blockIdx.y / CS;     // N tile
     const int slice = blockIdx.y % CS;  // column slice of the tile
-    // Packed weights of this N tile: nblk_pad blocks = nchunks whole chunks.
-    const char* __restrict__ wpt =
-        static_cast<const char*>(a.wp) + (size_t)nt * (size_t)a.nblk_pad * BLKBL;
+    // K split (workgroup z): chunks [c_beg, c_beg + nch) of the tile; the
+    // loop below counts chunks from c_beg (one split: the whole tile).
+    const int c_beg = blockIdx.z * a.cps;
+    const int nch = min(a.cps, a.nchunks - c_beg);
+    // Packed weights of this N tile (nblk_pad blocks = nchunks whole chunks),
+    // from the split's first chunk.
+    const char* __restrict__ wpt = static_cast<const char*>(a.wp) +
+                                   (size_t)nt * (size_t)a.nblk_pad * BLKBL +
+                                   (size_t)c_beg * (KB * BLKBL);
 
     // x and the N tile's packed weights are read through buffer resources
     // with 32-bit byte offsets: x from a per-workgroup base (the host rejects
@@ -326,7 +332,7 @@ void layer_kernel(LayerArgs a) {
     typedef u32x4 WSet[DPW];
     const uint32_t wlane = (uint32_t)(wave * 1024 + lane * 16);
     const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<char*>(wpt), (short)0, (int)((uint32_t)a.nblk_pad * (uint32_t)BLKBL),
+        const_cast<char*>(wpt), (short)0, (int)((uint32_t)nch * (uint32_t)(KB * BLKBL)),
         kBufferWord3);
     uint32_t goff[CS == 1 ? 1 : DPW];
     if constexpr (CS > 1) {
@@ -342,7 +348,7 @@ void layer_kernel(LayerArgs a) {
 #pragma unroll
         for (int t = 0; t < KBW; ++t) {
             int pr = p.pair;
-            if constexpr (SPK) pr = c * PPC + wk + WK * (t / 2);
+            if constexpr (SPK) pr = (c_beg + c) * PPC + wk + WK * (t / 2);
             pr = pr < a.npairs ? pr : a.npairs - 1;
             const bool odd = pr == last_pair_odd;  // wave-uniform
             // The split generation reads x only at a feature's first block.
@@ -365,7 +371,7 @@ void layer_kernel(LayerArgs a) {
             }
             p = advance<WK>(p, nsb);
         }
-        const int cc = c < a.nchunks ? c : a.nchunks - 1;
+        const int cc = c < nch ? c : nch - 1;
         const int cofs = (int)((uint32_t)cc * (uint32_t)(KB * BLKBL));  // the chunk's bytes
 #pragma unroll
         for (int i = 0; i < DPW; ++i) {
@@ -662,7 +668,11 @@ void layer_kernel(LayerArgs a) {
     // memory loads, which would also count)
     constexpr int WAIT_XA = 0xF | (0x7 << 4) | ((2 * NFW) << 8) | (0x3 << 14);
     static_assert(!PRE || 2 * NFW <= 15, "lgkmcnt field");
-    const int nq = wk < a.nblk ? (a.nblk - wk + WK - 1) / WK : 0;  // real blocks of this wave
+    // real blocks of the split, and of this wave; SP: the end of the split's
+    // feature pairs (a chunk holds KB / 2 of them)
+    const int nblk_s = min(a.nblk - c_beg * KB, nch * KB);
+    const int pair_end = min(a.npairs, (c_beg + nch) * (KB / 2));
+    const int nq = wk < nblk_s ? (nblk_s - wk + WK - 1) / WK : 0;
 
     XSet xq[L];
     WSet wq[L];
@@ -687,7 +697,12 @@ void layer_kernel(LayerArgs a) {
     };
     BFrag bq[2];
     // first block of the current chunk (SPK: the first block of pair wk)
-    Pos pos_c = SPK ? Pos{2 * wk, wk, 0} : advance_n(Pos{0, 0, 0}, wk, nsb);
+    Pos pos_c;
+    {
+        const int b0 = c_beg * KB;  // the split's first block (a whole pair when SPK)
+        pos_c = SPK ? Pos{b0 + 2 * wk, b0 / 2 + wk, 0}
+                    : advance_n(Pos{b0, b0 / nsb, b0 % nsb}, wk, nsb);
+    }
     Pos pos_l = pos_c;                               // first block of the next chunk to load
 
     // prologue: loads of chunks 0 .. L - 1, chunk 0 to stage 0
@@ -722,6 +737,20 @@ void layer_kernel(LayerArgs a) {
         }
         if constexpr (!XA) gen_first_sparse();
     } else if constexpr (GEN_SPLIT) {
+        if constexpr (!DIRECT) {
+            // A K split across workgroups can start inside a feature: seed the
+            // carried coordinate with that of the block before the first (the
+            // generation subtracts KJ from it).  Wave-uniform branch.
+            if (pos_c.bsub != 0) {
+                const float c = a.a_int + 1.0f - (float)(KJ * (pos_c.bsub - 1));
+#pragma unroll
+                for (int rf = 0; rf < RF; ++rf) {
+                    const float xv = x_value(pos_c, xq[0][0][rf], rf);
+                    sc[rf] = __builtin_fmaf(xv, a.inv_h, c) +
+                             coord_lo(xv, a.xlim, a.inv_lo, a.a_frac);
+                }
+            }
+        }
         gen_split(pos_c, xq[0][0], A_cur);
     } else {
         float x0[RF];
@@ -815,7 +844,9 @@ void layer_kernel(LayerArgs a) {
 #pragma unroll
                 for (int rf = 0; rf < GRF; ++rf) xf[rf] = x_value(pn, xr[2 * q + 1][rf], rf);
                 if constexpr (LASTG) {
-                    if (pos_c.pair + WK * q >= a.npairs) {  // a padding pair: contributes 0
+                    // a pair past the split's range (padding of the layer,
+                    // or the next split's) contributes 0
+                    if (pos_c.pair + WK * q >= pair_end) {
 #pragma unroll
                         for (int rf = 0; rf < RF; ++rf) zero_frag(A_cur, rf);
                     }
@@ -915,7 +946,7 @@ void layer_kernel(LayerArgs a) {
     };
 
     // Every wave's blocks are all real in every group but the final one.
-    const int ngroups = (a.nchunks + U - 1) / U;
+    const int ngroups = (nch + U - 1) / U;
 #pragma unroll 1
     for (int gi = 0; gi + 1 < ngroups; ++gi) {
         auto group = [&](auto kk) {
@@ -944,8 +975,13 @@ void layer_kernel(LayerArgs a) {
 #pragma unroll
                 for (int q = 0; q < 16; ++q) {
                     const int64_t row = row0 + (rf ^ ch) * 32 + 8 * (q / 4) + 4 * h + (q % 4);
-                    if (full || (row < a.batch && col < a.out))
-                        Tr<T>::store(y + row * a.out + col, 2.0f * acc[rf][nf][q]);
+                    if (full || (row < a.batch && col < a.out)) {
+                        if (a.P != nullptr)
+                            a.P[((int64_t)blockIdx.z * a.batch + row) * a.out + col] =
+                                2.0f * acc[rf][nf][q];
+                        else
+                            Tr<T>::store(y + row * a.out + col, 2.0f * acc[rf][nf][q]);
+                    }
                 }
             }
         }
@@ -978,7 +1014,12 @@ void layer_kernel(LayerArgs a) {
             for (int w = 0; w < WK; ++w) sum += red(g + WM * w)[rem];
             const int64_t row = bm0 + g * 32 * RF + rl;
             const int col = col0 + cl;
-            if (row < a.batch && col < a.out) Tr<T>::store(y + row * a.out + col, 2.0f * sum);
+            if (row < a.batch && col < a.out) {
+                if (a.P != nullptr)
+                    a.P[((int64_t)blockIdx.z * a.batch + row) * a.out + col] = 2.0f * sum;
+                else
+                    Tr<T>::store(y + row * a.out + col, 2.0f * sum);
+            }
         }
     }
 }
@@ -991,7 +1032,8 @@ hipError_t launch_cfg(const LayerGeom& g, LayerArgs a, hipStream_t s) {
     static_assert(BM <= kLayerMaxRows, "rows per workgroup (32-bit x byte offsets)");
     a.nblk_pad = g.nblk_pad;
     a.nchunks = g.nblk_pad / g.kb;
-    const dim3 grid((unsigned)((a.batch + BM - 1) / BM), (unsigned)(g.ntiles * (NFL / NF)));
+    const unsigned ks = (unsigned)((a.nchunks + a.cps - 1) / a.cps);
+    const dim3 grid((unsigned)((a.batch + BM - 1) / BM), (unsigned)(g.ntiles * (NFL / NF)), ks);
     // The sparse packed layout (bf16, two blocks per feature, 5 <= G <= 12)
     // runs only on the structured-sparse MFMA: no K split, whole feature
     // pairs per chunk (every block's place in its feature is a compile-time

@@ -31,7 +31,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_abi_version_and_status_strings():
-    assert kb.kan_abi_version() == 3
+    assert kb.kan_abi_version() == 4
     names = ["KAN_OK", "KAN_ERR_INVALID_ARG", "KAN_ERR_UNSUPPORTED", "KAN_ERR_DEVICE",
              "KAN_ERR_SCRATCH_LIMIT"]
     for code, name in enumerate(names):
@@ -119,13 +119,16 @@ def test_layer_argument_checks():
         assert kb.kan_layer_packed_bytes(g1, dt, 2 ** 22, 1)[0] == bad
         assert kb.kan_layer_packed_bytes(g1, dt, 2 ** 22 - 1, 1)[0] == kb.KAN_OK
     # workspace: null, misaligned (16 bytes), short, overlapping any tensor
-    need = kb.kan_layer_forward_workspace_bytes(g, f32, 16, 4, 4)[1]
-    assert need == kb.kan_layer_packed_bytes(g, f32, 4, 4)[1]
-    assert kb.kan_layer_forward(g, f32, 16, 4, 4, X, C, W, 0, need, Y) == bad
-    assert kb.kan_layer_forward(g, f32, 16, 4, 4, X, C, W, WS + 8, need, Y) == bad
-    assert kb.kan_layer_forward(g, f32, 16, 4, 4, X, C, W, WS, need - 1, Y) == bad
+    # (16 rows of 784 -> 4: the packed weights, then the partial sums of the
+    # split contraction; the packed weights' size is the least accepted)
+    need = kb.kan_layer_forward_workspace_bytes(g, f32, 16, 784, 4)[1]
+    packed = kb.kan_layer_packed_bytes(g, f32, 784, 4)[1]
+    assert need > packed
+    assert kb.kan_layer_forward(g, f32, 16, 784, 4, X, C, W, 0, need, Y) == bad
+    assert kb.kan_layer_forward(g, f32, 16, 784, 4, X, C, W, WS + 8, need, Y) == bad
+    assert kb.kan_layer_forward(g, f32, 16, 784, 4, X, C, W, WS, packed - 1, Y) == bad
     for p in (X, C, W, Y):
-        assert kb.kan_layer_forward(g, f32, 16, 4, 4, X, C, W, p - 16, need, Y) == bad
+        assert kb.kan_layer_forward(g, f32, 16, 784, 4, X, C, W, p - 16, need, Y) == bad
     # empty batch: OK without launching
     assert kb.kan_layer_forward(g, f32, 0, 4, 4, 0, 0, 0, 0, 0, 0) == kb.KAN_OK
 
@@ -170,10 +173,15 @@ def test_workspace_bytes_checks():
     assert kb.kan_layer_forward_workspace_bytes(g, kb.KAN_F32, 16, 0, 4)[0] == bad
     assert kb.kan_layer_forward_workspace_bytes(kb.make_grid(10, spline_order=8), kb.KAN_F32,
                                                 16, 4, 4)[0] == kb.KAN_ERR_UNSUPPORTED
-    # the packed weights, whatever the batch
-    for B in (0, 1, 65536):
+    # the packed weights, plus the split contraction's fp32 partial sums for
+    # batches too small to fill the GPU
+    for B in (0, 65536):
         st, n = kb.kan_layer_forward_workspace_bytes(g, kb.KAN_BF16, B, 784, 256)
         assert st == kb.KAN_OK and n == 392 * 2 * 8192
+    st, n = kb.kan_layer_forward_workspace_bytes(g, kb.KAN_BF16, 1, 784, 256)
+    st2, ks = kb.kan_layer_plan(g, kb.KAN_BF16, 1, 784, 256)
+    assert st == st2 == kb.KAN_OK and ks[5] > 1
+    assert n == 392 * 2 * 8192 + -(-ks[5] * 1 * 256 * 4 // 256) * 256
 
 
 def test_packed_entry_point_checks():
@@ -327,7 +335,7 @@ def test_other_degrees_accepted(k):
     assert kb.kan_basis_eval(g, kb.KAN_F32, X, 0, PHI) == kb.KAN_OK
     for dt in (kb.KAN_F32, kb.KAN_BF16):
         st, plan = kb.kan_layer_plan(g, dt, 65536, 784, 256)
-        assert st == kb.KAN_OK and plan == (1, 1, 4, 1, 0)
+        assert st == kb.KAN_OK and plan == (1, 1, 4, 1, 0, 1)
         assert kb.kan_layer_plan(g, dt, 65536, 784, 256, "2,1")[0] == kb.KAN_ERR_INVALID_ARG
         st, n = kb.kan_layer_packed_bytes(g, dt, 5, 7)
         assert st == kb.KAN_OK
@@ -388,3 +396,30 @@ def test_span_workspace_bytes(G, n_in, n_out, B):
         assert st == kb.KAN_OK
         w = n_in * (G + 4) * n_out * 4
         assert w <= n <= n_in * (G + 4) * (n_out + 63) * 4 + 512 * B * n_out * 4 + 512
+
+
+def test_packed_forward_workspace_host_checks():
+    """kan_layer_forward_packed's workspace (the split contraction's partial
+    sums of small batches): the size query, and a workspace that would be
+    used is checked for alignment and overlap on the host."""
+    g = kb.make_grid(10)
+    f32, bad = kb.KAN_F32, kb.KAN_ERR_INVALID_ARG
+    P, WS = 0x600000000, 0x700000000
+    pk = kb.kan_layer_packed_bytes(g, f32, 784, 64)[1]
+    st, need = kb.kan_layer_forward_packed_workspace_bytes(g, f32, 256, 784, 64)
+    st2, plan = kb.kan_layer_plan(g, f32, 256, 784, 64)
+    assert st == st2 == kb.KAN_OK and plan[5] > 1
+    assert need == -(-plan[5] * 256 * 64 * 4 // 256) * 256
+    # no split for a full batch, nor for an empty one
+    assert kb.kan_layer_forward_packed_workspace_bytes(g, f32, 65536, 784, 64) == (kb.KAN_OK, 0)
+    assert kb.kan_layer_forward_packed_workspace_bytes(g, f32, 0, 784, 64) == (kb.KAN_OK, 0)
+    assert kb.kan_layer_forward_packed_workspace_bytes(g, f32, -1, 784, 64)[0] == bad
+    lib = kb.load_library()
+    assert lib.kan_layer_forward_packed_workspace_bytes(ctypes.byref(g), 0, 256, 784, 64, None,
+                                                        None) == bad
+    call = lambda ws, nb, y=Y: kb.kan_layer_forward_packed(g, f32, 256, 784, 64, X, P, pk, y,
+                                                           workspace=ws, workspace_bytes=nb)
+    assert call(WS + 8, need) == bad                  # misaligned, would be used
+    assert call(X - 16, need) == bad                  # over x
+    assert call(P + 64, need) == bad                  # over the packed weights
+    assert call(Y - 16, need) == bad                  # over y

@@ -13,9 +13,16 @@ DT = {"f32": kb.KAN_F32, "bf16": kb.KAN_BF16}
 
 
 def _plan(G, dtype_name, B, n_in, n_out, cfg=None):
+    """(rf, wk, nw, cs, sparse) of the planned or forced shape."""
     st, plan = kb.kan_layer_plan(kb.make_grid(G), DT[dtype_name], B, n_in, n_out, cfg)
     assert st == kb.KAN_OK
-    return plan
+    return plan[:5]
+
+
+def _splits(G, dtype_name, B, n_in, n_out, cfg=None):
+    st, plan = kb.kan_layer_plan(kb.make_grid(G), DT[dtype_name], B, n_in, n_out, cfg)
+    assert st == kb.KAN_OK
+    return plan[5]
 
 
 def _rejected(G, dtype_name, B, n_in, n_out, cfg):
@@ -130,3 +137,45 @@ def test_plan_argument_checks():
     lib = kb.load_library()
     assert lib.kan_layer_plan(None, 0, 16, 4, 4, None, None) == bad
     assert lib.kan_layer_plan(g, 0, 16, 4, 4, None, None) == bad
+
+
+@pytest.mark.parametrize("dtype_name", ["f32", "bf16"])
+def test_k_split_only_for_small_batches(dtype_name):
+    """Batches whose workgroups number fewer than 512 split the contraction
+    across workgroups; the MLP's full batch and layers of few chunks never
+    split."""
+    for n_in, n_out in ((784, 256), (256, 256), (256, 10)):
+        assert _splits(10, dtype_name, 65536, n_in, n_out) == 1
+    assert _splits(10, dtype_name, 256, 784, 64) > 1
+    assert _splits(10, dtype_name, 1, 784, 256) > 1
+    assert _splits(10, dtype_name, 256, 2, 5) == 1   # one chunk
+    # the split count falls as the batch grows
+    ks = [_splits(5, dtype_name, B, 784, 64) for B in (1, 256, 4096, 65536)]
+    assert ks == sorted(ks, reverse=True) and ks[-1] == 1
+
+
+def test_k_split_needs_two_splits_of_four_chunks():
+    """A layer splits only if its K chunks make at least two splits of 4
+    chunks and 16 blocks: bf16 32 -> 10 at G = 10 (4 chunks of 8 blocks)
+    never does, 64 -> 10 (8 chunks) does; bf16 256-column tiles (2 blocks per
+    chunk) need 16 chunks: 32 -> 256 (16 chunks) does, 16 -> 256 (8) not."""
+    for B in (1, 64, 1024):
+        assert _splits(10, "bf16", B, 32, 10) == 1
+        assert _splits(10, "bf16", B, 64, 10) > 1
+    assert _splits(10, "bf16", 1, 32, 256) == 2
+    assert _splits(10, "bf16", 1, 16, 256) == 1
+
+
+@pytest.mark.parametrize("dtype_name", ["f32", "bf16"])
+def test_k_split_partial_sums_bounded(dtype_name):
+    """The fp32 partial sums of a split stay within 16 MiB, and the workspace
+    size query covers them."""
+    code = DT[dtype_name]
+    for B, n_in, n_out, G in ((1, 784, 256, 10), (4096, 784, 256, 10), (8192, 784, 256, 10),
+                              (2048, 2000, 512, 10), (64, 784, 64, 5)):
+        ks = _splits(G, dtype_name, B, n_in, n_out)
+        assert ks * B * n_out * 4 <= 16 << 20 or ks == 1
+        st, n = kb.kan_layer_forward_packed_workspace_bytes(kb.make_grid(G), code, B, n_in, n_out)
+        assert st == kb.KAN_OK
+        assert (n == 0) == (ks == 1)
+        assert n == 0 or n >= ks * B * n_out * 4

@@ -21,8 +21,11 @@ def test_noalloc_matches_workspace_entry_point(dtype_name):
     code = kb.KAN_F32 if dtype_name == "f32" else kb.KAN_BF16
     tol = F32_LAYER_TOL if dtype_name == "f32" else BF16_LAYER_TOL
     stream = int(torch.cuda.current_stream().cuda_stream)
-    # a layer of the 784-wide MLP input at a reduced batch, then a smaller one
-    for B, n_in, n_out, G in [(1000, 784, 256, 10), (300, 17, 40, 7)]:
+    cap = kb.KAN_NOALLOC_SCRATCH_BYTES
+    # a layer of the 784-wide MLP input at a reduced batch, then smaller ones:
+    # the second splits its contraction with the partial sums in the scratch
+    # array too
+    for B, n_in, n_out, G in [(1000, 784, 256, 10), (64, 784, 64, 5), (300, 17, 40, 7)]:
         x, C, Wb = wl.make_layer(wl.LayerShape(B, n_in, n_out, G, off_grid_frac=0.1),
                                  seed=B + n_in)
         if dtype_name == "bf16":
@@ -32,9 +35,16 @@ def test_noalloc_matches_workspace_entry_point(dtype_name):
         y_na = torch.full((B, n_out), float("nan"), dtype=dt, device=device())
         y_ws = torch.empty((B, n_out), dtype=dt, device=device())
         st, need = kb.kan_layer_forward_workspace_bytes(g, code, B, n_in, n_out)
-        assert st == kb.KAN_OK and need <= kb.KAN_NOALLOC_SCRATCH_BYTES
-        ws = torch.empty(need, dtype=torch.uint8, device=device())
-        say(f"noalloc {dtype_name} B={B} in={n_in} out={n_out} G={G}")
+        packed = kb.kan_layer_packed_bytes(g, code, n_in, n_out)[1]
+        assert st == kb.KAN_OK and packed <= cap
+        st, plan = kb.kan_layer_plan(g, code, B, n_in, n_out)
+        if (B, n_in) == (64, 784):
+            assert plan[5] > 1 and packed < need <= cap
+        # the workspace entry point gets the bytes the scratch array offers:
+        # where the partial sums do not fit there, both run unsplit
+        ws = torch.empty(min(need, cap), dtype=torch.uint8, device=device())
+        say(f"noalloc {dtype_name} B={B} in={n_in} out={n_out} G={G} splits={plan[5]} "
+            f"need={need}")
         assert kb.kan_layer_forward_noalloc(g, code, B, n_in, n_out, xt.data_ptr(), Ct.data_ptr(),
                                             Wt.data_ptr(), y_na.data_ptr(), stream) == kb.KAN_OK
         assert kb.kan_layer_forward(g, code, B, n_in, n_out, xt.data_ptr(), Ct.data_ptr(),
