@@ -152,6 +152,96 @@ def _time_us(fn, warmup: int = 5, reps: int = 20) -> float:
     return float(np.median([e0.elapsed_time(e1) * 1e3 for e0, e1 in ev]))
 
 
+def _graph_time_us(fn, check=None, calls: int = 20, reps: int = 15) -> tuple:
+    """Per-call GPU time of fn with no host time between its kernels: `calls`
+    calls captured in one graph (torch.cuda.graph on its capture stream), the
+    graph replayed `reps` times, each replay between two HIP events on
+    torch's current stream; the median replay over `calls` (microseconds).
+    check() runs after every replay (outside the timed region); returns
+    (us, all checks true)."""
+    import numpy as np
+    import torch
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        for _ in range(3):
+            fn()
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for _ in range(calls):
+            fn()
+    ok = True
+    ts = []
+    for i in range(reps + 3):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        if i >= 3:
+            ts.append(e0.elapsed_time(e1) * 1e3 / calls)
+        if check is not None:
+            ok = ok and bool(check())
+    return float(np.median(ts)), ok
+
+
+SMALL_BATCHES = (1, 64, 1024)
+
+
+def small_batch_block(W) -> dict:
+    """The MLP's three layers (the workload's weights, seeded uniform inputs
+    on the grid interval) at small batches in both dtypes: per-call time of
+    kan_layer_forward_packed with its workspace, where the contraction splits
+    across workgroups (kan_layer_plan's plan[5] splits), and without it
+    (unsplit), timed by graph replay.  Every replay's output is compared
+    with an eager call's (bitwise: same kernels, same summation order)."""
+    import numpy as np
+    import torch
+
+    from paper_2609_01956_amd import binding as kb
+    from paper_2609_01956_amd import workloads as wl
+
+    G, lo, hi = W["G"], W["lo"], W["hi"]
+    rng = np.random.default_rng(17)
+    out = {}
+    for dtype in ("bf16", "f32"):
+        tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+        code = kb.KAN_BF16 if dtype == "bf16" else kb.KAN_F32
+        prep = (lambda a: wl.round_to_bf16_f32(a)) if dtype == "bf16" else (lambda a: a)
+        rows = {}
+        for li, (C, Wb) in enumerate(W["layers"]):
+            n_out, n_in = Wb.shape
+            Ct = torch.from_numpy(prep(C)).to("cuda").to(tdt).contiguous()
+            Wt = torch.from_numpy(prep(Wb)).to("cuda").to(tdt).contiguous()
+            pk = kb.pack_layer(Ct, Wt, G, lo, hi)
+            for B in SMALL_BATCHES:
+                x = torch.from_numpy(rng.uniform(lo, hi, (B, n_in)).astype(np.float32))
+                x = x.to("cuda").to(tdt).contiguous()
+                st, plan = kb.kan_layer_plan(kb.make_grid(G, lo, hi), code, B, n_in, n_out)
+                kb.check(st)
+                st, nbytes = kb.kan_layer_forward_packed_workspace_bytes(
+                    kb.make_grid(G, lo, hi), code, B, n_in, n_out)
+                kb.check(st)
+                ws = torch.empty(max(nbytes, 1), dtype=torch.uint8, device="cuda")
+                y = torch.empty((B, n_out), dtype=tdt, device="cuda")
+                ref_split = kb.layer_forward_packed(x, pk, workspace=ws)
+                ref_plain = kb.layer_forward_packed(x, pk, split=False)
+                split_us, ok1 = _graph_time_us(
+                    lambda: kb.layer_forward_packed(x, pk, out=y, workspace=ws),
+                    check=lambda: torch.equal(y, ref_split))
+                plain_us, ok2 = _graph_time_us(
+                    lambda: kb.layer_forward_packed(x, pk, out=y, split=False),
+                    check=lambda: torch.equal(y, ref_plain))
+                rows[f"layer{li + 1}_{n_in}x{n_out}_b{B}"] = {
+                    "splits": plan[5], "split_us": split_us, "unsplit_us": plain_us,
+                    "replays_match_eager": ok1 and ok2}
+        out[dtype] = rows
+    return {"timing": "per call, 20 calls per graph replay, median of 15 replays",
+            "layers": out}
+
+
 def configs_sweep(dtype: str) -> None:
     """Every configured workload, one JSON line each (each kernel the median of
     200 launches after 50): the fused layer (packed weights, per layer of the
@@ -492,7 +582,9 @@ def table1_context() -> dict:
     kernel), the two contractions by the vendor GEMM through torch (context
     only, not part of the library), and the library's fused layer, which
     never materialises the basis, on the same inputs.  Median of 200
-    launches after 50, each between HIP events."""
+    launches after 50, each between HIP events (host time of the call
+    included where it exceeds the kernel's); the fused layer also per call
+    under graph replay."""
     import numpy as np
     import torch
     import torch.nn.functional as F
@@ -517,12 +609,13 @@ def table1_context() -> dict:
     spline = med(lambda: torch.matmul(phi.view(B, -1), Ct))
     base = med(lambda: torch.matmul(F.silu(x), Wt))
     fused = med(lambda: kb.layer_forward_packed(x, pk, out=y))
+    fused_graph, _ = _graph_time_us(lambda: kb.layer_forward_packed(x, pk, out=y))
     total = cdb + spline + base
     return {"layer": "256 x 784 -> 64, G = 5, fp32",
             "basis_cox_de_boor_us": cdb, "basis_truncated_power_us": tp,
             "spline_contraction_gemm_us": spline, "silu_branch_us": base,
             "unfused_total_us": total, "basis_share": cdb / total,
-            "fused_layer_us": fused,
+            "fused_layer_us": fused, "fused_layer_graph_replay_us": fused_graph,
             "paper_context": "Table 1: basis 91% of 1.58 ms on an Apple MPS GPU; Table 3: "
                              "2.8-3.5x forward latency of the truncated-power form over Cox-de "
                              "Boor on its own hardware"}
@@ -637,6 +730,7 @@ def main() -> int:
     line["grid_sweep"] = grid_sweep_block("f32")
     line["cox_de_boor_context"] = cdb_context()
     line["table1_cost_breakdown_context"] = table1_context()
+    line["small_batch"] = small_batch_block(W)
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(W, args.cpu_seconds)
     print(json.dumps(line), flush=True)
