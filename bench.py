@@ -57,6 +57,10 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=20)
     p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--clock-warmup-s", type=float, default=2.0,
+                   help="seconds of untimed steps run before the --warmup steps, so the timed "
+                        "steps run at the clock of a continuous job rather than the ramp out "
+                        "of idle")
     p.add_argument("--dtype", choices=["bf16", "f32"], default="bf16")
     p.add_argument("--cpu-seconds", type=float, default=12.0,
                    help="target wall time of the CPU oracle sample (three runs)")
@@ -135,11 +139,16 @@ def traffic_record(dtype: str, kernel: str, root: str = ROOT):
     return kib * 1024.0
 
 
-def _time_us(fn, warmup: int = 5, reps: int = 20) -> float:
+def _time_us(fn, warmup: int = 5, reps: int = 20, warm_s: float = 0.0) -> float:
     """Median over `reps` launches of fn, each between two HIP events on
-    torch's current stream, after `warmup` untimed ones (microseconds)."""
+    torch's current stream, after `warm_s` seconds of untimed calls (bringing
+    an idle GPU to its working clock) and `warmup` more (microseconds)."""
     import numpy as np
     import torch
+    t_end = time.perf_counter() + warm_s
+    while time.perf_counter() < t_end:
+        fn()
+        torch.cuda.synchronize()
     for _ in range(warmup):
         fn()
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
@@ -242,9 +251,14 @@ def small_batch_block(W) -> dict:
             "layers": out}
 
 
+# Seconds of untimed calls before each timing of the configs sweep (the
+# inputs of the next workload are generated on the host in between).
+CONFIG_WARM_S = 0.5
+
+
 def configs_sweep(dtype: str) -> None:
     """Every configured workload, one JSON line each (each kernel the median of
-    200 launches after 50): the fused layer (packed weights, per layer of the
+    200 launches after 0.5 s of calls and 50 more): the fused layer (packed weights, per layer of the
     MLP) against its roofline, the basis-only kernel
     of its input, and for the grid-size sweep the partition-of-unity error of
     the basis kernel on the same x plus 2001 points spread over the grid and
@@ -267,7 +281,7 @@ def configs_sweep(dtype: str) -> None:
         x = torch.from_numpy(prep(W["x"])).to("cuda").to(tdt).contiguous()
         B, n_in0 = x.shape
         phi = torch.empty((B, n_in0, nb), dtype=tdt, device="cuda")
-        us = _time_us(lambda: kb.basis(x, G, lo, hi, out=phi), 50, 200)
+        us = _time_us(lambda: kb.basis(x, G, lo, hi, out=phi), 50, 200, CONFIG_WARM_S)
         line = {"workload": name, "dtype": dtype, "batch": B, "grid_size": G,
                 "basis_eval": {"us": us, "gbasis_per_s": B * n_in0 * nb / us / 1e3,
                                "hbm_frac": B * n_in0 * (nb + 1) * es / us / 1e3 / PEAK_HBM_GBS}}
@@ -282,7 +296,8 @@ def configs_sweep(dtype: str) -> None:
             Wt = torch.from_numpy(prep(Wb)).to("cuda").to(tdt).contiguous()
             pk = kb.pack_layer(Ct, Wt, G, lo, hi)
             out = torch.empty((B, C.shape[0]), dtype=tdt, device="cuda")
-            lus = _time_us(lambda: kb.layer_forward_packed(h, pk, out=out), 50, 200)
+            lus = _time_us(lambda: kb.layer_forward_packed(h, pk, out=out), 50, 200,
+                           CONFIG_WARM_S)
             k = layer_roofline(dtype, B, C.shape[1], C.shape[0], nb)
             k.pop("valu_gops")
             k.pop("valu_gops_dense")
@@ -303,7 +318,7 @@ def configs_sweep(dtype: str) -> None:
             ws = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
             y = torch.empty((B, n_out), dtype=tdt, device="cuda")
             sus = _time_us(lambda: kb.layer_forward_span(x, Ct, Wt, G, lo, hi, out=y, workspace=ws),
-                           50, 200)
+                           50, 200, CONFIG_WARM_S)
             line["span_sparse_layer"] = {
                 "us": sus, "samples_per_s": B / sus * 1e6,
                 "valu_frac": B * n_in * (5.0 * n_out + 38.0) / (sus * 1e-6) / 1e9 / PEAK_VALU_GOPS}
@@ -345,11 +360,12 @@ def cpu_baseline(W, target_s: float):
                       f"after a 64-row warm-up, on {threads} threads"}
 
 
-def measure_step(dtype: str, W, steps: int, warmup: int) -> dict:
-    """Times `steps` steps of the hot path in `dtype` (after `warmup` untimed
-    ones) with a HIP event between consecutive kernels on torch's current
-    stream, the stream every kernel is launched on.  Returns the step time,
-    per-kernel averages and rooflines, and the outputs of the last step."""
+def measure_step(dtype: str, W, steps: int, warmup: int, clock_warmup_s: float = 0.0) -> dict:
+    """Times `steps` steps of the hot path in `dtype` (after `clock_warmup_s`
+    seconds of untimed steps, then `warmup` more) with a HIP event between
+    consecutive kernels on torch's current stream, the stream every kernel is
+    launched on.  Returns the step time, per-kernel averages and rooflines,
+    and the outputs of the last step."""
     import numpy as np
     import torch
 
@@ -398,6 +414,14 @@ def measure_step(dtype: str, W, steps: int, warmup: int) -> dict:
                 events[k].record()
             h = out
 
+    # Out of idle the GPU takes tens of milliseconds to reach its working
+    # clock: with 5 warm-up steps alone the bf16 step measured 0.744 ms, after
+    # 0.5, 2 or 5 s of continuous steps 0.662, 0.661 and 0.669 ms on the same
+    # box.  A continuous job runs at the latter.
+    t_end = time.perf_counter() + clock_warmup_s
+    while time.perf_counter() < t_end:
+        step()
+        torch.cuda.synchronize()
     for _ in range(warmup):
         step()
     torch.cuda.synchronize()
@@ -687,7 +711,7 @@ def main() -> int:
     other = "f32" if args.dtype == "bf16" else "bf16"
     res = {}
     for dt in (args.dtype, other):
-        res[dt] = measure_step(dt, W, args.steps, args.warmup)
+        res[dt] = measure_step(dt, W, args.steps, args.warmup, args.clock_warmup_s)
         try:
             res[dt]["parity"] = layer_parity(dt, W, res[dt])
         except Exception as e:  # the oracle is optional for timing
@@ -702,6 +726,7 @@ def main() -> int:
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
+        "clock_warmup_s": args.clock_warmup_s,
         "ms_per_step": r["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
