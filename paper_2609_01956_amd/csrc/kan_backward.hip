@@ -187,10 +187,11 @@ __global__ __launch_bounds__(64 * NW) void dx_kernel(DxArgs<T> a) {
     constexpr int NT = 64 * NW;
     constexpr int UPT = (SM * 64 + NT - 1) / NT;  // 16-byte units per thread per tile
     __shared__ u32x4 lds[2][SM * 64];
-    // per wave: one lane's 16 accumulators at a time (stride 80 bytes, so the
-    // 16-byte writes of 16 lanes fall in distinct banks), read back at the
+    // per wave: a lane's 16 accumulators after 4 zero floats (stride 80 bytes,
+    // so the 16-byte writes of 16 lanes fall in distinct banks; the next
+    // lane's zeros, and 4 after the last lane, follow them), read back at the
     // four columns the clamped derivative can make nonzero
-    __shared__ u32x4 gat[NW][64 * 5];
+    __shared__ u32x4 gat[NW][64 * 5 + 1];
 
     const int tid = threadIdx.x;
     const int wave = tid >> 6, lane = tid & 63, r = lane & 31, h = lane >> 5;
@@ -231,6 +232,25 @@ __global__ __launch_bounds__(64 * NW) void dx_kernel(DxArgs<T> a) {
 
     typedef u32x4 WSet[UPT];
     typedef T XSet[RF];
+    // Tile t's rows are features f0(t) + h of 16 columns each (cp = 16), or
+    // columns 16 h .. 16 h + 15 of feature f0(t) (cp a multiple of 32):
+    // f0(t) is the same for the whole wave.
+    const bool cp16 = a.cp == 16;
+    auto feat0 = [&](int t) -> int { return cp16 ? 2 * t : (32 * t) / a.cp; };
+    // per-lane offsets fixed for the whole kernel: units of the weight loads,
+    // x rows (in x transposed, relative to feature f0), dx rows
+    int wl[UPT];
+#pragma unroll
+    for (int k = 0; k < UPT; ++k) wl[k] = min(tid + k * NT, S * 64 - 1);
+    int64_t xl[RF], dxo[RF];
+    bool rowok[RF];
+#pragma unroll
+    for (int rf = 0; rf < RF; ++rf) {
+        const int64_t row = row0 + 32 * rf;
+        xl[rf] = rowc[rf] + (cp16 && h ? a.bpad : 0);
+        rowok[rf] = row < a.batch;
+        dxo[rf] = (a.dxp != nullptr ? (int64_t)ch * a.batch + row : row) * a.in;
+    }
     // Register sets: tile t's loads go to set t % L, issued L tiles before
     // the tile and stored to LDS one tile before it, so each store waits for
     // loads issued L - 1 tiles earlier (a tile is short: with one tile of
@@ -247,10 +267,10 @@ __global__ __launch_bounds__(64 * NW) void dx_kernel(DxArgs<T> a) {
         const int tc = min(t, t_end - 1);
         const u32x4* src = a.wtp + ((int64_t)tc * a.groups + g0) * 64;
 #pragma unroll
-        for (int k = 0; k < UPT; ++k) w[k] = src[min(tid + k * NT, S * 64 - 1)];
-        const int f = min((32 * tc + 16 * h) / a.cp, a.in - 1);
+        for (int k = 0; k < UPT; ++k) w[k] = src[wl[k]];
+        const T* xb = a.xt + (int64_t)feat0(tc) * a.bpad;  // (the lane half's rows: xl)
 #pragma unroll
-        for (int rf = 0; rf < RF; ++rf) xs[rf] = a.xt[(int64_t)f * a.bpad + rowc[rf]];
+        for (int rf = 0; rf < RF; ++rf) xs[rf] = xb[xl[rf]];
     };
     auto put = [&](int buf, const WSet& w) {
 #pragma unroll
@@ -264,12 +284,11 @@ __global__ __launch_bounds__(64 * NW) void dx_kernel(DxArgs<T> a) {
         else return v;
     };
     auto store_dx = [&](int rf, int f, float v) {
-        const int64_t row = row0 + 32 * rf;
-        if (row < a.batch && f < a.in) {
+        if (rowok[rf] && f < a.in) {
             if (a.dxp != nullptr)
-                a.dxp[((int64_t)ch * a.batch + row) * a.in + f] = v;
+                a.dxp[dxo[rf] + f] = v;
             else
-                B<T>::st(a.dx + row * a.in + f, v);
+                B<T>::st(a.dx + dxo[rf] + f, v);
         }
     };
 
@@ -278,9 +297,11 @@ __global__ __launch_bounds__(64 * NW) void dx_kernel(DxArgs<T> a) {
 #pragma unroll
     for (int rf = 0; rf < RF; ++rf) dxacc[rf] = 0.0f;
 
-    // Tile t from LDS stage `buf`, with the x of its epilogue in xs.
-    auto tile = [&](int t, int buf, const XSet& xs) {
-        floatx16 acc[RF];
+    // The MFMAs of the tile in LDS stage `buf`: acc[rf][q] = Gm[row][K row of
+    // the tile's local row q (lane half h)].  Groups past S multiply zeros
+    // (the LDS rows past the chunk's are zero, and so is dyr there), so the
+    // loop has no branch and its LDS reads can run ahead of the MFMAs.
+    auto mma = [&](int buf, floatx16 (&acc)[RF]) {
 #pragma unroll
         for (int rf = 0; rf < RF; ++rf)
 #pragma unroll
@@ -288,40 +309,45 @@ __global__ __launch_bounds__(64 * NW) void dx_kernel(DxArgs<T> a) {
         const u32x4* st = lds[buf];
 #pragma unroll
         for (int s = 0; s < SM; ++s) {
-            if (s < S) {
-                const u32x4 w = st[s * 64 + lane];
+            const u32x4 w = st[s * 64 + lane];
 #pragma unroll
-                for (int rf = 0; rf < RF; ++rf) {
-                    if constexpr (BF) {
-                        acc[rf] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                            __builtin_bit_cast(bf16x8, w), __builtin_bit_cast(bf16x8, dyr[rf][s]),
-                            acc[rf], 0, 0, 0);
-                    } else {
+            for (int rf = 0; rf < RF; ++rf) {
+                if constexpr (BF) {
+                    acc[rf] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                        __builtin_bit_cast(bf16x8, w), __builtin_bit_cast(bf16x8, dyr[rf][s]),
+                        acc[rf], 0, 0, 0);
+                } else {
 #pragma unroll
-                        for (int j = 0; j < 4; ++j)
-                            acc[rf] = __builtin_amdgcn_mfma_f32_32x32x2f32(
-                                __uint_as_float(w[j]), __uint_as_float(dyr[rf][s][j]), acc[rf], 0,
-                                0, 0);
-                    }
+                    for (int j = 0; j < 4; ++j)
+                        acc[rf] = __builtin_amdgcn_mfma_f32_32x32x2f32(
+                            __uint_as_float(w[j]), __uint_as_float(dyr[rf][s][j]), acc[rf], 0, 0,
+                            0);
                 }
             }
         }
-        // acc[rf][q] = Gm[row][feature f, column c0 + q].  Of the basis
-        // columns only the four with |v| < 2 have a nonzero derivative: with
-        // s the coordinate of column 0 of the feature, tau = s - floor(s) and
-        // clo = floor(s) - 1, column clo + k has u = tau + 3 - k, where the
-        // derivative of the cubic (its segment form on the span) is
-        //   k = 0: -(1 - tau)^2 / 2      k = 1: (3 tau^2 - 4 tau) / 2
-        //   k = 2: (1 + 2 tau - 3 tau^2) / 2   k = 3: tau^2 / 2.
-        // Column 0 carries the SiLU derivative.  The four accumulators are read
-        // back from a wave-private LDS copy (their index differs per lane).
-        const int R0 = 32 * t + 16 * h;
-        const int f = R0 / a.cp;
-        const int c0 = R0 - f * a.cp;
+    };
+
+    // The epilogue of tile t, without stores: acc[rf][q] = Gm[row][feature f,
+    // column c0 + q].  Of the basis columns only the four with |v| < 2 have a
+    // nonzero derivative: with s the coordinate of column 0 of the feature,
+    // tau = s - floor(s) and clo = floor(s) - 1, column clo + k has u = tau +
+    // 3 - k, where the derivative of the cubic (its segment form on the span)
+    // is
+    //   k = 0: -(1 - tau)^2 / 2      k = 1: (3 tau^2 - 4 tau) / 2
+    //   k = 2: (1 + 2 tau - 3 tau^2) / 2   k = 3: tau^2 / 2.
+    // Column 0 carries the SiLU derivative.  The four accumulators are read
+    // back from a wave-private LDS copy (their index differs per lane).  xvs:
+    // the lane's x of the tile's feature, per row tile.  Returns the tile's
+    // contribution to dx per row tile in sum.
+    auto epi_sum = [&](int t, const floatx16 (&acc)[RF], const float (&xvs)[RF],
+                       float (&sum)[RF]) {
+        const int fu = feat0(t);
+        const int f = cp16 ? fu + h : fu;
+        const int c0 = cp16 ? 0 : 32 * t - fu * a.cp + 16 * h;
         char* gl = reinterpret_cast<char*>(gat[wave]) + lane * 80;
 #pragma unroll
         for (int rf = 0; rf < RF; ++rf) {
-            const float xv = f < a.in ? to_f(xs[rf]) : 0.0f;
+            const float xv = f < a.in ? xvs[rf] : 0.0f;
             // coordinate of column c0 (its integer offset folded into the fma),
             // clamped to keep the window index small for far-out inputs; +-Inf
             // lands outside every column, NaN is carried by the SiLU term
@@ -331,64 +357,142 @@ __global__ __launch_bounds__(64 * NW) void dx_kernel(DxArgs<T> a) {
                 -8.0f, 24.0f);
             const float fl = __builtin_floorf(sc);
             const float tau = sc - fl;
-            const int qlo = (int)fl - 1;  // first window column, relative to c0
             const float t2 = tau * tau;
             float d[4];
             d[0] = -0.5f * (1.0f - tau) * (1.0f - tau);
             d[1] = __builtin_fmaf(1.5f, t2, -2.0f * tau);
             d[2] = __builtin_fmaf(-1.5f, t2, __builtin_fmaf(tau, 1.0f, 0.5f));
             d[3] = 0.5f * t2;
+            // the lane's 16 columns after its 4 zeros; the SiLU column (c = 0)
+            // is not a basis column and reads as 0 too
 #pragma unroll
             for (int m = 0; m < 4; ++m)
-                *reinterpret_cast<floatx4*>(gl + 16 * m) =
-                    floatx4{acc[rf][4 * m], acc[rf][4 * m + 1], acc[rf][4 * m + 2], acc[rf][4 * m + 3]};
+                *reinterpret_cast<floatx4*>(gl + 16 + 16 * m) =
+                    floatx4{m == 0 && c0 == 0 ? 0.0f : acc[rf][4 * m], acc[rf][4 * m + 1],
+                            acc[rf][4 * m + 2], acc[rf][4 * m + 3]};
+            // window columns q = qlo .. qlo + 3 relative to c0: columns outside
+            // the lane's 16 read the zeros around them (padding columns past
+            // nb hold exact zeros: their weights are 0), and a window wholly
+            // outside is moved onto 4 zeros
+            const int qlo = min(max((int)fl - 1, -4), 16);
+            const float* gw = reinterpret_cast<const float*>(gl + 16 + 4 * qlo);
             float sb = 0.0f;
 #pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                const int q = qlo + k;
-                const int c = c0 + q;
-                const bool ok = q >= 0 && q < 16 && c >= 1 && c <= a.nb;
-                const float g = *reinterpret_cast<const float*>(gl + 4 * min(max(q, 0), 15));
-                sb = __builtin_fmaf(ok ? g : 0.0f, d[k], sb);
-            }
-            const float sum = __builtin_fmaf(c0 == 0 ? acc[rf][0] : 0.0f, silu_deriv(xv), a.inv_h * sb);
-            if (a.cp == 16) {
-                store_dx(rf, f, sum);
-            } else {
-                dxacc[rf] += sum;
-            }
+            for (int k = 0; k < 4; ++k) sb = __builtin_fmaf(gw[k], d[k], sb);
+            sum[rf] = __builtin_fmaf(c0 == 0 ? acc[rf][0] : 0.0f, silu_deriv(xv), a.inv_h * sb);
         }
-        if (a.cp != 16 && (t + 1) % tpf == 0) {  // the feature's last tile: add the two halves
+    };
+    // The tile's stores: dx of its feature, or (features of two tiles) the
+    // running sum, stored at the feature's last tile.
+    auto epi_store = [&](int t, const float (&sum)[RF]) {
+        const int f = cp16 ? feat0(t) + h : feat0(t);
+        if (a.cp == 16) {
 #pragma unroll
-            for (int rf = 0; rf < RF; ++rf) {
-                const float tot = dxacc[rf] + __shfl_xor(dxacc[rf], 32);
-                if (h == 0) store_dx(rf, f, tot);
-                dxacc[rf] = 0.0f;
+            for (int rf = 0; rf < RF; ++rf) store_dx(rf, f, sum[rf]);
+        } else {
+#pragma unroll
+            for (int rf = 0; rf < RF; ++rf) dxacc[rf] += sum[rf];
+            if ((t + 1) % tpf == 0) {  // the feature's last tile: add the two halves
+#pragma unroll
+                for (int rf = 0; rf < RF; ++rf) {
+                    const float tot = dxacc[rf] + __shfl_xor(dxacc[rf], 32);
+                    if (h == 0) store_dx(rf, f, tot);
+                    dxacc[rf] = 0.0f;
+                }
             }
         }
     };
+    auto xfloat = [&](const XSet& xs, float (&xv)[RF]) {
+#pragma unroll
+        for (int rf = 0; rf < RF; ++rf) xv[rf] = to_f(xs[rf]);
+    };
 
+    // LDS rows of groups past the chunk's are never written by put: zero them
+    // once (the MFMAs of those groups then add exact zeros).  Likewise the
+    // zeros around each lane's gather slot, never written after this.
+    for (int u = S * 64 + tid; u < SM * 64; u += NT) {
+        lds[0][u] = u32x4{0u, 0u, 0u, 0u};
+        lds[1][u] = u32x4{0u, 0u, 0u, 0u};
+    }
+    {
+        char* gw0 = reinterpret_cast<char*>(gat[wave]);
+        *reinterpret_cast<u32x4*>(gw0 + lane * 80) = u32x4{0u, 0u, 0u, 0u};
+        if (lane == 63) *reinterpret_cast<u32x4*>(gw0 + 64 * 80) = u32x4{0u, 0u, 0u, 0u};
+    }
 #pragma unroll
     for (int j = 0; j < L; ++j) issue(t_begin + j, wq[j], xq[j]);
     put(0, wq[0]);
     __syncthreads();
-    // tile t = t_begin + L i + j: LDS stage j % 2, register set j
-#pragma unroll 1
-    for (int tb = t_begin; tb < t_end; tb += L) {
-        bool done = false;
-        StaticFor<0, L>::run([&](auto jj) {
-            constexpr int j = decltype(jj)::value;
-            const int t = tb + j;
-            if (done || t >= t_end) {
-                done = true;
-                return;
-            }
-            tile(t, j & 1, xq[j]);
-            issue(t + L, wq[j], xq[j]);
-            if (t + 1 < t_end) put((j + 1) & 1, wq[(j + 1) % L]);
+    if constexpr (BF) {
+        // bf16 (a tile's MFMAs are short next to its epilogue): software
+        // pipelined over two accumulator sets.  The iteration of tile t issues
+        // its MFMAs and computes tile t - 1's epilogue in the same straight-line
+        // code, so that VALU and LDS work overlaps the MFMAs; the stores
+        // follow.  x of tile t is kept as floats (xp) before its register set
+        // is reloaded.  Tile t_begin + i uses LDS stage i % 2, register set
+        // i % L and accumulator set i % 2 (L is even).
+        floatx16 acc[2][RF];
+        float xp[2][RF];
+        float sum[RF];
+        if (t_begin < t_end) {  // the first tile: MFMAs only
+            mma(0, acc[0]);
+            xfloat(xq[0], xp[0]);
+            issue(t_begin + L, wq[0], xq[0]);
+            if (t_begin + 1 < t_end) put(1, wq[1 % L]);
             __syncthreads();
-            __builtin_amdgcn_sched_barrier(0);  // (tiles are not interleaved)
-        });
+        }
+#pragma unroll 1
+        for (int tb = t_begin + 1; tb < t_end; tb += L) {
+            bool done = false;
+            StaticFor<0, L>::run([&](auto jj) {
+                constexpr int j = decltype(jj)::value;
+                constexpr int i = j + 1;  // t - t_begin, mod L
+                constexpr int p = i & 1;
+                const int t = tb + j;
+                if (done || t >= t_end) {
+                    done = true;
+                    return;
+                }
+                mma(p, acc[p]);
+                epi_sum(t - 1, acc[p ^ 1], xp[p ^ 1], sum);
+                epi_store(t - 1, sum);
+                xfloat(xq[i % L], xp[p]);
+                issue(t + L, wq[i % L], xq[i % L]);
+                if (t + 1 < t_end) put((i + 1) & 1, wq[(i + 1) % L]);
+                __syncthreads();
+                __builtin_amdgcn_sched_barrier(0);
+            });
+        }
+        const int tl = t_end - 1;  // the last tile's epilogue
+        if (tl >= t_begin) {
+            if (((tl - t_begin) & 1) == 0) epi_sum(tl, acc[0], xp[0], sum);
+            else epi_sum(tl, acc[1], xp[1], sum);
+            epi_store(tl, sum);
+        }
+    } else {
+        // tile t = t_begin + L i + j: LDS stage j % 2, register set j
+#pragma unroll 1
+        for (int tb = t_begin; tb < t_end; tb += L) {
+            bool done = false;
+            StaticFor<0, L>::run([&](auto jj) {
+                constexpr int j = decltype(jj)::value;
+                const int t = tb + j;
+                if (done || t >= t_end) {
+                    done = true;
+                    return;
+                }
+                floatx16 acc[RF];
+                float xv[RF], sum[RF];
+                mma(j & 1, acc);
+                xfloat(xq[j], xv);
+                epi_sum(t, acc, xv, sum);
+                epi_store(t, sum);
+                issue(t + L, wq[j], xq[j]);
+                if (t + 1 < t_end) put((j + 1) & 1, wq[(j + 1) % L]);
+                __syncthreads();
+                __builtin_amdgcn_sched_barrier(0);  // (tiles are not interleaved)
+            });
+        }
     }
 }
 
