@@ -550,7 +550,9 @@ __global__ __launch_bounds__(kThreads) void dw_kernel(DwArgs<T> a) {
     constexpr int XU = (32 * NFEAT + kThreads - 1) / kThreads;  // (row, feature) pairs per thread
     static_assert(KT == 256, "K rows per workgroup");
     __shared__ u32x4 dys[2][OT * ROWU];
-    __shared__ u32x4 as[2][KT * ROWU];
+    // (row KT of each stage: a dummy row that takes the writes of lanes with
+    // nothing to write, so that building the A chunk has no branch)
+    __shared__ u32x4 as[2][(KT + 1) * ROWU];
     // features with a NaN input in this workgroup's rows: their basis
     // gradients are NaN (N_j(NaN) is NaN; the clamped form would give 0)
     __shared__ int nanf[NFEAT];
@@ -568,15 +570,20 @@ __global__ __launch_bounds__(kThreads) void dw_kernel(DwArgs<T> a) {
     const int nchunks = (int)((b_end - b_begin) / 32);
 
     for (int i = tid; i < NFEAT; i += kThreads) nanf[i] = 0;
-    for (int i = tid; i < 2 * KT * ROWU; i += kThreads) (&as[0][0])[i] = u32x4{0u, 0u, 0u, 0u};
+    for (int i = tid; i < 2 * (KT + 1) * ROWU; i += kThreads)
+        (&as[0][0])[i] = u32x4{0u, 0u, 0u, 0u};
 
     typedef u32x4 DSet[DU];
     typedef T XSet[XU];
     DSet dq[2];
     XSet xq[2];
     int prev[2][XU];  // first window column written two chunks ago in each stage (or -8)
+    bool nanx[XU];    // a NaN input seen in the thread's (batch row, feature) pairs
 #pragma unroll
-    for (int k = 0; k < XU; ++k) prev[0][k] = prev[1][k] = -8;
+    for (int k = 0; k < XU; ++k) {
+        prev[0][k] = prev[1][k] = -8;
+        nanx[k] = false;
+    }
 
     // Loads of chunk ck: unconditional (chunks past the split's last, units
     // past the tile's and features past `in` re-read valid addresses; their
@@ -599,63 +606,64 @@ __global__ __launch_bounds__(kThreads) void dw_kernel(DwArgs<T> a) {
             xs[k] = a.xt[(int64_t)f * a.bpad + b0 + bl];
         }
     };
-    // one A entry: K row R (absolute), batch row bl of the chunk
-    auto put_a = [&](int buf, int R, int bl, float v) {
+    // one A entry: K row R (absolute), batch row bl of the chunk; with ok
+    // false, or R outside the workgroup's K rows, the dummy row takes it
+    auto put_a = [&](int buf, int R, int bl, float v, bool ok) {
         const int lr = R - kt0;
-        if (lr >= 0 && lr < KT) {
-            const int pos = BF ? bl : 16 * (bl & 1) + (bl >> 1);
-            char* p = reinterpret_cast<char*>(&as[buf][lr * ROWU]) + pos * ES;
-            if constexpr (BF)
-                *reinterpret_cast<uint16_t*>(p) = f32_to_bf16(v);
-            else
-                *reinterpret_cast<float*>(p) = v;
-        }
+        const int lre = ok && lr >= 0 && lr < KT ? lr : KT;
+        const int pos = BF ? bl : 16 * (bl & 1) + (bl >> 1);
+        char* p = reinterpret_cast<char*>(&as[buf][lre * ROWU]) + pos * ES;
+        if constexpr (BF)
+            *reinterpret_cast<uint16_t*>(p) = f32_to_bf16(v);
+        else
+            *reinterpret_cast<float*>(p) = v;
     };
+    // Stage chunk data: dy by plain copies, and the A chunk: per (batch row,
+    // feature) pair of the thread the SiLU column and the four window columns,
+    // after clearing the four written two chunks earlier in this stage.
+    // Straight-line code (no branch on lanes), so that the compiler can
+    // interleave it with the MFMAs of the other stage.
     auto stage = [&](int buf, const DSet& d, const XSet& xs, int (&pv)[XU]) {
 #pragma unroll
         for (int k = 0; k < DU; ++k) {
             const int u = tid + k * kThreads;
-            if (u < OT * UR) dys[buf][(u / UR) * ROWU + u % UR] = d[k];
+            if ((OT * UR) % kThreads == 0 || u < OT * UR)
+                dys[buf][(u / UR) * ROWU + u % UR] = d[k];
         }
 #pragma unroll
         for (int k = 0; k < XU; ++k) {
+            if (k > 0 && k * kThreads >= 32 * nfeat) break;  // (the same for every lane)
             const int idx = tid + k * kThreads;
-            if (idx < 32 * nfeat) {
-                const int bl = idx % 32, fl = idx / 32;
-                const int Rf = (F0 + fl) * a.cp;  // K row of the feature's column 0
-                float xv;
-                if constexpr (BF) xv = bf16_to_f32(xs[k]);
-                else xv = xs[k];
-                if (F0 + fl >= a.in) xv = 0.0f;  // (a padding feature)
-                // clear the window written two chunks ago in this stage
+            const bool valid = idx < 32 * nfeat;
+            const int bl = idx % 32, fl = idx / 32;
+            const int Rf = (F0 + fl) * a.cp;  // K row of the feature's column 0
+            float xv;
+            if constexpr (BF) xv = bf16_to_f32(xs[k]);
+            else xv = xs[k];
+            xv = F0 + fl >= a.in ? 0.0f : xv;  // (a padding feature)
+            const bool isn = xv != xv;
+            nanx[k] = nanx[k] || (valid && isn);
+            // clear the window written two chunks ago in this stage
 #pragma unroll
-                for (int m = 0; m < 4; ++m) {
-                    const int c = pv[k] + m;
-                    if (c >= 1 && c <= a.nb) put_a(buf, Rf + c, bl, 0.0f);
-                }
-                put_a(buf, Rf, bl, half_silu_b(xv));
-                if (xv != xv) {
-                    nanf[fl] = 1;
-                    pv[k] = -8;
-                    continue;
-                }
-                // coordinate of column 0 (clamped so that the column index
-                // stays small for far-out or infinite inputs), the window's
-                // first column, then each value with its column folded into
-                // the fma's exact integer addend
-                const float lot = coord_lo(xv, a.xlim, a.inv_lo, a.a_frac);
-                const float s0 = __builtin_amdgcn_fmed3f(
-                    __builtin_fmaf(xv, a.inv_h, a.a_int + 1.0f) + lot, -8.0f, (float)(a.nb + 8));
-                const int clo = (int)__builtin_floorf(s0) - 1;
-                pv[k] = clo;
+            for (int m = 0; m < 4; ++m) {
+                const int c = pv[k] + m;
+                put_a(buf, Rf + c, bl, 0.0f, valid && c >= 1 && c <= a.nb);
+            }
+            put_a(buf, Rf, bl, half_silu_b(xv), valid);
+            // coordinate of column 0 (clamped so that the column index stays
+            // small for far-out or infinite inputs), the window's first
+            // column, then each value with its column folded into the fma's
+            // exact integer addend; a NaN input writes no basis value
+            const float lot = coord_lo(xv, a.xlim, a.inv_lo, a.a_frac);
+            const float s0 = __builtin_amdgcn_fmed3f(
+                __builtin_fmaf(xv, a.inv_h, a.a_int + 1.0f) + lot, -8.0f, (float)(a.nb + 8));
+            const int clo = isn ? -8 : (int)__builtin_floorf(s0) - 1;
+            pv[k] = clo;
 #pragma unroll
-                for (int m = 0; m < 4; ++m) {
-                    const int c = clo + m;
-                    if (c >= 1 && c <= a.nb) {
-                        const float v = __builtin_fmaf(xv, a.inv_h, a.a_int + 1.0f - (float)c) + lot;
-                        put_a(buf, Rf + c, bl, half_basis(v));
-                    }
-                }
+            for (int m = 0; m < 4; ++m) {
+                const int c = clo + m;
+                const float v = __builtin_fmaf(xv, a.inv_h, a.a_int + 1.0f - (float)c) + lot;
+                put_a(buf, Rf + c, bl, half_basis(v), valid && c >= 1 && c <= a.nb);
             }
         }
     };
@@ -718,25 +726,33 @@ __global__ __launch_bounds__(kThreads) void dw_kernel(DwArgs<T> a) {
     };
 
     // Pipeline: stage ck % 2 holds chunk ck; register set ck % 2 is loaded two
-    // chunks ahead (loop unrolled by two so the sets are compile-time
-    // choices), staged one chunk before its use.
+    // chunks ahead, staged one chunk before its use.  The loop takes two
+    // chunks per trip (the stages and sets are compile-time choices); it
+    // stages one chunk past the last (the loads are clamped to the last
+    // chunk; that stage is never multiplied), and an odd last chunk follows.
     __syncthreads();  // (stages cleared, flags reset)
     issue(0, dq[0], xq[0]);
     issue(1, dq[1], xq[1]);
-    if (nchunks > 0) stage(0, dq[0], xq[0], prev[0]);
-    __syncthreads();
-    for (int ck = 0; ck < nchunks; ck += 2) {
-        chunk(0);
-        issue(ck + 2, dq[0], xq[0]);
-        if (ck + 1 < nchunks) stage(1, dq[1], xq[1], prev[1]);
+    if (nchunks > 0) {
+        stage(0, dq[0], xq[0], prev[0]);
         __syncthreads();
-        if (ck + 1 < nchunks) {
+        int ck = 0;
+        for (; ck + 1 < nchunks; ck += 2) {
+            chunk(0);
+            issue(ck + 2, dq[0], xq[0]);
+            stage(1, dq[1], xq[1], prev[1]);
+            __syncthreads();
             chunk(1);
             issue(ck + 3, dq[1], xq[1]);
-            if (ck + 2 < nchunks) stage(0, dq[0], xq[0], prev[0]);
+            stage(0, dq[0], xq[0], prev[0]);
             __syncthreads();
         }
+        if (ck < nchunks) chunk(0);
     }
+#pragma unroll
+    for (int k = 0; k < XU; ++k)
+        if (nanx[k]) nanf[(tid + k * kThreads) / 32] = 1;
+    __syncthreads();
 
     // acc[rt][nf][q] = (dW^T / 2)[K row kt0 + 32 (kg RF + rt) + 8 (q / 4) + 4 h + q % 4][output o]
 #pragma unroll
