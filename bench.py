@@ -327,9 +327,11 @@ def configs_sweep(dtype: str) -> None:
 
 def cpu_baseline(W, target_s: float):
     """The float64 oracle, untuned, on a row sample of the same step: the
-    basis of the input and the 3-layer forward of its first rows.  One
-    64-row warm-up sizes the sample so that one run takes about target_s / 3;
-    three runs follow and their median is reported (cost is linear in rows)."""
+    basis of the input and the 3-layer forward of its first rows.  A 64-row
+    warm-up, then a sizing run of about a second (the warm-up's time is
+    mostly fixed cost), size the sample so that one run takes about
+    target_s / 3; three runs follow and their median is reported (cost is
+    linear in rows)."""
     import numpy as np
     import oracle
 
@@ -347,7 +349,11 @@ def cpu_baseline(W, target_s: float):
     t0 = time.perf_counter()
     step(64)
     dt64 = time.perf_counter() - t0
-    rows = int(max(64, min(x.shape[0], 64 * (target_s / 3.0) / max(dt64, 1e-6))))
+    n1 = int(max(64, min(x.shape[0], 64 * 1.0 / max(dt64, 1e-6))))
+    t0 = time.perf_counter()
+    step(n1)
+    dt1 = time.perf_counter() - t0
+    rows = int(max(64, min(x.shape[0], n1 * (target_s / 3.0) / max(dt1, 1e-6))))
     runs = []
     for _ in range(3):
         t0 = time.perf_counter()
@@ -357,7 +363,7 @@ def cpu_baseline(W, target_s: float):
     return {"value": rows / dt, "unit": "samples/s", "cores": threads, "kind": "oracle",
             "sample": f"first {rows} rows of the {x.shape[0]}-row batch: float64 basis of the "
                       f"input + 3-layer forward; median of 3 runs ({', '.join(f'{r:.2f}' for r in runs)} s) "
-                      f"after a 64-row warm-up, on {threads} threads"}
+                      f"after a 64-row warm-up and a {n1}-row sizing run, on {threads} threads"}
 
 
 def measure_step(dtype: str, W, steps: int, warmup: int, clock_warmup_s: float = 0.0) -> dict:
