@@ -756,14 +756,22 @@ def main() -> int:
                                     "valu_frac_dense_count")}
                                for n, kk in o["kernels"].items()},
                    "parity": o["parity"]}
-    line["backward"] = backward_block(args.dtype, W, r)
-    line[other]["backward"] = backward_block(other, W, o)
-    line["grid_sweep"] = grid_sweep_block("f32")
-    line["cox_de_boor_context"] = cdb_context()
-    line["table1_cost_breakdown_context"] = table1_context()
-    line["small_batch"] = small_batch_block(W)
+    # The blocks below add to the line; a failure in one is recorded in its
+    # place rather than losing the measured step.
+    def optional(fn, *a):
+        try:
+            return fn(*a)
+        except Exception as e:  # noqa: BLE001 (reported in the line)
+            return {"error": f"{type(e).__name__}: {e}"}
+
+    line["backward"] = optional(backward_block, args.dtype, W, r)
+    line[other]["backward"] = optional(backward_block, other, W, o)
+    line["grid_sweep"] = optional(grid_sweep_block, "f32")
+    line["cox_de_boor_context"] = optional(cdb_context)
+    line["table1_cost_breakdown_context"] = optional(table1_context)
+    line["small_batch"] = optional(small_batch_block, W)
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(W, args.cpu_seconds)
+        line["cpu_baseline"] = optional(cpu_baseline, W, args.cpu_seconds)
     print(json.dumps(line), flush=True)
     return 0
 
