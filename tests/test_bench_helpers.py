@@ -73,3 +73,18 @@ def test_more_than_one_gpu_is_refused():
                        capture_output=True, text=True, timeout=60)
     assert r.returncode == 2
     assert "one GPU" in r.stderr
+
+
+def test_cpu_baseline_sample_is_sized_by_a_sizing_run():
+    """The oracle baseline sizes its sample from a second, longer run (the
+    64-row warm-up is mostly fixed cost), reports the median of three runs
+    and the threads it used."""
+    from paper_2609_01956_amd import workloads as wl
+
+    W = wl.make_workload("c2_layer_64x64_g5")
+    r = bench.cpu_baseline(W, 0.6)
+    assert r["kind"] == "oracle" and r["unit"] == "samples/s" and r["value"] > 0
+    assert r["cores"] >= 1
+    assert "sizing run" in r["sample"] and "median of 3 runs" in r["sample"]
+    rows = int(r["sample"].split("first ")[1].split(" rows")[0])
+    assert 64 <= rows <= W["x"].shape[0]
