@@ -544,3 +544,51 @@ def test_layer_k_split_forced_shapes():
         say(f"layer K split forced {cfg} splits={plan[5]}")
         y = _gpu_layer(x, C, Wb, G, "f32", shape=cfg)
         assert normwise(y, ref) <= F32_LAYER_TOL, cfg
+
+
+def _random_split_cases(n_per_dtype=8, seed=2026):
+    """Seeded random layers (degree 1-5, grids 3-40, both dtypes) at batches
+    small enough that kan_layer_plan splits the contraction."""
+    rng = np.random.default_rng(seed)
+    cases = {"f32": [], "bf16": []}
+    while min(len(v) for v in cases.values()) < n_per_dtype:
+        dtype_name = "f32" if rng.random() < 0.5 else "bf16"
+        if len(cases[dtype_name]) >= n_per_dtype:
+            continue
+        k = int(rng.choice([3, 3, 3, 1, 2, 5]))
+        G = int(rng.choice([3, 5, 8, 10, 12, 20, 40]))
+        B = int(rng.integers(1, 97))
+        n_in = int(rng.integers(40, 401))
+        n_out = int(rng.integers(1, 129))
+        code = kb.KAN_F32 if dtype_name == "f32" else kb.KAN_BF16
+        st, plan = kb.kan_layer_plan(kb.make_grid(G, spline_order=k), code, B, n_in, n_out)
+        if st == kb.KAN_OK and plan[5] > 1:
+            cases[dtype_name].append((dtype_name, B, n_in, n_out, G, k))
+    return cases["f32"] + cases["bf16"]
+
+
+@pytest.mark.parametrize("dtype_name,B,n_in,n_out,G,k", _random_split_cases())
+def test_layer_k_split_random_layers(dtype_name, B, n_in, n_out, G, k):
+    """The split contraction on random layer sizes: within tolerance of the
+    oracle, equal to the unsplit layer up to the fp32 summation order, and
+    the same on a second call."""
+    dt = _dtype(dtype_name)
+    rng = np.random.default_rng(B * 1000 + n_in + n_out + G)
+    h = 2.0 / G
+    x = rng.uniform(-1 - 2 * h, 1 + 2 * h, (B, n_in)).astype(np.float32)
+    _, C, Wb = wl.make_layer(wl.LayerShape(B, n_in, n_out, G), B + n_out, k=k)
+    if dtype_name == "bf16":
+        x, C, Wb = (wl.round_to_bf16_f32(a) for a in (x, C, Wb))
+    say(f"layer K split random {dtype_name} B={B} in={n_in} out={n_out} G={G} k={k}")
+    pk = kb.pack_layer(to_dev(C, dt), to_dev(Wb, dt), G, spline_order=k)
+    xd = to_dev(x, dt)
+    y1 = kb.layer_forward_packed(xd, pk)
+    y2 = kb.layer_forward_packed(xd, pk)
+    y0 = kb.layer_forward_packed(xd, pk, split=False)
+    torch.cuda.synchronize()
+    assert torch.equal(y1, y2)
+    ref = oracle.layer(x, C, Wb, G, k=k)
+    if dtype_name == "bf16":
+        ref = oracle.round_bf16(ref)
+    assert normwise(to_host64(y1), ref) <= _tol(dtype_name)
+    assert normwise(to_host64(y1), to_host64(y0)) <= _tol(dtype_name)
