@@ -86,15 +86,23 @@ def copy_calibration(nbytes: int) -> None:
     print(json.dumps({"copy_calibration_bytes": n * 4, "launches": 10}), flush=True)
 
 
-def layer_roofline(dtype: str, batch: int, n_in: int, n_out: int, nb: int) -> dict:
+def layer_roofline(dtype: str, batch: int, n_in: int, n_out: int, nb: int,
+                   narrow: bool = False) -> dict:
     """Roofline of one fused layer: bound by the matrix cores (dense flops,
     all nb bases plus the SiLU column per input) unless generating its basis
     values (the least VALU work, four nonzero columns per input) takes longer
     at the VALU peak than the contraction at the MFMA peak (narrow outputs);
-    then it is reported against the VALU."""
+    then it is reported against the VALU.  A layer that runs on the
+    vector-ALU kernel of narrow fp32 layers (`narrow`) is reported against the
+    VALU with that kernel's least work: the basis generation plus one fma per
+    output for each of the five nonzero columns (SiLU and four bases)."""
     flop = 2.0 * batch * n_out * n_in * (nb + 1)
     valu = VALU_OPS_PER_FEATURE[dtype] * batch * n_in
-    if valu / (PEAK_VALU_GOPS * 1e9) > flop / (PEAK_TFLOPS[dtype] * 1e12):
+    if narrow:
+        k = {"bound": "alu", "unit": "Gop/s", "peak": PEAK_VALU_GOPS,
+             "algorithmic": (VALU_OPS_PER_FEATURE[dtype] + 5.0 * n_out) * batch * n_in / 1e9,
+             "kernel": "vector ALU (narrow layer)"}
+    elif valu / (PEAK_VALU_GOPS * 1e9) > flop / (PEAK_TFLOPS[dtype] * 1e12):
         k = {"bound": "alu", "unit": "Gop/s", "peak": PEAK_VALU_GOPS,
              "algorithmic": valu / 1e9}  # G lane-ops
     else:
@@ -103,6 +111,16 @@ def layer_roofline(dtype: str, batch: int, n_in: int, n_out: int, nb: int) -> di
     k["valu_gops"] = valu / 1e9
     k["valu_gops_dense"] = (VALU_OPS_PER_VALUE_DENSE * nb + 4.0) * batch * n_in / 1e9
     return k
+
+
+def planned_narrow(kb, dtype: str, G: int, lo: float, hi: float, batch: int, n_in: int,
+                   n_out: int) -> bool:
+    """Whether the library plans the vector-ALU kernel of narrow layers
+    (kan_layer_plan's shape {0, 4, 4, 1}) for this layer and batch."""
+    code = kb.KAN_BF16 if dtype == "bf16" else kb.KAN_F32
+    st, plan = kb.kan_layer_plan(kb.make_grid(G, lo, hi), code, batch, n_in, n_out)
+    kb.check(st)
+    return plan[0] == 0
 
 
 KERNEL_SOURCES = ["kan_layer_kernel.h", "kan_layer.hip", "kan_internal.h", "kan_device.h"]
@@ -298,7 +316,8 @@ def configs_sweep(dtype: str) -> None:
             out = torch.empty((B, C.shape[0]), dtype=tdt, device="cuda")
             lus = _time_us(lambda: kb.layer_forward_packed(h, pk, out=out), 50, 200,
                            CONFIG_WARM_S)
-            k = layer_roofline(dtype, B, C.shape[1], C.shape[0], nb)
+            k = layer_roofline(dtype, B, C.shape[1], C.shape[0], nb,
+                               planned_narrow(kb, dtype, G, lo, hi, B, C.shape[1], C.shape[0]))
             k.pop("valu_gops")
             k.pop("valu_gops_dense")
             k.update(us=lus, samples_per_s=B / lus * 1e6, achieved=k["algorithmic"] / (lus * 1e-6))
@@ -457,7 +476,8 @@ def measure_step(dtype: str, W, steps: int, warmup: int, clock_warmup_s: float =
         kern[names[1 + 2 * li]] = {
             "bound": "hbm", "unit": "GB/s", "peak": PEAK_HBM_GBS,
             "algorithmic": (o * i_ * (nb + 1) * es + packs[li].nbytes) / 1e9}
-        kern[names[2 + 2 * li]] = layer_roofline(dtype, B, i_, o, nb)
+        kern[names[2 + 2 * li]] = layer_roofline(dtype, B, i_, o, nb,
+                                                 planned_narrow(kb, dtype, G, lo, hi, B, i_, o))
         # HBM bytes the layer must move: x, the packed weights once, y
         kern[names[2 + 2 * li]]["algorithmic_bytes"] = (B * (i_ + o) * es + packs[li].nbytes)
     for name, ms in zip(names, per_kernel_ms):

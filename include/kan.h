@@ -254,7 +254,8 @@ kan_status kan_layer_forward_packed_workspace_bytes(const kan_grid* grid, kan_dt
  *   shape    NULL for the library's own choice, or a forced {rf, wk, nw, cs}
  *            as accepted by kan_layer_forward_packed (validated here the same
  *            way: an invalid one is KAN_ERR_INVALID_ARG)
- *   plan[0]  32-row MFMA tiles per wave (1 or 2)
+ *   plan[0]  32-row MFMA tiles per wave (1 or 2), or 0 for the vector-ALU
+ *            kernel of narrow layers (below)
  *   plan[1]  waves splitting the contraction (K) of a workgroup (1, 2 or 4)
  *   plan[2]  waves per workgroup (4 or 8)
  *   plan[3]  workgroups splitting the columns of an output tile (1, 2 or 4)
@@ -267,6 +268,14 @@ kan_status kan_layer_forward_packed_workspace_bytes(const kan_grid* grid, kan_dt
  *            splits as keep the fp32 partial sums within 16 MiB.
  *
  * Degrees other than 3 run one shape, {1, 1, 4, 1}.
+ *
+ * Narrow layers: fp32, k = 3, 1 <= out_features <= 16 and G <= 26 can also
+ * run the shape {0, 4, 4, 1}, a kernel without matrix instructions (one batch
+ * row per lane, 64 rows per workgroup, four waves each taking a quarter of
+ * the features, only the k + 1 nonzero basis values and the SiLU value of
+ * each input multiplied into the outputs; the same eq. kan_forward up to the
+ * fp32 summation order).  It is planned for batches of 16384 rows or more
+ * and never splits (plan[5] = 1).
  *
  * Writes plan[0..5].  Returns KAN_OK, KAN_ERR_INVALID_ARG (plan == NULL, bad
  * grid or sizes, batch < 1, an invalid forced shape) or KAN_ERR_UNSUPPORTED.

@@ -18,7 +18,7 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libkan.so")
 SOURCES = ["kan_api.cpp", "kan_basis.hip", "kan_layer.hip", "kan_layer_bf16.hip",
-           "kan_layer_f32.hip", "kan_backward.hip", "kan_span.hip"]
+           "kan_layer_f32.hip", "kan_narrow.hip", "kan_backward.hip", "kan_span.hip"]
 ARCH = "gfx950"
 
 

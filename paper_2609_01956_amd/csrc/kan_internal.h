@@ -73,6 +73,7 @@ struct LayerGeom {
     int kb;       // blocks per chunk
     int nf;       // 32-column MFMA fragments per N tile (1, 2, 4 or 8)
     int ntiles;   // ceil(out / (32 * nf))
+    int out;      // output features
     // bf16 with two blocks per feature (5 <= G <= 12): packed for the
     // structured-sparse MFMA (block = feature of the pair, half = column
     // half, element e of half w = column 4 (e % 4) + 2 w + e / 4), and only
@@ -92,8 +93,11 @@ bool layer_geom(int nb, int kdeg, bool bf16, int in, int out, LayerGeom* g);
 // On the sparse layout eight waves of two row tiles (rf = 2, nw = 8) pair up:
 // the two waves of a 64-row group take the two column halves of the tile and
 // pass each other the A of one row tile each.
+// rf = 0 (wk = nw = 4, cs = 1) is instead the vector-ALU kernel of narrow
+// fp32 layers (kan_narrow.hip): one batch row per lane, 64 rows per
+// workgroup, the four waves splitting the features.
 struct LayerCfg {
-    int rf;  // 1 or 2
+    int rf;  // 1 or 2 (0: the narrow-layer kernel)
     int wk;  // 1, 2 or 4
     int nw;  // waves per workgroup: 4, or 8 (wk = 1, cs = 1; rf = 2 sparse only)
     int cs;  // column slices per N tile: 1, 2 or 4 (rf = 1, nw = 4 only)
@@ -101,8 +105,12 @@ struct LayerCfg {
 // Most rows any workgroup shape covers (x is addressed per workgroup with
 // 32-bit byte offsets, so kLayerMaxRows * in * 4 must stay below 2^32).
 constexpr int kLayerMaxRows = 256;
+// Rows per workgroup and most outputs of the narrow-layer kernel.
+constexpr int kNarrowRows = 64;
+constexpr int kNarrowMaxOut = 16;
 // Rows per workgroup of a shape.
 inline int64_t layer_cfg_rows(const LayerCfg& c) {
+    if (c.rf == 0) return kNarrowRows;
     return 32LL * c.rf * (c.nw / c.wk) / (c.rf == 2 && c.nw == 8 ? 2 : 1);
 }
 
@@ -187,6 +195,9 @@ hipError_t launch_layer_bf16(const LayerGeom& g, const LayerCfg& c, const LayerA
                              hipStream_t s);
 hipError_t launch_layer_f32(const LayerGeom& g, const LayerCfg& c, const LayerArgs& a,
                             hipStream_t s);
+// The narrow-layer kernel: fp32, k = 3, 1 <= out <= kNarrowMaxOut, G <= 26.
+bool narrow_ok(const LayerGeom& g);
+hipError_t launch_narrow(const LayerGeom& g, const LayerArgs& a, hipStream_t s);
 
 // ------------------------------------------------------------- backward
 //

@@ -92,6 +92,7 @@ __global__ __launch_bounds__(kThreads) void pack_kernel(const T* __restrict__ co
 bool layer_geom(int nb, int kdeg, bool bf16, int in, int out, LayerGeom* g) {
     g->nb = nb;
     g->kdeg = kdeg;
+    g->out = out;
     g->kj = bf16 ? 8 : 2;
     g->nsb = (nb + 1 + g->kj - 1) / g->kj;
     g->npairs = (in + 1) / 2;
@@ -119,6 +120,7 @@ bool layer_geom(int nb, int kdeg, bool bf16, int in, int out, LayerGeom* g) {
 }
 
 bool layer_cfg_valid(const LayerGeom& g, const LayerCfg& c) {
+    if (c.rf == 0) return c.wk == 4 && c.nw == 4 && c.cs == 1 && narrow_ok(g);
     // other degrees: the run-time degree build of one shape (one row tile per
     // wave, four waves, whole K and N tile)
     if (g.kdeg != 3) return c.rf == 1 && c.wk == 1 && c.nw == 4 && c.cs == 1;
@@ -142,6 +144,9 @@ bool layer_cfg_valid(const LayerGeom& g, const LayerCfg& c) {
 
 LayerCfg plan_layer(const LayerGeom& g, bool bf16, int64_t batch) {
     if (g.kdeg != 3) return LayerCfg{1, 1, 4, 1};
+    // Narrow fp32 layers on the vector ALUs (kan_narrow.hip) once the batch
+    // gives every CU workgroups.
+    if (narrow_ok(g) && batch >= 16384) return LayerCfg{0, 4, 4, 1};
     auto wgs = [&](const LayerCfg& c) {
         const int64_t bm = layer_cfg_rows(c);
         return ((batch + bm - 1) / bm) * g.ntiles * c.cs;
@@ -309,7 +314,7 @@ int layer_k_splits(const LayerGeom& g, const LayerCfg& c, int64_t batch, int out
     const int64_t bm = layer_cfg_rows(c);
     const int64_t wgs = ((batch + bm - 1) / bm) * g.ntiles * c.cs;
     const int nch = layer_chunks(g);
-    if (nch < 2 * kSplitMinChunks || wgs >= kSplitBelowWgs) return 1;
+    if (c.rf == 0 || nch < 2 * kSplitMinChunks || wgs >= kSplitBelowWgs) return 1;
     int64_t ks = (kSplitTargetWgs + wgs - 1) / wgs;
     ks = std::min<int64_t>(ks, nch / kSplitMinChunks);
     ks = std::min<int64_t>(ks, kSplitMaxPartialBytes / (batch * (int64_t)out * 4));
@@ -327,6 +332,7 @@ size_t layer_partial_bytes(const LayerGeom& g, const LayerCfg& c, int64_t batch,
 hipError_t launch_layer(bool bf16, const LayerGeom& g, const LayerCfg& c, LayerArgs a, int ks,
                         void* partial, hipStream_t s) {
     if (!layer_cfg_valid(g, c)) return hipErrorInvalidValue;
+    if (c.rf == 0) return ks == 1 ? launch_narrow(g, a, s) : hipErrorInvalidValue;
     const int nch = layer_chunks(g);
     if (ks < 1 || ks > nch || (ks > 1 && partial == nullptr)) return hipErrorInvalidValue;
     a.cps = (nch + ks - 1) / ks;

@@ -37,6 +37,15 @@ def test_layer_roofline_work_counts():
     assert n["peak"] == pytest.approx(256 * 4 * 32 * 2.4)
 
 
+def test_narrow_kernel_layer_roofline():
+    # the vector-ALU kernel: 36 lane-ops of basis generation plus 5 x out fmas
+    # per (row, feature), against the VALU peak
+    k = bench.layer_roofline("f32", 65536, 256, 10, 13, narrow=True)
+    assert k["bound"] == "alu" and k["unit"] == "Gop/s"
+    assert k["algorithmic"] == pytest.approx((36.0 + 50.0) * 65536 * 256 / 1e9)
+    assert k["peak"] == pytest.approx(256 * 4 * 32 * 2.4)
+
+
 def _fake_tree(tmp_path, record_md5):
     csrc = tmp_path / "paper_2609_01956_amd" / "csrc"
     csrc.mkdir(parents=True)

@@ -412,7 +412,7 @@ def test_mlp_full_size_production_launch_per_layer(dtype_name):
               for C, Wb in W["layers"]]
     code = kb.KAN_BF16 if bf else kb.KAN_F32
     want_shape = {"bf16": [(2, 1, 8, 1, 1), (2, 1, 8, 1, 1), (1, 2, 8, 1, 1)],
-                  "f32": [(2, 1, 4, 1, 0), (2, 1, 4, 1, 0), (1, 2, 4, 1, 0)]}[dtype_name]
+                  "f32": [(2, 1, 4, 1, 0), (2, 1, 4, 1, 0), (0, 4, 4, 1, 0)]}[dtype_name]
     for (C, _), want in zip(layers, want_shape):
         st, plan = kb.kan_layer_plan(kb.make_grid(G), code, B, C.shape[1], C.shape[0])
         assert st == kb.KAN_OK and plan[:5] == want and plan[5] == 1, (plan, want)
@@ -445,6 +445,79 @@ def test_mlp_full_size_production_launch_per_layer(dtype_name):
     say(info)
 
 
+# Narrow fp32 layers (at most 16 outputs) on the vector-ALU kernel, shape
+# {0, 4, 4, 1}: one row per lane, the features split over four waves and
+# staged 16 at a time.  Ragged batches (one row, a partial last workgroup),
+# one input feature, odd counts, partial feature chunks, grids 1 .. 26 (the
+# largest it takes), x 10% off the grid.
+NARROW_F32 = [
+    (1, 2, 5, 5),
+    (63, 1, 1, 10),
+    (65, 9, 7, 10),
+    (1000, 33, 10, 10),
+    (130, 17, 16, 26),
+    (777, 40, 11, 1),
+    (300, 256, 3, 3),
+    (129, 784, 13, 10),
+]
+
+
+@pytest.mark.parametrize("B,n_in,n_out,G", NARROW_F32)
+def test_layer_f32_narrow_kernel(B, n_in, n_out, G):
+    x, C, Wb = _inputs(B, n_in, n_out, G, seed=B + n_in + n_out + G, off=0.1)
+    say(f"layer f32 narrow B={B} in={n_in} out={n_out} G={G}")
+    y = _gpu_layer(x, C, Wb, G, "f32", shape="0,4")
+    ref = oracle.layer(x, C, Wb, G)
+    assert normwise(y, ref) <= F32_LAYER_TOL, normwise(y, ref)
+    # the MFMA kernel on the same inputs: another fp32 summation order
+    y2 = _gpu_layer(x, C, Wb, G, "f32", shape="1,1")
+    assert normwise(y, y2) <= F32_LAYER_TOL
+
+
+@pytest.mark.parametrize("n_out", list(range(1, 17)))
+def test_layer_f32_narrow_every_output_count(n_out):
+    """Each instantiation of the narrow kernel (outputs rounded up to even,
+    LDS rows padded to four floats)."""
+    B, n_in, G = 200, 21, 10
+    x, C, Wb = _inputs(B, n_in, n_out, G, seed=n_out, off=0.1)
+    say(f"layer f32 narrow out={n_out}")
+    y = _gpu_layer(x, C, Wb, G, "f32", shape="0,4")
+    ref = oracle.layer(x, C, Wb, G)
+    assert normwise(y, ref) <= F32_LAYER_TOL, normwise(y, ref)
+
+
+def test_layer_f32_narrow_nan_row_determinism_and_guard():
+    """A NaN input makes only its own row NaN; two runs are bitwise equal;
+    nothing is written around the output (a batch that ends inside a
+    workgroup)."""
+    B, n_in, n_out, G = 200, 37, 10, 10
+    x, C, Wb = _inputs(B, n_in, n_out, G, seed=6, off=0.2)
+    x[17, 30] = np.nan
+    say("layer f32 narrow nan/determinism/guard")
+    dt = torch.float32
+    p = kb.pack_layer(to_dev(C, dt), to_dev(Wb, dt), G)
+    xt = to_dev(x, dt)
+    buf = torch.full((B * n_out + 128,), 3.0, device=device())
+    out = buf[64:64 + B * n_out].view(B, n_out)
+    kb.layer_forward_packed(xt, p, out=out, shape="0,4")
+    y1 = out.clone()
+    kb.layer_forward_packed(xt, p, out=out, shape="0,4")
+    torch.cuda.synchronize()
+    assert torch.equal(y1.isnan(), out.isnan())
+    assert torch.equal(torch.nan_to_num(y1), torch.nan_to_num(out))
+    y = to_host64(out)
+    assert np.all(np.isnan(y[17]))
+    ok = np.ones(B, bool)
+    ok[17] = False
+    assert not np.any(np.isnan(y[ok]))
+    xr = x.copy()
+    xr[17, 30] = 0.0
+    ref = oracle.layer(xr, C, Wb, G)
+    assert normwise(y[ok], ref[ok]) <= F32_LAYER_TOL
+    b = to_host64(buf)
+    assert np.all(b[:64] == 3.0) and np.all(b[64 + B * n_out:] == 3.0)
+
+
 def _knot_inputs(G, dtype_name, lo=-1.0, hi=1.0):
     """Every knot t_0 .. t_{G+6} in the storage dtype, each one unit in the
     last place below and above it, lo, hi, zero and a few points past the
@@ -472,6 +545,8 @@ KNOT_CASES = [
     ("bf16", 8, 18, 10, "1,2,8"), ("bf16", 10, 18, 256, "2,1,8"), ("bf16", 10, 18, 10, None),
     ("bf16", 10, 17, 45, "1,1,4,2"), ("bf16", 16, 18, 256, None), ("bf16", 16, 18, 45, "1,2"),
     ("f32", 8, 18, 256, None), ("f32", 10, 18, 45, "2,1"), ("f32", 10, 17, 10, "1,4"),
+    # fp32 narrow layers on the vector-ALU kernel (its own window arithmetic)
+    ("f32", 8, 18, 10, "0,4"), ("f32", 10, 17, 16, "0,4"), ("f32", 26, 5, 1, "0,4"),
 ]
 
 

@@ -42,10 +42,11 @@ def _shape(cfg):
     ("bf16", 784, 256, (2, 1, 8, 1, 1)),
     ("bf16", 256, 256, (2, 1, 8, 1, 1)),
     ("bf16", 256, 10, (1, 2, 8, 1, 1)),
-    # fp32: 64-row waves over 128-column tiles; the narrow layer splits K
+    # fp32: 64-row waves over 128-column tiles; the narrow layer on the
+    # vector-ALU kernel
     ("f32", 784, 256, (2, 1, 4, 1, 0)),
     ("f32", 256, 256, (2, 1, 4, 1, 0)),
-    ("f32", 256, 10, (1, 2, 4, 1, 0)),
+    ("f32", 256, 10, (0, 4, 4, 1, 0)),
 ])
 def test_mlp_layers_planned_shapes(dtype_name, n_in, n_out, want):
     assert _plan(10, dtype_name, 65536, n_in, n_out) == want
@@ -89,6 +90,29 @@ def test_sparse_k_split_only_on_narrow_tiles():
         assert _rejected(G, dt, 65536, 256, n_out, cfg)
 
 
+def test_narrow_kernel_shape():
+    """The vector-ALU kernel {0, 4, 4, 1}: fp32 cubic layers of 1 .. 16
+    outputs with G <= 26, planned from batch 16384 on (below that the MFMA
+    kernel's K split fills the GPU), never split."""
+    assert _plan(10, "f32", 16384, 256, 10) == (0, 4, 4, 1, 0)
+    assert _splits(10, "f32", 16384, 256, 10) == 1
+    assert _plan(10, "f32", 16383, 256, 10)[0] != 0
+    assert _plan(10, "f32", 65536, 2, 5) == (0, 4, 4, 1, 0)
+    assert _plan(26, "f32", 65536, 256, 16) == (0, 4, 4, 1, 0)
+    assert _plan(10, "f32", 65536, 256, 17)[0] != 0
+    assert _plan(27, "f32", 65536, 256, 10)[0] != 0
+    assert _plan(10, "bf16", 65536, 256, 10)[0] != 0
+    # forced: any batch; the same limits
+    assert _plan(10, "f32", 1, 256, 10, "0,4") == (0, 4, 4, 1, 0)
+    assert _splits(10, "f32", 64, 784, 10, "0,4") == 1
+    for G, dt, n_out, cfg in [(10, "bf16", 10, "0,4"), (10, "f32", 17, "0,4"),
+                              (27, "f32", 10, "0,4"), (10, "f32", 10, "0,4,8"),
+                              (10, "f32", 10, "0,2"), (10, "f32", 10, "0,4,4,2")]:
+        assert _rejected(G, dt, 65536, 256, n_out, cfg), (G, dt, n_out, cfg)
+    st, _ = kb.kan_layer_plan(kb.make_grid(10, spline_order=2), DT["f32"], 65536, 256, 10, "0,4")
+    assert st == kb.KAN_ERR_INVALID_ARG
+
+
 @pytest.mark.parametrize("cfg", ["3,1", "1,3", "1,1,6", "1,1,4,3", "0,1", "1,2,8"])
 def test_invalid_forced_shape_is_rejected(cfg):
     assert _rejected(10, "bf16", 65536, 784, 256, cfg)
@@ -118,6 +142,8 @@ def _forced_cases():
     for dtype_name, G, n_in, n_out, cfg in gl.KNOT_CASES:
         if cfg is not None:
             yield dtype_name, G, 300, n_in, n_out, cfg
+    for B, n_in, n_out, G in gl.NARROW_F32:
+        yield "f32", G, B, n_in, n_out, "0,4"
 
 
 @pytest.mark.parametrize("dtype_name,G,B,n_in,n_out,cfg", list(_forced_cases()))
