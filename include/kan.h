@@ -269,7 +269,7 @@ kan_status kan_layer_forward_packed_workspace_bytes(const kan_grid* grid, kan_dt
  *
  * Degrees other than 3 run one shape, {1, 1, 4, 1}.
  *
- * Narrow layers: fp32, k = 3, 1 <= out_features <= 16 and G <= 26 can also
+ * Narrow layers: fp32, k = 3, 1 <= out_features <= 16 and G <= 58 can also
  * run the shape {0, 4, 4, 1}, a kernel without matrix instructions (one batch
  * row per lane, 64 rows per workgroup, four waves each taking a quarter of
  * the features, only the k + 1 nonzero basis values and the SiLU value of

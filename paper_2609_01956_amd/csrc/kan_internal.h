@@ -195,7 +195,7 @@ hipError_t launch_layer_bf16(const LayerGeom& g, const LayerCfg& c, const LayerA
                              hipStream_t s);
 hipError_t launch_layer_f32(const LayerGeom& g, const LayerCfg& c, const LayerArgs& a,
                             hipStream_t s);
-// The narrow-layer kernel: fp32, k = 3, 1 <= out <= kNarrowMaxOut, G <= 26.
+// The narrow-layer kernel: fp32, k = 3, 1 <= out <= kNarrowMaxOut, G <= 58.
 bool narrow_ok(const LayerGeom& g);
 hipError_t launch_narrow(const LayerGeom& g, const LayerArgs& a, hipStream_t s);
 

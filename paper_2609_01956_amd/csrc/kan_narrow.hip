@@ -14,10 +14,10 @@
 // with the columns of a feature ordered [SiLU weight, coef[.., 0 .. nb - 1]]
 // as in the packed buffer and c0 the first column of x's window.  The four
 // waves of a workgroup take the same 64 rows and a quarter of the features
-// each (four consecutive features of every chunk of 16), and add their
-// partial sums through LDS at the end, in wave order.
+// each (two consecutive features of every chunk of 8), and add their partial
+// sums through LDS at the end, in wave order.
 //
-// The weights of a chunk of 16 features go from the packed buffer (the MFMA
+// The weights of a chunk of 8 features go from the packed buffer (the MFMA
 // layout, kan_internal.h) through registers into LDS as a table
 // [feature][column][output]: one row of RS floats per column, the columns
 // zero-padded up to the last window column (nb + 2).  Each lane reads the
@@ -32,7 +32,10 @@ namespace kan {
 
 namespace {
 
-constexpr int kNarrowFeat = 16;  // features per staged chunk (four per wave)
+// Features per staged chunk, two per wave (256 -> 10 at batch 65536: 58 us,
+// against 63 with 16 features per chunk, 66 with 4 and 76 with 32).
+constexpr int kNarrowFeat = 8;
+constexpr int kFW = kNarrowFeat / 4;  // features per wave and chunk
 
 // Columns of a feature's LDS rows: the SiLU column, nb coefficients and the
 // zero columns up to nb + 2 (the last window column), rounded up to even.
@@ -59,7 +62,7 @@ void narrow_kernel(LayerArgs a, int cw) {
     const int nchunks = (a.in + kNarrowFeat - 1) / kNarrowFeat;
     const int fpk = 2 * a.npairs;  // features the packed buffer holds (zero past in)
 
-    // Staging: thread t < 16 * cw / 2 moves unit (feature fl, column pair cp)
+    // Staging: thread t < 8 * cw / 2 moves unit (feature fl, column pair cp)
     // of every chunk: in the packed buffer outputs 0 .. RS - 1 of block
     // (pair, cp), half fl % 2, are 2 RS consecutive floats (columns 2 cp and
     // 2 cp + 1 interleaved); in LDS they become rows 2 cp and 2 cp + 1 of the
@@ -68,7 +71,7 @@ void narrow_kernel(LayerArgs a, int cw) {
     const bool stager = tid < kNarrowFeat * cpn;
     const int sfl = tid / cpn, scp = tid - (tid / cpn) * cpn;
     const bool s_cols = scp < a.nsb;
-    // float offset of the unit in chunk 0; a chunk is 8 pairs further on
+    // float offset of the unit in chunk 0; a chunk is 4 pairs further on
     const int64_t s_off = ((((int64_t)(sfl >> 1) * a.nsb + scp) * 2 + (sfl & 1)) * 32) * 2;
     const int64_t chunk_floats = (int64_t)(kNarrowFeat / 2) * a.nsb * 128;
     const int s_row = (sfl * cw + 2 * scp) * RS;
@@ -96,12 +99,12 @@ void narrow_kernel(LayerArgs a, int cw) {
             d1[q] = floatx4{wv[8 * q + 1], wv[8 * q + 3], wv[8 * q + 5], wv[8 * q + 7]};
         }
     };
-    // x of the wave's four features of chunk c (0 past in: their weights are 0)
-    float xc[4], xn[4];
-    auto load_x = [&](int c, float (&xv)[4]) {
-        const int f0 = c * kNarrowFeat + 4 * wave;
+    // x of the wave's features of chunk c (0 past in: their weights are 0)
+    float xc[kFW], xn[kFW];
+    auto load_x = [&](int c, float (&xv)[kFW]) {
+        const int f0 = c * kNarrowFeat + kFW * wave;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) xv[j] = f0 + j < a.in ? xr[f0 + j] : 0.0f;
+        for (int j = 0; j < kFW; ++j) xv[j] = f0 + j < a.in ? xr[f0 + j] : 0.0f;
     };
 
     float acc[NO];
@@ -136,10 +139,10 @@ void narrow_kernel(LayerArgs a, int cw) {
             load_x(c + 1, xn);
         }
         const float* stg = lds + (c & 1) * stage_floats;
-        // (one feature at a time: unrolled, the LDS rows of all four are
-        // loaded up front and the registers run out)
+        // (one feature at a time: unrolled, the LDS rows of every feature
+        // are loaded up front and the registers run out)
 #pragma unroll 1
-        for (int j = 0; j < 4; ++j) {
+        for (int j = 0; j < kFW; ++j) {
             const float xv = xc[j];
             // v of column c is sv - c (column c is basis c - 1); the window
             // c0 .. c0 + 3 holds every basis with |v| < 2, c0 in [1, nb - 1]
@@ -148,7 +151,7 @@ void narrow_kernel(LayerArgs a, int cw) {
             const float f1 = __builtin_amdgcn_fmed3f(__builtin_floorf(sv), 2.0f, nbf);
             const int c0 = min(max((int)f1 - 1, 1), a.nb - 1);
             const float d = sv - (f1 - 1.0f);  // v of column c0
-            const float* tb = stg + (4 * wave + j) * cw * RS;
+            const float* tb = stg + (kFW * wave + j) * cw * RS;
             fma_row(layer_detail::half_silu(xv), tb);
             const float* tw = tb + c0 * RS;
 #pragma unroll
@@ -158,7 +161,7 @@ void narrow_kernel(LayerArgs a, int cw) {
         __syncthreads();
         if (more) {
 #pragma unroll
-            for (int j = 0; j < 4; ++j) xc[j] = xn[j];
+            for (int j = 0; j < kFW; ++j) xc[j] = xn[j];
         }
     }
 
@@ -193,10 +196,11 @@ hipError_t launch_no(const LayerArgs& a, int cw, hipStream_t s) {
 }  // namespace
 
 bool narrow_ok(const LayerGeom& g) {
-    // fp32 cubic layers of at most 16 outputs whose two LDS stages fit in
-    // 64 KB (G <= 26)
+    // fp32 cubic layers of at most 16 outputs with at most 64 columns per
+    // feature (G <= 58): two LDS stages of at most 64 KB, one staging unit
+    // per thread
     return g.kj == 2 && g.kdeg == 3 && g.out >= 1 && g.out <= kNarrowMaxOut &&
-           narrow_cols(g.nb) <= 32;
+           narrow_cols(g.nb) <= 64;
 }
 
 hipError_t launch_narrow(const LayerGeom& g, const LayerArgs& a, hipStream_t s) {

@@ -447,8 +447,8 @@ def test_mlp_full_size_production_launch_per_layer(dtype_name):
 
 # Narrow fp32 layers (at most 16 outputs) on the vector-ALU kernel, shape
 # {0, 4, 4, 1}: one row per lane, the features split over four waves and
-# staged 16 at a time.  Ragged batches (one row, a partial last workgroup),
-# one input feature, odd counts, partial feature chunks, grids 1 .. 26 (the
+# staged 8 at a time.  Ragged batches (one row, a partial last workgroup),
+# one input feature, odd counts, partial feature chunks, grids 1 .. 58 (the
 # largest it takes), x 10% off the grid.
 NARROW_F32 = [
     (1, 2, 5, 5),
@@ -459,6 +459,7 @@ NARROW_F32 = [
     (777, 40, 11, 1),
     (300, 256, 3, 3),
     (129, 784, 13, 10),
+    (150, 19, 9, 58),
 ]
 
 
@@ -547,6 +548,7 @@ KNOT_CASES = [
     ("f32", 8, 18, 256, None), ("f32", 10, 18, 45, "2,1"), ("f32", 10, 17, 10, "1,4"),
     # fp32 narrow layers on the vector-ALU kernel (its own window arithmetic)
     ("f32", 8, 18, 10, "0,4"), ("f32", 10, 17, 16, "0,4"), ("f32", 26, 5, 1, "0,4"),
+    ("f32", 58, 7, 16, "0,4"),
 ]
 
 

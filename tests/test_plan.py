@@ -92,21 +92,21 @@ def test_sparse_k_split_only_on_narrow_tiles():
 
 def test_narrow_kernel_shape():
     """The vector-ALU kernel {0, 4, 4, 1}: fp32 cubic layers of 1 .. 16
-    outputs with G <= 26, planned from batch 16384 on (below that the MFMA
+    outputs with G <= 58, planned from batch 16384 on (below that the MFMA
     kernel's K split fills the GPU), never split."""
     assert _plan(10, "f32", 16384, 256, 10) == (0, 4, 4, 1, 0)
     assert _splits(10, "f32", 16384, 256, 10) == 1
     assert _plan(10, "f32", 16383, 256, 10)[0] != 0
     assert _plan(10, "f32", 65536, 2, 5) == (0, 4, 4, 1, 0)
-    assert _plan(26, "f32", 65536, 256, 16) == (0, 4, 4, 1, 0)
+    assert _plan(58, "f32", 65536, 256, 16) == (0, 4, 4, 1, 0)
     assert _plan(10, "f32", 65536, 256, 17)[0] != 0
-    assert _plan(27, "f32", 65536, 256, 10)[0] != 0
+    assert _plan(59, "f32", 65536, 256, 10)[0] != 0
     assert _plan(10, "bf16", 65536, 256, 10)[0] != 0
     # forced: any batch; the same limits
     assert _plan(10, "f32", 1, 256, 10, "0,4") == (0, 4, 4, 1, 0)
     assert _splits(10, "f32", 64, 784, 10, "0,4") == 1
     for G, dt, n_out, cfg in [(10, "bf16", 10, "0,4"), (10, "f32", 17, "0,4"),
-                              (27, "f32", 10, "0,4"), (10, "f32", 10, "0,4,8"),
+                              (59, "f32", 10, "0,4"), (10, "f32", 10, "0,4,8"),
                               (10, "f32", 10, "0,2"), (10, "f32", 10, "0,4,4,2")]:
         assert _rejected(G, dt, 65536, 256, n_out, cfg), (G, dt, n_out, cfg)
     st, _ = kb.kan_layer_plan(kb.make_grid(10, spline_order=2), DT["f32"], 65536, 256, 10, "0,4")
