@@ -10,7 +10,9 @@ Inputs and weights are resident in HBM before timing starts; every launch goes
 through the C ABI onto torch's current stream.
 
 Prints ONE JSON line: samples/s (value), Gbasis/s, the roofline of the
-dominant kernel (per-kernel durations from HIP events on the launch stream),
+dominant kernel (its duration from HIP events around it in every timed step,
+the other kernels' from an untimed pass with an event between consecutive
+launches, all on the launch stream),
 per-layer parity of the run's output against the float64 oracle, the same
 step in the other dtype (bf16 and fp32 are both measured) and the float64
 CPU oracle timed on a bounded row sample of the same step.
@@ -387,10 +389,13 @@ def cpu_baseline(W, target_s: float):
 
 def measure_step(dtype: str, W, steps: int, warmup: int, clock_warmup_s: float = 0.0) -> dict:
     """Times `steps` steps of the hot path in `dtype` (after `clock_warmup_s`
-    seconds of untimed steps, then `warmup` more) with a HIP event between
-    consecutive kernels on torch's current stream, the stream every kernel is
-    launched on.  Returns the step time, per-kernel averages and rooflines,
-    and the outputs of the last step."""
+    seconds of untimed steps, then `warmup` more).  Per-kernel durations come
+    from `steps` untimed steps with a HIP event between consecutive kernels on
+    torch's current stream (the stream every kernel is launched on); the
+    timed steps then carry only a pair of events around the dominant kernel,
+    whose duration (the roofline's) is taken from them.  Returns the step
+    time, per-kernel averages and rooflines, and the outputs of the last
+    step."""
     import numpy as np
     import torch
 
@@ -417,27 +422,30 @@ def measure_step(dtype: str, W, steps: int, warmup: int, clock_warmup_s: float =
     for i, (i_, o) in enumerate(shapes):
         names += [f"pack{i + 1}_{i_}x{o}", f"layer{i + 1}_{i_}x{o}"]
 
-    def step(events=None):
-        """kan_basis_eval of the input, then per layer kan_layer_pack +
-        kan_layer_forward_packed (the weights are re-packed every step)."""
-        k = 0
-        if events is not None:
-            events[k].record()
-        kb.basis(x, G, lo, hi, out=phi)
-        k += 1
-        if events is not None:
-            events[k].record()
-        h = x
-        for (C, Wb), pk, out in zip(layers, packs, hs):
-            kb.pack_layer(C, Wb, G, lo, hi, out=pk)
-            k += 1
+    # The step's launches in order: kan_basis_eval of the input, then per
+    # layer kan_layer_pack + kan_layer_forward_packed (the weights are
+    # re-packed every step).
+    launches = [lambda: kb.basis(x, G, lo, hi, out=phi)]
+    h = x
+    for (C, Wb), pk, out in zip(layers, packs, hs):
+        launches.append(lambda C=C, Wb=Wb, pk=pk: kb.pack_layer(C, Wb, G, lo, hi, out=pk))
+        launches.append(lambda h=h, pk=pk, out=out: kb.layer_forward_packed(h, pk, out=out))
+        h = out
+
+    def step(events=None, only=None):
+        """One step.  events: with only=None an event before every launch and
+        one after the last; else a pair around launch `only`."""
+        for k, f in enumerate(launches):
             if events is not None:
-                events[k].record()
-            kb.layer_forward_packed(h, pk, out=out)
-            k += 1
-            if events is not None:
-                events[k].record()
-            h = out
+                if only is None:
+                    events[k].record()
+                elif k == only:
+                    events[0].record()
+            f()
+            if events is not None and k == only:
+                events[1].record()
+        if events is not None and only is None:
+            events[len(launches)].record()
 
     # Out of idle the GPU takes tens of milliseconds to reach its working
     # clock: with 5 warm-up steps alone the bf16 step measured 0.744 ms, after
@@ -451,18 +459,29 @@ def measure_step(dtype: str, W, steps: int, warmup: int, clock_warmup_s: float =
         step()
     torch.cuda.synchronize()
 
-    # Timed region: exactly `steps` steps, bracketed by synchronisations.
+    # Per-kernel durations: `steps` untimed steps with an event between
+    # consecutive launches (each event costs the step a few us, so the timed
+    # region below brackets only the dominant kernel).
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(names) + 1)]
           for _ in range(steps)]
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
     for k in range(steps):
         step(ev[k])
     torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    ms_per_step = (t1 - t0) * 1e3 / steps
     per_kernel_ms = [float(np.mean([e[i].elapsed_time(e[i + 1]) for e in ev]))
                      for i in range(len(names))]
+    dom_i = int(np.argmax(per_kernel_ms))
+
+    # Timed region: exactly `steps` steps, bracketed by synchronisations, with
+    # a pair of events around the dominant kernel in every step.
+    evd = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(steps):
+        step(evd[k], only=dom_i)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_per_step = (t1 - t0) * 1e3 / steps
+    per_kernel_ms[dom_i] = float(np.mean([e[0].elapsed_time(e[1]) for e in evd]))
 
     # Algorithmic work per launch.
     basis_values = B * n_in0 * nb
@@ -488,7 +507,7 @@ def measure_step(dtype: str, W, steps: int, warmup: int, clock_warmup_s: float =
         if "valu_gops" in k:  # the basis generation's share of the VALU peak
             k["valu_frac"] = k.pop("valu_gops") / (ms * 1e-3) / PEAK_VALU_GOPS
             k["valu_frac_dense_count"] = k.pop("valu_gops_dense") / (ms * 1e-3) / PEAK_VALU_GOPS
-    dom = max(names, key=lambda n: kern[n]["avg_us"])
+    dom = names[dom_i]
     dk = kern[dom]
     traffic = traffic_record(dtype, dom)
     roof = {"kernel": dom, "bound": dk["bound"], "achieved": dk["achieved"], "peak": dk["peak"],
@@ -765,6 +784,9 @@ def main() -> int:
                    "step": "kan_basis_eval(x) + 3 x (kan_layer_pack + kan_layer_forward_packed)"},
         "gbasis_per_s": r["gbasis_per_s"],
         "roofline": r["roofline"],
+        "kernel_timing": ("dominant kernel: HIP events around it in every timed step; the "
+                          "others: an untimed pass of as many steps with an event between "
+                          "consecutive launches"),
         "kernels": r["kernels"],
         "parity": r["parity"],
     }
