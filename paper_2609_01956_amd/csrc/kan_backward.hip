@@ -31,6 +31,8 @@
 // holds the coordinate constant.
 #include "kan_internal.h"
 
+#include <algorithm>
+
 namespace kan {
 
 namespace {
@@ -67,11 +69,18 @@ template <typename T> struct B;  // storage helpers
 template <> struct B<float> {
     static __device__ __forceinline__ float ld(const float* p) { return *p; }
     static __device__ __forceinline__ void st(float* p, float v) { *p = v; }
+    // two consecutive elements, p aligned to both
+    static __device__ __forceinline__ void st2(float* p, float v0, float v1) {
+        *reinterpret_cast<floatx2*>(p) = floatx2{v0, v1};
+    }
     static constexpr int E = 4;   // elements per 16-byte unit
 };
 template <> struct B<uint16_t> {
     static __device__ __forceinline__ float ld(const uint16_t* p) { return bf16_to_f32(*p); }
     static __device__ __forceinline__ void st(uint16_t* p, float v) { *p = f32_to_bf16(v); }
+    static __device__ __forceinline__ void st2(uint16_t* p, float v0, float v1) {
+        *reinterpret_cast<uint32_t*>(p) = pack2_bf16(v0, v1);
+    }
     static constexpr int E = 8;
 };
 
@@ -855,6 +864,206 @@ hipError_t launch_dw(const BwdGeom& g, const DwArgs<T>& d, hipStream_t s) {
     return hipGetLastError();
 }
 
+// ------------------------------------------------------- dx of narrow layers
+//
+// Layers of at most 16 outputs at large batches: dx on the vector ALUs.  Of a
+// (row, feature)'s columns only the SiLU column and the four basis columns
+// whose support holds x have a nonzero derivative, so
+//   dx[b, i] = silu'(x) t_0 + (1/h) sum_{k<4} N'(u of column c0 + k) t_{c0+k},
+//   t_c = sum_o dy[b, o] W[o, (i, c)],
+// with a feature's columns [SiLU weight, coef[o, i, 0 .. nb - 1]] and c0 the
+// window's first column, placed as in the forward's narrow-layer kernel
+// (c0 in [1, nb - 1]; a column the clamp takes in has |v| >= 2, where the
+// closed form of N' is exactly 0).  narrow_dx_table_kernel writes the weights
+// as an fp32 table [feature][column][output] (rows of nrs floats, zeros past
+// out, nb and in) into the workspace; narrow_dx_kernel stages 8 features of
+// it at a time in LDS (two stages, one barrier per chunk).  Each lane owns one
+// batch row with its dy in registers; the four waves of a 64-row workgroup
+// take two features of every chunk each.  dx goes through LDS and out as one
+// row's 8 consecutive features per thread.
+constexpr int kNdxRows = 64;
+constexpr int kNdxFeat = 8;
+
+template <typename T>
+__global__ __launch_bounds__(256) void narrow_dx_table_kernel(const T* __restrict__ coef,
+                                                              const T* __restrict__ bw,
+                                                              float* __restrict__ tab, int in,
+                                                              int nfeat, int out, int nb, int ncw,
+                                                              int nrs) {
+    const int64_t u = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (u >= (int64_t)nfeat * ncw * nrs) return;
+    const int o = (int)(u % nrs);
+    const int64_t r = u / nrs;
+    const int c = (int)(r % ncw);
+    const int f = (int)(r / ncw);
+    float v = 0.0f;
+    if (f < in && o < out) {
+        if (c == 0) v = B<T>::ld(bw + (int64_t)o * in + f);
+        else if (c <= nb) v = B<T>::ld(coef + ((int64_t)o * in + f) * nb + (c - 1));
+    }
+    tab[u] = v;
+}
+
+template <typename T>
+struct NdxArgs {
+    const T* xt;       // x transposed: [in][bpad]
+    int64_t bpad;
+    const T* dy;       // [batch][out]
+    const float* tab;  // [nfeat][ncw][nrs] (narrow_dx_table_kernel)
+    T* dx;             // [batch][in]
+    int64_t batch;
+    int in, out, nb, ncw;
+    float inv_h, inv_lo, xlim, a_int, a_frac;
+};
+
+// NO: outputs per lane (even, >= out); RS: table row stride in floats.
+template <typename T, int NO>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4)))
+void narrow_dx_kernel(NdxArgs<T> a) {
+    constexpr int RS = (NO + 3) / 4 * 4;
+    extern __shared__ floatx4 nds4[];
+    float* stg0 = reinterpret_cast<float*>(nds4);
+    __shared__ float dxs[2][kNdxRows][kNdxFeat + 1];
+    const int stage_floats = kNdxFeat * a.ncw * RS;  // a multiple of 4, at most 2048
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int64_t row0 = (int64_t)blockIdx.x * kNdxRows;
+    // rows past the batch read the last row (their dx is not stored)
+    const int64_t rowc = row0 + lane < a.batch ? row0 + lane : a.batch - 1;
+    float dyv[NO];
+#pragma unroll
+    for (int o = 0; o < NO; ++o) dyv[o] = o < a.out ? B<T>::ld(a.dy + rowc * a.out + o) : 0.0f;
+    const int nchunks = (a.in + kNdxFeat - 1) / kNdxFeat;
+
+    // the chunk's table rows are contiguous: at most two 16-byte units per thread
+    const int n4 = stage_floats / 4;
+    floatx4 wv[2];
+    auto load_w = [&](int c) {
+        const floatx4* src = reinterpret_cast<const floatx4*>(a.tab + (int64_t)c * stage_floats);
+#pragma unroll
+        for (int m = 0; m < 2; ++m) {
+            const int i = tid + 256 * m;
+            wv[m] = i < n4 ? src[i] : floatx4{0.0f, 0.0f, 0.0f, 0.0f};
+        }
+    };
+    auto store_w = [&](int st) {
+        floatx4* d = reinterpret_cast<floatx4*>(stg0 + st * stage_floats);
+#pragma unroll
+        for (int m = 0; m < 2; ++m) {
+            const int i = tid + 256 * m;
+            if (i < n4) d[i] = wv[m];
+        }
+    };
+    float xc[2], xn[2];
+    auto load_x = [&](int c, float (&xv)[2]) {
+        const int f0 = c * kNdxFeat + 2 * wave;
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+            xv[j] = f0 + j < a.in ? B<T>::ld(a.xt + (int64_t)(f0 + j) * a.bpad + rowc) : 0.0f;
+    };
+    // sum over the outputs of dy times one table row
+    auto tdot = [&](const float* r) -> float {
+        float t = 0.0f;
+#pragma unroll
+        for (int q = 0; q < NO / 4; ++q) {
+            const floatx4 w = reinterpret_cast<const floatx4*>(r)[q];
+            t = __builtin_fmaf(dyv[4 * q], w[0], t);
+            t = __builtin_fmaf(dyv[4 * q + 1], w[1], t);
+            t = __builtin_fmaf(dyv[4 * q + 2], w[2], t);
+            t = __builtin_fmaf(dyv[4 * q + 3], w[3], t);
+        }
+        if constexpr (NO % 4 != 0) {
+            const floatx2 w = reinterpret_cast<const floatx2*>(r)[NO / 2 - 1];
+            t = __builtin_fmaf(dyv[NO - 2], w[0], t);
+            t = __builtin_fmaf(dyv[NO - 1], w[1], t);
+        }
+        return t;
+    };
+    const float nbf = (float)a.nb;
+    // pairs of dx elements stored together: even rows of dx and an aligned base
+    const bool pair_st = (a.in & 1) == 0 &&
+                         reinterpret_cast<uintptr_t>(a.dx) % (2 * sizeof(T)) == 0;
+
+    load_w(0);
+    load_x(0, xc);
+    store_w(0);
+    __syncthreads();
+    for (int c = 0; c < nchunks; ++c) {
+        const bool more = c + 1 < nchunks;
+        if (more) {
+            load_w(c + 1);
+            load_x(c + 1, xn);
+        }
+        const float* stg = stg0 + (c & 1) * stage_floats;
+#pragma unroll 1
+        for (int j = 0; j < 2; ++j) {
+            const float xv = xc[j];
+            const float sv = __builtin_fmaf(xv, a.inv_h, a.a_int + 1.0f) +
+                             coord_lo(xv, a.xlim, a.inv_lo, a.a_frac);
+            const float f1 = __builtin_amdgcn_fmed3f(__builtin_floorf(sv), 2.0f, nbf);
+            const int c0 = min(max((int)f1 - 1, 1), a.nb - 1);
+            const float d = sv - (f1 - 1.0f);  // v of column c0
+            const float* tb = stg + (2 * wave + j) * a.ncw * RS;
+            const float* tw = tb + c0 * RS;
+            float sb = 0.0f;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) sb = __builtin_fmaf(dbasis(d - (float)k), tdot(tw + k * RS), sb);
+            dxs[c & 1][lane][2 * wave + j] = __builtin_fmaf(tdot(tb), silu_deriv(xv), a.inv_h * sb);
+        }
+        if (more) store_w((c + 1) & 1);
+        __syncthreads();
+        // dx of chunk c: thread t stores features 2 (t % 4) and 2 (t % 4) + 1
+        // of row row0 + t / 4 (four threads write a row's 8 features), as one
+        // two-element store where the pair is whole and aligned
+        {
+            const int rl = tid >> 2;
+            const int fl = 2 * (tid & 3);
+            const int64_t row = row0 + rl;
+            const int f = c * kNdxFeat + fl;
+            if (row < a.batch && f < a.in) {
+                T* dst = a.dx + row * a.in + f;
+                const float v0 = dxs[c & 1][rl][fl], v1 = dxs[c & 1][rl][fl + 1];
+                if (pair_st && f + 1 < a.in) {
+                    B<T>::st2(dst, v0, v1);
+                } else {
+                    B<T>::st(dst, v0);
+                    if (f + 1 < a.in) B<T>::st(dst + 1, v1);
+                }
+            }
+        }
+        if (more) {
+            xc[0] = xn[0];
+            xc[1] = xn[1];
+        }
+    }
+}
+
+template <typename T, int NO>
+hipError_t launch_ndx_no(const BwdGeom& g, const NdxArgs<T>& d, hipStream_t s) {
+    const size_t lds = (size_t)2 * kNdxFeat * g.ncw * g.nrs * sizeof(float);
+    const unsigned blocks = (unsigned)((d.batch + kNdxRows - 1) / kNdxRows);
+    hipLaunchKernelGGL((narrow_dx_kernel<T, NO>), dim3(blocks), dim3(256), lds, s, d);
+    return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_narrow_dx(const BwdGeom& g, const NdxArgs<T>& d, hipStream_t s) {
+    const int no = (d.out + 1) & ~1;
+    if (g.nrs != (no + 3) / 4 * 4) return hipErrorInvalidValue;
+    switch (no) {
+        case 2: return launch_ndx_no<T, 2>(g, d, s);
+        case 4: return launch_ndx_no<T, 4>(g, d, s);
+        case 6: return launch_ndx_no<T, 6>(g, d, s);
+        case 8: return launch_ndx_no<T, 8>(g, d, s);
+        case 10: return launch_ndx_no<T, 10>(g, d, s);
+        case 12: return launch_ndx_no<T, 12>(g, d, s);
+        case 14: return launch_ndx_no<T, 14>(g, d, s);
+        case 16: return launch_ndx_no<T, 16>(g, d, s);
+        default: return hipErrorInvalidValue;
+    }
+}
+
 template <typename T>
 hipError_t backward_t(const BwdGeom& g, const BwdArgs& a, hipStream_t s) {
     char* ws = static_cast<char*>(a.ws);
@@ -868,7 +1077,31 @@ hipError_t backward_t(const BwdGeom& g, const BwdArgs& a, hipStream_t s) {
                            s, x, xt, a.batch, a.in, g.bpad);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
-    if (a.dx != nullptr && a.batch > 0) {
+    if (a.dx != nullptr && a.batch > 0 && g.nx) {
+        float* tab = reinterpret_cast<float*>(ws + g.off_wt);
+        const int64_t n = (int64_t)g.nfeat * g.ncw * g.nrs;
+        hipLaunchKernelGGL(narrow_dx_table_kernel<T>, dim3((unsigned)((n + 255) / 256)), dim3(256),
+                           0, s, static_cast<const T*>(a.coef), static_cast<const T*>(a.bw), tab,
+                           a.in, g.nfeat, a.out, g.nb, g.ncw, g.nrs);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        NdxArgs<T> d;
+        d.xt = xt;
+        d.bpad = g.bpad;
+        d.dy = static_cast<const T*>(a.dy);
+        d.tab = tab;
+        d.dx = static_cast<T*>(a.dx);
+        d.batch = a.batch;
+        d.in = a.in;
+        d.out = a.out;
+        d.nb = g.nb;
+        d.ncw = g.ncw;
+        d.inv_h = a.inv_h;
+        d.inv_lo = a.inv_lo;
+        d.xlim = a.xlim;
+        d.a_int = a.a_int;
+        d.a_frac = a.a_frac;
+        if ((e = launch_narrow_dx<T>(g, d, s)) != hipSuccess) return e;
+    } else if (a.dx != nullptr && a.batch > 0) {
         T* wtp = reinterpret_cast<T*>(ws + g.off_wt);
         const int64_t units = (int64_t)g.ntiles * g.groups * 64;
         hipLaunchKernelGGL(pack_dx_kernel<T>, dim3((unsigned)((units + 255) / 256)), dim3(256), 0,
@@ -996,10 +1229,18 @@ bool bwd_geom(int nb, bool bf16, int64_t batch, int in, int out, BwdGeom* g) {
     g->rows_per_split = (int)(rps_chunks * 32);
     g->split = nck > 0 ? (int)((nck + rps_chunks - 1) / rps_chunks) : 0;
     if (g->split > 65535 || (batch + 255) / 256 > 0x7fffffffLL) return false;
+    // dx of narrow layers (at most 16 outputs, from 16384 rows) on the vector
+    // ALUs, with its fp32 weight table in the place of the packed weights
+    g->ncw = (nb + 4) & ~1;
+    g->nrs = (((out + 1) & ~1) + 3) / 4 * 4;
+    g->nfeat = (in + 7) / 8 * 8;
+    g->nx = out <= 16 && g->ncw * g->nrs <= 256 && batch >= 16384;
     const size_t es = bf16 ? 2 : 4;
     size_t off = 0;
     g->off_wt = off;
-    off = align256(off + (size_t)g->ntiles * g->groups * 1024);
+    size_t wt_bytes = (size_t)g->ntiles * g->groups * 1024;
+    if (g->nx) wt_bytes = std::max(wt_bytes, (size_t)g->nfeat * g->ncw * g->nrs * 4);
+    off = align256(off + wt_bytes);
     g->off_dyt = off;
     off = align256(off + (size_t)g->out32 * (size_t)g->bpad * es);
     g->off_xt = off;

@@ -222,6 +222,9 @@ struct BwdGeom {
     int dx_bm;      // dx: batch rows per workgroup
     int dx_ksplit;  // dx: workgroups splitting the K tiles of a row block
     int dx_tiles_per_split;  // dx: K tiles per such workgroup (whole features)
+    bool nx;        // dx on the vector-ALU kernel of narrow layers (else the MFMA kernel)
+    int ncw, nrs;   // nx: columns per feature and floats per column of its weight table
+    int nfeat;      // nx: features of the table (in rounded up to 8)
     int oh, nfw;    // dW: waves across outputs, 32-output fragments per wave
     int kt;         // dW: K rows per workgroup (256)
     int ktiles;     // dW: K tiles of kt rows

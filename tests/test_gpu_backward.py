@@ -1,5 +1,6 @@
 """GPU parity of kan_layer_backward (dx on the matrix cores with the clamped
-derivative contracted in the epilogue; dC and dWb on the matrix cores with
+derivative contracted in the epilogue, or for narrow layers at large batches
+on the vector ALUs over the window's columns; dC and dWb on the matrix cores with
 the basis regenerated in registers, batch splits summed in a fixed order)
 against the float64 oracle's layer_backward, through the C ABI.  Tolerances,
 normwise max|g - ref| / max|ref| per gradient: 1e-5 in fp32, 2e-2 in bf16
@@ -67,6 +68,53 @@ def test_backward_matches_oracle(B, n_in, n_out, G, dtype_name):
     _check(dx, rx, dtype_name, "dx")
     _check(dC, rC, dtype_name, "dC")
     _check(dW, rW, dtype_name, "dWb")
+
+
+# Layers of at most 16 outputs from 16384 rows on take dx on the vector-ALU
+# kernel (an fp32 weight table in the workspace, one batch row per lane, 8
+# features staged at a time): outputs 1, 3, 7, 10 and 16, grids 1 .. 26, odd
+# feature counts and partial feature chunks, batches that end inside a 64-row
+# workgroup.
+NARROW_BWD = [
+    (16384, 9, 10, 10),
+    (16400, 17, 1, 5),
+    (16411, 33, 16, 10),
+    (16384, 5, 3, 26),
+    (16390, 3, 7, 1),
+]
+
+
+@pytest.mark.parametrize("dtype_name", ["f32", "bf16"])
+@pytest.mark.parametrize("B,n_in,n_out,G", NARROW_BWD)
+def test_backward_narrow_dx(B, n_in, n_out, G, dtype_name):
+    x, C, Wb, dy = _case(B, n_in, n_out, G, seed=B + n_in + n_out, dtype_name=dtype_name)
+    say(f"backward narrow dx {dtype_name} B={B} in={n_in} out={n_out} G={G}")
+    dx, dC, dW = _run(x, C, Wb, dy, G, dtype_name)
+    rx, rC, rW = oracle.layer_backward(x, C, Wb, dy, G)
+    _check(dx, rx, dtype_name, "dx")
+    _check(dC, rC, dtype_name, "dC")
+    _check(dW, rW, dtype_name, "dWb")
+
+
+def test_backward_narrow_dx_nan_and_determinism():
+    """A NaN input on the narrow dx kernel: NaN at its own dx entry only (the
+    SiLU derivative carries it), every other entry as the oracle's; repeats
+    are bit-identical."""
+    B, n_in, n_out, G = 16500, 11, 10, 10
+    x, C, Wb, dy = _case(B, n_in, n_out, G, seed=8, dtype_name="f32")
+    x[16450, 4] = np.nan
+    say("backward narrow dx nan / determinism")
+    dx, _, _ = _run(x, C, Wb, dy, G, "f32", need_dw=False)
+    dx2, _, _ = _run(x, C, Wb, dy, G, "f32", need_dw=False)
+    np.testing.assert_array_equal(dx, dx2)
+    assert np.isnan(dx[16450, 4])
+    ok = np.ones_like(dx, bool)
+    ok[16450, 4] = False
+    assert not np.any(np.isnan(dx[ok]))
+    xr = x.copy()
+    xr[16450, 4] = 0.0
+    rx, _, _ = oracle.layer_backward(xr, C, Wb, dy, G)
+    assert normwise(dx[ok], rx[ok]) <= F32_LAYER_TOL
 
 
 @pytest.mark.parametrize("dtype_name", ["f32", "bf16"])
