@@ -24,8 +24,10 @@ def test_noalloc_matches_workspace_entry_point(dtype_name):
     cap = kb.KAN_NOALLOC_SCRATCH_BYTES
     # a layer of the 784-wide MLP input at a reduced batch, then smaller ones:
     # the second splits its contraction with the partial sums in the scratch
-    # array too
-    for B, n_in, n_out, G in [(1000, 784, 256, 10), (64, 784, 64, 5), (300, 17, 40, 7)]:
+    # array too; last a narrow layer at a batch where fp32 runs the vector-ALU
+    # kernel
+    for B, n_in, n_out, G in [(1000, 784, 256, 10), (64, 784, 64, 5), (300, 17, 40, 7),
+                              (16400, 33, 10, 10)]:
         x, C, Wb = wl.make_layer(wl.LayerShape(B, n_in, n_out, G, off_grid_frac=0.1),
                                  seed=B + n_in)
         if dtype_name == "bf16":
@@ -40,6 +42,8 @@ def test_noalloc_matches_workspace_entry_point(dtype_name):
         st, plan = kb.kan_layer_plan(g, code, B, n_in, n_out)
         if (B, n_in) == (64, 784):
             assert plan[5] > 1 and packed < need <= cap
+        if B == 16400 and dtype_name == "f32":
+            assert plan[:4] == (0, 4, 4, 1)
         # the workspace entry point gets the bytes the scratch array offers:
         # where the partial sums do not fit there, both run unsplit
         ws = torch.empty(min(need, cap), dtype=torch.uint8, device=device())
