@@ -265,7 +265,8 @@ kan_status kan_layer_forward_packed_workspace_bytes(const kan_grid* grid, kan_dt
  *            the caller gives kan_layer_forward_packed its workspace (1: no
  *            split).  Only batches that give fewer than 512 workgroups split,
  *            only layers with a long contraction, and into at most as many
- *            splits as keep the fp32 partial sums within 16 MiB.
+ *            splits as keep the fp32 partial sums within 16 MiB; the shape
+ *            {2, 1, 8, 1} and the narrow-layer kernel never split.
  *
  * Degrees other than 3 run one shape, {1, 1, 4, 1}.
  *

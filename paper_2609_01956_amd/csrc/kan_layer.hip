@@ -314,7 +314,11 @@ int layer_k_splits(const LayerGeom& g, const LayerCfg& c, int64_t batch, int out
     const int64_t bm = layer_cfg_rows(c);
     const int64_t wgs = ((batch + bm - 1) / bm) * g.ntiles * c.cs;
     const int nch = layer_chunks(g);
-    if (c.rf == 0 || nch < 2 * kSplitMinChunks || wgs >= kSplitBelowWgs) return 1;
+    // (the narrow-layer kernel and the shared-A shape, whose epilogue stores
+    // bf16 rows through LDS, never split)
+    if (c.rf == 0 || (c.rf == 2 && c.nw == 8) || nch < 2 * kSplitMinChunks ||
+        wgs >= kSplitBelowWgs)
+        return 1;
     int64_t ks = (kSplitTargetWgs + wgs - 1) / wgs;
     ks = std::min<int64_t>(ks, nch / kSplitMinChunks);
     ks = std::min<int64_t>(ks, kSplitMaxPartialBytes / (batch * (int64_t)out * 4));

@@ -965,7 +965,58 @@ void layer_kernel(LayerArgs a) {
 
     // ---- epilogue: y = 2 acc (the operands carry N / 2 and silu / 2)
     const int col0 = nt * (32 * NFL) + slice * NTILE;
-    if constexpr (WK == 1) {
+    // The shared-A shape (bf16, 256-column tiles; never K-split) stores y
+    // through LDS (the weight stages are free now): in two rounds, each wave
+    // writes one of its row tiles there as bf16, so a round holds 128 rows x
+    // 256 columns of the workgroup's tile (64 KB), and every thread then
+    // stores 16-byte row segments (element stores where out % 8 != 0 or y is
+    // not 16-byte aligned).  The accumulator layout alone gives 2-byte
+    // stores of 32 columns (C5 784 -> 256: 8.9 us of stores against about 5
+    // at the HBM write rate).
+    if constexpr (XA) {
+        static_assert(BF16 && NST * CHB >= 128 * 256 * 2, "staged epilogue");
+        const bool vec = (a.out & 7) == 0 && (reinterpret_cast<uintptr_t>(a.y) & 15) == 0;
+        uint16_t* st = reinterpret_cast<uint16_t*>(smem);  // [128][256]
+        const int64_t wg_row0 = (int64_t)blockIdx.x * BM;
+        // round R: every wave writes its row tile R (workgroup rows 64 wm +
+        // 32 (R ^ ch) + (0 .. 31), columns 128 ch + (0 .. 127)) at LDS rows
+        // 32 wm + (0 .. 31); the column half thus tells a unit's row tile.
+        // (acc is indexed by compile-time constants only: a tile chosen by
+        // ch at run time would move acc out of registers.)
+        auto out_round = [&](auto rr) __attribute__((always_inline)) {
+            constexpr int R = decltype(rr)::value;
+#pragma unroll
+            for (int nf = 0; nf < NFW; ++nf)
+#pragma unroll
+                for (int q = 0; q < 16; ++q) {
+                    const int rl = wm * 32 + 8 * (q / 4) + 4 * h + (q % 4);
+                    const int cl = (ch * NFW + nf) * 32 + r;
+                    st[rl * 256 + cl] = f32_to_bf16(2.0f * acc[R][nf][q]);
+                }
+            __syncthreads();
+#pragma unroll
+            for (int m = 0; m < 128 * 32 / NT; ++m) {
+                const int u = tid + NT * m;  // 16-byte unit: 32 per LDS row
+                const int rl = u >> 5;
+                const int cu = (u & 31) * 8;
+                const int col = col0 + cu;
+                const int k = cu < 128 ? R : 1 - R;  // the row tile of this column half
+                const int64_t row = wg_row0 + (rl >> 5) * 64 + k * 32 + (rl & 31);
+                if (row >= a.batch || col >= a.out) continue;
+                const uint16_t* src = st + rl * 256 + cu;
+                if (vec) {
+                    *reinterpret_cast<u32x4*>(y + row * a.out + col) =
+                        *reinterpret_cast<const u32x4*>(src);
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 8; ++e)
+                        if (col + e < a.out) y[row * a.out + col + e] = src[e];
+                }
+            }
+            __syncthreads();
+        };
+        StaticFor<0, 2>::run(out_round);
+    } else if constexpr (WK == 1) {
         const bool full = row0 + 32 * RF <= a.batch && col0 + NTILE <= a.out;
 #pragma unroll
         for (int rf = 0; rf < RF; ++rf) {
