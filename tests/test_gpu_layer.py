@@ -196,6 +196,30 @@ def test_layer_bf16_sparse_k_split(B, n_in, n_out, G, cfg):
     assert normwise(y, ref) <= BF16_LAYER_TOL, normwise(y, ref)
 
 
+STAGED_CASES = [(256, 0), (250, 0), (256, 1), (136, 3)]
+
+
+@pytest.mark.parametrize("n_out,offset", STAGED_CASES)
+def test_layer_shared_a_staged_epilogue(n_out, offset):
+    """The shared-A shape stores y through LDS: 16-byte row segments where
+    out % 8 == 0 and y is 16-byte aligned, else element stores (out = 250,
+    136, or y one or three elements past an aligned address); a ragged batch
+    ends inside the 256-row workgroup; nothing is written around y."""
+    B, n_in, G = 300, 13, 10
+    x, C, Wb = _inputs(B, n_in, n_out, G, seed=n_out + offset, off=0.1, dtype_name="bf16")
+    say(f"layer shared-A epilogue out={n_out} offset={offset}")
+    dt = torch.bfloat16
+    p = kb.pack_layer(to_dev(C, dt), to_dev(Wb, dt), G)
+    buf = torch.full((B * n_out + 64,), 3.0, dtype=dt, device=device())
+    out = buf[offset:offset + B * n_out].view(B, n_out)
+    kb.layer_forward_packed(to_dev(x, dt), p, out=out, shape="2,1,8")
+    torch.cuda.synchronize()
+    ref = oracle.round_bf16(oracle.layer(x, C, Wb, G))
+    assert normwise(to_host64(out), ref) <= BF16_LAYER_TOL
+    b = to_host64(buf)
+    assert np.all(b[:offset] == 3.0) and np.all(b[offset + B * n_out:] == 3.0)
+
+
 @pytest.mark.parametrize("B,n_in,n_out,G", SPARSE_SHAPES)
 def test_layer_bf16_sparse_mfma(B, n_in, n_out, G):
     x, C, Wb = _inputs(B, n_in, n_out, G, seed=B + G, off=0.2, dtype_name="bf16")

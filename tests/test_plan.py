@@ -75,6 +75,10 @@ def test_sparse_instruction_for_two_blocks_per_feature(G, sparse):
 
 def test_shared_a_shape_only_on_sparse_256_column_tiles():
     assert _plan(10, "bf16", 65536, 784, 256, "2,1,8") == (2, 1, 8, 1, 1)
+    # its epilogue stores bf16 rows through LDS: it never splits the
+    # contraction, also when forced on a batch that splits on other shapes
+    assert _splits(10, "bf16", 64, 784, 256, "2,1,8") == 1
+    assert _splits(10, "bf16", 64, 784, 256, "1,1,8") > 1
     # dense bf16, fp32 and narrower sparse tiles reject it
     for G, dt, n_out in [(20, "bf16", 256), (10, "f32", 256), (10, "bf16", 45)]:
         assert _rejected(G, dt, 65536, 784, n_out, "2,1,8")
@@ -144,6 +148,8 @@ def _forced_cases():
             yield dtype_name, G, 300, n_in, n_out, cfg
     for B, n_in, n_out, G in gl.NARROW_F32:
         yield "f32", G, B, n_in, n_out, "0,4"
+    for n_out, _ in gl.STAGED_CASES:
+        yield "bf16", 10, 300, 13, n_out, "2,1,8"
 
 
 @pytest.mark.parametrize("dtype_name,G,B,n_in,n_out,cfg", list(_forced_cases()))
