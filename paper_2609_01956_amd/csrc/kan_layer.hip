@@ -167,7 +167,7 @@ LayerCfg plan_layer(const LayerGeom& g, bool bf16, int64_t batch) {
     // Sparse layers (bf16, two blocks per feature): one row tile per wave and
     // no K split; eight waves per workgroup when that fills the chip, else
     // four over the whole tile (not for 256-column tiles), else column slices
-    // below.  (C5 layer 3, 256 -> 10: 49 us; 256 -> 100: 73 us with eight
+    // below.  (256 -> 10 at batch 65536: 49 us; 256 -> 100: 73 us with eight
     // waves against 82 us with four.)
     if (g.sparse) {
         // Tiles of one or two fragments: two wave slices splitting the

@@ -971,7 +971,7 @@ void layer_kernel(LayerArgs a) {
     // 256 columns of the workgroup's tile (64 KB), and every thread then
     // stores 16-byte row segments (element stores where out % 8 != 0 or y is
     // not 16-byte aligned).  The accumulator layout alone gives 2-byte
-    // stores of 32 columns (C5 784 -> 256: 8.9 us of stores against about 5
+    // stores of 32 columns (784 -> 256 at batch 65536: 8.9 us of stores, about 5
     // at the HBM write rate).
     if constexpr (XA) {
         static_assert(BF16 && NST * CHB >= 128 * 256 * 2, "staged epilogue");
