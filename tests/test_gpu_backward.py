@@ -81,6 +81,7 @@ NARROW_BWD = [
     (16411, 33, 16, 10),
     (16384, 5, 3, 26),
     (16390, 3, 7, 1),
+    (16384, 6, 4, 58),   # the largest table: 64 columns x 4 floats per feature
 ]
 
 

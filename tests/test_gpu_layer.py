@@ -511,6 +511,20 @@ def test_layer_f32_narrow_every_output_count(n_out):
     assert normwise(y, ref) <= F32_LAYER_TOL, normwise(y, ref)
 
 
+@pytest.mark.parametrize("B,n_in,n_out,G", [(16384, 19, 16, 58), (20000, 40, 5, 10)])
+def test_layer_f32_narrow_planned(B, n_in, n_out, G):
+    """The planner's own choice from 16384 rows on: the vector-ALU kernel,
+    at the largest grid it takes and at a batch that ends inside a
+    workgroup."""
+    st, plan = kb.kan_layer_plan(kb.make_grid(G), kb.KAN_F32, B, n_in, n_out)
+    assert st == kb.KAN_OK and plan[:4] == (0, 4, 4, 1)
+    x, C, Wb = _inputs(B, n_in, n_out, G, seed=B + G, off=0.1)
+    say(f"layer f32 narrow planned B={B} in={n_in} out={n_out} G={G}")
+    y = _gpu_layer(x, C, Wb, G, "f32")
+    ref = oracle.layer(x, C, Wb, G)
+    assert normwise(y, ref) <= F32_LAYER_TOL, normwise(y, ref)
+
+
 def test_layer_f32_narrow_nan_row_determinism_and_guard():
     """A NaN input makes only its own row NaN; two runs are bitwise equal;
     nothing is written around the output (a batch that ends inside a
