@@ -940,11 +940,20 @@ hipError_t launch_dw(const BwdGeom& g, const DwArgs<T>& d, hipStream_t s) {
 // window's first column, placed as in the forward's narrow-layer kernel
 // (c0 in [1, nb - 1]; a column the clamp takes in has |v| >= 2, where the
 // closed form of N' is exactly 0).  narrow_dx_table_kernel writes the weights
-// as an fp32 table [feature][column][output] (rows of nrs floats, zeros past
-// out, nb and in) into the workspace; narrow_dx_kernel stages 8 features of
-// it at a time in LDS (two stages, one barrier per chunk).  Each lane owns one
-// batch row with its dy in registers; the four waves of a 64-row workgroup
-// take two features of every chunk each.  dx goes through LDS and out as one
+// as a table [feature][column][output] (zeros past out, nb and in) into the
+// workspace, in 32-bit words: rows of nrs fp32 weights, or in bf16 of nrs / 2
+// words that each hold two consecutive outputs' bf16 weights unchanged;
+// narrow_dx_kernel stages 8 features of it at a time in LDS (two stages, one
+// barrier per chunk).  Each lane owns one batch row with its dy in registers;
+// the four waves of a 64-row workgroup take two features of every chunk each.
+// dx has no sum over features, so the chunks can be split over blockIdx.y
+// (cpg chunks per workgroup) to give the CUs more waves, as far as they all
+// fit at once (a second, partial round of workgroups costs more than the
+// waves gain: 784 -> 16 at batch 65536).
+// In bf16 each t_c is a chain of two-term dot products (v_dot2_f32_bf16) of
+// dy and weight pairs: both are bf16 inputs, so the products are exact and
+// only the fp32 sums round, as with fp32 FMAs; it halves the VALU
+// instructions and LDS bytes of the sums.  dx goes through LDS and out as one
 // row's 8 consecutive features per thread.
 constexpr int kNdxRows = 64;
 constexpr int kNdxFeat = 8;
@@ -952,19 +961,30 @@ constexpr int kNdxFeat = 8;
 template <typename T>
 __global__ __launch_bounds__(256) void narrow_dx_table_kernel(const T* __restrict__ coef,
                                                               const T* __restrict__ bw,
-                                                              float* __restrict__ tab, int in,
+                                                              uint32_t* __restrict__ tab, int in,
                                                               int nfeat, int out, int nb, int ncw,
                                                               int nrs) {
+    constexpr int PW = sizeof(T) == 2 ? 2 : 1;  // outputs per word
+    const int rw = nrs / PW;
     const int64_t u = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    if (u >= (int64_t)nfeat * ncw * nrs) return;
-    const int o = (int)(u % nrs);
-    const int64_t r = u / nrs;
+    if (u >= (int64_t)nfeat * ncw * rw) return;
+    const int p = (int)(u % rw);
+    const int64_t r = u / rw;
     const int c = (int)(r % ncw);
     const int f = (int)(r / ncw);
-    float v = 0.0f;
-    if (f < in && o < out) {
-        if (c == 0) v = B<T>::ld(bw + (int64_t)o * in + f);
-        else if (c <= nb) v = B<T>::ld(coef + ((int64_t)o * in + f) * nb + (c - 1));
+    uint32_t v = 0;
+#pragma unroll
+    for (int e = 0; e < PW; ++e) {
+        const int o = PW * p + e;
+        T w = T(0);
+        if (f < in && o < out) {
+            if (c == 0) w = bw[(int64_t)o * in + f];
+            else if (c <= nb) w = coef[((int64_t)o * in + f) * nb + (c - 1)];
+        }
+        if constexpr (PW == 2)
+            v |= (uint32_t)w << (16 * e);
+        else
+            v = __float_as_uint(w);
     }
     tab[u] = v;
 }
@@ -974,22 +994,26 @@ struct NdxArgs {
     const T* xt;       // x transposed: [in][bpad]
     int64_t bpad;
     const T* dy;       // [batch][out]
-    const float* tab;  // [nfeat][ncw][nrs] (narrow_dx_table_kernel)
+    const uint32_t* tab;  // [nfeat][ncw][row words] (narrow_dx_table_kernel)
     T* dx;             // [batch][in]
     int64_t batch;
     int in, out, nb, ncw;
+    int cpg;  // feature chunks per workgroup (blockIdx.y)
     float inv_h, inv_lo, xlim, a_int, a_frac;
 };
 
-// NO: outputs per lane (even, >= out); RS: table row stride in floats.
+// NO: outputs per lane (even, >= out); RS: outputs per table row; RW: its
+// 32-bit words (even).
 template <typename T, int NO>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4)))
 void narrow_dx_kernel(NdxArgs<T> a) {
+    constexpr bool BF = sizeof(T) == 2;
     constexpr int RS = (NO + 3) / 4 * 4;
+    constexpr int RW = BF ? RS / 2 : RS;
     extern __shared__ floatx4 nds4[];
-    float* stg0 = reinterpret_cast<float*>(nds4);
+    float* stg0 = reinterpret_cast<float*>(nds4);  // table words (bf16: pairs)
     __shared__ float dxs[2][kNdxRows][kNdxFeat + 1];
-    const int stage_floats = kNdxFeat * a.ncw * RS;  // a multiple of 4, at most 2048
+    const int stage_floats = kNdxFeat * a.ncw * RW;  // a multiple of 4, at most 2048
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -999,7 +1023,12 @@ void narrow_dx_kernel(NdxArgs<T> a) {
     float dyv[NO];
 #pragma unroll
     for (int o = 0; o < NO; ++o) dyv[o] = o < a.out ? B<T>::ld(a.dy + rowc * a.out + o) : 0.0f;
-    const int nchunks = (a.in + kNdxFeat - 1) / kNdxFeat;
+    // bf16: dy of outputs 2 q, 2 q + 1 as one operand (exact: dy is bf16)
+    bf16x2_t dyp[NO / 2];
+#pragma unroll
+    for (int q = 0; q < NO / 2; ++q) dyp[q] = bf16x2_t{(__bf16)dyv[2 * q], (__bf16)dyv[2 * q + 1]};
+    const int c_begin = blockIdx.y * a.cpg;
+    const int nchunks = min((a.in + kNdxFeat - 1) / kNdxFeat, c_begin + a.cpg);
 
     // the chunk's table rows are contiguous: at most two 16-byte units per thread
     const int n4 = stage_floats / 4;
@@ -1030,6 +1059,16 @@ void narrow_dx_kernel(NdxArgs<T> a) {
     // sum over the outputs of dy times one table row
     auto tdot = [&](const float* r) -> float {
         float t = 0.0f;
+        if constexpr (BF) {
+            // (the words are read as bf16 pairs directly: with this compiler,
+            // __builtin_bit_cast of element 1 of a two-float vector produced
+            // element 0's bits)
+            const bf16x2_t* rb = reinterpret_cast<const bf16x2_t*>(r);
+#pragma unroll
+            for (int q = 0; q < NO / 2; ++q)
+                t = __builtin_amdgcn_fdot2_f32_bf16(dyp[q], rb[q], t, false);
+            return t;
+        }
 #pragma unroll
         for (int q = 0; q < NO / 4; ++q) {
             const floatx4 w = reinterpret_cast<const floatx4*>(r)[q];
@@ -1050,11 +1089,11 @@ void narrow_dx_kernel(NdxArgs<T> a) {
     const bool pair_st = (a.in & 1) == 0 &&
                          reinterpret_cast<uintptr_t>(a.dx) % (2 * sizeof(T)) == 0;
 
-    load_w(0);
-    load_x(0, xc);
-    store_w(0);
+    load_w(c_begin);
+    load_x(c_begin, xc);
+    store_w(c_begin & 1);
     __syncthreads();
-    for (int c = 0; c < nchunks; ++c) {
+    for (int c = c_begin; c < nchunks; ++c) {
         const bool more = c + 1 < nchunks;
         if (more) {
             load_w(c + 1);
@@ -1069,11 +1108,11 @@ void narrow_dx_kernel(NdxArgs<T> a) {
             const float f1 = __builtin_amdgcn_fmed3f(__builtin_floorf(sv), 2.0f, nbf);
             const int c0 = min(max((int)f1 - 1, 1), a.nb - 1);
             const float d = sv - (f1 - 1.0f);  // v of column c0
-            const float* tb = stg + (2 * wave + j) * a.ncw * RS;
-            const float* tw = tb + c0 * RS;
+            const float* tb = stg + (2 * wave + j) * a.ncw * RW;
+            const float* tw = tb + c0 * RW;
             float sb = 0.0f;
 #pragma unroll
-            for (int k = 0; k < 4; ++k) sb = __builtin_fmaf(dbasis(d - (float)k), tdot(tw + k * RS), sb);
+            for (int k = 0; k < 4; ++k) sb = __builtin_fmaf(dbasis(d - (float)k), tdot(tw + k * RW), sb);
             dxs[c & 1][lane][2 * wave + j] = __builtin_fmaf(tdot(tb), silu_deriv(xv), a.inv_h * sb);
         }
         if (more) store_w((c + 1) & 1);
@@ -1105,10 +1144,22 @@ void narrow_dx_kernel(NdxArgs<T> a) {
 }
 
 template <typename T, int NO>
-hipError_t launch_ndx_no(const BwdGeom& g, const NdxArgs<T>& d, hipStream_t s) {
-    const size_t lds = (size_t)2 * kNdxFeat * g.ncw * g.nrs * sizeof(float);
-    const unsigned blocks = (unsigned)((d.batch + kNdxRows - 1) / kNdxRows);
-    hipLaunchKernelGGL((narrow_dx_kernel<T, NO>), dim3(blocks), dim3(256), lds, s, d);
+hipError_t launch_ndx_no(const BwdGeom& g, const NdxArgs<T>& d0, hipStream_t s) {
+    // (bf16 table words hold two outputs)
+    const size_t lds = (size_t)2 * kNdxFeat * g.ncw * g.nrs * (sizeof(T) == 2 ? 2 : 4);
+    const int64_t blocks = (d0.batch + kNdxRows - 1) / kNdxRows;
+    // Feature groups: as many as keep every workgroup resident at once on the
+    // 256 CUs: at most eight per CU (eight waves per SIMD, as these kernels
+    // take at most 64 VGPRs) and as many as the CU's 160 KB of LDS holds.
+    const int64_t lds_wg = (int64_t)lds + 2 * kNdxRows * (kNdxFeat + 1) * (int64_t)sizeof(float);
+    const int64_t per_cu = std::min<int64_t>(8, (160 * 1024) / lds_wg);
+    const int64_t nch = (d0.in + kNdxFeat - 1) / kNdxFeat;
+    const int64_t fg = std::max<int64_t>(1, std::min<int64_t>(nch, 256 * per_cu / blocks));
+    NdxArgs<T> d = d0;
+    d.cpg = (int)((nch + fg - 1) / fg);
+    const unsigned groups = (unsigned)((nch + d.cpg - 1) / d.cpg);
+    hipLaunchKernelGGL((narrow_dx_kernel<T, NO>), dim3((unsigned)blocks, groups), dim3(256), lds, s,
+                       d);
     return hipGetLastError();
 }
 
@@ -1155,8 +1206,8 @@ hipError_t backward_t(const BwdGeom& g, const BwdArgs& a, hipStream_t s) {
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     if (a.dx != nullptr && a.batch > 0 && g.nx) {
-        float* tab = reinterpret_cast<float*>(ws + g.off_wt);
-        const int64_t n = (int64_t)g.nfeat * g.ncw * g.nrs;
+        uint32_t* tab = reinterpret_cast<uint32_t*>(ws + g.off_wt);
+        const int64_t n = (int64_t)g.nfeat * g.ncw * g.nrs / (sizeof(T) == 2 ? 2 : 1);
         hipLaunchKernelGGL(narrow_dx_table_kernel<T>, dim3((unsigned)((n + 255) / 256)), dim3(256),
                            0, s, static_cast<const T*>(a.coef), static_cast<const T*>(a.bw), tab,
                            a.in, g.nfeat, a.out, g.nb, g.ncw, g.nrs);
@@ -1172,6 +1223,7 @@ hipError_t backward_t(const BwdGeom& g, const BwdArgs& a, hipStream_t s) {
         d.out = a.out;
         d.nb = g.nb;
         d.ncw = g.ncw;
+        d.cpg = 1;  // (set at launch)
         d.inv_h = a.inv_h;
         d.inv_lo = a.inv_lo;
         d.xlim = a.xlim;

@@ -82,6 +82,7 @@ NARROW_BWD = [
     (16384, 5, 3, 26),
     (16390, 3, 7, 1),
     (16384, 6, 4, 58),   # the largest table: 64 columns x 4 floats per feature
+    (65536, 37, 10, 10),  # two feature groups of 3 and 2 chunks, the last chunk ragged
 ]
 
 
