@@ -319,8 +319,9 @@ kan_status kan_layer_plan(const kan_grid* grid, kan_dtype dtype, int64_t batch,
  * down to even, times its outputs rounded up to a multiple of 4 stay within
  * 256) dx runs instead on the vector ALUs over the SiLU column and the four
  * basis columns whose support holds x (the others' derivatives are exactly 0),
- * one batch row per lane, with an fp32 copy of the weights in the workspace;
- * the same sums up to the fp32 summation order.  The weight
+ * one batch row per lane, with a copy of the weights in the workspace (fp32,
+ * or in bf16 the weights as given, summed by two-term bf16 dot products with
+ * fp32 accumulation): the same sums up to the fp32 summation order.  The weight
  * gradients sum the batch in a fixed order (deterministic).  Outputs are
  * fully overwritten; with batch == 0 the weight gradients are written as 0.
  * Outputs must not overlap each other, any input or the workspace.
