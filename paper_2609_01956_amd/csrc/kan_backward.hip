@@ -1378,7 +1378,8 @@ bool bwd_geom(int nb, bool bf16, int64_t batch, int in, int out, BwdGeom* g) {
     g->split = nck > 0 ? (int)((nck + rps_chunks - 1) / rps_chunks) : 0;
     if (g->split > 65535 || (batch + 255) / 256 > 0x7fffffffLL) return false;
     // dx of narrow layers (at most 16 outputs, from 16384 rows) on the vector
-    // ALUs, with its fp32 weight table in the place of the packed weights
+    // ALUs, with its weight table (fp32 weights, or bf16 weights in pairs) in
+    // the place of the packed weights
     g->ncw = (nb + 4) & ~1;
     g->nrs = (((out + 1) & ~1) + 3) / 4 * 4;
     g->nfeat = (in + 7) / 8 * 8;
@@ -1387,7 +1388,7 @@ bool bwd_geom(int nb, bool bf16, int64_t batch, int in, int out, BwdGeom* g) {
     size_t off = 0;
     g->off_wt = off;
     size_t wt_bytes = (size_t)g->ntiles * g->groups * 1024;
-    if (g->nx) wt_bytes = std::max(wt_bytes, (size_t)g->nfeat * g->ncw * g->nrs * 4);
+    if (g->nx) wt_bytes = std::max(wt_bytes, (size_t)g->nfeat * g->ncw * g->nrs * es);
     off = align256(off + wt_bytes);
     g->off_dyt = off;
     off = align256(off + (size_t)g->out32 * (size_t)g->bpad * es);

@@ -328,11 +328,12 @@ def test_backward_workspace_bytes(G, n_in, n_out, B, bf16):
 
 def test_backward_workspace_holds_the_narrow_dx_table():
     """Layers of at most 16 outputs take dx on the vector-ALU kernel from
-    16384 rows on; its fp32 weight table [in rounded up to 8][G + 7 rounded
-    down to even][out rounded up to even, then to a multiple of 4] takes the
-    place of the packed weights (256 x 16 x 12 floats for 256 -> 10 at
-    G = 10, 64 KiB more than the bf16 packed weights), and only when a
-    feature's table (columns x row floats) fits 256 floats."""
+    16384 rows on; its weight table [in rounded up to 8][G + 7 rounded down
+    to even][out rounded up to even, then to a multiple of 4] (fp32 weights,
+    or bf16 weights in pairs) takes the place of the packed weights (for
+    256 -> 10 at G = 10, 256 x 16 x 12 elements: 192 KiB in fp32, within the
+    256 KiB of packed fp32 weights; 96 KiB in bf16, within their 128 KiB), and
+    only when a feature's table (columns x row elements) fits 256."""
     g = kb.make_grid(10)
     for dt in (kb.KAN_BF16, kb.KAN_F32):
         st, small = kb.kan_layer_backward_workspace_bytes(g, dt, 16383, 256, 10)
@@ -340,11 +341,10 @@ def test_backward_workspace_holds_the_narrow_dx_table():
         assert st == st2 == kb.KAN_OK
         es = 2 if dt == kb.KAN_BF16 else 4
         grow = big - small  # the new row's share of dy^T and x^T, plus the table
-        table = 256 * 16 * 12 * 4
+        table = 256 * 16 * 12 * es
         packed = 128 * (1 if dt == kb.KAN_BF16 else 2) * 1024
-        assert grow - max(table - packed, 0) < 4096 * es, (dt, grow)
-        if dt == kb.KAN_BF16:
-            assert grow >= table - packed
+        assert table < packed
+        assert grow < 4096 * es, (dt, grow)
     # 17 outputs, or a grid whose table rows pass 256 floats: the MFMA kernel
     for n_out, G in [(17, 10), (16, 12)]:
         a = kb.kan_layer_backward_workspace_bytes(kb.make_grid(G), kb.KAN_BF16, 16383, 256, n_out)[1]
